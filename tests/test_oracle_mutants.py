@@ -1,0 +1,90 @@
+"""The oracle pins must catch plausible mistakes (no GPU).
+
+Each case below plants one mistake in a copy of the oracle's C source (a
+dropped term, a wrong sign, a wrong index, a transposed layout), builds it
+with gcc into a temporary directory, and runs every pin of
+``test_oracle_pins.py`` against it in a child process (a mistake may crash).
+At least one pin must fail for every mutant; the unmodified source must pass
+all of them.
+"""
+import os
+import subprocess
+import sys
+import textwrap
+
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "pda_oracle.c")
+
+MUTANTS = {
+    "kv head = h mod Hkv": ("int g = h / G;", "int g = h % P->Hkv;"),
+    "block and slot swapped": ("bt[t / P->BS], g, t % P->BS", "bt[t % P->BS], g, t / P->BS"),
+    "no max subtraction": ("exp(scores[t] - m)", "exp(scores[t])"),
+    "exp sign flipped": ("exp(scores[t] - m)", "exp(m - scores[t])"),
+    "scale dropped": ("scores[t] = P->scale * dot;", "scores[t] = dot;"),
+    "no normalisation": ("for (int t = 0; t < L; ++t) scores[t] /= Z;", ""),
+    "sum starts at one": ("double Z = 0.0;", "double Z = 1.0;"),
+    "cache layout [p][o][g]": ("(((size_t)p * P->Hkv + g) * P->BS + o) * P->D",
+                               "(((size_t)p * P->BS + o) * P->Hkv + g) * P->D"),
+    "q row of the kv head": ("((size_t)b * P->Hq + h) * P->D", "((size_t)b * P->Hq + g) * P->D"),
+    "V read from K": ("const uint16_t *vrow = P->v +", "const uint16_t *vrow = P->k +"),
+    "bf16 widened wrongly": ("(uint32_t)bits << 16", "(uint32_t)bits << 15"),
+    "last token dropped from V sum": ("for (int t = 0; t < L; ++t) {\n    const uint16_t *vrow",
+                                      "for (int t = 0; t + 1 < L; ++t) {\n    const uint16_t *vrow"),
+    "min instead of max": ("if (scores[t] > m) m = scores[t];", "if (scores[t] < m || t == 0) m = scores[t];"),
+    "table row stride = B": ("P->block_table + (size_t)b * P->max_blocks_per_seq",
+                             "P->block_table + (size_t)b * P->B"),
+    "zero length not zeroed": ("for (int d = 0; d < P->D; ++d) out_row[d] = 0.0;\n  int L",
+                               "int L"),
+}
+
+RUNNER = textwrap.dedent("""
+    import sys, traceback
+    sys.path[:0] = [{root!r}, {tests!r}]
+    import numpy as np
+    np.seterr(all="ignore")
+    import oracle, test_oracle_pins as T
+    O = oracle.Oracle({lib!r})
+    failed = []
+    for pin in T.PINS:
+        try:
+            pin(O)
+        except BaseException:
+            failed.append(pin.__name__)
+    print("FAILED:" + ",".join(failed))
+""")
+
+
+def run_pins_in_child(lib_path):
+    code = RUNNER.format(root=ROOT, tests=os.path.join(ROOT, "tests"), lib=lib_path)
+    p = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    lines = [l for l in p.stdout.splitlines() if l.startswith("FAILED:")]
+    if p.returncode != 0 or not lines:
+        return None  # crashed: the mistake is caught, loudly
+    return [f for f in lines[-1][len("FAILED:"):].split(",") if f]
+
+
+def build_variant(tmp_path, old, new):
+    src = open(SRC).read()
+    assert old in src, f"mutation anchor not found: {old!r}"
+    path = tmp_path / "pda_oracle_mut.c"
+    path.write_text(src.replace(old, new))
+    lib = str(tmp_path / "libpda_oracle_mut.so")
+    oracle.build(src=str(path), lib=lib)
+    return lib
+
+
+def test_unmodified_source_passes_all_pins(tmp_path):
+    lib = str(tmp_path / "libpda_oracle_copy.so")
+    oracle.build(lib=lib)
+    assert run_pins_in_child(lib) == []
+
+
+@pytest.mark.parametrize("name", list(MUTANTS))
+def test_mutant_is_caught(tmp_path, name):
+    old, new = MUTANTS[name]
+    failed = run_pins_in_child(build_variant(tmp_path, old, new))
+    assert failed is None or len(failed) > 0, f"no pin caught mutant {name!r}"

@@ -1,0 +1,311 @@
+"""Seeded synthetic inputs for paged decode attention.
+
+This module only draws inputs; it holds none of the attention arithmetic.  It
+is the one piece shared by the GPU tests, the benchmark and the oracle tests.
+
+A workload has two parts:
+
+* the *structure*, drawn on the host with numpy's counter-based Philox
+  generator: context lengths, the block table and the physical block pool;
+* the *values* q, K, V, drawn with torch's seeded generator on any device
+  (``cpu`` for the CPU tests, ``cuda`` for the large configurations, where
+  only a device generator is fast enough) and rounded to bf16 to nearest
+  even by ``Tensor.to(torch.bfloat16)``.
+
+The five named configurations are the rollout decode steps the build is
+measured on: the paper's long chain-of-thought rollouts (Section 4.1 uses
+inputs of at most 1024 tokens and generations up to 8K tokens, Section 3.2
+describes vLLM's PagedAttention with block sharing for parallel sampling)
+stand in as Llama-3-shaped synthetic batches, since no model weights or
+datasets are available.
+
+Streams of the Philox generator (seed, stream):
+    1 lengths, 2 pool permutation, 3 q, 4 K, 5 V, 6 per-head K offset.
+Pool blocks that no sequence references, and the slots of a block beyond the
+longest context that references it, can be filled with bf16 NaN ("poison")
+so that any read of them shows up in the output.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Dict, Optional, Sequence
+
+import numpy as np
+
+BLOCK_SIZE = 16
+_STREAM_LENS, _STREAM_POOL, _STREAM_Q, _STREAM_K, _STREAM_V, _STREAM_KOFF = 1, 2, 3, 4, 5, 6
+_POOL_CHUNK_BLOCKS = 4096  # the value draw walks the pool in fixed chunks (deterministic)
+
+
+# Named configurations.  `lens` is (kind, lo, hi); `pool` is either a fixed block
+# count or the slack factor over the referenced (unique) blocks.
+CONFIGS: Dict[str, dict] = {
+    "tiny": dict(index=0, B=4, Hq=8, Hkv=2, D=64, lens=("uniform", 1, 257), pool_fixed=128,
+                 desc="tiny: B=4, 8 q / 2 kv heads, D=64, L~U[1,257], 128-block pool"),
+    "llama3_8b": dict(index=1, B=256, Hq=32, Hkv=8, D=128, lens=("uniform", 512, 4096), pool_slack=1.1,
+                      desc="Llama-3-8B decode: B=256, 32 q / 8 kv heads, D=128, L~U[512,4096]"),
+    "long_cot": dict(index=2, B=64, Hq=32, Hkv=8, D=128, lens=("loguniform", 1024, 16384), pool_slack=1.1,
+                     k_offset_std=0.5,
+                     desc="long CoT decode: B=64, 32/8 heads, D=128, L log-uniform [1024,16384], "
+                          "per-KV-head K mean offset N(0, 0.5^2)"),
+    "llama3_70b_tp8": dict(index=3, B=512, Hq=8, Hkv=1, D=128, lens=("uniform", 1024, 8192), pool_slack=1.1,
+                           desc="Llama-3-70B TP=8 one-GPU share: B=512, 8 q / 1 kv head, D=128, L~U[1024,8192]"),
+    "shared_prefix": dict(index=4, B=256, Hq=32, Hkv=8, D=128, prompts=32, samples=8, prefix_len=1024,
+                          lens=("uniform", 256, 8192), pool_slack=1.1,
+                          desc="shared-prefix rollouts: 32 prompts x 8 samples, 1024-token shared prefix "
+                               "+ response ~U[256,8192], 32/8 heads, D=128"),
+}
+CONFIG_NAMES = sorted(CONFIGS, key=lambda n: CONFIGS[n]["index"])
+
+
+def default_seed(name: str) -> int:
+    return 2405 + CONFIGS[name]["index"]
+
+
+def _rng(seed: int, stream: int) -> np.random.Generator:
+    return np.random.Generator(np.random.Philox(np.random.SeedSequence([int(seed), int(stream)])))
+
+
+def _torch_seed(seed: int, stream: int) -> int:
+    return int(np.random.SeedSequence([int(seed), int(stream)]).generate_state(1, np.uint64)[0]) & (2**63 - 1)
+
+
+@dataclasses.dataclass
+class Structure:
+    """Host-side shape of one decode step (everything except q/K/V values)."""
+    name: str
+    seed: int
+    B: int
+    Hq: int
+    Hkv: int
+    D: int
+    num_blocks: int
+    max_blocks_per_seq: int
+    context_lens: np.ndarray   # int32 [B]
+    block_table: np.ndarray    # int32 [B][max_blocks_per_seq]; -1 where unused
+    k_offset_std: float = 0.0
+    block_size: int = BLOCK_SIZE
+
+    @property
+    def G(self) -> int:
+        return self.Hq // self.Hkv
+
+    @property
+    def scale(self) -> float:
+        return float(np.float32(1.0 / math.sqrt(self.D)))
+
+    @property
+    def max_context_len(self) -> int:
+        return int(max(int(self.context_lens.max(initial=0)), 0))
+
+    def blocks_used(self) -> np.ndarray:
+        """Number of block-table entries each sequence reads: ceil(L/16)."""
+        L = np.maximum(self.context_lens.astype(np.int64), 0)
+        return (L + self.block_size - 1) // self.block_size
+
+    def valid_slots(self) -> np.ndarray:
+        """Per physical block, the number of leading slots some sequence reads."""
+        valid = np.zeros(self.num_blocks, dtype=np.int64)
+        nb = self.blocks_used()
+        for b in range(self.B):
+            n = int(nb[b])
+            if n == 0:
+                continue
+            j = np.arange(n)
+            cnt = np.minimum(self.block_size, int(self.context_lens[b]) - self.block_size * j)
+            np.maximum.at(valid, self.block_table[b, :n].astype(np.int64), cnt)
+        return valid
+
+    @property
+    def logical_tokens(self) -> int:
+        return int(np.maximum(self.context_lens.astype(np.int64), 0).sum())
+
+    @property
+    def unique_tokens(self) -> int:
+        return int(self.valid_slots().sum())
+
+    def algorithmic_bytes(self, unique: bool = True) -> int:
+        """Bytes a decode step must move: K and V rows of the context (each
+        shared physical row once when ``unique``), q, the fp32 output, the
+        block-table entries read and the context lengths."""
+        tokens = self.unique_tokens if unique else self.logical_tokens
+        kv = tokens * self.Hkv * self.D * 2 * 2
+        q = self.B * self.Hq * self.D * 2
+        out = self.B * self.Hq * self.D * 4
+        bt = int(self.blocks_used().sum()) * 4
+        return int(kv + q + out + bt + self.B * 4)
+
+
+def _draw_lens(rng: np.random.Generator, kind: str, lo: int, hi: int, n: int) -> np.ndarray:
+    if kind == "uniform":
+        return rng.integers(lo, hi, size=n, endpoint=True).astype(np.int32)
+    if kind == "loguniform":
+        x = np.exp(rng.uniform(math.log(lo), math.log(hi), size=n))
+        return np.clip(np.rint(x), lo, hi).astype(np.int32)
+    raise ValueError(kind)
+
+
+def make_structure(name: str, seed: Optional[int] = None) -> Structure:
+    """The block table, pool size and context lengths of a named configuration."""
+    cfg = CONFIGS[name]
+    seed = default_seed(name) if seed is None else int(seed)
+    B, BS = cfg["B"], BLOCK_SIZE
+    kind, lo, hi = cfg["lens"]
+    rl = _rng(seed, _STREAM_LENS)
+    rp = _rng(seed, _STREAM_POOL)
+    if "prompts" in cfg:
+        P, S, prefix = cfg["prompts"], cfg["samples"], cfg["prefix_len"]
+        assert P * S == B and prefix % BS == 0
+        resp = _draw_lens(rl, kind, lo, hi, B)
+        lens = (prefix + resp).astype(np.int32)
+        mbs = (prefix + hi + BS - 1) // BS
+        pre_blocks = prefix // BS
+        priv = (resp.astype(np.int64) + BS - 1) // BS
+        unique = P * pre_blocks + int(priv.sum())
+        num_blocks = int(math.ceil(cfg["pool_slack"] * unique))
+        perm = rp.permutation(num_blocks).astype(np.int32)
+        table = np.full((B, mbs), -1, dtype=np.int32)
+        cur = 0
+        for p in range(P):  # each prompt's prefix blocks, shared by its S samples
+            ids = perm[cur:cur + pre_blocks]
+            cur += pre_blocks
+            table[p * S:(p + 1) * S, :pre_blocks] = ids
+        for b in range(B):  # private response blocks
+            n = int(priv[b])
+            table[b, pre_blocks:pre_blocks + n] = perm[cur:cur + n]
+            cur += n
+        assert cur == unique
+    else:
+        lens = _draw_lens(rl, kind, lo, hi, B)
+        mbs = (hi + BS - 1) // BS
+        nblk = (lens.astype(np.int64) + BS - 1) // BS
+        total = int(nblk.sum())
+        num_blocks = cfg["pool_fixed"] if "pool_fixed" in cfg else int(math.ceil(cfg["pool_slack"] * total))
+        assert num_blocks >= total
+        perm = rp.permutation(num_blocks).astype(np.int32)
+        table = np.full((B, mbs), -1, dtype=np.int32)
+        cur = 0
+        for b in range(B):
+            n = int(nblk[b])
+            table[b, :n] = perm[cur:cur + n]
+            cur += n
+    return Structure(name=name, seed=seed, B=B, Hq=cfg["Hq"], Hkv=cfg["Hkv"], D=cfg["D"],
+                     num_blocks=num_blocks, max_blocks_per_seq=int(mbs), context_lens=lens,
+                     block_table=table, k_offset_std=float(cfg.get("k_offset_std", 0.0)))
+
+
+def custom_structure(B: int, Hq: int, Hkv: int, D: int, lens: Sequence[int], seed: int = 0,
+                     pool_slack: float = 1.25, max_blocks_per_seq: Optional[int] = None,
+                     name: str = "custom") -> Structure:
+    """Independent sequences with the given context lengths, each logical block
+    mapped to a random physical block of a pool with `pool_slack` spare room."""
+    BS = BLOCK_SIZE
+    lens = np.asarray(lens, dtype=np.int32)
+    assert lens.shape == (B,)
+    nblk = (np.maximum(lens.astype(np.int64), 0) + BS - 1) // BS
+    total = int(nblk.sum())
+    mbs = int(max_blocks_per_seq or max(1, int(nblk.max(initial=1))))
+    assert mbs >= int(nblk.max(initial=0))
+    num_blocks = max(1, int(math.ceil(pool_slack * max(total, 1))))
+    perm = _rng(seed, _STREAM_POOL).permutation(num_blocks).astype(np.int32)
+    table = np.full((B, mbs), -1, dtype=np.int32)
+    cur = 0
+    for b in range(B):
+        n = int(nblk[b])
+        table[b, :n] = perm[cur:cur + n]
+        cur += n
+    return Structure(name=name, seed=seed, B=B, Hq=Hq, Hkv=Hkv, D=D, num_blocks=num_blocks,
+                     max_blocks_per_seq=mbs, context_lens=lens, block_table=table)
+
+
+def fill_values(st: Structure, device="cpu", fill: Optional[str] = "nan"):
+    """Draw q [B][Hq][D] and the K/V pools [num_blocks][Hkv][16][D] (bf16) on
+    `device`.  `fill` is 'nan', 'zero' or None: what to write into pool slots
+    no sequence reads."""
+    import torch
+
+    dev = torch.device(device)
+
+    def gen(stream):
+        g = torch.Generator(device=dev)
+        g.manual_seed(_torch_seed(st.seed, stream))
+        return g
+
+    q = torch.randn((st.B, st.Hq, st.D), generator=gen(_STREAM_Q), device=dev,
+                    dtype=torch.float32).to(torch.bfloat16)
+    mu = None
+    if st.k_offset_std:
+        mu = (torch.randn((st.Hkv, 1, st.D), generator=gen(_STREAM_KOFF), device=dev,
+                          dtype=torch.float32) * st.k_offset_std)
+    shape = (st.num_blocks, st.Hkv, st.block_size, st.D)
+    k = torch.empty(shape, dtype=torch.bfloat16, device=dev)
+    v = torch.empty(shape, dtype=torch.bfloat16, device=dev)
+    gk, gv = gen(_STREAM_K), gen(_STREAM_V)
+    for c0 in range(0, st.num_blocks, _POOL_CHUNK_BLOCKS):
+        c1 = min(st.num_blocks, c0 + _POOL_CHUNK_BLOCKS)
+        sub = (c1 - c0,) + shape[1:]
+        kf = torch.randn(sub, generator=gk, device=dev, dtype=torch.float32)
+        if mu is not None:
+            kf += mu
+        k[c0:c1] = kf.to(torch.bfloat16)
+        v[c0:c1] = torch.randn(sub, generator=gv, device=dev, dtype=torch.float32).to(torch.bfloat16)
+        del kf
+    if fill is not None:
+        apply_fill(st, k, v, fill)
+    return q, k, v
+
+
+def unread_slot_mask(st: Structure) -> np.ndarray:
+    """bool [num_blocks][16]: True for pool slots that no sequence reads."""
+    valid = st.valid_slots()
+    return np.arange(st.block_size)[None, :] >= valid[:, None]
+
+
+def apply_fill(st: Structure, k, v, fill: str = "nan"):
+    """Overwrite every unread pool slot of k and v (in place) with NaN or zero."""
+    import torch
+
+    value = {"nan": float("nan"), "zero": 0.0}[fill]
+    mask = torch.from_numpy(unread_slot_mask(st)).to(k.device)[:, None, :, None]
+    k.masked_fill_(mask, value)
+    v.masked_fill_(mask, value)
+
+
+def permute_pool(st: Structure, k, v, seed: int):
+    """Move every physical block p to pi(p) (new_pool[pi(p)] = pool[p]) and
+    rewrite the block table through pi; returns (structure, k, v)."""
+    import torch
+
+    pi = _rng(seed, 99).permutation(st.num_blocks).astype(np.int64)
+    inv = np.empty_like(pi)
+    inv[pi] = np.arange(st.num_blocks)
+    idx = torch.from_numpy(inv).to(k.device)
+    k2 = k.index_select(0, idx)
+    v2 = v.index_select(0, idx)
+    table = st.block_table.copy()
+    used = table >= 0
+    table[used] = pi[table[used]].astype(np.int32)
+    return dataclasses.replace(st, block_table=table), k2, v2
+
+
+def bf16_bits(t) -> np.ndarray:
+    """Raw uint16 bit patterns of a bf16 tensor, on the host."""
+    import torch
+
+    assert t.dtype == torch.bfloat16
+    return t.detach().contiguous().cpu().view(torch.int16).numpy().view(np.uint16)
+
+
+def sample_rows(st: Structure, n: int, seed: int = 7) -> np.ndarray:
+    """(b, h) pairs for spot checks at full size: the longest and shortest
+    sequences, every query head of one sequence, and random pairs."""
+    r = _rng(seed, 100)
+    L = st.context_lens
+    picks = [(int(np.argmax(L)), 0), (int(np.argmax(L)), st.Hq - 1),
+             (int(np.argmin(L)), 0), (int(np.argmin(L)), st.Hq - 1)]
+    b0 = int(r.integers(0, st.B))
+    picks += [(b0, h) for h in range(st.Hq)]
+    while len(picks) < n:
+        picks.append((int(r.integers(0, st.B)), int(r.integers(0, st.Hq))))
+    return np.asarray(picks[:max(n, len(picks))], dtype=np.int32)
