@@ -1,0 +1,199 @@
+"""Benchmark of one paged decode-attention step on one MI355X.
+
+A step is one pda_decode call (partition pass + merge pass) over a whole
+batch: every sequence's new query token attends over its paged KV cache.
+The default workload is the Llama-3-8B-shaped rollout step (B=256, 32 query
+/ 8 KV heads, head_dim 128, contexts uniform in [512, 4096], random block
+placement in a pool of the used blocks + 10%); inputs are synthetic and
+already resident in HBM when the timed region starts.
+
+Prints one JSON line:
+  value      algorithmic HBM bytes per step / step time, in GB/s
+             (K and V rows of every context token -- shared rows once --
+             plus q, the fp32 output, the block-table entries and lengths)
+  roofline   the partition kernel alone: the same algorithmic bytes / its
+             average launch time (HIP events on its stream), against the
+             8 TB/s HBM peak; `traffic` is the measured HBM bytes per launch
+             from rocprofv3 counters when they were taken on this kernel source
+  cpu_baseline  the fp64 oracle on the host cores, same workload
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_GBS = 8000.0  # MI355X HBM3E, datasheet
+METRIC = "decode-attention HBM GB/s (% of peak) + seq-steps/s, Llama-3-8B shape"
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = ["paper_2405_11143_amd/csrc/pda_partition.hip", "paper_2405_11143_amd/csrc/pda_internal.h"]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per partition-kernel launch from the committed counter summary,
+    or None when it is missing or was taken on another kernel source."""
+    path = os.path.join(PROFILES, f"traffic_partition_kernel_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_hash = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
+    m_bytes = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m_hash or not m_bytes or m_hash.group(1) != kernel_source_hash():
+        return None
+    return float(m_bytes.group(1))
+
+
+def cpu_baseline(st, q, k, v, min_seconds: float, max_reps: int):
+    import numpy as np
+
+    import oracle
+    import workloads as W
+
+    threads = max(1, min(16, os.cpu_count() or 1))
+    qb, kb, vb = W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v)
+    reps, t_total = 0, 0.0
+    while reps < max_reps and (reps == 0 or t_total < min_seconds):
+        t0 = time.perf_counter()
+        oracle.decode(qb, kb, vb, st.block_table, st.context_lens, st.scale, threads=threads)
+        t_total += time.perf_counter() - t0
+        reps += 1
+    per_step = t_total / reps
+    return {"value": round(st.algorithmic_bytes() / per_step / 1e9, 4), "unit": "GB/s",
+            "seq_steps_per_s": round(st.B / per_step, 3), "s_per_step": round(per_step, 4),
+            "cores": threads, "kind": "oracle",
+            "sample": f"the full {st.name} step (all {st.B} sequences x {st.Hq} heads), "
+                      f"{reps} repetition(s), {t_total:.1f} s total, fp64, {threads} threads"}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="llama3_8b")
+    ap.add_argument("--partition-tokens", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-min-seconds", type=float, default=10.0)
+    ap.add_argument("--cpu-max-reps", type=int, default=20)
+    ap.add_argument("--pass1-only", action="store_true",
+                    help="time and launch only the partition kernel (for counter runs)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a device copy of this many MiB (counter calibration) and exit")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the decode step shards by "
+              "sequence or KV head with no exchange, and this build runs on a single MI355X.",
+              file=sys.stderr)
+        return 2
+
+    import torch
+
+    import workloads as W
+    from paper_2405_11143_amd import make_problem, pda_decode, pda_partition_attention, pda_plan
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        a = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n, "copies": 3}))
+        return 0
+
+    st = W.make_structure(args.config)
+    q, k, v = W.fill_values(st, dev, fill="nan")
+    bt = torch.from_numpy(st.block_table).to(dev)
+    lens = torch.from_numpy(st.context_lens).to(dev)
+    prob = make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq,
+                        st.max_context_len, args.partition_tokens)
+    tp, nparts, ws_bytes = pda_plan(prob)
+    out = torch.empty((st.B, st.Hq, st.D), dtype=torch.float32, device=dev)
+    ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    kw = dict(max_context_len=st.max_context_len, partition_tokens=args.partition_tokens,
+              workspace=ws, stream=stream)
+
+    def step():
+        pda_decode(q, k, v, bt, lens, st.scale, out, **kw)
+
+    def pass1():
+        pda_partition_attention(q, k, v, bt, lens, st.scale, out, **kw)
+
+    fn = pass1 if args.pass1_only else step
+    for _ in range(args.warmup):
+        fn()
+    torch.cuda.synchronize()
+
+    def timed(f, n):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(n):
+            f()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n  # ms
+
+    ms_step = timed(fn, args.steps)
+    ms_pass1 = ms_step if args.pass1_only else timed(pass1, args.steps)
+
+    alg = st.algorithmic_bytes()
+    value = alg / (ms_step * 1e-3) / 1e9
+    achieved = alg / (ms_pass1 * 1e-3) / 1e9
+    traffic = measured_traffic(args.config)
+    cfg = W.CONFIGS[args.config]
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) bf16 q/K/V, random block placement)",
+        "config": {"workload": cfg["desc"], "name": args.config, "batch": st.B, "q_heads": st.Hq,
+                   "kv_heads": st.Hkv, "head_dim": st.D, "block_size": st.block_size,
+                   "pool_blocks": st.num_blocks, "context_tokens": st.logical_tokens,
+                   "unique_context_tokens": st.unique_tokens, "partition_tokens": tp,
+                   "partitions_max": nparts, "timed": "pass1 only" if args.pass1_only else "full step"},
+        "seq_steps_per_s": round(st.B / (ms_step * 1e-3), 1),
+        "pct_of_peak": round(100.0 * value / PEAK_GBS, 2),
+        "algorithmic_bytes_per_step": alg,
+        "roofline": {"bound": "hbm", "kernel": "partition_kernel", "achieved": round(achieved, 2),
+                     "peak": PEAK_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_GBS, 4),
+                     "traffic": traffic, "ms_per_launch": round(ms_pass1, 5)},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline and not args.pass1_only:
+        result["cpu_baseline"] = cpu_baseline(st, q, k, v, args.cpu_min_seconds, args.cpu_max_reps)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

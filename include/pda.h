@@ -1,0 +1,135 @@
+/*
+ * pda.h -- paged decode attention for AMD MI355X (gfx950).
+ *
+ * The operation.  The paper (OpenRLHF) puts the rollout generation phase at
+ * over 90% of RLHF/RLVR runtime (Section 1) and runs it on vLLM, whose key
+ * technique is PagedAttention: every sequence's attention key and value
+ * memory lives in fixed-size blocks of a shared pool, reached through a
+ * per-sequence block table, with blocks shareable between sequences for
+ * parallel sampling (Section 3.2, "Accelerated CoT Inference with vLLM";
+ * Appendix C, stage 1 "Rollout Generation", KV-cache management and
+ * PagedAttention).  Each autoregressive step gives every sequence one new
+ * query token that attends over its cached context.  This library computes
+ * that step for a whole batch, with grouped-query heads:
+ *
+ *   for sequence b, query head h:   g = floor(h / G),  G = Hq / Hkv
+ *     L = context_lens[b]  (clamped to [0, max_context_len]); L == 0 gives 0
+ *     token t in [0, L) lives in block block_table[b][t / 16], slot t % 16
+ *     s_t = scale * dot(q[b][h], K[block][g][slot])
+ *     out[b][h] = sum_t softmax(s)_t * V[block][g][slot]
+ *
+ * Layouts (row-major; all pointers below are DEVICE pointers):
+ *   q            bf16  [num_seqs][num_q_heads][head_dim]
+ *   k_cache      bf16  [num_blocks][num_kv_heads][block_size][head_dim]
+ *   v_cache      bf16  [num_blocks][num_kv_heads][block_size][head_dim]
+ *   block_table  int32 [num_seqs][max_blocks_per_seq]  (entries past
+ *                       ceil(L/16) are never read and may hold anything)
+ *   context_lens int32 [num_seqs]
+ *   out          fp32  [num_seqs][num_q_heads][head_dim]
+ *   workspace    opaque, pda_workspace_bytes() bytes (split-K partials)
+ * Pool slots past a sequence's context (the tail of its last block) and pool
+ * blocks no sequence references are never used, whatever they hold.
+ *
+ * Long contexts are split into partitions of `partition_tokens` tokens that
+ * are processed independently; a second pass merges the partial softmax
+ * states.  The partition size depends only on the problem descriptor, never
+ * on physical block ids, so for a given descriptor the output is bit-for-bit
+ * reproducible and independent of where blocks sit in the pool.
+ *
+ * Ownership and errors.  The caller owns every buffer; the library allocates
+ * nothing and keeps no mutable global state, so concurrent calls are safe.
+ * Every entry point validates its scalar arguments and pointers on the host
+ * and returns a pda_status without touching the GPU when they are invalid.
+ * Work is enqueued asynchronously on `stream` (NULL = the null stream); a
+ * failed launch returns PDA_ERR_HIP.  Device-resident contents are the
+ * caller's contract (block ids in [0, num_blocks), lengths at most
+ * max_context_len); the kernels clamp lengths to [0, max_context_len] and
+ * never read outside the pool: a (b, kv head) whose block table holds an
+ * out-of-range id gets NaN output rows.  pda_validate_host() checks host
+ * copies of the contents.
+ */
+#ifndef PDA_H
+#define PDA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum pda_status {
+  PDA_OK = 0,
+  PDA_ERR_NULL = 1,        /* a required pointer is NULL */
+  PDA_ERR_SHAPE = 2,       /* a size is negative, zero where it must not be, or inconsistent */
+  PDA_ERR_UNSUPPORTED = 3, /* valid but not built: head_dim not 64/128, block_size not 16, G > 16 */
+  PDA_ERR_WORKSPACE = 4,   /* workspace NULL or smaller than pda_workspace_bytes() */
+  PDA_ERR_ALIGNMENT = 5,   /* q, k_cache, v_cache or workspace not 16-byte aligned; out not 4-byte */
+  PDA_ERR_VALUE = 6,       /* non-finite scale, or a host-side content check failed */
+  PDA_ERR_HIP = 7          /* a HIP launch failed (hipGetLastError) */
+};
+
+/* Sizes of one decode step.  All fields are plain host integers. */
+typedef struct pda_problem {
+  int32_t num_seqs;           /* B >= 0 */
+  int32_t num_q_heads;        /* Hq >= 1 */
+  int32_t num_kv_heads;       /* Hkv >= 1, divides Hq; G = Hq / Hkv must be <= 16 */
+  int32_t head_dim;           /* D: 64 or 128 */
+  int32_t block_size;         /* tokens per KV block: must be 16 */
+  int32_t num_blocks;         /* rows of k_cache / v_cache, >= 1 */
+  int32_t max_blocks_per_seq; /* row stride of block_table, >= 1 */
+  int32_t max_context_len;    /* host-known bound on context_lens[]; 0 <= it <= 16*max_blocks_per_seq */
+  int32_t partition_tokens;   /* split-K partition size: 0 lets the library choose, otherwise a
+                                 positive multiple of 16 */
+} pda_problem;
+
+/* The plan for `prob`: the partition size in tokens, the number of
+ * partitions of the longest context, and the workspace size in bytes (0 when
+ * no context needs more than one partition).  Any output pointer may be NULL.
+ * Returns PDA_OK or the validation error of the descriptor. */
+int pda_plan(const pda_problem *prob, int32_t *partition_tokens, int32_t *num_partitions,
+             size_t *workspace_bytes);
+
+/* Workspace bytes pda_decode needs for `prob` (0 when none). */
+int pda_workspace_bytes(const pda_problem *prob, size_t *bytes);
+
+/* One decode-attention step for the whole batch: pda_partition_attention
+ * followed by pda_merge_partitions on the same stream.  `scale` is the
+ * softmax scale (usually 1/sqrt(head_dim)); it must be finite.  `workspace`
+ * may be NULL when pda_workspace_bytes() is 0. */
+int pda_decode(const pda_problem *prob, const void *q, const void *k_cache, const void *v_cache,
+               const int32_t *block_table, const int32_t *context_lens, float scale, float *out,
+               void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Pass 1 alone: attention of each (sequence, KV head, partition).  Rows of
+ * sequences that fit one partition are final in `out` after this pass; the
+ * others are left as partial softmax states in `workspace`. */
+int pda_partition_attention(const pda_problem *prob, const void *q, const void *k_cache,
+                            const void *v_cache, const int32_t *block_table,
+                            const int32_t *context_lens, float scale, float *out,
+                            void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Pass 2 alone: merge the partial states that pass 1 left in `workspace` into
+ * `out` for every sequence with more than one partition, in ascending
+ * partition order.  Must follow pass 1 for the same descriptor and lengths. */
+int pda_merge_partitions(const pda_problem *prob, const int32_t *context_lens, float *out,
+                         const void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Host-side check of device contents, on HOST copies: every context length
+ * is at most max_context_len and every block id a sequence reads is in
+ * [0, num_blocks).  Returns PDA_OK or PDA_ERR_VALUE; on error *first_bad (if
+ * not NULL) receives the flat index of the first offending entry, in
+ * context_lens for a length and in block_table for a block id. */
+int pda_validate_host(const pda_problem *prob, const int32_t *block_table,
+                      const int32_t *context_lens, int64_t *first_bad);
+
+/* A static, human-readable name for a pda_status value. */
+const char *pda_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PDA_H */

@@ -1,0 +1,358 @@
+// Pass 1 of paged decode attention on gfx950: one workgroup per
+// (partition of a context, sequence, KV head).
+//
+// What is computed: single-query attention over a paged KV cache with
+// grouped-query heads -- the rollout decode step the paper runs through
+// vLLM's PagedAttention (Section 3.2; Appendix C, rollout generation).  Each
+// workgroup handles the G query heads that share one KV head over a range of
+// `partition_tokens` logical tokens of one sequence, and leaves either the
+// final output rows (context fits one partition) or a partial softmax state
+// (max, denominator, unnormalised output) for the merge pass.
+//
+// Mapping onto CDNA4 (64-wide wavefronts, MFMA, LDS):
+//  * The partition's 16-token blocks are split into 4 contiguous runs, one per
+//    wavefront; each wavefront keeps its own online-softmax state and
+//    prefetches the next block's K and V tiles (2 x 16 x D bf16) into
+//    registers while it computes on the current one.
+//  * Scores S[G][16] = Q_g K^T are one small dense contraction per block:
+//    D/32 MFMA f32_16x16x32_bf16 with the G query heads (repeated to fill 16
+//    rows) as the A operand and the K tile as the B operand.  A lane's B
+//    fragment is 8 consecutive d of one token row, so K goes from HBM straight
+//    into MFMA registers.  The reduction index d is assigned to (k-group,
+//    k-step) pairs so that each lane reads D/4 contiguous elements of its row;
+//    A uses the same assignment, so the contraction is unchanged.
+//  * The online softmax runs on the MFMA output layout: a lane holds the
+//    scores of 4 head rows for one token; the block max of a row is a 16-lane
+//    all-reduce made of four DPP moves (quad swaps, half-row and row mirror).
+//    Each lane accumulates the denominator of its own token column; columns
+//    are summed once, at the end.
+//  * P V runs on the VALU in fp32: lane (phase, chunk) owns 8 consecutive d
+//    for all G heads and the tokens of its phase, so each V load instruction
+//    reads 1 KiB of contiguous tile.  The probabilities and rescale factors
+//    of a block travel from the MFMA layout to this layout through LDS
+//    (double-buffered per wavefront; only a wavefront barrier is needed).
+//  * Tokens past the context in the last block are removed by selection, not
+//    by multiplying with zero, so whatever those slots hold (NaN included)
+//    never reaches the result.
+//  * The 4 wavefront states are merged through LDS in a fixed order.  Nothing
+//    depends on physical block ids or on timing, so results are bit-for-bit
+//    reproducible and independent of block placement.
+#include "pda_internal.h"
+
+namespace pda {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float floatx4_t __attribute__((ext_vector_type(4)));
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+
+// All-reduce over each row of 16 lanes; every lane of the row gets the same bits.
+__device__ __forceinline__ float row16_max(float x) {
+  x = fmaxf(x, dpp_move<0xB1>(x));   // quad_perm(1,0,3,2)
+  x = fmaxf(x, dpp_move<0x4E>(x));   // quad_perm(2,3,0,1)
+  x = fmaxf(x, dpp_move<0x141>(x));  // row_half_mirror
+  x = fmaxf(x, dpp_move<0x140>(x));  // row_mirror
+  return x;
+}
+__device__ __forceinline__ float row16_sum(float x) {
+  x += dpp_move<0xB1>(x);
+  x += dpp_move<0x4E>(x);
+  x += dpp_move<0x141>(x);
+  x += dpp_move<0x140>(x);
+  return x;
+}
+
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Widen 8 packed bf16 (a 16-byte load) to fp32: bf16 is the top half of fp32.
+__device__ __forceinline__ void unpack8(const uint4 u, float (&f)[8]) {
+  f[0] = __uint_as_float(u.x << 16);
+  f[1] = __uint_as_float(u.x & 0xffff0000u);
+  f[2] = __uint_as_float(u.y << 16);
+  f[3] = __uint_as_float(u.y & 0xffff0000u);
+  f[4] = __uint_as_float(u.z << 16);
+  f[5] = __uint_as_float(u.z & 0xffff0000u);
+  f[6] = __uint_as_float(u.w << 16);
+  f[7] = __uint_as_float(u.w & 0xffff0000u);
+}
+
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+template <int G, int D>
+__global__ void __launch_bounds__(kWaves * kWaveSize)
+partition_kernel(const StepArgs a) {
+  static_assert(G >= 1 && G <= kMaxGroup, "query heads per KV head");
+  static_assert(D == 64 || D == 128, "head_dim");
+  constexpr int NC = D / 32;                 // MFMA k-steps per block
+  constexpr int KQ = D / 4;                  // d elements per MFMA k-group
+  constexpr int CPR = D / 8;                 // 16-byte chunks per K/V row
+  constexpr int NPH = kWaveSize / CPR;       // token phases of the P.V layout
+  constexpr int TPL = kBlockTokens / NPH;    // tokens per lane per block in P.V
+  constexpr int GP = (G + 3) & ~3;           // head count padded to float4
+  constexpr float kNegInf = -__builtin_huge_valf();
+
+  __shared__ __align__(16) float s_p[kWaves][2][kBlockTokens][GP];
+  __shared__ __align__(16) float s_alpha[kWaves][2][GP];
+  __shared__ __align__(16) float s_o[kWaves][G][D];
+  __shared__ float s_m[kWaves][GP];
+  __shared__ float s_l[kWaves][GP];
+  __shared__ int s_bad[kWaves];
+
+  const int Hkv = a.num_kv_heads;
+  const int Hq = a.num_q_heads;
+  const int item = blockIdx.x;
+  const int g = item % Hkv;
+  const int b = (item / Hkv) % a.num_seqs;
+  const int p = item / (Hkv * a.num_seqs);
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWaveSize - 1);
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int head0 = g * G;
+
+  int L = a.lens[b];
+  L = L < 0 ? 0 : (L > a.max_context_len ? a.max_context_len : L);
+  if (L == 0) {
+    if (p == 0) {
+      float* o = a.out + ((size_t)b * Hq + head0) * D;
+      for (int i = tid; i < G * D; i += kWaves * kWaveSize) o[i] = 0.f;
+    }
+    return;
+  }
+  const int Tp = a.partition_tokens;
+  const int nparts = (L + Tp - 1) / Tp;
+  if (p >= nparts) return;
+  const int t_end = min(L, (p + 1) * Tp);
+  const int j_begin = (p * Tp) / kBlockTokens;
+  const int j_end = (t_end + kBlockTokens - 1) / kBlockTokens;
+  const int per_wave = (j_end - j_begin + kWaves - 1) / kWaves;
+  const int wj0 = min(j_end, j_begin + w * per_wave);
+  const int wj1 = min(j_end, wj0 + per_wave);
+
+  // MFMA fragment coordinates: n = row of A (head) / column of B (token), kg = k-group.
+  const int n = lane & 15;
+  const int kg = lane >> 4;
+  // P.V coordinates: this lane owns d in [8*dc, 8*dc+8) for tokens tp, tp+NPH, ...
+  const int dc = lane % CPR;
+  const int tp = lane / CPR;
+
+  // A operand: query head (n mod G) of this KV head; reduction index d = kg*KQ + 8*c + e.
+  bf16x8_t qa[NC];
+  {
+    const uint16_t* qrow = a.q + ((size_t)b * Hq + head0 + (n % G)) * D + kg * KQ;
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+      qa[c] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(qrow + 8 * c));
+  }
+
+  const size_t block_stride = (size_t)Hkv * kBlockTokens * D;  // elements per pool block
+  const uint16_t* kbase = a.k + (size_t)g * kBlockTokens * D + n * D + kg * KQ;
+  const uint16_t* vbase = a.v + (size_t)g * kBlockTokens * D + tp * D + dc * 8;
+  const int32_t* trow = a.table + (size_t)b * a.max_blocks_per_seq;
+  bool bad = false;
+
+  auto load_tiles = [&](uint4 (&kr)[NC], uint4 (&vr)[TPL], int j) {
+    int phys = trow[j];
+    if ((unsigned)phys >= (unsigned)a.num_blocks) {  // contract violation: never read outside the pool
+      bad = true;
+      phys = 0;
+    }
+    const size_t off = (size_t)phys * block_stride;
+    const uint16_t* kt = kbase + off;
+    const uint16_t* vt = vbase + off;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) kr[c] = *reinterpret_cast<const uint4*>(kt + 8 * c);
+#pragma unroll
+    for (int i = 0; i < TPL; ++i) vr[i] = *reinterpret_cast<const uint4*>(vt + i * NPH * D);
+  };
+
+  float o[G][8];
+#pragma unroll
+  for (int h = 0; h < G; ++h)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[h][e] = 0.f;
+  float m_run[4], l_run[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    m_run[i] = kNegInf;
+    l_run[i] = 0.f;
+  }
+
+  auto process = [&](const uint4 (&kr)[NC], const uint4 (&vr)[TPL], int j, int par) {
+    // ---- scores: S = Q_g K^T on MFMA; lane holds rows 4*kg+i, column n ----
+    floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[c], __builtin_bit_cast(bf16x8_t, kr[c]), acc, 0, 0, 0);
+    const bool tail = (j + 1) * kBlockTokens > L;  // wave-uniform
+    const int tok0 = j * kBlockTokens;
+    float pr[4], al[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float s = acc[i] * a.scale_log2;
+      if (tail && tok0 + n >= L) s = kNegInf;
+      const float mn = fmaxf(m_run[i], row16_max(s));  // finite: the block has a valid token
+      al[i] = exp2_fast(m_run[i] - mn);
+      pr[i] = exp2_fast(s - mn);
+      l_run[i] = fmaf(l_run[i], al[i], pr[i]);
+      m_run[i] = mn;
+    }
+    if (4 * kg < G) {
+      *reinterpret_cast<float4*>(&s_p[w][par][n][4 * kg]) = make_float4(pr[0], pr[1], pr[2], pr[3]);
+      if (n == 0) *reinterpret_cast<float4*>(&s_alpha[w][par][4 * kg]) = make_float4(al[0], al[1], al[2], al[3]);
+    }
+    wave_lds_sync();
+
+    // ---- O = alpha * O + P V on the VALU ----
+    float alpha[GP];
+#pragma unroll
+    for (int h4 = 0; h4 < GP; h4 += 4) {
+      const float4 t = *reinterpret_cast<const float4*>(&s_alpha[w][par][h4]);
+      alpha[h4] = t.x; alpha[h4 + 1] = t.y; alpha[h4 + 2] = t.z; alpha[h4 + 3] = t.w;
+    }
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[h][e] *= alpha[h];
+#pragma unroll
+    for (int i = 0; i < TPL; ++i) {
+      const int row = i * NPH + tp;
+      float f[8];
+      unpack8(vr[i], f);
+      if (tail && tok0 + row >= L) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[e] = 0.f;
+      }
+      float ph[GP];
+#pragma unroll
+      for (int h4 = 0; h4 < GP; h4 += 4) {
+        const float4 t = *reinterpret_cast<const float4*>(&s_p[w][par][row][h4]);
+        ph[h4] = t.x; ph[h4 + 1] = t.y; ph[h4 + 2] = t.z; ph[h4 + 3] = t.w;
+      }
+#pragma unroll
+      for (int h = 0; h < G; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[h][e] = fmaf(ph[h], f[e], o[h][e]);
+    }
+  };
+
+  {
+    uint4 k0[NC], v0[TPL], k1[NC], v1[TPL];
+    int j = wj0;
+    if (j < wj1) load_tiles(k0, v0, j);
+    for (; j < wj1; j += 2) {
+      if (j + 1 < wj1) load_tiles(k1, v1, j + 1);
+      process(k0, v0, j, 0);
+      if (j + 1 >= wj1) break;
+      if (j + 2 < wj1) load_tiles(k0, v0, j + 2);
+      process(k1, v1, j + 1, 1);
+    }
+  }
+
+  // ---- wavefront state: sum denominators over token columns, O over phases ----
+#pragma unroll
+  for (int i = 0; i < 4; ++i) l_run[i] = row16_sum(l_run[i]);
+#pragma unroll
+  for (int h = 0; h < G; ++h)
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+#pragma unroll
+      for (int x = CPR; x < kWaveSize; x <<= 1) o[h][e] += __shfl_xor(o[h][e], x);
+
+  if (lane < CPR) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      *reinterpret_cast<float4*>(&s_o[w][h][8 * lane]) = make_float4(o[h][0], o[h][1], o[h][2], o[h][3]);
+      *reinterpret_cast<float4*>(&s_o[w][h][8 * lane + 4]) = make_float4(o[h][4], o[h][5], o[h][6], o[h][7]);
+    }
+  }
+  if (n == 0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 4 * kg + i;
+      if (r < G) {
+        s_m[w][r] = m_run[i];
+        s_l[w][r] = l_run[i];
+      }
+    }
+  }
+  if (lane == 0) s_bad[w] = bad ? 1 : 0;
+  __syncthreads();
+
+  // ---- merge the 4 wavefront states in a fixed order ----
+  const bool any_bad = (s_bad[0] | s_bad[1] | s_bad[2] | s_bad[3]) != 0;
+  const bool single = nparts == 1;
+  for (int idx = tid; idx < G * D; idx += kWaves * kWaveSize) {
+    const int h = idx / D;
+    const int d = idx % D;
+    float M = kNegInf;
+#pragma unroll
+    for (int x = 0; x < kWaves; ++x) M = fmaxf(M, s_m[x][h]);
+    float acc = 0.f, lsum = 0.f;
+#pragma unroll
+    for (int x = 0; x < kWaves; ++x) {
+      const float sc = exp2_fast(s_m[x][h] - M);  // 0 for a wavefront without tokens
+      acc = fmaf(sc, s_o[x][h][d], acc);
+      lsum = fmaf(sc, s_l[x][h], lsum);
+    }
+    if (any_bad) acc = __builtin_nanf("");
+    const size_t row = (size_t)b * Hq + head0 + h;
+    if (single) {
+      a.out[row * D + d] = acc / lsum;
+    } else {
+      const size_t slot = row * a.num_partitions + p;
+      a.part_o[slot * D + d] = acc;
+      if (d == 0) {
+        a.part_m[slot] = M;
+        a.part_l[slot] = lsum;
+      }
+    }
+  }
+}
+
+template <int G, int D>
+hipError_t launch_gd(const StepArgs& a, hipStream_t stream) {
+  const unsigned grid = (unsigned)a.num_partitions * (unsigned)a.num_seqs * (unsigned)a.num_kv_heads;
+  hipLaunchKernelGGL((partition_kernel<G, D>), dim3(grid), dim3(kWaves * kWaveSize), 0, stream, a);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_d(const StepArgs& a, int group, hipStream_t stream) {
+  switch (group) {
+    case 1: return launch_gd<1, D>(a, stream);
+    case 2: return launch_gd<2, D>(a, stream);
+    case 3: return launch_gd<3, D>(a, stream);
+    case 4: return launch_gd<4, D>(a, stream);
+    case 5: return launch_gd<5, D>(a, stream);
+    case 6: return launch_gd<6, D>(a, stream);
+    case 7: return launch_gd<7, D>(a, stream);
+    case 8: return launch_gd<8, D>(a, stream);
+    case 9: return launch_gd<9, D>(a, stream);
+    case 10: return launch_gd<10, D>(a, stream);
+    case 11: return launch_gd<11, D>(a, stream);
+    case 12: return launch_gd<12, D>(a, stream);
+    case 13: return launch_gd<13, D>(a, stream);
+    case 14: return launch_gd<14, D>(a, stream);
+    case 15: return launch_gd<15, D>(a, stream);
+    case 16: return launch_gd<16, D>(a, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_partition(const StepArgs& a, int group, int head_dim, hipStream_t stream) {
+  if (head_dim == 64) return launch_d<64>(a, group, stream);
+  if (head_dim == 128) return launch_d<128>(a, group, stream);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace pda

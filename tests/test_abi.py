@@ -1,0 +1,148 @@
+"""The C ABI on the host (no GPU): the library loads, exports every symbol the
+header declares, and rejects bad arguments before touching the GPU.
+
+Every call here that passes pointers is built to fail host validation, so no
+kernel is ever launched from these tests."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import paper_2405_11143_amd as pda
+import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pda.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pda_\w+)\s*\(", text)))
+
+
+def test_header_declarations_match_binding():
+    assert declared_functions() == sorted(pda.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = pda.load_library()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    nm = subprocess.run(["nm", "-D", "--defined-only", pda.LIB_PATH], capture_output=True, text=True,
+                        check=True).stdout
+    exported = set(re.findall(r"\bT (pda_\w+)", nm))
+    assert set(declared_functions()) <= exported
+
+
+def prob(**kw):
+    base = dict(num_seqs=4, num_q_heads=8, num_kv_heads=2, head_dim=64, num_blocks=128,
+                max_blocks_per_seq=17, max_context_len=257, partition_tokens=0)
+    base.update(kw)
+    return pda.make_problem(**base)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(num_seqs=-1), pda.pda.PDA_ERR_SHAPE),
+    (dict(num_q_heads=0), pda.pda.PDA_ERR_SHAPE),
+    (dict(num_q_heads=6, num_kv_heads=4), pda.pda.PDA_ERR_SHAPE),
+    (dict(num_blocks=0), pda.pda.PDA_ERR_SHAPE),
+    (dict(max_context_len=17 * 16 + 1), pda.pda.PDA_ERR_SHAPE),
+    (dict(max_context_len=-1), pda.pda.PDA_ERR_SHAPE),
+    (dict(partition_tokens=24), pda.pda.PDA_ERR_SHAPE),
+    (dict(partition_tokens=-16), pda.pda.PDA_ERR_SHAPE),
+    (dict(head_dim=96), pda.pda.PDA_ERR_UNSUPPORTED),
+    (dict(block_size=32), pda.pda.PDA_ERR_UNSUPPORTED),
+    (dict(num_q_heads=34, num_kv_heads=2), pda.pda.PDA_ERR_UNSUPPORTED),
+])
+def test_plan_rejects(kw, status):
+    with pytest.raises(pda.PdaError) as e:
+        pda.pda_plan(prob(**kw))
+    assert e.value.status == status
+
+
+def test_plan_values():
+    # contexts up to 512 tokens: one partition, no workspace
+    assert pda.pda_plan(prob()) == (272, 1, 0)
+    assert pda.pda_plan(prob(max_context_len=0)) == (16, 1, 0)
+    # longer: 512-token partitions, fp32 partials (D values + max + denominator)
+    tp, n, ws = pda.pda_plan(prob(num_seqs=256, num_q_heads=32, num_kv_heads=8, head_dim=128,
+                                  max_blocks_per_seq=256, max_context_len=4096))
+    assert (tp, n) == (512, 8) and ws == 256 * 32 * 8 * (128 + 2) * 4
+    # forced partition size
+    assert pda.pda_plan(prob(partition_tokens=64)) == (64, 5, 4 * 8 * 5 * 66 * 4)
+
+
+def call(fn, p, q=0x1000, k=0x1000, v=0x1000, bt=0x1000, lens=0x1000, scale=0.125, out=0x1000,
+         ws=None, ws_bytes=0):
+    lib = pda.load_library()
+    return getattr(lib, fn)(ctypes.byref(p), q, k, v, bt, lens, ctypes.c_float(scale), out, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("fn", ["pda_decode", "pda_partition_attention"])
+def test_step_validation(fn):
+    lib = pda.load_library()
+    assert call(fn, prob(), q=None) == pda.pda.PDA_ERR_NULL
+    assert call(fn, prob(), lens=None) == pda.pda.PDA_ERR_NULL
+    assert call(fn, prob(), out=None) == pda.pda.PDA_ERR_NULL
+    assert call(fn, prob(), scale=float("nan")) == pda.pda.PDA_ERR_VALUE
+    assert call(fn, prob(), scale=float("inf")) == pda.pda.PDA_ERR_VALUE
+    assert call(fn, prob(), q=0x1008) == pda.pda.PDA_ERR_ALIGNMENT
+    assert call(fn, prob(), k=0x1004) == pda.pda.PDA_ERR_ALIGNMENT
+    assert call(fn, prob(), out=0x1002) == pda.pda.PDA_ERR_ALIGNMENT
+    split = prob(partition_tokens=64)
+    assert call(fn, split) == pda.pda.PDA_ERR_WORKSPACE
+    assert call(fn, split, ws=0x1000, ws_bytes=100) == pda.pda.PDA_ERR_WORKSPACE
+    need = pda.pda_workspace_bytes(split)
+    assert call(fn, split, ws=0x1008, ws_bytes=need) == pda.pda.PDA_ERR_ALIGNMENT
+    assert call(fn, prob(head_dim=80)) == pda.pda.PDA_ERR_UNSUPPORTED
+    assert getattr(lib, fn)(None, None, None, None, None, None, ctypes.c_float(1), None, None, 0,
+                            None) == pda.pda.PDA_ERR_NULL
+    # an empty batch is valid and launches nothing, even with NULL pointers
+    assert call(fn, prob(num_seqs=0), q=None, k=None, v=None, bt=None, lens=None, out=None) == pda.pda.PDA_OK
+
+
+def test_merge_validation():
+    lib = pda.load_library()
+    split = prob(partition_tokens=64)
+    need = pda.pda_workspace_bytes(split)
+    f = lib.pda_merge_partitions
+    assert f(ctypes.byref(split), None, 0x1000, 0x1000, need, None) == pda.pda.PDA_ERR_NULL
+    assert f(ctypes.byref(split), 0x1000, 0x1000, 0x1000, need - 1, None) == pda.pda.PDA_ERR_WORKSPACE
+    assert f(ctypes.byref(split), 0x1000, 0x1000, 0x1004, need, None) == pda.pda.PDA_ERR_ALIGNMENT
+    # nothing split: nothing to merge, no launch
+    assert f(ctypes.byref(prob()), None, None, None, 0, None) == pda.pda.PDA_OK
+
+
+def test_validate_host():
+    st = W.make_structure("tiny")
+    p = prob(num_blocks=st.num_blocks, max_blocks_per_seq=st.max_blocks_per_seq,
+             max_context_len=st.max_context_len)
+    assert pda.pda_validate_host(p, st.block_table, st.context_lens)[0] == pda.pda.PDA_OK
+    bt = st.block_table.copy()
+    b = int(np.argmax(st.context_lens))
+    bt[b, 3] = st.num_blocks
+    rc, bad = pda.pda_validate_host(p, bt, st.context_lens)
+    assert rc == pda.pda.PDA_ERR_VALUE and bad == b * st.max_blocks_per_seq + 3
+    lens = st.context_lens.copy()
+    lens[2] = st.max_context_len + 1
+    rc, bad = pda.pda_validate_host(p, st.block_table, lens)
+    assert rc == pda.pda.PDA_ERR_VALUE and bad == 2
+    # entries past ceil(L/16) are never read and may hold anything
+    bt = st.block_table.copy()
+    bt[bt < 0] = 999999
+    assert pda.pda_validate_host(p, bt, st.context_lens)[0] == pda.pda.PDA_OK
+
+
+def test_status_strings():
+    for s in range(8):
+        assert pda.pda_status_string(s).startswith("PDA_")
+    assert "unknown" in pda.pda_status_string(99)
+
+
+def test_binding_has_no_fallback(tmp_path):
+    with pytest.raises(RuntimeError, match="no fallback"):
+        pda.load_library(str(tmp_path / "missing.so"))

@@ -1,0 +1,172 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Bar (floating point): over every compared element, max-abs error <= 8e-3 and
+mean-abs error <= 1e-3 against the oracle's fp64 result.  Bitwise where the
+method fixes the bits: a one-token context returns its V row exactly, moving
+physical blocks around the pool or filling unread slots with NaN leaves the
+output bit-identical, and two runs give identical bits.
+
+Small problems are compared on every element; the five named decode
+configurations run at full size in the launch configuration the benchmark
+times, and are compared on sampled (sequence, head) rows that the oracle
+computes one by one.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from paper_2405_11143_amd import pda_decode, pda_plan, make_problem
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS, MEAN_ABS = 8e-3, 1e-3
+THREADS = max(1, min(16, os.cpu_count() or 1))
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return torch.device("cuda:0")
+
+
+def gpu_tensors(st, dev):
+    return (torch.from_numpy(st.block_table).to(dev), torch.from_numpy(st.context_lens).to(dev))
+
+
+def run(st, q, k, v, dev, partition_tokens=0, max_context_len=None):
+    bt, lens = gpu_tensors(st, dev)
+    mcl = st.max_context_len if max_context_len is None else max_context_len
+    out = pda_decode(q, k, v, bt, lens, st.scale, max_context_len=mcl, partition_tokens=partition_tokens)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def reference(st, q, k, v):
+    return oracle.decode(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
+                         st.context_lens, st.scale, threads=THREADS)
+
+
+def check(got, ref, what):
+    got = got.astype(np.float64)
+    assert np.isfinite(got).all(), f"{what}: non-finite output"
+    err = np.abs(got - ref)
+    print(f"{what}: max-abs {err.max():.3e} mean-abs {err.mean():.3e} over {err.size} elements", flush=True)
+    assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS, what
+
+
+# ------------------------------------------------------------ small, full --
+
+@pytest.mark.parametrize("partition_tokens", [0, 16, 64, 128])
+def test_tiny_config(dev, partition_tokens):
+    st = W.make_structure("tiny")
+    q, k, v = W.fill_values(st, dev, fill="nan")
+    check(run(st, q, k, v, dev, partition_tokens), reference(st, q, k, v), f"tiny Tp={partition_tokens}")
+
+
+EDGE_LENS = [1, 15, 16, 17, 31, 32, 33, 63, 64, 65, 127, 511, 512, 513, 1000, 2049]
+SHAPES = [(8, 2, 64), (32, 8, 128), (8, 1, 128), (4, 4, 128), (12, 2, 128), (28, 4, 128),
+          (40, 8, 128), (16, 1, 64), (6, 2, 64), (3, 1, 128)]
+
+
+@pytest.mark.parametrize("Hq,Hkv,D", SHAPES, ids=lambda x: str(x))
+@pytest.mark.parametrize("partition_tokens", [0, 64])
+def test_shapes_and_edge_lengths(dev, Hq, Hkv, D, partition_tokens):
+    """Every group size kind (G = 1, 3, 4, 5, 6, 7, 8, 16), both head dims, and
+    context lengths at block and partition boundaries."""
+    st = W.custom_structure(len(EDGE_LENS), Hq, Hkv, D, EDGE_LENS, seed=Hq * 100 + D)
+    q, k, v = W.fill_values(st, dev, fill="nan")
+    check(run(st, q, k, v, dev, partition_tokens), reference(st, q, k, v),
+          f"Hq={Hq} Hkv={Hkv} D={D} Tp={partition_tokens}")
+
+
+@pytest.mark.parametrize("partition_tokens", [16, 48, 256, 512, 4096])
+def test_split_sizes_agree(dev, partition_tokens):
+    lens = [3000, 1, 700, 4096, 513, 2222, 17, 1024]
+    st = W.custom_structure(len(lens), 32, 8, 128, lens, seed=5)
+    q, k, v = W.fill_values(st, dev, fill="nan")
+    check(run(st, q, k, v, dev, partition_tokens), reference(st, q, k, v), f"split Tp={partition_tokens}")
+
+
+# ------------------------------------------------------------ invariants --
+
+def test_length_one_returns_v_exactly(dev):
+    for (Hq, Hkv, D, tp) in [(32, 8, 128, 0), (8, 2, 64, 16), (16, 1, 128, 0)]:
+        st = W.custom_structure(40, Hq, Hkv, D, [1] * 40, seed=3)
+        q, k, v = W.fill_values(st, dev, fill="nan")
+        got = run(st, q, k, v, dev, tp)
+        vf = v.float().cpu().numpy()
+        G = Hq // Hkv
+        for b in range(st.B):
+            p = st.block_table[b, 0]
+            for h in range(Hq):
+                assert np.array_equal(got[b, h], vf[p, h // G, 0]), (Hq, Hkv, D, b, h)
+
+
+def test_constant_v_gives_constant(dev):
+    lens = [1, 16, 17, 300, 2000, 5000]
+    st = W.custom_structure(len(lens), 32, 8, 128, lens, seed=4)
+    q, k, v = W.fill_values(st, dev, fill="nan")
+    mask = torch.from_numpy(W.unread_slot_mask(st)).to(dev)[:, None, :, None]
+    v = torch.ones_like(v).masked_fill_(mask, float("nan"))
+    for tp in (0, 64):
+        got = run(st, q, k, v, dev, tp)
+        assert np.abs(got - 1.0).max() <= 1e-6
+
+
+def test_gqa_mapping(dev):
+    for (Hq, Hkv) in [(32, 8), (8, 1), (12, 4), (10, 2)]:
+        st = W.custom_structure(3, Hq, Hkv, 128, [50, 700, 1], seed=6)
+        q, k, _ = W.fill_values(st, dev, fill=None)
+        v = (torch.arange(Hkv, device=dev, dtype=torch.float32) + 1).view(1, Hkv, 1, 1)
+        v = v.expand(st.num_blocks, Hkv, 16, 128).contiguous().to(torch.bfloat16)
+        got = run(st, q, k, v, dev, 64)
+        G = Hq // Hkv
+        for h in range(Hq):
+            assert np.abs(got[:, h] - (h // G + 1)).max() <= 1e-5, (Hq, Hkv, h)
+
+
+def test_block_shuffle_and_poison_bit_identical(dev):
+    lens = [33, 1, 900, 2047, 64, 129]
+    st = W.custom_structure(len(lens), 32, 8, 128, lens, seed=7)
+    for tp in (0, 64):
+        q, k, v = W.fill_values(st, dev, fill="nan")
+        base = run(st, q, k, v, dev, tp)
+        assert np.array_equal(base, run(st, q, k, v, dev, tp)), "run-to-run"
+        st2, k2, v2 = W.permute_pool(st, k, v, seed=11)
+        assert np.array_equal(base, run(st2, q, k2, v2, dev, tp)), "block shuffle"
+        qz, kz, vz = W.fill_values(st, dev, fill="zero")
+        assert np.array_equal(base, run(st, qz, kz, vz, dev, tp)), "NaN poison vs zero fill"
+
+
+def test_empty_and_nonpositive_lengths(dev):
+    st = W.custom_structure(4, 8, 2, 64, [0, 20, -5, 1], seed=8)
+    q, k, v = W.fill_values(st, dev, fill="nan")
+    got = run(st, q, k, v, dev, 0)
+    assert np.all(got[0] == 0) and np.all(got[2] == 0)
+    check(got, reference(st, q, k, v), "lengths 0, 20, -5, 1")
+    # an empty batch launches nothing
+    e = torch.empty((0, 8, 64), dtype=torch.bfloat16, device=dev)
+    out = pda_decode(e, k, v, torch.empty((0, 2), dtype=torch.int32, device=dev),
+                     torch.empty((0,), dtype=torch.int32, device=dev), 0.125, max_context_len=0)
+    assert out.shape == (0, 8, 64)
+
+
+# ------------------------------------------------- full-size configurations --
+
+@pytest.mark.parametrize("name", ["llama3_8b", "long_cot", "llama3_70b_tp8", "shared_prefix"])
+def test_full_config_sampled(dev, name):
+    st = W.make_structure(name)
+    print(f"{name}: B={st.B} pool={st.num_blocks} blocks, plan={pda_plan(make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq, st.max_context_len))}", flush=True)
+    q, k, v = W.fill_values(st, dev, fill="nan")
+    got = run(st, q, k, v, dev)
+    assert np.isfinite(got).all()
+    vmax = float(torch.nan_to_num(v.float().abs(), nan=0.0).max())
+    assert np.abs(got).max() <= vmax  # each output is a convex combination of V rows
+    rows = W.sample_rows(st, 64)
+    ref = oracle.decode_rows(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
+                             st.context_lens, st.scale, rows, threads=THREADS)
+    check(got[rows[:, 0], rows[:, 1]], ref, f"{name} sampled rows")
