@@ -158,8 +158,15 @@ partition_kernel(const StepArgs a) {
   const int32_t* trow = a.table + (size_t)b * a.max_blocks_per_seq;
   bool bad = false;
 
-  auto load_tiles = [&](uint4 (&kr)[NC], uint4 (&vr)[TPL], int j) {
-    int phys = trow[j];
+  // Block ids of this wavefront's run, one per lane (64 blocks at a time), so
+  // the loop never waits on a scalar load before issuing a tile load.
+  int ids = 0;
+  auto fetch_ids = [&](int first) {
+    const int j = first + lane;
+    ids = j < wj1 ? trow[j] : 0;
+  };
+  auto load_tiles = [&](uint4 (&kr)[NC], uint4 (&vr)[TPL], int i) {
+    int phys = __builtin_amdgcn_readlane(ids, i);
     if ((unsigned)phys >= (unsigned)a.num_blocks) {  // contract violation: never read outside the pool
       bad = true;
       phys = 0;
@@ -170,7 +177,7 @@ partition_kernel(const StepArgs a) {
 #pragma unroll
     for (int c = 0; c < NC; ++c) kr[c] = *reinterpret_cast<const uint4*>(kt + 8 * c);
 #pragma unroll
-    for (int i = 0; i < TPL; ++i) vr[i] = *reinterpret_cast<const uint4*>(vt + i * NPH * D);
+    for (int i2 = 0; i2 < TPL; ++i2) vr[i2] = *reinterpret_cast<const uint4*>(vt + i2 * NPH * D);
   };
 
   float o[G][8];
@@ -244,15 +251,27 @@ partition_kernel(const StepArgs a) {
   };
 
   {
+    // Two register buffers: the tiles of block i+1 are in flight while block i
+    // is computed.  The prefetch is unconditional (past the end it requests the
+    // last block again, an L2 hit) so that the compiler counts outstanding loads
+    // exactly; the scheduling barrier keeps the prefetch ahead of the first use
+    // of the current tiles.  Block ids come in chunks of 64, one per lane.
+    const int cnt = wj1 - wj0;
     uint4 k0[NC], v0[TPL], k1[NC], v1[TPL];
-    int j = wj0;
-    if (j < wj1) load_tiles(k0, v0, j);
-    for (; j < wj1; j += 2) {
-      if (j + 1 < wj1) load_tiles(k1, v1, j + 1);
-      process(k0, v0, j, 0);
-      if (j + 1 >= wj1) break;
-      if (j + 2 < wj1) load_tiles(k0, v0, j + 2);
-      process(k1, v1, j + 1, 1);
+    for (int c0 = 0; c0 < cnt; c0 += kWaveSize) {
+      const int cn = min(kWaveSize, cnt - c0);
+      const int jc = wj0 + c0;
+      fetch_ids(jc);
+      load_tiles(k0, v0, 0);
+      for (int i = 0; i < cn; i += 2) {
+        load_tiles(k1, v1, min(i + 1, cn - 1));
+        __builtin_amdgcn_sched_barrier(0);
+        process(k0, v0, jc + i, 0);
+        if (i + 1 >= cn) break;
+        load_tiles(k0, v0, min(i + 2, cn - 1));
+        __builtin_amdgcn_sched_barrier(0);
+        process(k1, v1, jc + i + 1, 1);
+      }
     }
   }
 
