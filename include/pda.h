@@ -14,13 +14,17 @@
  *
  *   for sequence b, query head h:   g = floor(h / G),  G = Hq / Hkv
  *     L = context_lens[b]  (clamped to [0, max_context_len]); L == 0 gives 0
- *     token t in [0, L) lives in block block_table[b][t / 16], slot t % 16
- *     s_t = scale * dot(q[b][h], K[block][g][slot])
- *     out[b][h] = sum_t softmax(s)_t * V[block][g][slot]
+ *     token t in [0, L) lives in block p = block_table[b][t / 16], slot o = t % 16
+ *     s_t = scale * sum_d q[b][h][d] * K[p][g][d / 8][o][d % 8]
+ *     out[b][h] = sum_t softmax(s)_t * V[p][g][o][:]
  *
  * Layouts (row-major; all pointers below are DEVICE pointers):
  *   q            bf16  [num_seqs][num_q_heads][head_dim]
- *   k_cache      bf16  [num_blocks][num_kv_heads][block_size][head_dim]
+ *   k_cache      bf16  [num_blocks][num_kv_heads][head_dim/8][block_size][8]
+ *                       each block's keys as head_dim/8 chunks of 16 slots x 8
+ *                       consecutive elements (key element d of slot o at
+ *                       [d/8][o][d%8]); a 16-byte load of lane l at offset 16*l
+ *                       is then exactly the MFMA operand fragment it needs
  *   v_cache      bf16  [num_blocks][num_kv_heads][block_size][head_dim]
  *   block_table  int32 [num_seqs][max_blocks_per_seq]  (entries past
  *                       ceil(L/16) are never read and may hold anything)

@@ -99,11 +99,13 @@ def _prep(q, k_cache, v_cache, block_table, context_lens):
     v_cache = np.ascontiguousarray(v_cache, dtype=np.uint16)
     block_table = np.ascontiguousarray(block_table, dtype=np.int32)
     context_lens = np.ascontiguousarray(context_lens, dtype=np.int32)
-    if q.ndim != 3 or k_cache.ndim != 4 or k_cache.shape != v_cache.shape:
-        raise ValueError("q must be [B][Hq][D]; k_cache, v_cache [num_blocks][Hkv][BS][D]")
+    if q.ndim != 3 or k_cache.ndim != 5 or v_cache.ndim != 4:
+        raise ValueError("q must be [B][Hq][D], k_cache [num_blocks][Hkv][D/8][BS][8], "
+                         "v_cache [num_blocks][Hkv][BS][D]")
     B, Hq, D = q.shape
-    NB, Hkv, BS, Dk = k_cache.shape
-    if Dk != D or block_table.ndim != 2 or block_table.shape[0] != B or context_lens.shape != (B,):
+    NB, Hkv, BS, Dv = v_cache.shape
+    if (k_cache.shape != (NB, Hkv, D // 8, BS, 8) or Dv != D or block_table.ndim != 2
+            or block_table.shape[0] != B or context_lens.shape != (B,)):
         raise ValueError("inconsistent shapes")
     dims = [B, Hq, Hkv, D, BS, NB, block_table.shape[1]]
     ptrs = [a.ctypes.data for a in (q, k_cache, v_cache, block_table, context_lens)]

@@ -25,7 +25,7 @@
  *       L   = context_lens[b]; if L <= 0 the output row is all zeros
  *       for t in [0, L):
  *         p   = block_table[b][floor(t / BS)],  o = t mod BS
- *         k_t = K[p][g][o][:],  v_t = V[p][g][o][:]  (bf16 widened exactly)
+ *         k_t = K[p][g][:][o],  v_t = V[p][g][o][:]  (bf16 widened exactly)
  *         s_t = scale * sum_d q[b][h][d] * k_t[d]
  *       m   = max_t s_t
  *       e_t = exp(s_t - m),  Z = sum_t e_t           (two passes, t ascending)
@@ -33,7 +33,9 @@
  *
  *   Layouts (all row-major, element counts):
  *     q            bf16  [B][Hq][D]
- *     k_cache      bf16  [num_blocks][Hkv][BS][D]
+ *     k_cache      bf16  [num_blocks][Hkv][D/8][BS][8]   key d of slot o sits at
+ *                        [p][g][d/8][o][d%8]: each block's keys are stored as
+ *                        D/8 chunks of BS rows of 8 consecutive elements
  *     v_cache      bf16  [num_blocks][Hkv][BS][D]
  *     block_table  int32 [B][max_blocks_per_seq]
  *     context_lens int32 [B]
@@ -69,7 +71,7 @@ static int check_problem(const problem_t *P) {
   if (P->B < 0 || P->Hq <= 0 || P->Hkv <= 0 || P->D <= 0 || P->BS <= 0 ||
       P->num_blocks <= 0 || P->max_blocks_per_seq <= 0)
     return -1;
-  if (P->Hq % P->Hkv != 0) return -2;
+  if (P->Hq % P->Hkv != 0 || P->D % 8 != 0) return -2;
   if (P->B > 0 && (!P->q || !P->k || !P->v || !P->block_table || !P->context_lens))
     return -3;
   for (int b = 0; b < P->B; ++b) {
@@ -85,8 +87,13 @@ static int check_problem(const problem_t *P) {
   return 0;
 }
 
-/* Address of row o of block p, KV head g: [p][g][o][0]. */
-static size_t kv_row(const problem_t *P, int32_t p, int g, int o) {
+/* Element d of key slot o, block p, KV head g: [p][g][d/8][o][d%8]. */
+static size_t k_elem(const problem_t *P, int32_t p, int g, int o, int d) {
+  return ((((size_t)p * P->Hkv + g) * (P->D / 8) + d / 8) * P->BS + o) * 8 + d % 8;
+}
+
+/* Start of value slot o of block p, KV head g: [p][g][o][0]. */
+static size_t v_row(const problem_t *P, int32_t p, int g, int o) {
   return (((size_t)p * P->Hkv + g) * P->BS + o) * P->D;
 }
 
@@ -102,9 +109,11 @@ static int row_weights(const problem_t *P, int b, int h, double *scores) {
   /* pass 1: scores and their maximum */
   double m = -INFINITY;
   for (int t = 0; t < L; ++t) {
-    const uint16_t *krow = P->k + kv_row(P, bt[t / P->BS], g, t % P->BS);
+    const int32_t p = bt[t / P->BS];
+    const int o = t % P->BS;
     double dot = 0.0;
-    for (int d = 0; d < P->D; ++d) dot += bf16_to_double(qrow[d]) * bf16_to_double(krow[d]);
+    for (int d = 0; d < P->D; ++d)
+      dot += bf16_to_double(qrow[d]) * bf16_to_double(P->k[k_elem(P, p, g, o, d)]);
     scores[t] = P->scale * dot;
     if (scores[t] > m) m = scores[t];
   }
@@ -126,7 +135,7 @@ static void row_output(const problem_t *P, int b, int h, double *w, double *out_
   int g = h / G;
   const int32_t *bt = P->block_table + (size_t)b * P->max_blocks_per_seq;
   for (int t = 0; t < L; ++t) {
-    const uint16_t *vrow = P->v + kv_row(P, bt[t / P->BS], g, t % P->BS);
+    const uint16_t *vrow = P->v + v_row(P, bt[t / P->BS], g, t % P->BS);
     for (int d = 0; d < P->D; ++d) out_row[d] += w[t] * bf16_to_double(vrow[d]);
   }
 }

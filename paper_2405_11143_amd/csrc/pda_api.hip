@@ -8,9 +8,16 @@
 
 namespace {
 
-// Contexts up to this many tokens run as one partition (no merge pass);
-// longer ones are split into partitions of this size.
-constexpr int kDefaultPartitionTokens = 512;
+// Split-K policy: partitions of kMaxPartitionTokens, halved (down to
+// kMinPartitionTokens) while the step would have fewer than kMinWorkItems
+// (sequence, KV head, partition) items -- too few to keep 256 compute units
+// busy -- and never longer than the longest context (then there is one
+// partition and no merge pass).  Larger partitions amortise each workgroup's start-up
+// (lengths, block ids, q) over more streamed tiles; on MI355X 2048 tokens
+// measured fastest on all four Llama-3-shaped decode steps.
+constexpr int kMaxPartitionTokens = 2048;
+constexpr int kMinPartitionTokens = 256;
+constexpr int64_t kMinWorkItems = 2048;
 
 int check_problem(const pda_problem* p) {
   if (!p) return PDA_ERR_NULL;
@@ -39,8 +46,12 @@ int make_plan(const pda_problem* p, Plan* plan) {
   if (rc != PDA_OK) return rc;
   int tp = p->partition_tokens;
   if (tp == 0) {
-    const int rounded = (p->max_context_len + pda::kBlockTokens - 1) / pda::kBlockTokens * pda::kBlockTokens;
-    tp = rounded <= kDefaultPartitionTokens ? (rounded > 0 ? rounded : pda::kBlockTokens) : kDefaultPartitionTokens;
+    const int64_t units = (int64_t)p->num_seqs * p->num_kv_heads;
+    const int64_t len = p->max_context_len > 0 ? p->max_context_len : 1;
+    tp = kMaxPartitionTokens;
+    while (tp > kMinPartitionTokens && units * ((len + tp - 1) / tp) < kMinWorkItems) tp /= 2;
+    const int rounded = (int)((len + pda::kBlockTokens - 1) / pda::kBlockTokens * pda::kBlockTokens);
+    if (rounded < tp) tp = rounded;  // the whole context fits one partition
   }
   const int64_t parts = p->max_context_len > 0 ? ((int64_t)p->max_context_len + tp - 1) / tp : 1;
   const int64_t grid = parts * p->num_seqs * p->num_kv_heads;

@@ -108,11 +108,11 @@ def pda_validate_host(prob: pda_problem, block_table, context_lens) -> Tuple[int
 def _problem_from(q, k_cache, block_table, max_context_len, partition_tokens) -> pda_problem:
     import torch
 
-    if q.dim() != 3 or k_cache.dim() != 4 or block_table.dim() != 2:
-        raise ValueError("q [B][Hq][D], k_cache [num_blocks][Hkv][16][D], block_table [B][max_blocks]")
+    if q.dim() != 3 or k_cache.dim() != 5 or block_table.dim() != 2:
+        raise ValueError("q [B][Hq][D], k_cache [num_blocks][Hkv][D/8][16][8], block_table [B][max_blocks]")
     B, Hq, D = q.shape
-    NB, Hkv, BS, Dk = k_cache.shape
-    if Dk != D or block_table.shape[0] != B:
+    NB, Hkv, C, BS, E = k_cache.shape
+    if C * E != D or E != 8 or block_table.shape[0] != B:
         raise ValueError("q, k_cache and block_table shapes disagree")
     if max_context_len is None:
         raise ValueError("max_context_len must be given (the host bound on context_lens)")
@@ -131,8 +131,9 @@ def _check_tensors(q, k_cache, v_cache, block_table, context_lens, out):
             raise ValueError(f"{name} must be a device tensor")
         if not t.is_contiguous():
             raise ValueError(f"{name} must be contiguous")
-    if v_cache.shape != k_cache.shape:
-        raise ValueError("v_cache must have the shape of k_cache")
+    NB, Hkv, C, BS, E = k_cache.shape
+    if tuple(v_cache.shape) != (NB, Hkv, BS, C * E):
+        raise ValueError("v_cache must be [num_blocks][Hkv][16][D] (k_cache is [num_blocks][Hkv][D/8][16][8])")
     if out.shape != q.shape:
         raise ValueError("out must have the shape of q")
     if context_lens.shape != (q.shape[0],):
@@ -172,7 +173,8 @@ def _step(fn_name, q, k_cache, v_cache, block_table, context_lens, scale, out, m
 def pda_decode(q, k_cache, v_cache, block_table, context_lens, scale: float, out=None, *,
                max_context_len: int, partition_tokens: int = 0, workspace=None, stream=None):
     """One decode-attention step (both passes).  Tensors on the GPU:
-    q bf16 [B][Hq][D], k_cache/v_cache bf16 [num_blocks][Hkv][16][D],
+    q bf16 [B][Hq][D], k_cache bf16 [num_blocks][Hkv][D/8][16][8] (each block's
+    keys as D/8 chunks of 16 slots x 8 elements), v_cache bf16 [num_blocks][Hkv][16][D],
     block_table int32 [B][max_blocks], context_lens int32 [B], out fp32 [B][Hq][D].
     `workspace` (uint8, >= pda_workspace_bytes) is allocated when not given."""
     return _step("pda_decode", q, k_cache, v_cache, block_table, context_lens, scale, out, max_context_len,

@@ -64,14 +64,24 @@ def test_plan_rejects(kw, status):
     assert e.value.status == status
 
 
+def llama(**kw):
+    base = dict(num_seqs=256, num_q_heads=32, num_kv_heads=8, head_dim=128, max_blocks_per_seq=1024,
+                max_context_len=4096, num_blocks=50000)
+    base.update(kw)
+    return prob(**base)
+
+
 def test_plan_values():
-    # contexts up to 512 tokens: one partition, no workspace
-    assert pda.pda_plan(prob()) == (272, 1, 0)
-    assert pda.pda_plan(prob(max_context_len=0)) == (16, 1, 0)
-    # longer: 512-token partitions, fp32 partials (D values + max + denominator)
-    tp, n, ws = pda.pda_plan(prob(num_seqs=256, num_q_heads=32, num_kv_heads=8, head_dim=128,
-                                  max_blocks_per_seq=256, max_context_len=4096))
-    assert (tp, n) == (512, 8) and ws == 256 * 32 * 8 * (128 + 2) * 4
+    # 2048-token partitions, fp32 partials (D values + max + denominator)
+    tp, n, ws = pda.pda_plan(llama())
+    assert (tp, n) == (2048, 2) and ws == 256 * 32 * 2 * (128 + 2) * 4
+    # a context that fits one partition: no merge pass, no workspace
+    assert pda.pda_plan(llama(max_context_len=2001)) == (2016, 1, 0)
+    assert pda.pda_plan(llama(max_context_len=0)) == (16, 1, 0)
+    # few (sequence, KV head) units: partitions shrink, not below 256 tokens
+    assert pda.pda_plan(llama(num_seqs=64, max_context_len=16384))[:2] == (2048, 8)
+    assert pda.pda_plan(llama(num_seqs=4, max_context_len=16384))[:2] == (256, 64)
+    assert pda.pda_plan(prob())[:2] == (256, 2)
     # forced partition size
     assert pda.pda_plan(prob(partition_tokens=64)) == (64, 5, 4 * 8 * 5 * 66 * 4)
 
@@ -114,7 +124,7 @@ def test_merge_validation():
     assert f(ctypes.byref(split), 0x1000, 0x1000, 0x1000, need - 1, None) == pda.pda.PDA_ERR_WORKSPACE
     assert f(ctypes.byref(split), 0x1000, 0x1000, 0x1004, need, None) == pda.pda.PDA_ERR_ALIGNMENT
     # nothing split: nothing to merge, no launch
-    assert f(ctypes.byref(prob()), None, None, None, 0, None) == pda.pda.PDA_OK
+    assert f(ctypes.byref(prob(max_context_len=200)), None, None, None, 0, None) == pda.pda.PDA_OK
 
 
 def test_validate_host():

@@ -149,7 +149,7 @@ def test_empty_and_nonpositive_lengths(dev):
     assert np.all(got[0] == 0) and np.all(got[2] == 0)
     check(got, reference(st, q, k, v), "lengths 0, 20, -5, 1")
     # an empty batch launches nothing
-    e = torch.empty((0, 8, 64), dtype=torch.bfloat16, device=dev)
+    e = torch.empty((0, 8, 64), dtype=torch.bfloat16, device=dev)  # k, v from the problem above
     out = pda_decode(e, k, v, torch.empty((0, 2), dtype=torch.int32, device=dev),
                      torch.empty((0,), dtype=torch.int32, device=dev), 0.125, max_context_len=0)
     assert out.shape == (0, 8, 64)

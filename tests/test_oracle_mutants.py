@@ -21,14 +21,19 @@ SRC = os.path.join(ROOT, "oracle", "pda_oracle.c")
 
 MUTANTS = {
     "kv head = h mod Hkv": ("int g = h / G;", "int g = h % P->Hkv;"),
-    "block and slot swapped": ("bt[t / P->BS], g, t % P->BS", "bt[t % P->BS], g, t / P->BS"),
+    "K block and slot swapped": ("const int32_t p = bt[t / P->BS];\n    const int o = t % P->BS;",
+                                 "const int32_t p = bt[t % P->BS];\n    const int o = t / P->BS;"),
+    "V block and slot swapped": ("bt[t / P->BS], g, t % P->BS", "bt[t % P->BS], g, t / P->BS"),
     "no max subtraction": ("exp(scores[t] - m)", "exp(scores[t])"),
     "exp sign flipped": ("exp(scores[t] - m)", "exp(m - scores[t])"),
     "scale dropped": ("scores[t] = P->scale * dot;", "scores[t] = dot;"),
     "no normalisation": ("for (int t = 0; t < L; ++t) scores[t] /= Z;", ""),
     "sum starts at one": ("double Z = 0.0;", "double Z = 1.0;"),
-    "cache layout [p][o][g]": ("(((size_t)p * P->Hkv + g) * P->BS + o) * P->D",
-                               "(((size_t)p * P->BS + o) * P->Hkv + g) * P->D"),
+    "V layout [p][o][g]": ("(((size_t)p * P->Hkv + g) * P->BS + o) * P->D",
+                           "(((size_t)p * P->BS + o) * P->Hkv + g) * P->D"),
+    "K layout read as rows": ("((((size_t)p * P->Hkv + g) * (P->D / 8) + d / 8) * P->BS + o) * 8 + d % 8",
+                              "(((size_t)p * P->Hkv + g) * P->BS + o) * P->D + d"),
+    "K chunk element order": ("* P->BS + o) * 8 + d % 8", "* P->BS + o) * 8 + (7 - d % 8)"),
     "q row of the kv head": ("((size_t)b * P->Hq + h) * P->D", "((size_t)b * P->Hq + g) * P->D"),
     "V read from K": ("const uint16_t *vrow = P->v +", "const uint16_t *vrow = P->k +"),
     "bf16 widened wrongly": ("(uint32_t)bits << 16", "(uint32_t)bits << 15"),

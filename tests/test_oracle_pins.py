@@ -74,7 +74,7 @@ class Case:
 
 def dense_reference(case: Case) -> np.ndarray:
     """Brute force: gather each sequence's K/V densely, softmax(scale q K^T) V."""
-    q, k, v = widen(case.q), widen(case.k), widen(case.v)
+    q, k, v = widen(case.q), W.k_cache_to_rows(widen(case.k)), widen(case.v)
     B, Hq, D = q.shape
     G = Hq // k.shape[1]
     out = np.zeros((B, Hq, D))
@@ -111,7 +111,7 @@ def golden_case(c) -> tuple:
                           for row in seq] for seq in c["expected"]], dtype=np.float64)
     bt = np.asarray(c["block_table"], dtype=np.int32)
     lens = np.asarray(c["context_lens"], dtype=np.int32)
-    return (q, bits_of(k), bits_of(v), bt, lens, float(np.float32(c["scale"]))), expected
+    return (q, bits_of(W.k_rows_to_cache(k)), bits_of(v), bt, lens, float(np.float32(c["scale"]))), expected
 
 
 # -------------------------------------------------------------------- pins --
@@ -145,13 +145,13 @@ def pin_length_one_is_v(O):
 
 def pin_identical_keys_mean(O):
     c = Case.random(3, 4, 2, 16, [5, 16, 33], seed=4)
-    k = c.k.copy()
+    k = W.k_cache_to_rows(c.k)
     for b in range(3):  # every key row of (b, g) equal to the first one of (b, g)
         L = int(c.lens[b])
         first = k[c.bt[b, 0], :, 0].copy()
         for t in range(L):
             k[c.bt[b, t // 16], :, t % 16] = first
-    c.k = k
+    c.k = W.k_rows_to_cache(k)
     out = c.run(O)
     v = widen(c.v)
     for b in range(3):
@@ -177,7 +177,7 @@ def pin_scale_zero_mean(O):
 
 def pin_weights_probability(O):
     c = Case.random(2, 4, 2, 32, [45, 3], seed=6)
-    q, k = widen(c.q), widen(c.k)
+    q, k = widen(c.q), W.k_cache_to_rows(widen(c.k))
     for b in range(2):
         for h in range(4):
             w = O.weights(*c.args(), b, h)
@@ -200,7 +200,7 @@ def pin_dominant_key(O):
     k = np.zeros((c.st.num_blocks, 1, 16, 8), np.float32)
     t_hot = 13
     k[c.bt[0, t_hot // 16], 0, t_hot % 16, 0] = 128.0
-    c.q, c.k, c.scale = bits_of(q), bits_of(k), 0.125
+    c.q, c.k, c.scale = bits_of(q), bits_of(W.k_rows_to_cache(k)), 0.125
     out = c.run(O)
     assert np.array_equal(out[0, 0], widen(c.v)[c.bt[0, t_hot // 16], 0, t_hot % 16])
 
@@ -233,12 +233,13 @@ def pin_token_permutation(O):
     out = c.run(O)
     L = 37
     perm = np.random.default_rng(0).permutation(L)
-    k, v = c.k.copy(), c.v.copy()
+    k0 = W.k_cache_to_rows(c.k)
+    k, v = k0.copy(), c.v.copy()
     for t in range(L):  # token t takes the K/V row of token perm[t]
         s = perm[t]
-        k[c.bt[0, t // 16], :, t % 16] = c.k[c.bt[0, s // 16], :, s % 16]
+        k[c.bt[0, t // 16], :, t % 16] = k0[c.bt[0, s // 16], :, s % 16]
         v[c.bt[0, t // 16], :, t % 16] = c.v[c.bt[0, s // 16], :, s % 16]
-    c.k, c.v = k, v
+    c.k, c.v = W.k_rows_to_cache(k), v
     np.testing.assert_allclose(c.run(O), out, rtol=0, atol=TIGHT)
 
 
@@ -251,8 +252,8 @@ def pin_uniform_shift(O):
     k = r.integers(-32, 33, size=(st.num_blocks, 2, 16, 16)).astype(np.float32) / 8
     mu = r.integers(-16, 17, size=(1, 2, 1, 16)).astype(np.float32) / 8
     q, _, v = W.fill_values(st, "cpu", fill=None)
-    base = Case(st, W.bf16_bits(q), bits_of(k), W.bf16_bits(v)).run(O)
-    shifted = Case(st, W.bf16_bits(q), bits_of(k + mu), W.bf16_bits(v)).run(O)
+    base = Case(st, W.bf16_bits(q), bits_of(W.k_rows_to_cache(k)), W.bf16_bits(v)).run(O)
+    shifted = Case(st, W.bf16_bits(q), bits_of(W.k_rows_to_cache(k + mu)), W.bf16_bits(v)).run(O)
     np.testing.assert_allclose(shifted, base, rtol=0, atol=1e-9)
 
 

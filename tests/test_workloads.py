@@ -72,10 +72,11 @@ def test_values_are_deterministic_and_poisoned():
         assert a.dtype == torch.bfloat16
         assert torch.equal(a.view(torch.int16), b.view(torch.int16))
     mask = torch.from_numpy(W.unread_slot_mask(st))
-    assert torch.isnan(k1.float()).any(dim=(1, 3)).eq(mask).all()
+    assert k1.shape == (st.num_blocks, 2, 8, 16, 8) and v1.shape == (st.num_blocks, 2, 16, 64)
+    assert torch.isnan(k1.float()).any(dim=(1, 2, 4)).eq(mask).all()
     assert torch.isnan(v1.float()).all(dim=(1, 3)).eq(mask).all()
     # read slots hold N(0,1) draws
-    read = k1.float().permute(0, 2, 1, 3)[~mask]
+    read = W.k_cache_to_rows(k1).float().permute(0, 2, 1, 3)[~mask]
     assert torch.isfinite(read).all() and abs(read.mean().item()) < 0.1 and abs(read.std().item() - 1) < 0.1
 
 
@@ -83,6 +84,19 @@ def test_bf16_rounds_to_nearest_even():
     x = torch.tensor([1 + 2**-8, 1 + 3 * 2**-8, 1 + 2**-8 + 2**-20, -(1 + 2**-8)], dtype=torch.float32)
     got = x.to(torch.bfloat16).float().tolist()
     assert got == [1.0, 1 + 2**-6, 1 + 2**-7, -1.0]
+
+
+def test_k_layout_round_trip():
+    rows = np.arange(3 * 2 * 16 * 24, dtype=np.float32).reshape(3, 2, 16, 24)
+    cache = W.k_rows_to_cache(rows)
+    assert cache.shape == (3, 2, 3, 16, 8)
+    # key d of slot o of block p, head g sits at [p][g][d // 8][o][d % 8]
+    for (p, g, o, d) in [(0, 0, 0, 0), (2, 1, 15, 23), (1, 0, 7, 9), (1, 1, 3, 16)]:
+        assert cache[p, g, d // 8, o, d % 8] == rows[p, g, o, d]
+    assert np.array_equal(W.k_cache_to_rows(cache), rows)
+    t = torch.from_numpy(rows)
+    assert torch.equal(W.k_rows_to_cache(t), torch.from_numpy(cache))
+    assert torch.equal(W.k_cache_to_rows(W.k_rows_to_cache(t)), t)
 
 
 def test_permute_pool_moves_blocks():

@@ -24,6 +24,11 @@ Streams of the Philox generator (seed, stream):
 Pool blocks that no sequence references, and the slots of a block beyond the
 longest context that references it, can be filled with bf16 NaN ("poison")
 so that any read of them shows up in the output.
+
+Cache layouts (the library's): V is [num_blocks][Hkv][16][D], one row of D
+values per token slot; K is [num_blocks][Hkv][D/8][16][8], each block's keys
+split into D/8 chunks of 16 slots x 8 consecutive elements.  Keys are drawn
+as rows [num_blocks][Hkv][16][D] and stored through `k_rows_to_cache`.
 """
 from __future__ import annotations
 
@@ -219,10 +224,28 @@ def custom_structure(B: int, Hq: int, Hkv: int, D: int, lens: Sequence[int], see
                      max_blocks_per_seq=mbs, context_lens=lens, block_table=table)
 
 
+def k_rows_to_cache(k_rows):
+    """[NB][Hkv][16][D] key rows -> the cache layout [NB][Hkv][D/8][16][8]
+    (numpy array or torch tensor)."""
+    NB, H, S, D = k_rows.shape
+    x = k_rows.reshape(NB, H, S, D // 8, 8)
+    if hasattr(x, "permute"):
+        return x.permute(0, 1, 3, 2, 4).contiguous()
+    return np.ascontiguousarray(x.transpose(0, 1, 3, 2, 4))
+
+
+def k_cache_to_rows(k_cache):
+    """The cache layout [NB][Hkv][D/8][16][8] -> key rows [NB][Hkv][16][D]."""
+    NB, H, C, S, E = k_cache.shape
+    if hasattr(k_cache, "permute"):
+        return k_cache.permute(0, 1, 3, 2, 4).reshape(NB, H, S, C * E).contiguous()
+    return np.ascontiguousarray(k_cache.transpose(0, 1, 3, 2, 4).reshape(NB, H, S, C * E))
+
+
 def fill_values(st: Structure, device="cpu", fill: Optional[str] = "nan"):
-    """Draw q [B][Hq][D] and the K/V pools [num_blocks][Hkv][16][D] (bf16) on
-    `device`.  `fill` is 'nan', 'zero' or None: what to write into pool slots
-    no sequence reads."""
+    """Draw q [B][Hq][D], the K pool [num_blocks][Hkv][D/8][16][8] and the V pool
+    [num_blocks][Hkv][16][D] (bf16) on `device`.  `fill` is 'nan', 'zero' or
+    None: what to write into pool slots no sequence reads."""
     import torch
 
     dev = torch.device(device)
@@ -239,7 +262,7 @@ def fill_values(st: Structure, device="cpu", fill: Optional[str] = "nan"):
         mu = (torch.randn((st.Hkv, 1, st.D), generator=gen(_STREAM_KOFF), device=dev,
                           dtype=torch.float32) * st.k_offset_std)
     shape = (st.num_blocks, st.Hkv, st.block_size, st.D)
-    k = torch.empty(shape, dtype=torch.bfloat16, device=dev)
+    k = torch.empty((st.num_blocks, st.Hkv, st.D // 8, st.block_size, 8), dtype=torch.bfloat16, device=dev)
     v = torch.empty(shape, dtype=torch.bfloat16, device=dev)
     gk, gv = gen(_STREAM_K), gen(_STREAM_V)
     for c0 in range(0, st.num_blocks, _POOL_CHUNK_BLOCKS):
@@ -248,7 +271,7 @@ def fill_values(st: Structure, device="cpu", fill: Optional[str] = "nan"):
         kf = torch.randn(sub, generator=gk, device=dev, dtype=torch.float32)
         if mu is not None:
             kf += mu
-        k[c0:c1] = kf.to(torch.bfloat16)
+        k[c0:c1] = k_rows_to_cache(kf.to(torch.bfloat16))
         v[c0:c1] = torch.randn(sub, generator=gv, device=dev, dtype=torch.float32).to(torch.bfloat16)
         del kf
     if fill is not None:
@@ -267,9 +290,9 @@ def apply_fill(st: Structure, k, v, fill: str = "nan"):
     import torch
 
     value = {"nan": float("nan"), "zero": 0.0}[fill]
-    mask = torch.from_numpy(unread_slot_mask(st)).to(k.device)[:, None, :, None]
-    k.masked_fill_(mask, value)
-    v.masked_fill_(mask, value)
+    mask = torch.from_numpy(unread_slot_mask(st)).to(k.device)
+    k.masked_fill_(mask[:, None, None, :, None], value)
+    v.masked_fill_(mask[:, None, :, None], value)
 
 
 def permute_pool(st: Structure, k, v, seed: int):
