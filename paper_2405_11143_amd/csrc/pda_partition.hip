@@ -13,10 +13,12 @@
 //  * The partition's 16-token blocks are split into 4 contiguous runs, one per
 //    wavefront; each wavefront keeps its own online-softmax state and
 //    prefetches the next block's K and V tiles (2 x 16 x D bf16) into
-//    registers while it computes on the current one.  Every tile load
-//    instruction reads 1 KiB of contiguous memory (whole cache lines) and is
-//    non-temporal: the cache is streamed once, and measured on MI355X the
-//    streaming hint lifts a plain tile gather from ~6.1 to ~6.9 TB/s.
+//    registers while it computes on the current one.  Every tile load is a
+//    buffer load (descriptor = the tile, so no read can leave it) whose
+//    instruction reads 1 KiB of contiguous memory (whole cache lines) with
+//    the non-temporal hint: the cache is streamed once, and measured on MI355X
+//    the hint lifts a plain 4 KiB-tile gather from ~6.1 to ~6.9 TB/s.  All K
+//    and V loads of a lane share one 32-bit offset register.
 //  * Scores S[G][16] = Q_g K^T are one small dense contraction per block:
 //    D/32 MFMA f32_16x16x32_bf16 with the G query heads (repeated to fill 16
 //    rows) as the A operand and the K tile as the B operand.  The K cache
@@ -27,10 +29,15 @@
 //    loads.  The A operand (q) uses the same assignment of d to (k-step,
 //    k-group, element), so the contraction is unchanged.
 //  * The online softmax runs on the MFMA output layout: a lane holds the
-//    scores of 4 head rows for one token; the block max of a row is a 16-lane
-//    all-reduce made of four DPP moves (quad swaps, half-row and row mirror).
-//    Each lane accumulates the denominator of its own token column; columns
-//    are summed once, at the end.
+//    scores of 4 head rows for one token.  The running maximum is moved only
+//    when some score of the block exceeds it by more than 2^8 (a wavefront
+//    vote); then the block max of each row is a 16-lane all-reduce of four
+//    DPP moves (quad swaps, half-row and row mirror) and the state is
+//    rescaled.  Otherwise probabilities are taken against the stale maximum
+//    (they stay below 2^8, far inside fp32), so most blocks need neither the
+//    reduction nor the O rescale; the result is the same softmax.  Each lane
+//    accumulates the denominator of its own token column; columns are summed
+//    once, at the end.
 //  * P V runs on the VALU in fp32: lane (phase, chunk) owns 8 consecutive d
 //    for all G heads and the tokens of its phase, so each V load instruction
 //    reads 1 KiB of contiguous tile.  The probabilities and rescale factors
@@ -75,9 +82,15 @@ __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_ex
 
 typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
 
-// 16-byte non-temporal load of data that is read once per step.
-__device__ __forceinline__ uint4 load_stream(const uint16_t* p) {
-  const u32x4_t t = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+// Raw buffer resource over `bytes` bytes at `base` (gfx9 dword-3 default:
+// 32-bit raw accesses, bounds-checked against num_records).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const void* base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
+}
+
+// 16-byte non-temporal load (cache policy NT) at byte `offset` of a tile.
+__device__ __forceinline__ uint4 load_stream(__amdgpu_buffer_rsrc_t r, int offset) {
+  const u32x4_t t = __builtin_amdgcn_raw_buffer_load_b128(r, offset, 0, 2);
   return make_uint4(t[0], t[1], t[2], t[3]);
 }
 
@@ -99,8 +112,11 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Occupancy: up to G = 8 the kernel fits 168 VGPRs, i.e. 3 wavefronts per
+// SIMD (12 per compute unit); the hint makes the compiler hold that line for
+// G = 8, which would otherwise take 170 registers and drop to 2.
 template <int G, int D>
-__global__ void __launch_bounds__(kWaves * kWaveSize)
+__global__ void __launch_bounds__(kWaves * kWaveSize) __attribute__((amdgpu_waves_per_eu(G <= 8 ? 3 : 1)))
 partition_kernel(const StepArgs a) {
   static_assert(G >= 1 && G <= kMaxGroup, "query heads per KV head");
   static_assert(D == 64 || D == 128, "head_dim");
@@ -110,6 +126,7 @@ partition_kernel(const StepArgs a) {
   constexpr int TPL = kBlockTokens / NPH;    // tokens per lane per block in P.V
   constexpr int GP = (G + 3) & ~3;           // head count padded to float4
   constexpr float kNegInf = -__builtin_huge_valf();
+  constexpr float kRescaleSlack = 8.f;       // log2 of the largest unnormalised probability
 
   __shared__ __align__(16) float s_p[kWaves][2][kBlockTokens][GP];
   __shared__ __align__(16) float s_alpha[kWaves][2][GP];
@@ -153,8 +170,8 @@ partition_kernel(const StepArgs a) {
   // d = 8 * (4c + kg) + e, e < 8 (chunk 4c + kg of the K tile).
   const int n = lane & 15;
   const int kg = lane >> 4;
-  // P.V coordinates: this lane owns d in [8*dc, 8*dc+8) for tokens tp, tp+NPH, ...
-  const int dc = lane % CPR;
+  // P.V coordinates: this lane owns d in [8*(lane % CPR), +8) for the tokens
+  // tp, tp + NPH, ... of each block.
   const int tp = lane / CPR;
 
   // A operand: query head (n mod G) of this KV head, d = 32c + 8kg + e.
@@ -166,9 +183,13 @@ partition_kernel(const StepArgs a) {
       qa[c] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(qrow + 32 * c));
   }
 
-  const size_t block_stride = (size_t)Hkv * kBlockTokens * D;  // elements per pool block
-  const uint16_t* kbase = a.k + (size_t)g * kBlockTokens * D + lane * 8;
-  const uint16_t* vbase = a.v + (size_t)g * kBlockTokens * D + tp * D + dc * 8;
+  constexpr int kTileBytes = kBlockTokens * D * 2;                // one (block, KV head) tile
+  const size_t block_bytes = (size_t)Hkv * kTileBytes;              // one pool block, all heads
+  const char* kpool = reinterpret_cast<const char*>(a.k) + (size_t)g * kTileBytes;
+  const char* vpool = reinterpret_cast<const char*>(a.v) + (size_t)g * kTileBytes;
+  // K: lane l's fragment for k-step c is the 16 bytes at 1024c + 16l of the
+  // tile.  V: the same offsets hold row NPH*i + tp, columns 8*(lane % CPR) + e.
+  const int lane_off = lane * 16;
   const int32_t* trow = a.table + (size_t)b * a.max_blocks_per_seq;
   bool bad = false;
 
@@ -179,19 +200,20 @@ partition_kernel(const StepArgs a) {
     const int j = first + lane;
     ids = j < wj1 ? trow[j] : 0;
   };
-  auto load_tiles = [&](uint4 (&kr)[NC], uint4 (&vr)[TPL], int i) {
+  auto load_tiles = [&](uint4 (&kr)[NC], uint4 (&vr)[TPL], int i, bool needed) {
     int phys = __builtin_amdgcn_readlane(ids, i);
     if ((unsigned)phys >= (unsigned)a.num_blocks) {  // contract violation: never read outside the pool
       bad = true;
       phys = 0;
     }
-    const size_t off = (size_t)phys * block_stride;
-    const uint16_t* kt = kbase + off;
-    const uint16_t* vt = vbase + off;
+    const size_t off = (size_t)phys * block_bytes;
+    const int bytes = needed ? kTileBytes : 0;
+    const __amdgpu_buffer_rsrc_t rk = tile_rsrc(kpool + off, bytes);
+    const __amdgpu_buffer_rsrc_t rv = tile_rsrc(vpool + off, bytes);
 #pragma unroll
-    for (int c = 0; c < NC; ++c) kr[c] = load_stream(kt + c * kWaveSize * 8);
+    for (int c = 0; c < NC; ++c) kr[c] = load_stream(rk, lane_off + c * 1024);
 #pragma unroll
-    for (int i2 = 0; i2 < TPL; ++i2) vr[i2] = load_stream(vt + i2 * NPH * D);
+    for (int i2 = 0; i2 < TPL; ++i2) vr[i2] = load_stream(rv, lane_off + i2 * 1024);
   };
 
   float o[G][8];
@@ -214,34 +236,52 @@ partition_kernel(const StepArgs a) {
       acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[c], __builtin_bit_cast(bf16x8_t, kr[c]), acc, 0, 0, 0);
     const bool tail = (j + 1) * kBlockTokens > L;  // wave-uniform
     const int tok0 = j * kBlockTokens;
-    float pr[4], al[4];
+    float sc[4];
+    bool grow = false;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      float s = acc[i] * a.scale_log2;
-      if (tail && tok0 + n >= L) s = kNegInf;
-      const float mn = fmaxf(m_run[i], row16_max(s));  // finite: the block has a valid token
-      al[i] = exp2_fast(m_run[i] - mn);
-      pr[i] = exp2_fast(s - mn);
-      l_run[i] = fmaf(l_run[i], al[i], pr[i]);
-      m_run[i] = mn;
+      sc[i] = acc[i] * a.scale_log2;
+      if (tail && tok0 + n >= L) sc[i] = kNegInf;
+      grow |= sc[i] > m_run[i] + kRescaleSlack;
+    }
+    // ---- move the running max only when a score outgrows it by 2^8 ----
+    const bool rescale = __builtin_amdgcn_ballot_w64(grow) != 0;  // wave-uniform
+    float al[4] = {1.f, 1.f, 1.f, 1.f};
+    if (rescale) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float mn = fmaxf(m_run[i], row16_max(sc[i]));  // finite: the block has a valid token
+        al[i] = exp2_fast(m_run[i] - mn);
+        l_run[i] *= al[i];
+        m_run[i] = mn;
+      }
+    }
+    float pr[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      pr[i] = exp2_fast(sc[i] - m_run[i]);
+      l_run[i] += pr[i];
     }
     if (4 * kg < G) {
       *reinterpret_cast<float4*>(&s_p[w][par][n][4 * kg]) = make_float4(pr[0], pr[1], pr[2], pr[3]);
-      if (n == 0) *reinterpret_cast<float4*>(&s_alpha[w][par][4 * kg]) = make_float4(al[0], al[1], al[2], al[3]);
+      if (rescale && n == 0)
+        *reinterpret_cast<float4*>(&s_alpha[w][par][4 * kg]) = make_float4(al[0], al[1], al[2], al[3]);
     }
     wave_lds_sync();
 
     // ---- O = alpha * O + P V on the VALU ----
-    float alpha[GP];
+    if (rescale) {
+      float alpha[GP];
 #pragma unroll
-    for (int h4 = 0; h4 < GP; h4 += 4) {
-      const float4 t = *reinterpret_cast<const float4*>(&s_alpha[w][par][h4]);
-      alpha[h4] = t.x; alpha[h4 + 1] = t.y; alpha[h4 + 2] = t.z; alpha[h4 + 3] = t.w;
+      for (int h4 = 0; h4 < GP; h4 += 4) {
+        const float4 t = *reinterpret_cast<const float4*>(&s_alpha[w][par][h4]);
+        alpha[h4] = t.x; alpha[h4 + 1] = t.y; alpha[h4 + 2] = t.z; alpha[h4 + 3] = t.w;
+      }
+#pragma unroll
+      for (int h = 0; h < G; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[h][e] *= alpha[h];
     }
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) o[h][e] *= alpha[h];
 #pragma unroll
     for (int i = 0; i < TPL; ++i) {
       const int row = i * NPH + tp;
@@ -266,23 +306,25 @@ partition_kernel(const StepArgs a) {
 
   {
     // Two register buffers: the tiles of block i+1 are in flight while block i
-    // is computed.  The prefetch is unconditional (past the end it requests the
-    // last block again, an L2 hit) so that the compiler counts outstanding loads
-    // exactly; the scheduling barrier keeps the prefetch ahead of the first use
-    // of the current tiles.  Block ids come in chunks of 64, one per lane.
+    // is computed.  Every load is unconditional, so the compiler counts
+    // outstanding loads exactly and waits only for the tiles it is about to
+    // use; the scheduling barriers keep each prefetch ahead of the first use
+    // of the current tiles.  Past the end of the run the prefetch gets a
+    // zero-length descriptor: the hardware drops it without touching memory.
+    // Block ids come in chunks of 64, one per lane.
     const int cnt = wj1 - wj0;
     uint4 k0[NC], v0[TPL], k1[NC], v1[TPL];
     for (int c0 = 0; c0 < cnt; c0 += kWaveSize) {
       const int cn = min(kWaveSize, cnt - c0);
       const int jc = wj0 + c0;
       fetch_ids(jc);
-      load_tiles(k0, v0, 0);
+      load_tiles(k0, v0, 0, true);
       for (int i = 0; i < cn; i += 2) {
-        load_tiles(k1, v1, min(i + 1, cn - 1));
+        load_tiles(k1, v1, min(i + 1, cn - 1), i + 1 < cn);
         __builtin_amdgcn_sched_barrier(0);
         process(k0, v0, jc + i, 0);
         if (i + 1 >= cn) break;
-        load_tiles(k0, v0, min(i + 2, cn - 1));
+        load_tiles(k0, v0, min(i + 2, cn - 1), i + 2 < cn);
         __builtin_amdgcn_sched_barrier(0);
         process(k1, v1, jc + i + 1, 1);
       }
