@@ -1,6 +1,6 @@
 """Benchmark of one paged decode-attention step on one MI355X.
 
-A step is one pda_decode call (partition pass + merge pass) over a whole
+A step is one pda_decode call (pass 1 + merge pass) over a whole
 batch: every sequence's new query token attends over its paged KV cache.
 The default workload is the Llama-3-8B-shaped rollout step (B=256, 32 query
 / 8 KV heads, head_dim 128, contexts uniform in [512, 4096], random block
@@ -11,7 +11,8 @@ Prints one JSON line:
   value      algorithmic HBM bytes per step / step time, in GB/s
              (K and V rows of every context token -- shared rows once --
              plus q, the fp32 output, the block-table entries and lengths)
-  roofline   the partition kernel alone: the same algorithmic bytes / its
+  roofline   the pass-1 kernel alone (stream_kernel, or partition_kernel when
+             --partition-tokens is set): the same algorithmic bytes / its
              average launch time (HIP events on its stream), against the
              8 TB/s HBM peak; `traffic` is the measured HBM bytes per launch
              from rocprofv3 counters when they were taken on this kernel source
@@ -33,27 +34,32 @@ sys.path.insert(0, ROOT)
 PEAK_GBS = 8000.0  # MI355X HBM3E, datasheet
 METRIC = "decode-attention HBM GB/s (% of peak) + seq-steps/s, Llama-3-8B shape"
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SOURCES = ["paper_2405_11143_amd/csrc/pda_partition.hip", "paper_2405_11143_amd/csrc/pda_internal.h"]
+CSRC = "paper_2405_11143_amd/csrc/"
+# The pass-1 kernel of each schedule and the sources it is compiled from.
+KERNEL_SOURCES = {
+    "stream_kernel": [CSRC + "pda_stream.hip", CSRC + "pda_wave.h", CSRC + "pda_internal.h"],
+    "partition_kernel": [CSRC + "pda_partition.hip", CSRC + "pda_wave.h", CSRC + "pda_internal.h"],
+}
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(kernel: str) -> str:
     h = hashlib.sha256()
-    for rel in KERNEL_SOURCES:
+    for rel in KERNEL_SOURCES[kernel]:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per partition-kernel launch from the committed counter summary,
-    or None when it is missing or was taken on another kernel source."""
-    path = os.path.join(PROFILES, f"traffic_partition_kernel_{workload}.md")
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or
+    None when it is missing or was taken on another kernel source."""
+    path = os.path.join(PROFILES, f"traffic_{kernel}_{workload}.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
     m_hash = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
     m_bytes = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
-    if not m_hash or not m_bytes or m_hash.group(1) != kernel_source_hash():
+    if not m_hash or not m_bytes or m_hash.group(1) != kernel_source_hash(kernel):
         return None
     return float(m_bytes.group(1))
 
@@ -86,12 +92,15 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="llama3_8b")
-    ap.add_argument("--partition-tokens", type=int, default=0)
+    ap.add_argument("--partition-tokens", type=int, default=0,
+                    help="> 0: partition schedule with this many tokens per partition")
+    ap.add_argument("--num-workers", type=int, default=0,
+                    help="stream schedule: wavefronts (0 = all the GPU holds at once)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-min-seconds", type=float, default=10.0)
     ap.add_argument("--cpu-max-reps", type=int, default=20)
     ap.add_argument("--pass1-only", action="store_true",
-                    help="time and launch only the partition kernel (for counter runs)")
+                    help="time and launch only the pass-1 kernel (for counter runs)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a device copy of this many MiB (counter calibration) and exit")
     args = ap.parse_args(argv)
@@ -126,13 +135,14 @@ def main(argv=None):
     bt = torch.from_numpy(st.block_table).to(dev)
     lens = torch.from_numpy(st.context_lens).to(dev)
     prob = make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq,
-                        st.max_context_len, args.partition_tokens)
-    tp, nparts, ws_bytes = pda_plan(prob)
+                        st.max_context_len, args.partition_tokens, num_workers=args.num_workers)
+    plan = pda_plan(prob)
+    ws_bytes = plan["workspace_bytes"]
     out = torch.empty((st.B, st.Hq, st.D), dtype=torch.float32, device=dev)
     ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
     kw = dict(max_context_len=st.max_context_len, partition_tokens=args.partition_tokens,
-              workspace=ws, stream=stream)
+              num_workers=args.num_workers, workspace=ws, stream=stream)
 
     def step():
         pda_decode(q, k, v, bt, lens, st.scale, out, **kw)
@@ -161,7 +171,8 @@ def main(argv=None):
     alg = st.algorithmic_bytes()
     value = alg / (ms_step * 1e-3) / 1e9
     achieved = alg / (ms_pass1 * 1e-3) / 1e9
-    traffic = measured_traffic(args.config)
+    kernel = "stream_kernel" if plan["schedule"] == 0 else "partition_kernel"
+    traffic = measured_traffic(kernel, args.config)
     cfg = W.CONFIGS[args.config]
     result = {
         "metric": METRIC,
@@ -179,12 +190,14 @@ def main(argv=None):
         "config": {"workload": cfg["desc"], "name": args.config, "batch": st.B, "q_heads": st.Hq,
                    "kv_heads": st.Hkv, "head_dim": st.D, "block_size": st.block_size,
                    "pool_blocks": st.num_blocks, "context_tokens": st.logical_tokens,
-                   "unique_context_tokens": st.unique_tokens, "partition_tokens": tp,
-                   "partitions_max": nparts, "timed": "pass1 only" if args.pass1_only else "full step"},
+                   "unique_context_tokens": st.unique_tokens,
+                   "schedule": "stream" if plan["schedule"] == 0 else "partition",
+                   "num_workers": plan["num_workers"], "partition_tokens": plan["partition_tokens"],
+                   "timed": "pass1 only" if args.pass1_only else "full step"},
         "seq_steps_per_s": round(st.B / (ms_step * 1e-3), 1),
         "pct_of_peak": round(100.0 * value / PEAK_GBS, 2),
         "algorithmic_bytes_per_step": alg,
-        "roofline": {"bound": "hbm", "kernel": "partition_kernel", "achieved": round(achieved, 2),
+        "roofline": {"bound": "hbm", "kernel": kernel, "achieved": round(achieved, 2),
                      "peak": PEAK_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_GBS, 4),
                      "traffic": traffic, "ms_per_launch": round(ms_pass1, 5)},
         "cpu_baseline": None,

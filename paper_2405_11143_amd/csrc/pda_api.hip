@@ -1,20 +1,22 @@
 // C ABI of the paged decode-attention library (declared in include/pda.h):
-// host-side validation, the split-K plan, and the two kernel launches.
-// Nothing here allocates memory or keeps state between calls.
+// host-side validation, the plan (schedule, workspace), and the launches.
+// Nothing here allocates memory; the only global state is a per-device cache
+// of the compute-unit count.
 #include <math.h>
+
+#include <atomic>
 
 #include "pda.h"
 #include "pda_internal.h"
 
 namespace {
 
-// Split-K policy: partitions of kMaxPartitionTokens, halved (down to
-// kMinPartitionTokens) while the step would have fewer than kMinWorkItems
-// (sequence, KV head, partition) items -- too few to keep 256 compute units
-// busy -- and never longer than the longest context (then there is one
-// partition and no merge pass).  Larger partitions amortise each workgroup's start-up
-// (lengths, block ids, q) over more streamed tiles; on MI355X 2048 tokens
-// measured fastest on all four Llama-3-shaped decode steps.
+// Partition schedule, when the batch is too large for the stream schedule and
+// the caller left the size to the library: partitions of kMaxPartitionTokens,
+// halved (down to kMinPartitionTokens) while the step would have fewer than
+// kMinWorkItems (sequence, KV head, partition) items, and never longer than
+// the longest context.  2048 measured fastest on MI355X for the Llama-3-shaped
+// steps with this schedule.
 constexpr int kMaxPartitionTokens = 2048;
 constexpr int kMinPartitionTokens = 256;
 constexpr int64_t kMinWorkItems = 2048;
@@ -22,10 +24,11 @@ constexpr int64_t kMinWorkItems = 2048;
 int check_problem(const pda_problem* p) {
   if (!p) return PDA_ERR_NULL;
   if (p->num_seqs < 0 || p->num_q_heads < 1 || p->num_kv_heads < 1 || p->num_blocks < 1 ||
-      p->max_blocks_per_seq < 1 || p->max_context_len < 0 || p->partition_tokens < 0)
+      p->max_blocks_per_seq < 1 || p->max_context_len < 0 || p->partition_tokens < 0 || p->num_workers < 0)
     return PDA_ERR_SHAPE;
   if (p->num_q_heads % p->num_kv_heads != 0) return PDA_ERR_SHAPE;
   if (p->partition_tokens % pda::kBlockTokens != 0) return PDA_ERR_SHAPE;
+  if (p->num_workers % pda::kWaves != 0) return PDA_ERR_SHAPE;
   if ((int64_t)p->max_context_len > (int64_t)pda::kBlockTokens * p->max_blocks_per_seq) return PDA_ERR_SHAPE;
   if (p->block_size != pda::kBlockTokens) return PDA_ERR_UNSUPPORTED;
   if (p->head_dim != 64 && p->head_dim != 128) return PDA_ERR_UNSUPPORTED;
@@ -34,19 +37,61 @@ int check_problem(const pda_problem* p) {
 }
 
 struct Plan {
-  int32_t partition_tokens;
-  int32_t num_partitions;  // partitions of the longest context, at least 1 (grid extent)
-  size_t workspace_bytes;
-  size_t part_o_floats;    // offset of part_m in floats
-  size_t part_ml_floats;   // length of part_m (and of part_l) in floats
+  pda_plan_info info;
+  size_t slots;           // partial states (one per head for partitions, G heads for stream)
+  size_t part_o_floats;   // offset of part_m in floats
+  size_t part_ml_floats;  // length of part_m (and of part_l) in floats
 };
+
+// Compute units of the current device, cached per device (an immutable fact).
+hipError_t device_cus(int* cus) {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < 64) {
+    const int c = cache[dev].load(std::memory_order_relaxed);
+    if (c > 0) {
+      *cus = c;
+      return hipSuccess;
+    }
+  }
+  e = hipDeviceGetAttribute(cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < 64) cache[dev].store(*cus, std::memory_order_relaxed);
+  return hipSuccess;
+}
 
 int make_plan(const pda_problem* p, Plan* plan) {
   int rc = check_problem(p);
   if (rc != PDA_OK) return rc;
+  const int G = p->num_q_heads / p->num_kv_heads;
+  const int64_t units = (int64_t)p->num_seqs * p->num_kv_heads;
+  const int64_t max_blocks = ((int64_t)p->max_context_len + pda::kBlockTokens - 1) / pda::kBlockTokens;
+  *plan = Plan{};
+  const bool stream = p->partition_tokens == 0 && p->num_seqs <= pda::kMaxStreamSeqs &&
+                      (int64_t)p->num_seqs * max_blocks < 0x7fffffff;
+  if (stream) {
+    int workers = p->num_workers;
+    if (workers == 0 && p->num_seqs > 0) {
+      int cus = 0, per_cu = 0;
+      if (device_cus(&cus) != hipSuccess) return PDA_ERR_HIP;
+      if (pda::stream_blocks_per_cu(G, p->head_dim, p->num_seqs, &per_cu) != hipSuccess) return PDA_ERR_HIP;
+      workers = cus * (per_cu > 0 ? per_cu : 1) * pda::kWaves;
+    }
+    plan->info.schedule = PDA_SCHEDULE_STREAM;
+    plan->info.num_workers = workers;
+    if (p->num_seqs > 0) {
+      plan->slots = (size_t)units + (size_t)workers;
+      plan->part_o_floats = plan->slots * G * p->head_dim;
+      plan->part_ml_floats = plan->slots * G;
+      plan->info.workspace_bytes =
+          (plan->part_o_floats + 2 * plan->part_ml_floats) * sizeof(float) + (size_t)units * 2 * sizeof(int32_t);
+    }
+    return PDA_OK;
+  }
   int tp = p->partition_tokens;
   if (tp == 0) {
-    const int64_t units = (int64_t)p->num_seqs * p->num_kv_heads;
     const int64_t len = p->max_context_len > 0 ? p->max_context_len : 1;
     tp = kMaxPartitionTokens;
     while (tp > kMinPartitionTokens && units * ((len + tp - 1) / tp) < kMinWorkItems) tp /= 2;
@@ -54,56 +99,67 @@ int make_plan(const pda_problem* p, Plan* plan) {
     if (rounded < tp) tp = rounded;  // the whole context fits one partition
   }
   const int64_t parts = p->max_context_len > 0 ? ((int64_t)p->max_context_len + tp - 1) / tp : 1;
-  const int64_t grid = parts * p->num_seqs * p->num_kv_heads;
-  if (grid > 0x7fffffff) return PDA_ERR_SHAPE;
-  plan->partition_tokens = tp;
-  plan->num_partitions = (int32_t)parts;
+  if (parts * units > 0x7fffffff) return PDA_ERR_SHAPE;
+  plan->info.schedule = PDA_SCHEDULE_PARTITION;
+  plan->info.partition_tokens = tp;
+  plan->info.num_partitions = (int32_t)parts;
   if (parts > 1) {
-    const size_t rows = (size_t)p->num_seqs * p->num_q_heads * (size_t)parts;
-    plan->part_o_floats = rows * p->head_dim;
-    plan->part_ml_floats = rows;
-    plan->workspace_bytes = (plan->part_o_floats + 2 * rows) * sizeof(float);
-  } else {
-    plan->part_o_floats = plan->part_ml_floats = 0;
-    plan->workspace_bytes = 0;
+    plan->slots = (size_t)p->num_seqs * p->num_q_heads * (size_t)parts;
+    plan->part_o_floats = plan->slots * p->head_dim;
+    plan->part_ml_floats = plan->slots;
+    plan->info.workspace_bytes = (plan->part_o_floats + 2 * plan->slots) * sizeof(float);
   }
   return PDA_OK;
 }
 
 bool aligned(const void* ptr, size_t a) { return ((uintptr_t)ptr % a) == 0; }
 
+// Sizes and workspace carving shared by both passes.
+void fill_args(const pda_problem* p, const Plan* plan, void* ws, pda::StepArgs* args) {
+  *args = pda::StepArgs{};
+  float* wsf = static_cast<float*>(ws);
+  if (plan->info.workspace_bytes > 0) {
+    args->part_o = wsf;
+    args->part_m = wsf + plan->part_o_floats;
+    args->part_l = wsf + plan->part_o_floats + plan->part_ml_floats;
+    if (plan->info.schedule == PDA_SCHEDULE_STREAM)
+      args->unit_info = reinterpret_cast<int32_t*>(wsf + plan->part_o_floats + 2 * plan->part_ml_floats);
+  }
+  args->num_seqs = p->num_seqs;
+  args->num_q_heads = p->num_q_heads;
+  args->num_kv_heads = p->num_kv_heads;
+  args->num_blocks = p->num_blocks;
+  args->max_blocks_per_seq = p->max_blocks_per_seq;
+  args->max_context_len = p->max_context_len;
+  args->partition_tokens = plan->info.partition_tokens;
+  args->num_partitions = plan->info.num_partitions;
+  args->num_workers = plan->info.num_workers;
+}
+
 // Validation shared by the entry points that launch pass 1; fills `args`.
 int prepare_step(const pda_problem* p, const void* q, const void* k, const void* v, const int32_t* bt,
                  const int32_t* lens, float scale, float* out, void* ws, size_t ws_bytes, Plan* plan,
                  pda::StepArgs* args) {
-  int rc = make_plan(p, plan);
+  // Everything that needs no device comes first; the plan may query the device.
+  int rc = check_problem(p);
   if (rc != PDA_OK) return rc;
   if (p->num_seqs > 0 && (!q || !k || !v || !bt || !lens || !out)) return PDA_ERR_NULL;
   if (!isfinite(scale)) return PDA_ERR_VALUE;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 4)) return PDA_ERR_ALIGNMENT;
-  if (plan->workspace_bytes > 0) {
-    if (!ws || ws_bytes < plan->workspace_bytes) return PDA_ERR_WORKSPACE;
+  rc = make_plan(p, plan);
+  if (rc != PDA_OK) return rc;
+  if (plan->info.workspace_bytes > 0) {
+    if (!ws || ws_bytes < plan->info.workspace_bytes) return PDA_ERR_WORKSPACE;
     if (!aligned(ws, 16)) return PDA_ERR_ALIGNMENT;
   }
-  float* wsf = static_cast<float*>(ws);
-  *args = pda::StepArgs{static_cast<const uint16_t*>(q),
-                        static_cast<const uint16_t*>(k),
-                        static_cast<const uint16_t*>(v),
-                        bt,
-                        lens,
-                        out,
-                        plan->workspace_bytes ? wsf : nullptr,
-                        plan->workspace_bytes ? wsf + plan->part_o_floats : nullptr,
-                        plan->workspace_bytes ? wsf + plan->part_o_floats + plan->part_ml_floats : nullptr,
-                        scale * 1.4426950408889634f,
-                        p->num_seqs,
-                        p->num_q_heads,
-                        p->num_kv_heads,
-                        p->num_blocks,
-                        p->max_blocks_per_seq,
-                        p->max_context_len,
-                        plan->partition_tokens,
-                        plan->num_partitions};
+  fill_args(p, plan, ws, args);
+  args->q = static_cast<const uint16_t*>(q);
+  args->k = static_cast<const uint16_t*>(k);
+  args->v = static_cast<const uint16_t*>(v);
+  args->table = bt;
+  args->lens = lens;
+  args->out = out;
+  args->scale_log2 = scale * 1.4426950408889634f;
   return PDA_OK;
 }
 
@@ -111,20 +167,22 @@ int prepare_step(const pda_problem* p, const void* q, const void* k, const void*
 
 extern "C" {
 
-int pda_plan(const pda_problem* prob, int32_t* partition_tokens, int32_t* num_partitions,
-             size_t* workspace_bytes) {
+int pda_plan(const pda_problem* prob, pda_plan_info* info) {
+  if (!info) return PDA_ERR_NULL;
   Plan plan;
   int rc = make_plan(prob, &plan);
   if (rc != PDA_OK) return rc;
-  if (partition_tokens) *partition_tokens = plan.partition_tokens;
-  if (num_partitions) *num_partitions = plan.num_partitions;
-  if (workspace_bytes) *workspace_bytes = plan.workspace_bytes;
+  *info = plan.info;
   return PDA_OK;
 }
 
 int pda_workspace_bytes(const pda_problem* prob, size_t* bytes) {
   if (!bytes) return PDA_ERR_NULL;
-  return pda_plan(prob, nullptr, nullptr, bytes);
+  Plan plan;
+  int rc = make_plan(prob, &plan);
+  if (rc != PDA_OK) return rc;
+  *bytes = plan.info.workspace_bytes;
+  return PDA_OK;
 }
 
 int pda_partition_attention(const pda_problem* prob, const void* q, const void* k_cache, const void* v_cache,
@@ -137,36 +195,33 @@ int pda_partition_attention(const pda_problem* prob, const void* q, const void* 
   if (rc != PDA_OK) return rc;
   if (prob->num_seqs == 0) return PDA_OK;
   const int group = prob->num_q_heads / prob->num_kv_heads;
-  if (pda::launch_partition(args, group, prob->head_dim, stream) != hipSuccess) return PDA_ERR_HIP;
-  return PDA_OK;
+  const hipError_t e = plan.info.schedule == PDA_SCHEDULE_STREAM
+                           ? pda::launch_stream(args, group, prob->head_dim, stream)
+                           : pda::launch_partition(args, group, prob->head_dim, stream);
+  return e == hipSuccess ? PDA_OK : PDA_ERR_HIP;
 }
 
 int pda_merge_partitions(const pda_problem* prob, const int32_t* context_lens, float* out, const void* workspace,
                          size_t workspace_bytes, hipStream_t stream) {
-  Plan plan;
-  int rc = make_plan(prob, &plan);
+  int rc = check_problem(prob);
   if (rc != PDA_OK) return rc;
-  if (prob->num_seqs == 0 || plan.workspace_bytes == 0) return PDA_OK;  // nothing was split
+  if (prob->num_seqs == 0) return PDA_OK;
   if (!context_lens || !out) return PDA_ERR_NULL;
-  if (!workspace || workspace_bytes < plan.workspace_bytes) return PDA_ERR_WORKSPACE;
   if (!aligned(workspace, 16) || !aligned(out, 4)) return PDA_ERR_ALIGNMENT;
-  const float* wsf = static_cast<const float*>(workspace);
-  pda::StepArgs args{};
+  Plan plan;
+  rc = make_plan(prob, &plan);
+  if (rc != PDA_OK) return rc;
+  if (plan.info.workspace_bytes == 0) return PDA_OK;  // nothing was split
+  if (!workspace || workspace_bytes < plan.info.workspace_bytes) return PDA_ERR_WORKSPACE;
+  pda::StepArgs args;
+  fill_args(prob, &plan, const_cast<void*>(workspace), &args);
   args.lens = context_lens;
   args.out = out;
-  args.part_o = const_cast<float*>(wsf);
-  args.part_m = const_cast<float*>(wsf + plan.part_o_floats);
-  args.part_l = const_cast<float*>(wsf + plan.part_o_floats + plan.part_ml_floats);
-  args.num_seqs = prob->num_seqs;
-  args.num_q_heads = prob->num_q_heads;
-  args.num_kv_heads = prob->num_kv_heads;
-  args.num_blocks = prob->num_blocks;
-  args.max_blocks_per_seq = prob->max_blocks_per_seq;
-  args.max_context_len = prob->max_context_len;
-  args.partition_tokens = plan.partition_tokens;
-  args.num_partitions = plan.num_partitions;
-  if (pda::launch_merge(args, prob->head_dim, stream) != hipSuccess) return PDA_ERR_HIP;
-  return PDA_OK;
+  const int group = prob->num_q_heads / prob->num_kv_heads;
+  const hipError_t e = plan.info.schedule == PDA_SCHEDULE_STREAM
+                           ? pda::launch_merge_stream(args, group, prob->head_dim, stream)
+                           : pda::launch_merge_partition(args, prob->head_dim, stream);
+  return e == hipSuccess ? PDA_OK : PDA_ERR_HIP;
 }
 
 int pda_decode(const pda_problem* prob, const void* q, const void* k_cache, const void* v_cache,
@@ -211,7 +266,7 @@ const char* pda_status_string(int status) {
     case PDA_ERR_WORKSPACE: return "PDA_ERR_WORKSPACE: workspace missing or smaller than pda_workspace_bytes()";
     case PDA_ERR_ALIGNMENT: return "PDA_ERR_ALIGNMENT: q/k_cache/v_cache/workspace need 16-byte alignment, out 4-byte";
     case PDA_ERR_VALUE: return "PDA_ERR_VALUE: non-finite scale or invalid device contents";
-    case PDA_ERR_HIP: return "PDA_ERR_HIP: a HIP kernel launch failed";
+    case PDA_ERR_HIP: return "PDA_ERR_HIP: a HIP call failed (kernel launch or device query)";
     default: return "unknown pda status";
   }
 }

@@ -1,11 +1,12 @@
-// Pass 2 of paged decode attention: merge per-partition softmax states.
+// Pass 2 of paged decode attention: merge partial softmax states.
 //
-// A context split into partitions p = 0..n-1 leaves, per query head, the
-// partition reference maximum m_p (log2 domain), denominator l_p and
-// unnormalised output O_p.  Softmax over the whole context is recovered
-// exactly by rescaling every partition to the common maximum M = max_p m_p:
-//   out = sum_p 2^(m_p - M) O_p / sum_p 2^(m_p - M) l_p.
-// The output sum runs in ascending p and the denominator in a fixed
+// A context split into pieces k = 0..n-1 (partitions or stream segments)
+// leaves, per query head, the piece's reference maximum m_k (log2 domain),
+// denominator l_k and unnormalised output O_k.  Softmax over the whole
+// context is recovered exactly by rescaling every piece to the common
+// maximum M = max_k m_k:
+//   out = sum_k 2^(m_k - M) O_k / sum_k 2^(m_k - M) l_k.
+// The output sum runs in ascending k and the denominator in a fixed
 // butterfly, so the result is reproducible.  One wavefront per (sequence,
 // query head); each lane owns D/64 output columns.
 #include "pda_internal.h"
@@ -25,59 +26,91 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
+// Merge n pieces whose states sit at index first + k * step (k < n) of
+// part_m / part_l, with outputs at (first + k * step) * D of part_o.
 template <int D>
-__global__ void __launch_bounds__(kWaveSize) merge_kernel(const StepArgs a) {
+__device__ __forceinline__ void merge_pieces(const StepArgs& a, size_t first, size_t step, int n, float* orow) {
   constexpr int PER = D / kWaveSize;
-  constexpr float kNegInf = -__builtin_huge_valf();
-  const int row = blockIdx.x;  // b * Hq + h
-  const int b = row / a.num_q_heads;
   const int lane = threadIdx.x;
-  int L = a.lens[b];
-  L = L < 0 ? 0 : (L > a.max_context_len ? a.max_context_len : L);
-  const int nparts = (L + a.partition_tokens - 1) / a.partition_tokens;
-  if (nparts <= 1) return;  // pass 1 wrote the final row
-  const size_t base = (size_t)row * a.num_partitions;
-  const float* pm = a.part_m + base;
-  const float* pl = a.part_l + base;
-  const float* po = a.part_o + base * D + lane * PER;
-
-  // Partition states are read lane-parallel (lane x holds partition p0 + x),
-  // so the dependent chain is lens -> states -> outputs, whatever nparts is.
-  float M = kNegInf;
-  for (int p0 = 0; p0 < nparts; p0 += kWaveSize)
-    if (p0 + lane < nparts) M = fmaxf(M, pm[p0 + lane]);
+  // States are read lane-parallel (lane x holds piece p0 + x), so the
+  // dependent chain is states -> outputs, whatever n is.
+  float M = -__builtin_huge_valf();
+  for (int p0 = 0; p0 < n; p0 += kWaveSize)
+    if (p0 + lane < n) M = fmaxf(M, a.part_m[first + (p0 + lane) * step]);
   M = wave_max(M);
-
   float acc[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) acc[e] = 0.f;
   float lpart = 0.f;
-  for (int p0 = 0; p0 < nparts; p0 += kWaveSize) {
+  for (int p0 = 0; p0 < n; p0 += kWaveSize) {
     const int p = p0 + lane;
-    const float wgt = p < nparts ? __builtin_amdgcn_exp2f(pm[p] - M) : 0.f;  // 2^(m_p - M)
-    if (p < nparts) lpart = fmaf(wgt, pl[p], lpart);
-    const int n = min(kWaveSize, nparts - p0);
-    for (int x = 0; x < n; ++x) {
+    const size_t idx = first + (size_t)p * step;
+    const float wgt = p < n ? __builtin_amdgcn_exp2f(a.part_m[idx] - M) : 0.f;  // 2^(m_p - M)
+    if (p < n) lpart = fmaf(wgt, a.part_l[idx], lpart);
+    const int cnt = min(kWaveSize, n - p0);
+    for (int x = 0; x < cnt; ++x) {
       const float sc = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, wgt), x));
-      const float* src = po + (size_t)(p0 + x) * D;
+      const float* src = a.part_o + (first + (size_t)(p0 + x) * step) * D + lane * PER;
 #pragma unroll
       for (int e = 0; e < PER; ++e) acc[e] = fmaf(sc, src[e], acc[e]);
     }
   }
   const float lsum = wave_sum(lpart);
-  float* o = a.out + (size_t)row * D + lane * PER;
 #pragma unroll
-  for (int e = 0; e < PER; ++e) o[e] = acc[e] / lsum;
+  for (int e = 0; e < PER; ++e) orow[lane * PER + e] = acc[e] / lsum;
+}
+
+__device__ __forceinline__ int clamped_len(const StepArgs& a, int b) {
+  const int L = a.lens[b];
+  return L < 0 ? 0 : (L > a.max_context_len ? a.max_context_len : L);
+}
+
+// Partition schedule: piece k of row (b, h) at slot row * P + k.
+template <int D>
+__global__ void __launch_bounds__(kWaveSize) merge_partition_kernel(const StepArgs a) {
+  const int row = blockIdx.x;  // b * Hq + h
+  const int L = clamped_len(a, row / a.num_q_heads);
+  const int nparts = (L + a.partition_tokens - 1) / a.partition_tokens;
+  if (nparts <= 1) return;  // pass 1 wrote the final row
+  merge_pieces<D>(a, (size_t)row * a.num_partitions, 1, nparts, a.out + (size_t)row * D);
+}
+
+// Stream schedule: pieces of unit u = b*Hkv + g at slots u + v0 + k, G heads
+// per slot; (v0, n) recorded by pass 1.
+template <int D>
+__global__ void __launch_bounds__(kWaveSize) merge_stream_kernel(const StepArgs a) {
+  const int row = blockIdx.x;  // b * Hq + h
+  const int b = row / a.num_q_heads;
+  const int h = row % a.num_q_heads;
+  const int G = a.num_q_heads / a.num_kv_heads;
+  if (clamped_len(a, b) == 0) return;  // pass 1 wrote the zero row
+  const int u = b * a.num_kv_heads + h / G;
+  const int v0 = a.unit_info[2 * u];
+  const int n = a.unit_info[2 * u + 1];
+  if (n <= 1) return;  // pass 1 wrote the final row
+  merge_pieces<D>(a, ((size_t)u + v0) * G + h % G, (size_t)G, n, a.out + (size_t)row * D);
 }
 
 }  // namespace
 
-hipError_t launch_merge(const StepArgs& a, int head_dim, hipStream_t stream) {
+hipError_t launch_merge_partition(const StepArgs& a, int head_dim, hipStream_t stream) {
   const unsigned grid = (unsigned)a.num_seqs * (unsigned)a.num_q_heads;
   if (head_dim == 64)
-    hipLaunchKernelGGL(merge_kernel<64>, dim3(grid), dim3(kWaveSize), 0, stream, a);
+    hipLaunchKernelGGL(merge_partition_kernel<64>, dim3(grid), dim3(kWaveSize), 0, stream, a);
   else if (head_dim == 128)
-    hipLaunchKernelGGL(merge_kernel<128>, dim3(grid), dim3(kWaveSize), 0, stream, a);
+    hipLaunchKernelGGL(merge_partition_kernel<128>, dim3(grid), dim3(kWaveSize), 0, stream, a);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_merge_stream(const StepArgs& a, int group, int head_dim, hipStream_t stream) {
+  (void)group;
+  const unsigned grid = (unsigned)a.num_seqs * (unsigned)a.num_q_heads;
+  if (head_dim == 64)
+    hipLaunchKernelGGL(merge_stream_kernel<64>, dim3(grid), dim3(kWaveSize), 0, stream, a);
+  else if (head_dim == 128)
+    hipLaunchKernelGGL(merge_stream_kernel<128>, dim3(grid), dim3(kWaveSize), 0, stream, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -25,10 +25,22 @@ EXPORTED = ("pda_plan", "pda_workspace_bytes", "pda_decode", "pda_partition_atte
             "pda_merge_partitions", "pda_validate_host", "pda_status_string")
 
 
+PDA_SCHEDULE_STREAM, PDA_SCHEDULE_PARTITION = 0, 1
+
+
 class pda_problem(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int32) for name in (
         "num_seqs", "num_q_heads", "num_kv_heads", "head_dim", "block_size", "num_blocks",
-        "max_blocks_per_seq", "max_context_len", "partition_tokens")]
+        "max_blocks_per_seq", "max_context_len", "partition_tokens", "num_workers")]
+
+
+class pda_plan_info(ctypes.Structure):
+    _fields_ = [("schedule", ctypes.c_int32), ("partition_tokens", ctypes.c_int32),
+                ("num_partitions", ctypes.c_int32), ("num_workers", ctypes.c_int32),
+                ("workspace_bytes", ctypes.c_size_t)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
 
 
 class PdaError(RuntimeError):
@@ -51,8 +63,7 @@ def load_library(path: str = LIB_PATH):
     lib = ctypes.CDLL(path)
     P = ctypes.POINTER(pda_problem)
     vp, i32, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
-    lib.pda_plan.argtypes = [P, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32),
-                             ctypes.POINTER(sz)]
+    lib.pda_plan.argtypes = [P, ctypes.POINTER(pda_plan_info)]
     lib.pda_workspace_bytes.argtypes = [P, ctypes.POINTER(sz)]
     step = [P, vp, vp, vp, vp, vp, ctypes.c_float, vp, vp, sz, vp]
     lib.pda_decode.argtypes = step
@@ -73,18 +84,20 @@ def pda_status_string(status: int) -> str:
 
 
 def make_problem(num_seqs, num_q_heads, num_kv_heads, head_dim, num_blocks, max_blocks_per_seq,
-                 max_context_len, partition_tokens=0, block_size=16) -> pda_problem:
+                 max_context_len, partition_tokens=0, block_size=16, num_workers=0) -> pda_problem:
     return pda_problem(int(num_seqs), int(num_q_heads), int(num_kv_heads), int(head_dim), int(block_size),
-                       int(num_blocks), int(max_blocks_per_seq), int(max_context_len), int(partition_tokens))
+                       int(num_blocks), int(max_blocks_per_seq), int(max_context_len), int(partition_tokens),
+                       int(num_workers))
 
 
-def pda_plan(prob: pda_problem) -> Tuple[int, int, int]:
-    """(partition_tokens, num_partitions, workspace_bytes) of a problem."""
-    tp, npart, ws = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_size_t()
-    rc = load_library().pda_plan(ctypes.byref(prob), ctypes.byref(tp), ctypes.byref(npart), ctypes.byref(ws))
+def pda_plan(prob: pda_problem) -> dict:
+    """The plan of a problem on the current device: schedule, partition_tokens,
+    num_partitions, num_workers, workspace_bytes."""
+    info = pda_plan_info()
+    rc = load_library().pda_plan(ctypes.byref(prob), ctypes.byref(info))
     if rc != PDA_OK:
         raise PdaError(rc, "pda_plan")
-    return tp.value, npart.value, ws.value
+    return info.as_dict()
 
 
 def pda_workspace_bytes(prob: pda_problem) -> int:
@@ -105,7 +118,7 @@ def pda_validate_host(prob: pda_problem, block_table, context_lens) -> Tuple[int
     return rc, bad.value
 
 
-def _problem_from(q, k_cache, block_table, max_context_len, partition_tokens) -> pda_problem:
+def _problem_from(q, k_cache, block_table, max_context_len, partition_tokens, num_workers) -> pda_problem:
     import torch
 
     if q.dim() != 3 or k_cache.dim() != 5 or block_table.dim() != 2:
@@ -116,7 +129,8 @@ def _problem_from(q, k_cache, block_table, max_context_len, partition_tokens) ->
         raise ValueError("q, k_cache and block_table shapes disagree")
     if max_context_len is None:
         raise ValueError("max_context_len must be given (the host bound on context_lens)")
-    return make_problem(B, Hq, Hkv, D, NB, block_table.shape[1], max_context_len, partition_tokens, BS)
+    return make_problem(B, Hq, Hkv, D, NB, block_table.shape[1], max_context_len, partition_tokens, BS,
+                        num_workers)
 
 
 def _check_tensors(q, k_cache, v_cache, block_table, context_lens, out):
@@ -149,13 +163,13 @@ def _stream_handle(stream, device):
 
 
 def _step(fn_name, q, k_cache, v_cache, block_table, context_lens, scale, out, max_context_len,
-          partition_tokens, workspace, stream):
+          partition_tokens, num_workers, workspace, stream):
     import torch
 
     if out is None:
         out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
     _check_tensors(q, k_cache, v_cache, block_table, context_lens, out)
-    prob = _problem_from(q, k_cache, block_table, max_context_len, partition_tokens)
+    prob = _problem_from(q, k_cache, block_table, max_context_len, partition_tokens, num_workers)
     need = pda_workspace_bytes(prob)
     if workspace is None and need > 0:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
@@ -171,21 +185,25 @@ def _step(fn_name, q, k_cache, v_cache, block_table, context_lens, scale, out, m
 
 
 def pda_decode(q, k_cache, v_cache, block_table, context_lens, scale: float, out=None, *,
-               max_context_len: int, partition_tokens: int = 0, workspace=None, stream=None):
+               max_context_len: int, partition_tokens: int = 0, num_workers: int = 0, workspace=None,
+               stream=None):
     """One decode-attention step (both passes).  Tensors on the GPU:
     q bf16 [B][Hq][D], k_cache bf16 [num_blocks][Hkv][D/8][16][8] (each block's
     keys as D/8 chunks of 16 slots x 8 elements), v_cache bf16 [num_blocks][Hkv][16][D],
     block_table int32 [B][max_blocks], context_lens int32 [B], out fp32 [B][Hq][D].
-    `workspace` (uint8, >= pda_workspace_bytes) is allocated when not given."""
+    `workspace` (uint8, >= pda_workspace_bytes) is allocated when not given.
+    partition_tokens > 0 selects the partition schedule; num_workers > 0 fixes
+    the wavefront count of the stream schedule."""
     return _step("pda_decode", q, k_cache, v_cache, block_table, context_lens, scale, out, max_context_len,
-                 partition_tokens, workspace, stream)
+                 partition_tokens, num_workers, workspace, stream)
 
 
 def pda_partition_attention(q, k_cache, v_cache, block_table, context_lens, scale: float, out=None, *,
-                            max_context_len: int, partition_tokens: int = 0, workspace=None, stream=None):
+                            max_context_len: int, partition_tokens: int = 0, num_workers: int = 0,
+                            workspace=None, stream=None):
     """Pass 1 only (see pda_decode)."""
     return _step("pda_partition_attention", q, k_cache, v_cache, block_table, context_lens, scale, out,
-                 max_context_len, partition_tokens, workspace, stream)
+                 max_context_len, partition_tokens, num_workers, workspace, stream)
 
 
 def pda_merge_partitions(prob: pda_problem, context_lens, out, workspace, stream=None):

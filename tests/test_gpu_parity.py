@@ -37,10 +37,11 @@ def gpu_tensors(st, dev):
     return (torch.from_numpy(st.block_table).to(dev), torch.from_numpy(st.context_lens).to(dev))
 
 
-def run(st, q, k, v, dev, partition_tokens=0, max_context_len=None):
+def run(st, q, k, v, dev, partition_tokens=0, max_context_len=None, num_workers=0):
     bt, lens = gpu_tensors(st, dev)
     mcl = st.max_context_len if max_context_len is None else max_context_len
-    out = pda_decode(q, k, v, bt, lens, st.scale, max_context_len=mcl, partition_tokens=partition_tokens)
+    out = pda_decode(q, k, v, bt, lens, st.scale, max_context_len=mcl, partition_tokens=partition_tokens,
+                     num_workers=num_workers)
     torch.cuda.synchronize()
     return out.cpu().numpy()
 
@@ -89,6 +90,37 @@ def test_split_sizes_agree(dev, partition_tokens):
     st = W.custom_structure(len(lens), 32, 8, 128, lens, seed=5)
     q, k, v = W.fill_values(st, dev, fill="nan")
     check(run(st, q, k, v, dev, partition_tokens), reference(st, q, k, v), f"split Tp={partition_tokens}")
+
+
+@pytest.mark.parametrize("workers", [4, 8, 12, 60, 256, 1000, 4096])
+@pytest.mark.parametrize("Hq,Hkv,D", [(32, 8, 128), (8, 1, 128), (12, 2, 64)], ids=lambda x: str(x))
+def test_stream_worker_counts(dev, workers, Hq, Hkv, D):
+    """Stream schedule with few and many wavefronts: shares that cross many
+    sequence boundaries, contexts cut into many segments, and wavefronts with
+    no work; empty contexts at the start, middle and end of the batch."""
+    lens = [0, 3000, 1, 700, 0, 4096, 513, 17, 1024, 2049, 16, 0]
+    st = W.custom_structure(len(lens), Hq, Hkv, D, lens, seed=21 + workers)
+    q, k, v = W.fill_values(st, dev, fill="nan")
+    got = run(st, q, k, v, dev, 0, num_workers=workers)
+    assert np.all(got[[0, 4, 11]] == 0)
+    check(got, reference(st, q, k, v), f"stream workers={workers} Hq={Hq} Hkv={Hkv} D={D}")
+
+
+@pytest.mark.parametrize("workers", [0, 8, 4096])
+def test_stream_dirty_workspace(dev, workers):
+    """The merge may only read the partial states pass 1 wrote: a workspace
+    full of NaN bytes must not matter (fewer blocks than wavefronts included)."""
+    for lens in ([5, 40, 1, 300, 0, 77], [2000, 3000, 1500]):
+        st = W.custom_structure(len(lens), 16, 4, 128, lens, seed=31)
+        q, k, v = W.fill_values(st, dev, fill="nan")
+        prob = make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq,
+                            st.max_context_len, num_workers=workers)
+        ws = torch.full((pda_plan(prob)["workspace_bytes"],), 0xFF, dtype=torch.uint8, device=dev)
+        bt, ln = gpu_tensors(st, dev)
+        out = pda_decode(q, k, v, bt, ln, st.scale, max_context_len=st.max_context_len, num_workers=workers,
+                         workspace=ws)
+        torch.cuda.synchronize()
+        check(out.cpu().numpy(), reference(st, q, k, v), f"dirty workspace workers={workers} lens={lens}")
 
 
 # ------------------------------------------------------------ invariants --
@@ -160,7 +192,9 @@ def test_empty_and_nonpositive_lengths(dev):
 @pytest.mark.parametrize("name", ["llama3_8b", "long_cot", "llama3_70b_tp8", "shared_prefix"])
 def test_full_config_sampled(dev, name):
     st = W.make_structure(name)
-    print(f"{name}: B={st.B} pool={st.num_blocks} blocks, plan={pda_plan(make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq, st.max_context_len))}", flush=True)
+    plan = pda_plan(make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq,
+                                 st.max_context_len))
+    print(f"{name}: B={st.B} pool={st.num_blocks} blocks, plan={plan}", flush=True)
     q, k, v = W.fill_values(st, dev, fill="nan")
     got = run(st, q, k, v, dev)
     assert np.isfinite(got).all()
