@@ -11,11 +11,11 @@ Prints one JSON line:
   value      algorithmic HBM bytes per step / step time, in GB/s
              (K and V rows of every context token -- shared rows once --
              plus q, the fp32 output, the block-table entries and lengths)
-  roofline   the pass-1 kernel alone (stream_kernel, or partition_kernel when
-             --partition-tokens is set): the same algorithmic bytes / its
-             average launch time (HIP events on its stream), against the
-             8 TB/s HBM peak; `traffic` is the measured HBM bytes per launch
-             from rocprofv3 counters when they were taken on this kernel source
+  roofline   the pass-1 kernel (partition_kernel, with the tiny work-order
+             kernel before it): the same algorithmic bytes / pass-1 time
+             (HIP events on its stream), against the 8 TB/s HBM peak;
+             `traffic` is the measured HBM bytes per launch from rocprofv3
+             counters when they were taken on this kernel source
   cpu_baseline  the fp64 oracle on the host cores, same workload
 """
 from __future__ import annotations
@@ -35,9 +35,9 @@ PEAK_GBS = 8000.0  # MI355X HBM3E, datasheet
 METRIC = "decode-attention HBM GB/s (% of peak) + seq-steps/s, Llama-3-8B shape"
 PROFILES = os.path.join(ROOT, "profiles")
 CSRC = "paper_2405_11143_amd/csrc/"
-# The pass-1 kernel of each schedule and the sources it is compiled from.
+# The dominant kernel and the sources it is compiled from.
+KERNEL = "partition_kernel"
 KERNEL_SOURCES = {
-    "stream_kernel": [CSRC + "pda_stream.hip", CSRC + "pda_wave.h", CSRC + "pda_internal.h"],
     "partition_kernel": [CSRC + "pda_partition.hip", CSRC + "pda_wave.h", CSRC + "pda_internal.h"],
 }
 
@@ -93,9 +93,7 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="llama3_8b")
     ap.add_argument("--partition-tokens", type=int, default=0,
-                    help="> 0: partition schedule with this many tokens per partition")
-    ap.add_argument("--num-workers", type=int, default=0,
-                    help="stream schedule: wavefronts (0 = all the GPU holds at once)")
+                    help="> 0: split-K partition size in tokens (0: the library's choice)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-min-seconds", type=float, default=10.0)
     ap.add_argument("--cpu-max-reps", type=int, default=20)
@@ -135,14 +133,14 @@ def main(argv=None):
     bt = torch.from_numpy(st.block_table).to(dev)
     lens = torch.from_numpy(st.context_lens).to(dev)
     prob = make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq,
-                        st.max_context_len, args.partition_tokens, num_workers=args.num_workers)
+                        st.max_context_len, args.partition_tokens)
     plan = pda_plan(prob)
     ws_bytes = plan["workspace_bytes"]
     out = torch.empty((st.B, st.Hq, st.D), dtype=torch.float32, device=dev)
     ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
     kw = dict(max_context_len=st.max_context_len, partition_tokens=args.partition_tokens,
-              num_workers=args.num_workers, workspace=ws, stream=stream)
+              workspace=ws, stream=stream)
 
     def step():
         pda_decode(q, k, v, bt, lens, st.scale, out, **kw)
@@ -171,7 +169,7 @@ def main(argv=None):
     alg = st.algorithmic_bytes()
     value = alg / (ms_step * 1e-3) / 1e9
     achieved = alg / (ms_pass1 * 1e-3) / 1e9
-    kernel = "stream_kernel" if plan["schedule"] == 0 else "partition_kernel"
+    kernel = KERNEL
     traffic = measured_traffic(kernel, args.config)
     cfg = W.CONFIGS[args.config]
     result = {
@@ -191,8 +189,7 @@ def main(argv=None):
                    "kv_heads": st.Hkv, "head_dim": st.D, "block_size": st.block_size,
                    "pool_blocks": st.num_blocks, "context_tokens": st.logical_tokens,
                    "unique_context_tokens": st.unique_tokens,
-                   "schedule": "stream" if plan["schedule"] == 0 else "partition",
-                   "num_workers": plan["num_workers"], "partition_tokens": plan["partition_tokens"],
+                   "partition_tokens": plan["partition_tokens"], "partitions": plan["num_partitions"],
                    "timed": "pass1 only" if args.pass1_only else "full step"},
         "seq_steps_per_s": round(st.B / (ms_step * 1e-3), 1),
         "pct_of_peak": round(100.0 * value / PEAK_GBS, 2),

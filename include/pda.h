@@ -34,21 +34,19 @@
  * Pool slots past a sequence's context (the tail of its last block) and pool
  * blocks no sequence references are never used, whatever they hold.
  *
- * Schedules.  With the default stream schedule the whole step's work --
- * every (sequence, KV head, 16-token block) -- is cut into equal contiguous
- * shares, one per wavefront the GPU holds at once; a share crosses sequence
- * boundaries, and every context that spans several shares is finished by a
- * merge pass over the partial softmax states.  With the partition schedule
- * (chosen by setting partition_tokens) each context is split into
- * partitions of that many tokens instead.  The pieces depend only on the
- * lengths and on the descriptor (and, for the stream schedule, the number of
- * wavefronts), never on physical block ids or timing, so for a given input
- * the output is bit-for-bit reproducible and independent of where blocks sit
- * in the pool.
+ * Long contexts are split into partitions of `partition_tokens` tokens that
+ * are processed independently; a second pass merges the partial softmax
+ * states.  Pass 1 runs one workgroup per (partition, sequence, KV head),
+ * largest partition first (a small kernel sorts the items by size on the
+ * GPU).  The partition size depends only on the problem descriptor and the
+ * arithmetic of an item only on its data, never on physical block ids,
+ * timing or the order the items run in, so for a given descriptor the output
+ * is bit-for-bit reproducible and independent of where blocks sit in the
+ * pool.
  *
  * Ownership and errors.  The caller owns every buffer; the library allocates
- * nothing.  Its only global state is a per-device cache of immutable facts
- * (the compute-unit count), so concurrent calls are safe.
+ * nothing and keeps no state, so concurrent calls (with separate workspaces)
+ * are safe.
  * Every entry point validates its scalar arguments and pointers on the host
  * and returns a pda_status without touching the GPU when they are invalid.
  * Work is enqueued asynchronously on `stream` (NULL = the null stream); a
@@ -92,56 +90,46 @@ typedef struct pda_problem {
   int32_t num_blocks;         /* rows of k_cache / v_cache, >= 1 */
   int32_t max_blocks_per_seq; /* row stride of block_table, >= 1 */
   int32_t max_context_len;    /* host-known bound on context_lens[]; 0 <= it <= 16*max_blocks_per_seq */
-  int32_t partition_tokens;   /* 0: stream schedule (the default); otherwise the partition schedule
-                                 with partitions of this many tokens, a positive multiple of 16 */
-  int32_t num_workers;        /* stream schedule: wavefronts sharing the work, a positive multiple of
-                                 4; 0 = as many as the current device holds at once */
+  int32_t partition_tokens;   /* split-K partition size: 0 lets the library choose, otherwise a
+                                 positive multiple of 16 */
 } pda_problem;
-
-enum pda_schedule {
-  PDA_SCHEDULE_STREAM = 0,    /* equal shares of all blocks, one per wavefront */
-  PDA_SCHEDULE_PARTITION = 1  /* one workgroup per (partition, sequence, KV head) */
-};
 
 /* What pda_decode will do for a descriptor. */
 typedef struct pda_plan_info {
-  int32_t schedule;           /* a pda_schedule value */
-  int32_t partition_tokens;   /* partition schedule: tokens per partition (0 otherwise) */
-  int32_t num_partitions;     /* partition schedule: partitions of the longest context (0 otherwise) */
-  int32_t num_workers;        /* stream schedule: wavefronts (0 otherwise) */
-  size_t workspace_bytes;     /* bytes of workspace the step needs (may be 0) */
+  int32_t partition_tokens;   /* tokens per partition */
+  int32_t num_partitions;     /* partitions of the longest context */
+  size_t workspace_bytes;     /* workspace the step needs: the work order (4 bytes per item) and,
+                                 when a context spans several partitions, the partial states;
+                                 0 only for an empty batch */
 } pda_plan_info;
 
-/* Plan `prob` for the current HIP device.  The stream schedule is used when
- * partition_tokens is 0 and num_seqs <= 8192 (with larger batches the library
- * picks partitions itself); with num_workers = 0 it asks the current device
- * for its compute units and the kernel's occupancy.  Returns PDA_OK, the
- * validation error of the descriptor, or PDA_ERR_HIP if that query fails. */
+/* Plan `prob`.  Returns PDA_OK or the validation error of the descriptor. */
 int pda_plan(const pda_problem *prob, pda_plan_info *plan);
 
-/* Workspace bytes pda_decode needs for `prob` on the current device (0 when none). */
+/* Workspace bytes pda_decode needs for `prob` (0 only for an empty batch). */
 int pda_workspace_bytes(const pda_problem *prob, size_t *bytes);
 
 /* One decode-attention step for the whole batch: pda_partition_attention
  * followed by pda_merge_partitions on the same stream.  `scale` is the
  * softmax scale (usually 1/sqrt(head_dim)); it must be finite.  `workspace`
- * may be NULL when pda_workspace_bytes() is 0. */
+ * (any contents) must hold pda_workspace_bytes() bytes; it may be NULL for
+ * an empty batch.  Calls that overlap on the GPU need separate workspaces. */
 int pda_decode(const pda_problem *prob, const void *q, const void *k_cache, const void *v_cache,
                const int32_t *block_table, const int32_t *context_lens, float scale, float *out,
                void *workspace, size_t workspace_bytes, hipStream_t stream);
 
-/* Pass 1 alone: attention of every piece of every context.  Rows of contexts
- * processed in one piece (and of empty contexts) are final in `out` after
- * this pass; the others are left as partial softmax states in `workspace`. */
+/* Pass 1 alone (the work-order kernel, then one workgroup per partition):
+ * rows of contexts that fit one partition, and of empty contexts, are final
+ * in `out` after this pass; the others are left as partial softmax states in
+ * `workspace`. */
 int pda_partition_attention(const pda_problem *prob, const void *q, const void *k_cache,
                             const void *v_cache, const int32_t *block_table,
                             const int32_t *context_lens, float scale, float *out,
                             void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Pass 2 alone: merge the partial states that pass 1 left in `workspace` into
- * `out` for every context processed in more than one piece, in ascending
- * piece order.  Must follow pass 1 for the same descriptor, lengths and
- * device. */
+ * `out` for every context with more than one partition, in ascending
+ * partition order.  Must follow pass 1 for the same descriptor and lengths. */
 int pda_merge_partitions(const pda_problem *prob, const int32_t *context_lens, float *out,
                          const void *workspace, size_t workspace_bytes, hipStream_t stream);
 

@@ -5,7 +5,6 @@ step's attention of every sequence's new query token over its paged KV cache,
 with grouped-query heads, as hand-written HIP kernels behind a C ABI
 (include/pda.h).  This package is the thin Python binding of that ABI.
 """
-from .pda import (EXPORTED, LIB_PATH, PDA_SCHEDULE_PARTITION, PDA_SCHEDULE_STREAM, PdaError,  # noqa: F401
-                  load_library, make_problem, pda_decode, pda_merge_partitions, pda_partition_attention,
-                  pda_plan, pda_plan_info, pda_problem, pda_status_string, pda_validate_host,
-                  pda_workspace_bytes)
+from .pda import (EXPORTED, LIB_PATH, PdaError, load_library, make_problem, pda_decode,  # noqa: F401
+                  pda_merge_partitions, pda_partition_attention, pda_plan, pda_plan_info, pda_problem,
+                  pda_status_string, pda_validate_host, pda_workspace_bytes)

@@ -1,34 +1,40 @@
 // C ABI of the paged decode-attention library (declared in include/pda.h):
-// host-side validation, the plan (schedule, workspace), and the launches.
-// Nothing here allocates memory; the only global state is a per-device cache
-// of the compute-unit count.
+// host-side validation, the plan (partition size, workspace), and the
+// launches.  Nothing here allocates memory or keeps state between calls.
 #include <math.h>
 
-#include <atomic>
+#include <algorithm>
 
 #include "pda.h"
 #include "pda_internal.h"
 
 namespace {
 
-// Partition schedule, when the batch is too large for the stream schedule and
-// the caller left the size to the library: partitions of kMaxPartitionTokens,
-// halved (down to kMinPartitionTokens) while the step would have fewer than
-// kMinWorkItems (sequence, KV head, partition) items, and never longer than
-// the longest context.  2048 measured fastest on MI355X for the Llama-3-shaped
-// steps with this schedule.
-constexpr int kMaxPartitionTokens = 2048;
+// Partition size when the caller leaves it to the library.  Pass 1 runs its
+// items largest first, a greedy schedule that ends at most one item's
+// duration after the ideal one, so an item should be short next to the work
+// each of the kConcurrentItems workgroups the GPU runs at once has to do;
+// longer items amortise each workgroup's start-up (order, length, block ids,
+// q) over more streamed tiles.  With only max_context_len on the host, the
+// work is estimated as B * Hkv * max_context_len / 2 tokens (the mean of
+// contexts spread up to the maximum), and the partition is that share rounded
+// up to kPartitionQuantum tokens, within [kMinPartitionTokens,
+// kMaxPartitionTokens] and never longer than the longest context (then there
+// is one partition and no merge pass).  On MI355X this picks the fastest or
+// within 1% of the fastest of the sizes measured on the four Llama-3-shaped
+// decode steps; above 4096 tokens the step slowed down on all of them.
+constexpr int kMaxPartitionTokens = 4096;
 constexpr int kMinPartitionTokens = 256;
-constexpr int64_t kMinWorkItems = 2048;
+constexpr int kPartitionQuantum = 256;
+constexpr int64_t kConcurrentItems = 768;  // 256 compute units x 3 workgroups of 4 wavefronts
 
 int check_problem(const pda_problem* p) {
   if (!p) return PDA_ERR_NULL;
   if (p->num_seqs < 0 || p->num_q_heads < 1 || p->num_kv_heads < 1 || p->num_blocks < 1 ||
-      p->max_blocks_per_seq < 1 || p->max_context_len < 0 || p->partition_tokens < 0 || p->num_workers < 0)
+      p->max_blocks_per_seq < 1 || p->max_context_len < 0 || p->partition_tokens < 0)
     return PDA_ERR_SHAPE;
   if (p->num_q_heads % p->num_kv_heads != 0) return PDA_ERR_SHAPE;
   if (p->partition_tokens % pda::kBlockTokens != 0) return PDA_ERR_SHAPE;
-  if (p->num_workers % pda::kWaves != 0) return PDA_ERR_SHAPE;
   if ((int64_t)p->max_context_len > (int64_t)pda::kBlockTokens * p->max_blocks_per_seq) return PDA_ERR_SHAPE;
   if (p->block_size != pda::kBlockTokens) return PDA_ERR_UNSUPPORTED;
   if (p->head_dim != 64 && p->head_dim != 128) return PDA_ERR_UNSUPPORTED;
@@ -38,76 +44,33 @@ int check_problem(const pda_problem* p) {
 
 struct Plan {
   pda_plan_info info;
-  size_t slots;           // partial states (one per head for partitions, G heads for stream)
-  size_t part_o_floats;   // offset of part_m in floats
-  size_t part_ml_floats;  // length of part_m (and of part_l) in floats
+  size_t items;           // P * B * Hkv work items (pass-1 workgroups)
+  size_t slots;           // partial states, one per (sequence, query head, partition); 0 when P == 1
 };
-
-// Compute units of the current device, cached per device (an immutable fact).
-hipError_t device_cus(int* cus) {
-  static std::atomic<int> cache[64];
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  if (dev >= 0 && dev < 64) {
-    const int c = cache[dev].load(std::memory_order_relaxed);
-    if (c > 0) {
-      *cus = c;
-      return hipSuccess;
-    }
-  }
-  e = hipDeviceGetAttribute(cus, hipDeviceAttributeMultiprocessorCount, dev);
-  if (e != hipSuccess) return e;
-  if (dev >= 0 && dev < 64) cache[dev].store(*cus, std::memory_order_relaxed);
-  return hipSuccess;
-}
 
 int make_plan(const pda_problem* p, Plan* plan) {
   int rc = check_problem(p);
   if (rc != PDA_OK) return rc;
-  const int G = p->num_q_heads / p->num_kv_heads;
   const int64_t units = (int64_t)p->num_seqs * p->num_kv_heads;
-  const int64_t max_blocks = ((int64_t)p->max_context_len + pda::kBlockTokens - 1) / pda::kBlockTokens;
-  *plan = Plan{};
-  const bool stream = p->partition_tokens == 0 && p->num_seqs <= pda::kMaxStreamSeqs &&
-                      (int64_t)p->num_seqs * max_blocks < 0x7fffffff;
-  if (stream) {
-    int workers = p->num_workers;
-    if (workers == 0 && p->num_seqs > 0) {
-      int cus = 0, per_cu = 0;
-      if (device_cus(&cus) != hipSuccess) return PDA_ERR_HIP;
-      if (pda::stream_blocks_per_cu(G, p->head_dim, p->num_seqs, &per_cu) != hipSuccess) return PDA_ERR_HIP;
-      workers = cus * (per_cu > 0 ? per_cu : 1) * pda::kWaves;
-    }
-    plan->info.schedule = PDA_SCHEDULE_STREAM;
-    plan->info.num_workers = workers;
-    if (p->num_seqs > 0) {
-      plan->slots = (size_t)units + (size_t)workers;
-      plan->part_o_floats = plan->slots * G * p->head_dim;
-      plan->part_ml_floats = plan->slots * G;
-      plan->info.workspace_bytes =
-          (plan->part_o_floats + 2 * plan->part_ml_floats) * sizeof(float) + (size_t)units * 2 * sizeof(int32_t);
-    }
-    return PDA_OK;
-  }
   int tp = p->partition_tokens;
   if (tp == 0) {
     const int64_t len = p->max_context_len > 0 ? p->max_context_len : 1;
-    tp = kMaxPartitionTokens;
-    while (tp > kMinPartitionTokens && units * ((len + tp - 1) / tp) < kMinWorkItems) tp /= 2;
+    const int64_t share = (units * len / 2 + kConcurrentItems - 1) / kConcurrentItems;
+    const int64_t quanta = (share + kPartitionQuantum - 1) / kPartitionQuantum;
+    tp = (int)std::min<int64_t>(kMaxPartitionTokens, std::max<int64_t>(kMinPartitionTokens, quanta * kPartitionQuantum));
     const int rounded = (int)((len + pda::kBlockTokens - 1) / pda::kBlockTokens * pda::kBlockTokens);
     if (rounded < tp) tp = rounded;  // the whole context fits one partition
   }
   const int64_t parts = p->max_context_len > 0 ? ((int64_t)p->max_context_len + tp - 1) / tp : 1;
-  if (parts * units > 0x7fffffff) return PDA_ERR_SHAPE;
-  plan->info.schedule = PDA_SCHEDULE_PARTITION;
+  if (parts * units > 0x7fffffff || parts * p->num_seqs > 0x7fffffff) return PDA_ERR_SHAPE;
+  *plan = Plan{};
   plan->info.partition_tokens = tp;
   plan->info.num_partitions = (int32_t)parts;
-  if (parts > 1) {
-    plan->slots = (size_t)p->num_seqs * p->num_q_heads * (size_t)parts;
-    plan->part_o_floats = plan->slots * p->head_dim;
-    plan->part_ml_floats = plan->slots;
-    plan->info.workspace_bytes = (plan->part_o_floats + 2 * plan->slots) * sizeof(float);
+  if (p->num_seqs > 0) {
+    plan->items = (size_t)(parts * units);
+    plan->slots = parts > 1 ? (size_t)p->num_seqs * p->num_q_heads * (size_t)parts : 0;
+    // partial states (O, m, l) first, then the work order
+    plan->info.workspace_bytes = plan->slots * (p->head_dim + 2) * sizeof(float) + plan->items * sizeof(int32_t);
   }
   return PDA_OK;
 }
@@ -119,11 +82,12 @@ void fill_args(const pda_problem* p, const Plan* plan, void* ws, pda::StepArgs* 
   *args = pda::StepArgs{};
   float* wsf = static_cast<float*>(ws);
   if (plan->info.workspace_bytes > 0) {
-    args->part_o = wsf;
-    args->part_m = wsf + plan->part_o_floats;
-    args->part_l = wsf + plan->part_o_floats + plan->part_ml_floats;
-    if (plan->info.schedule == PDA_SCHEDULE_STREAM)
-      args->unit_info = reinterpret_cast<int32_t*>(wsf + plan->part_o_floats + 2 * plan->part_ml_floats);
+    if (plan->slots > 0) {
+      args->part_o = wsf;
+      args->part_m = wsf + plan->slots * p->head_dim;
+      args->part_l = wsf + plan->slots * (p->head_dim + 1);
+    }
+    args->order = reinterpret_cast<int32_t*>(wsf + plan->slots * (p->head_dim + 2));
   }
   args->num_seqs = p->num_seqs;
   args->num_q_heads = p->num_q_heads;
@@ -133,7 +97,6 @@ void fill_args(const pda_problem* p, const Plan* plan, void* ws, pda::StepArgs* 
   args->max_context_len = p->max_context_len;
   args->partition_tokens = plan->info.partition_tokens;
   args->num_partitions = plan->info.num_partitions;
-  args->num_workers = plan->info.num_workers;
 }
 
 // Validation shared by the entry points that launch pass 1; fills `args`.
@@ -195,10 +158,9 @@ int pda_partition_attention(const pda_problem* prob, const void* q, const void* 
   if (rc != PDA_OK) return rc;
   if (prob->num_seqs == 0) return PDA_OK;
   const int group = prob->num_q_heads / prob->num_kv_heads;
-  const hipError_t e = plan.info.schedule == PDA_SCHEDULE_STREAM
-                           ? pda::launch_stream(args, group, prob->head_dim, stream)
-                           : pda::launch_partition(args, group, prob->head_dim, stream);
-  return e == hipSuccess ? PDA_OK : PDA_ERR_HIP;
+  if (pda::launch_order(args, stream) != hipSuccess) return PDA_ERR_HIP;
+  if (pda::launch_partition(args, group, prob->head_dim, stream) != hipSuccess) return PDA_ERR_HIP;
+  return PDA_OK;
 }
 
 int pda_merge_partitions(const pda_problem* prob, const int32_t* context_lens, float* out, const void* workspace,
@@ -211,17 +173,13 @@ int pda_merge_partitions(const pda_problem* prob, const int32_t* context_lens, f
   Plan plan;
   rc = make_plan(prob, &plan);
   if (rc != PDA_OK) return rc;
-  if (plan.info.workspace_bytes == 0) return PDA_OK;  // nothing was split
+  if (plan.slots == 0) return PDA_OK;  // nothing was split
   if (!workspace || workspace_bytes < plan.info.workspace_bytes) return PDA_ERR_WORKSPACE;
   pda::StepArgs args;
   fill_args(prob, &plan, const_cast<void*>(workspace), &args);
   args.lens = context_lens;
   args.out = out;
-  const int group = prob->num_q_heads / prob->num_kv_heads;
-  const hipError_t e = plan.info.schedule == PDA_SCHEDULE_STREAM
-                           ? pda::launch_merge_stream(args, group, prob->head_dim, stream)
-                           : pda::launch_merge_partition(args, prob->head_dim, stream);
-  return e == hipSuccess ? PDA_OK : PDA_ERR_HIP;
+  return pda::launch_merge(args, prob->head_dim, stream) == hipSuccess ? PDA_OK : PDA_ERR_HIP;
 }
 
 int pda_decode(const pda_problem* prob, const void* q, const void* k_cache, const void* v_cache,
@@ -266,7 +224,7 @@ const char* pda_status_string(int status) {
     case PDA_ERR_WORKSPACE: return "PDA_ERR_WORKSPACE: workspace missing or smaller than pda_workspace_bytes()";
     case PDA_ERR_ALIGNMENT: return "PDA_ERR_ALIGNMENT: q/k_cache/v_cache/workspace need 16-byte alignment, out 4-byte";
     case PDA_ERR_VALUE: return "PDA_ERR_VALUE: non-finite scale or invalid device contents";
-    case PDA_ERR_HIP: return "PDA_ERR_HIP: a HIP call failed (kernel launch or device query)";
+    case PDA_ERR_HIP: return "PDA_ERR_HIP: a HIP kernel launch failed";
     default: return "unknown pda status";
   }
 }

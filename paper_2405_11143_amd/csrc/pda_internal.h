@@ -9,11 +9,12 @@
 
 namespace pda {
 
-constexpr int kBlockTokens = 16;     // tokens per KV-cache block
-constexpr int kWaveSize = 64;        // CDNA wavefront
-constexpr int kWaves = 4;            // wavefronts per workgroup
-constexpr int kMaxGroup = 16;        // query heads per KV head handled by one MFMA row tile
-constexpr int kMaxStreamSeqs = 8192; // stream schedule keeps per-sequence block prefix sums in LDS
+constexpr int kBlockTokens = 16;  // tokens per KV-cache block
+constexpr int kWaveSize = 64;     // CDNA wavefront
+constexpr int kWaves = 4;         // wavefronts per partition workgroup
+constexpr int kMaxGroup = 16;     // query heads per KV head handled by one MFMA row tile
+constexpr int kOrderThreads = 1024;  // the work-order kernel is one workgroup of this size
+constexpr int kOrderBuckets = 256;   // size classes of its counting sort (partition blocks, capped)
 
 // Kernel arguments for one decode step (passed by value).
 struct StepArgs {
@@ -23,13 +24,10 @@ struct StepArgs {
   const int32_t* table;    // int32 [B][max_blocks_per_seq]
   const int32_t* lens;     // int32 [B]
   float* out;              // fp32 [B][Hq][D]
-  // Partial softmax states.  Partition schedule: slot = (b*Hq + h)*P + p, one
-  // head per slot.  Stream schedule: slot = unit + wave (unit = b*Hkv + g),
-  // G heads per slot.
-  float* part_o;           // fp32 [slots][D]  unnormalised outputs
-  float* part_m;           // fp32 [slots]     reference max, log2 domain
-  float* part_l;           // fp32 [slots]     softmax denominators
-  int32_t* unit_info;      // stream schedule: int32 [B*Hkv][2] = (first wave, segments)
+  int32_t* order;          // int32 [P*B*Hkv]: work items, largest partition first
+  float* part_o;           // fp32 [B*Hq*P][D]  unnormalised partition outputs (P > 1)
+  float* part_m;           // fp32 [B*Hq*P]     partition reference max, log2 domain
+  float* part_l;           // fp32 [B*Hq*P]     partition softmax denominators
   float scale_log2;        // softmax scale * log2(e)
   int32_t num_seqs;        // B
   int32_t num_q_heads;     // Hq
@@ -37,9 +35,8 @@ struct StepArgs {
   int32_t num_blocks;
   int32_t max_blocks_per_seq;
   int32_t max_context_len;
-  int32_t partition_tokens;  // partition schedule: T_p, multiple of 16
-  int32_t num_partitions;    // partition schedule: P = max(1, ceil(max_context_len / T_p))
-  int32_t num_workers;       // stream schedule: wavefronts sharing the work (multiple of kWaves)
+  int32_t partition_tokens;  // T_p, multiple of 16
+  int32_t num_partitions;    // P = max(1, ceil(max_context_len / T_p))
 };
 
 // Calls f(integral_constant<G>, integral_constant<D>) for the runtime (group, head_dim).
@@ -60,14 +57,8 @@ hipError_t dispatch_gd(int group, int head_dim, F&& f) {
 }
 
 // Launchers (asynchronous; return the hipGetLastError() of the launch).
+hipError_t launch_order(const StepArgs& a, hipStream_t stream);
 hipError_t launch_partition(const StepArgs& a, int group, int head_dim, hipStream_t stream);
-hipError_t launch_stream(const StepArgs& a, int group, int head_dim, hipStream_t stream);
-hipError_t launch_merge_partition(const StepArgs& a, int head_dim, hipStream_t stream);
-hipError_t launch_merge_stream(const StepArgs& a, int group, int head_dim, hipStream_t stream);
-
-// Stream schedule: dynamic LDS bytes of pass 1 and the number of its
-// workgroups one compute unit holds at once (HIP occupancy query).
-size_t stream_lds_bytes(int num_seqs);
-hipError_t stream_blocks_per_cu(int group, int head_dim, int num_seqs, int* blocks);
+hipError_t launch_merge(const StepArgs& a, int head_dim, hipStream_t stream);
 
 }  // namespace pda

@@ -1,10 +1,9 @@
 // Pass 2 of paged decode attention: merge partial softmax states.
 //
-// A context split into pieces k = 0..n-1 (partitions or stream segments)
-// leaves, per query head, the piece's reference maximum m_k (log2 domain),
-// denominator l_k and unnormalised output O_k.  Softmax over the whole
-// context is recovered exactly by rescaling every piece to the common
-// maximum M = max_k m_k:
+// A context split into partitions k = 0..n-1 leaves, per query head, the
+// partition's reference maximum m_k (log2 domain), denominator l_k and
+// unnormalised output O_k.  Softmax over the whole context is recovered
+// exactly by rescaling every partition to the common maximum M = max_k m_k:
 //   out = sum_k 2^(m_k - M) O_k / sum_k 2^(m_k - M) l_k.
 // The output sum runs in ascending k and the denominator in a fixed
 // butterfly, so the result is reproducible.  One wavefront per (sequence,
@@ -26,13 +25,13 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
-// Merge n pieces whose states sit at index first + k * step (k < n) of
+// Merge n partitions whose states sit at index first + k * step (k < n) of
 // part_m / part_l, with outputs at (first + k * step) * D of part_o.
 template <int D>
-__device__ __forceinline__ void merge_pieces(const StepArgs& a, size_t first, size_t step, int n, float* orow) {
+__device__ __forceinline__ void merge_partitions(const StepArgs& a, size_t first, size_t step, int n, float* orow) {
   constexpr int PER = D / kWaveSize;
   const int lane = threadIdx.x;
-  // States are read lane-parallel (lane x holds piece p0 + x), so the
+  // States are read lane-parallel (lane x holds partition p0 + x), so the
   // dependent chain is states -> outputs, whatever n is.
   float M = -__builtin_huge_valf();
   for (int p0 = 0; p0 < n; p0 += kWaveSize)
@@ -65,52 +64,24 @@ __device__ __forceinline__ int clamped_len(const StepArgs& a, int b) {
   return L < 0 ? 0 : (L > a.max_context_len ? a.max_context_len : L);
 }
 
-// Partition schedule: piece k of row (b, h) at slot row * P + k.
+// Partition k of row (b, h) sits at slot row * P + k.
 template <int D>
-__global__ void __launch_bounds__(kWaveSize) merge_partition_kernel(const StepArgs a) {
+__global__ void __launch_bounds__(kWaveSize) merge_kernel(const StepArgs a) {
   const int row = blockIdx.x;  // b * Hq + h
   const int L = clamped_len(a, row / a.num_q_heads);
   const int nparts = (L + a.partition_tokens - 1) / a.partition_tokens;
   if (nparts <= 1) return;  // pass 1 wrote the final row
-  merge_pieces<D>(a, (size_t)row * a.num_partitions, 1, nparts, a.out + (size_t)row * D);
-}
-
-// Stream schedule: pieces of unit u = b*Hkv + g at slots u + v0 + k, G heads
-// per slot; (v0, n) recorded by pass 1.
-template <int D>
-__global__ void __launch_bounds__(kWaveSize) merge_stream_kernel(const StepArgs a) {
-  const int row = blockIdx.x;  // b * Hq + h
-  const int b = row / a.num_q_heads;
-  const int h = row % a.num_q_heads;
-  const int G = a.num_q_heads / a.num_kv_heads;
-  if (clamped_len(a, b) == 0) return;  // pass 1 wrote the zero row
-  const int u = b * a.num_kv_heads + h / G;
-  const int v0 = a.unit_info[2 * u];
-  const int n = a.unit_info[2 * u + 1];
-  if (n <= 1) return;  // pass 1 wrote the final row
-  merge_pieces<D>(a, ((size_t)u + v0) * G + h % G, (size_t)G, n, a.out + (size_t)row * D);
+  merge_partitions<D>(a, (size_t)row * a.num_partitions, 1, nparts, a.out + (size_t)row * D);
 }
 
 }  // namespace
 
-hipError_t launch_merge_partition(const StepArgs& a, int head_dim, hipStream_t stream) {
+hipError_t launch_merge(const StepArgs& a, int head_dim, hipStream_t stream) {
   const unsigned grid = (unsigned)a.num_seqs * (unsigned)a.num_q_heads;
   if (head_dim == 64)
-    hipLaunchKernelGGL(merge_partition_kernel<64>, dim3(grid), dim3(kWaveSize), 0, stream, a);
+    hipLaunchKernelGGL(merge_kernel<64>, dim3(grid), dim3(kWaveSize), 0, stream, a);
   else if (head_dim == 128)
-    hipLaunchKernelGGL(merge_partition_kernel<128>, dim3(grid), dim3(kWaveSize), 0, stream, a);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
-}
-
-hipError_t launch_merge_stream(const StepArgs& a, int group, int head_dim, hipStream_t stream) {
-  (void)group;
-  const unsigned grid = (unsigned)a.num_seqs * (unsigned)a.num_q_heads;
-  if (head_dim == 64)
-    hipLaunchKernelGGL(merge_stream_kernel<64>, dim3(grid), dim3(kWaveSize), 0, stream, a);
-  else if (head_dim == 128)
-    hipLaunchKernelGGL(merge_stream_kernel<128>, dim3(grid), dim3(kWaveSize), 0, stream, a);
+    hipLaunchKernelGGL(merge_kernel<128>, dim3(grid), dim3(kWaveSize), 0, stream, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

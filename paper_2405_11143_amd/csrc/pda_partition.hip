@@ -1,8 +1,8 @@
-// Pass 1, partition schedule: one workgroup per (partition of a context,
-// sequence, KV head).
+// Pass 1: one workgroup per (partition of a context, sequence, KV head),
+// taken in the order pda_order.hip computed (largest partition first).
 //
-// Used when the caller fixes the split-K partition size.  The partition's
-// 16-token blocks are split into 4 contiguous runs, one per wavefront; each
+// The partition's 16-token blocks are split into 4 contiguous runs, one per
+// wavefront; each
 // wavefront streams its run with WaveAttention (pda_wave.h) and the 4 states
 // are merged through LDS in a fixed order.  The workgroup leaves the final
 // output rows (context fits one partition) or a partial softmax state (max,
@@ -29,7 +29,7 @@ partition_kernel(const StepArgs a) {
 
   const int Hkv = a.num_kv_heads;
   const int Hq = a.num_q_heads;
-  const int item = blockIdx.x;
+  const int item = a.order[blockIdx.x];  // (p * B + b) * Hkv + g
   const int g = item % Hkv;
   const int b = (item / Hkv) % a.num_seqs;
   const int p = item / (Hkv * a.num_seqs);

@@ -25,18 +25,14 @@ EXPORTED = ("pda_plan", "pda_workspace_bytes", "pda_decode", "pda_partition_atte
             "pda_merge_partitions", "pda_validate_host", "pda_status_string")
 
 
-PDA_SCHEDULE_STREAM, PDA_SCHEDULE_PARTITION = 0, 1
-
-
 class pda_problem(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int32) for name in (
         "num_seqs", "num_q_heads", "num_kv_heads", "head_dim", "block_size", "num_blocks",
-        "max_blocks_per_seq", "max_context_len", "partition_tokens", "num_workers")]
+        "max_blocks_per_seq", "max_context_len", "partition_tokens")]
 
 
 class pda_plan_info(ctypes.Structure):
-    _fields_ = [("schedule", ctypes.c_int32), ("partition_tokens", ctypes.c_int32),
-                ("num_partitions", ctypes.c_int32), ("num_workers", ctypes.c_int32),
+    _fields_ = [("partition_tokens", ctypes.c_int32), ("num_partitions", ctypes.c_int32),
                 ("workspace_bytes", ctypes.c_size_t)]
 
     def as_dict(self):
@@ -84,15 +80,13 @@ def pda_status_string(status: int) -> str:
 
 
 def make_problem(num_seqs, num_q_heads, num_kv_heads, head_dim, num_blocks, max_blocks_per_seq,
-                 max_context_len, partition_tokens=0, block_size=16, num_workers=0) -> pda_problem:
+                 max_context_len, partition_tokens=0, block_size=16) -> pda_problem:
     return pda_problem(int(num_seqs), int(num_q_heads), int(num_kv_heads), int(head_dim), int(block_size),
-                       int(num_blocks), int(max_blocks_per_seq), int(max_context_len), int(partition_tokens),
-                       int(num_workers))
+                       int(num_blocks), int(max_blocks_per_seq), int(max_context_len), int(partition_tokens))
 
 
 def pda_plan(prob: pda_problem) -> dict:
-    """The plan of a problem on the current device: schedule, partition_tokens,
-    num_partitions, num_workers, workspace_bytes."""
+    """The plan of a problem: partition_tokens, num_partitions, workspace_bytes."""
     info = pda_plan_info()
     rc = load_library().pda_plan(ctypes.byref(prob), ctypes.byref(info))
     if rc != PDA_OK:
@@ -118,7 +112,7 @@ def pda_validate_host(prob: pda_problem, block_table, context_lens) -> Tuple[int
     return rc, bad.value
 
 
-def _problem_from(q, k_cache, block_table, max_context_len, partition_tokens, num_workers) -> pda_problem:
+def _problem_from(q, k_cache, block_table, max_context_len, partition_tokens) -> pda_problem:
     import torch
 
     if q.dim() != 3 or k_cache.dim() != 5 or block_table.dim() != 2:
@@ -129,8 +123,7 @@ def _problem_from(q, k_cache, block_table, max_context_len, partition_tokens, nu
         raise ValueError("q, k_cache and block_table shapes disagree")
     if max_context_len is None:
         raise ValueError("max_context_len must be given (the host bound on context_lens)")
-    return make_problem(B, Hq, Hkv, D, NB, block_table.shape[1], max_context_len, partition_tokens, BS,
-                        num_workers)
+    return make_problem(B, Hq, Hkv, D, NB, block_table.shape[1], max_context_len, partition_tokens, BS)
 
 
 def _check_tensors(q, k_cache, v_cache, block_table, context_lens, out):
@@ -163,13 +156,13 @@ def _stream_handle(stream, device):
 
 
 def _step(fn_name, q, k_cache, v_cache, block_table, context_lens, scale, out, max_context_len,
-          partition_tokens, num_workers, workspace, stream):
+          partition_tokens, workspace, stream):
     import torch
 
     if out is None:
         out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
     _check_tensors(q, k_cache, v_cache, block_table, context_lens, out)
-    prob = _problem_from(q, k_cache, block_table, max_context_len, partition_tokens, num_workers)
+    prob = _problem_from(q, k_cache, block_table, max_context_len, partition_tokens)
     need = pda_workspace_bytes(prob)
     if workspace is None and need > 0:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
@@ -185,25 +178,22 @@ def _step(fn_name, q, k_cache, v_cache, block_table, context_lens, scale, out, m
 
 
 def pda_decode(q, k_cache, v_cache, block_table, context_lens, scale: float, out=None, *,
-               max_context_len: int, partition_tokens: int = 0, num_workers: int = 0, workspace=None,
-               stream=None):
+               max_context_len: int, partition_tokens: int = 0, workspace=None, stream=None):
     """One decode-attention step (both passes).  Tensors on the GPU:
     q bf16 [B][Hq][D], k_cache bf16 [num_blocks][Hkv][D/8][16][8] (each block's
     keys as D/8 chunks of 16 slots x 8 elements), v_cache bf16 [num_blocks][Hkv][16][D],
     block_table int32 [B][max_blocks], context_lens int32 [B], out fp32 [B][Hq][D].
-    `workspace` (uint8, >= pda_workspace_bytes) is allocated when not given.
-    partition_tokens > 0 selects the partition schedule; num_workers > 0 fixes
-    the wavefront count of the stream schedule."""
+    `workspace` (uint8, >= pda_workspace_bytes) is allocated when not given;
+    partition_tokens > 0 fixes the split-K partition size."""
     return _step("pda_decode", q, k_cache, v_cache, block_table, context_lens, scale, out, max_context_len,
-                 partition_tokens, num_workers, workspace, stream)
+                 partition_tokens, workspace, stream)
 
 
 def pda_partition_attention(q, k_cache, v_cache, block_table, context_lens, scale: float, out=None, *,
-                            max_context_len: int, partition_tokens: int = 0, num_workers: int = 0,
-                            workspace=None, stream=None):
+                            max_context_len: int, partition_tokens: int = 0, workspace=None, stream=None):
     """Pass 1 only (see pda_decode)."""
     return _step("pda_partition_attention", q, k_cache, v_cache, block_table, context_lens, scale, out,
-                 max_context_len, partition_tokens, num_workers, workspace, stream)
+                 max_context_len, partition_tokens, workspace, stream)
 
 
 def pda_merge_partitions(prob: pda_problem, context_lens, out, workspace, stream=None):

@@ -39,10 +39,9 @@ def test_library_exports_every_declared_symbol():
 
 
 def prob(**kw):
-    """A valid descriptor; the stream schedule with a fixed wavefront count, so
-    that planning needs no device."""
+    """A valid descriptor (planning needs no device)."""
     base = dict(num_seqs=4, num_q_heads=8, num_kv_heads=2, head_dim=64, num_blocks=128,
-                max_blocks_per_seq=17, max_context_len=257, partition_tokens=0, num_workers=64)
+                max_blocks_per_seq=17, max_context_len=257, partition_tokens=0)
     base.update(kw)
     return pda.make_problem(**base)
 
@@ -56,8 +55,6 @@ def prob(**kw):
     (dict(max_context_len=-1), pda.pda.PDA_ERR_SHAPE),
     (dict(partition_tokens=24), pda.pda.PDA_ERR_SHAPE),
     (dict(partition_tokens=-16), pda.pda.PDA_ERR_SHAPE),
-    (dict(num_workers=-4), pda.pda.PDA_ERR_SHAPE),
-    (dict(num_workers=6), pda.pda.PDA_ERR_SHAPE),
     (dict(head_dim=96), pda.pda.PDA_ERR_UNSUPPORTED),
     (dict(block_size=32), pda.pda.PDA_ERR_UNSUPPORTED),
     (dict(num_q_heads=34, num_kv_heads=2), pda.pda.PDA_ERR_UNSUPPORTED),
@@ -75,39 +72,38 @@ def llama(**kw):
     return prob(**base)
 
 
-def test_plan_stream_schedule():
-    p = pda.pda_plan(llama(num_workers=3072))
-    units, slots = 256 * 8, 256 * 8 + 3072
-    assert p == dict(schedule=pda.PDA_SCHEDULE_STREAM, partition_tokens=0, num_partitions=0, num_workers=3072,
-                     workspace_bytes=slots * 4 * (128 + 2) * 4 + units * 8)
-    assert pda.pda_plan(llama(num_seqs=0, num_workers=0))["workspace_bytes"] == 0
-    # batches beyond the stream schedule's LDS table fall back to partitions
-    assert pda.pda_plan(llama(num_seqs=8193))["schedule"] == pda.PDA_SCHEDULE_PARTITION
+def plan(**kw):
+    d = pda.pda_plan(llama(**kw))
+    return d["partition_tokens"], d["num_partitions"], d["workspace_bytes"]
 
 
-def test_plan_partition_schedule():
-    P = pda.PDA_SCHEDULE_PARTITION
+def test_plan_workspace():
+    # one fp32 partial state (D values + max + denominator) per query head and
+    # partition when contexts are split, then one int32 per work item
+    # (partition, sequence, KV head)
+    assert plan(partition_tokens=2048) == (2048, 2, 256 * 32 * 2 * (128 + 2) * 4 + 2 * 256 * 8 * 4)
+    assert plan(partition_tokens=4096) == (4096, 1, 256 * 8 * 4)
+    assert plan(partition_tokens=8192) == (8192, 1, 256 * 8 * 4)
+    assert pda.pda_plan(prob(partition_tokens=64))["workspace_bytes"] == 4 * 8 * 5 * 66 * 4 + 5 * 4 * 2 * 4
+    assert plan(num_seqs=0)[2] == 0
+    assert pda.pda_workspace_bytes(llama()) == plan()[2]
 
-    def plan(**kw):
-        d = pda.pda_plan(llama(**kw))
-        assert d["schedule"] == P and d["num_workers"] == 0
-        return d["partition_tokens"], d["num_partitions"], d["workspace_bytes"]
-    # forced sizes: one fp32 partial (D values + max + denominator) per head and partition
-    assert plan(partition_tokens=2048) == (2048, 2, 256 * 32 * 2 * (128 + 2) * 4)
-    assert plan(partition_tokens=4096) == (4096, 1, 0)
-    assert pda.pda_plan(prob(partition_tokens=64))["workspace_bytes"] == 4 * 8 * 5 * 66 * 4
-    # the library's own choice for batches too large for the stream schedule
-    assert plan(num_seqs=9000)[:2] == (2048, 2)
+
+def test_plan_partition_choice():
+    # B * Hkv * max_len / 2 tokens over 768 concurrent workgroups, rounded up
+    # to 256 tokens, within [256, 4096]
+    assert plan()[:2] == (4096, 1)                        # share 5462 -> 4096
+    assert plan(num_seqs=9000)[:2] == (4096, 1)
+    assert plan(num_seqs=64)[:2] == (1536, 3)             # share 1366
+    assert plan(num_seqs=32)[:2] == (768, 6)              # share 683
+    assert plan(num_seqs=1)[:2] == (256, 16)              # share 22
+    assert plan(num_seqs=512, num_kv_heads=1, num_q_heads=8, max_context_len=8183)[:2] == (2816, 3)
+    assert plan(num_seqs=64, max_context_len=15288)[:2] == (4096, 4)
+    # never longer than the longest context, rounded up to a whole block
     assert plan(num_seqs=9000, max_context_len=2001)[:2] == (2016, 1)
-
-
-def test_plan_auto_workers_needs_a_device():
-    import torch
-    if torch.cuda.is_available():
-        pytest.skip("a GPU is present: the query succeeds")
-    with pytest.raises(pda.PdaError) as e:
-        pda.pda_plan(llama(num_workers=0))
-    assert e.value.status == pda.pda.PDA_ERR_HIP
+    assert plan(max_context_len=0)[:2] == (16, 1)
+    # a forced size is kept
+    assert plan(partition_tokens=16)[:2] == (16, 256)
 
 
 def call(fn, p, q=0x1000, k=0x1000, v=0x1000, bt=0x1000, lens=0x1000, scale=0.125, out=0x1000,
@@ -127,7 +123,7 @@ def test_step_validation(fn):
     assert call(fn, prob(), q=0x1008) == pda.pda.PDA_ERR_ALIGNMENT
     assert call(fn, prob(), k=0x1004) == pda.pda.PDA_ERR_ALIGNMENT
     assert call(fn, prob(), out=0x1002) == pda.pda.PDA_ERR_ALIGNMENT
-    assert call(fn, prob()) == pda.pda.PDA_ERR_WORKSPACE  # the stream schedule always needs one
+    assert call(fn, prob()) == pda.pda.PDA_ERR_WORKSPACE  # the work order always needs one
     split = prob(partition_tokens=64)
     assert call(fn, split) == pda.pda.PDA_ERR_WORKSPACE
     assert call(fn, split, ws=0x1000, ws_bytes=100) == pda.pda.PDA_ERR_WORKSPACE
