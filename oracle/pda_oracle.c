@@ -42,6 +42,33 @@
  *     out          fp64  [B][Hq][D]
  *   bf16 values are passed as their raw 16-bit patterns.
  *
+ * Several new query tokens per sequence (pda_oracle_decode_multi).  When a
+ * sequence brings n new tokens at once -- the draft tokens of speculative
+ * decoding, or a chunk of a prompt in chunked prefill, both of which the
+ * paper lists among vLLM's features (Section 3.2) -- their keys and values
+ * are already in the cache as the last n of its L positions, and new token i
+ * (0 <= i < n, in sequence order) sits at position L - n + i.  It attends to
+ * every position up to and including its own (causal attention), i.e. to the
+ * first L - n + 1 + i tokens; with n = 1 this is the decode step above.
+ *   q, out  [B][n][Hq][D]
+ *
+ * KV-cache append (pda_oracle_append).  Before attention runs, the step
+ * stores the new tokens' keys and values in the cache (the KV-cache
+ * management of the rollout stage, Appendix C): new token i of sequence b
+ * goes to position t = L - n + i, i.e. block block_table[b][t / BS], slot
+ * t mod BS, in the layouts above.  context_lens already counts the new
+ * tokens.  Positions t < 0 (L < n) are skipped; nothing else is written.
+ *   k_new, v_new  bf16 [B][n][Hkv][D]
+ *
+ * Token log-probabilities (pda_oracle_logprob).  After the LM head, the
+ * rollout records the log-probability of each sampled token (Appendix C),
+ * and the policy loss uses the entropy of the same distribution (Appendix C,
+ * the entropy bonus).  With x_j = logits[b][j] * inv_temperature over the
+ * vocabulary j in [0, V):
+ *   lse        = log sum_j exp(x_j)       (computed as m + log sum_j exp(x_j - m))
+ *   logprob[b] = x_{tokens[b]} - lse
+ *   entropy[b] = lse - sum_j softmax(x)_j * x_j
+ *
  * Every entry point returns 0 on success and a negative value when an
  * argument is out of range (including a block id outside [0, num_blocks) or a
  * context length beyond the block table); on error nothing is written.
@@ -57,6 +84,7 @@ typedef struct {
   const uint16_t *q, *k, *v;
   const int32_t *block_table, *context_lens;
   double scale;
+  int nq; /* new query tokens per sequence (1: decode) */
 } problem_t;
 
 /* bf16 is the upper half of an IEEE binary32: widening is a 16-bit shift. */
@@ -69,7 +97,7 @@ static double bf16_to_double(uint16_t bits) {
 
 static int check_problem(const problem_t *P) {
   if (P->B < 0 || P->Hq <= 0 || P->Hkv <= 0 || P->D <= 0 || P->BS <= 0 ||
-      P->num_blocks <= 0 || P->max_blocks_per_seq <= 0)
+      P->num_blocks <= 0 || P->max_blocks_per_seq <= 0 || P->nq <= 0)
     return -1;
   if (P->Hq % P->Hkv != 0 || P->D % 8 != 0) return -2;
   if (P->B > 0 && (!P->q || !P->k || !P->v || !P->block_table || !P->context_lens))
@@ -97,14 +125,23 @@ static size_t v_row(const problem_t *P, int32_t p, int g, int o) {
   return (((size_t)p * P->Hkv + g) * P->BS + o) * P->D;
 }
 
-/* The softmax weights w_t = e_t / Z of (b, h), t in [0, L); returns L.
- * `scores` must hold max(L, 1) doubles. */
-static int row_weights(const problem_t *P, int b, int h, double *scores) {
+/* Tokens that new query token i of sequence b attends to: positions
+ * [0, L - nq + 1 + i), none when that is empty or L <= 0. */
+static int visible_len(const problem_t *P, int b, int i) {
   int L = P->context_lens[b];
+  if (L <= 0) return 0;
+  int n = L - P->nq + 1 + i;
+  return n > 0 ? n : 0;
+}
+
+/* The softmax weights w_t = e_t / Z of query row (b, i, h), t in [0, L) with
+ * L its visible length; returns L.  `scores` must hold max(L, 1) doubles. */
+static int row_weights(const problem_t *P, int b, int i, int h, double *scores) {
+  int L = visible_len(P, b, i);
   if (L <= 0) return 0;
   int G = P->Hq / P->Hkv;
   int g = h / G;
-  const uint16_t *qrow = P->q + ((size_t)b * P->Hq + h) * P->D;
+  const uint16_t *qrow = P->q + (((size_t)b * P->nq + i) * P->Hq + h) * P->D;
   const int32_t *bt = P->block_table + (size_t)b * P->max_blocks_per_seq;
   /* pass 1: scores and their maximum */
   double m = -INFINITY;
@@ -127,9 +164,9 @@ static int row_weights(const problem_t *P, int b, int h, double *scores) {
   return L;
 }
 
-static void row_output(const problem_t *P, int b, int h, double *w, double *out_row) {
+static void row_output(const problem_t *P, int b, int i, int h, double *w, double *out_row) {
   for (int d = 0; d < P->D; ++d) out_row[d] = 0.0;
-  int L = row_weights(P, b, h, w);
+  int L = row_weights(P, b, i, h, w);
   if (L == 0) return;
   int G = P->Hq / P->Hkv;
   int g = h / G;
@@ -143,7 +180,7 @@ static void row_output(const problem_t *P, int b, int h, double *w, double *out_
 /* ---- work split over host threads: rows r = tid, tid + T, tid + 2T, ... ---- */
 typedef struct {
   const problem_t *P;
-  const int32_t *rows; /* (b, h) pairs, or NULL for all rows in order */
+  const int32_t *rows; /* (b, i, h) triples, or NULL for all rows in order */
   int n_rows, tid, nthreads, max_len;
   double *out;
   int failed;
@@ -154,10 +191,10 @@ static void *worker(void *arg) {
   double *w = (double *)malloc(sizeof(double) * (size_t)(J->max_len > 0 ? J->max_len : 1));
   if (!w) { J->failed = 1; return NULL; }
   for (int r = J->tid; r < J->n_rows; r += J->nthreads) {
-    int b, h;
-    if (J->rows) { b = J->rows[2 * r]; h = J->rows[2 * r + 1]; }
-    else { b = r / J->P->Hq; h = r % J->P->Hq; }
-    row_output(J->P, b, h, w, J->out + (size_t)r * J->P->D);
+    int b, i, h;
+    if (J->rows) { b = J->rows[3 * r]; i = J->rows[3 * r + 1]; h = J->rows[3 * r + 2]; }
+    else { b = r / (J->P->nq * J->P->Hq); i = (r / J->P->Hq) % J->P->nq; h = r % J->P->Hq; }
+    row_output(J->P, b, i, h, w, J->out + (size_t)r * J->P->D);
   }
   free(w);
   return NULL;
@@ -168,7 +205,8 @@ static int run_rows(const problem_t *P, const int32_t *rows, int n_rows, double 
   if (rc) return rc;
   if (rows)
     for (int r = 0; r < n_rows; ++r)
-      if (rows[2 * r] < 0 || rows[2 * r] >= P->B || rows[2 * r + 1] < 0 || rows[2 * r + 1] >= P->Hq)
+      if (rows[3 * r] < 0 || rows[3 * r] >= P->B || rows[3 * r + 1] < 0 || rows[3 * r + 1] >= P->nq ||
+          rows[3 * r + 2] < 0 || rows[3 * r + 2] >= P->Hq)
         return -6;
   if (n_rows <= 0) return 0;
   int max_len = 1;
@@ -196,29 +234,128 @@ static int run_rows(const problem_t *P, const int32_t *rows, int n_rows, double 
   int B, int Hq, int Hkv, int D, int block_size, int num_blocks, int max_blocks_per_seq, \
       const uint16_t *q, const uint16_t *k_cache, const uint16_t *v_cache,           \
       const int32_t *block_table, const int32_t *context_lens, double scale
-#define PROBLEM_INIT                                                                  \
+#define PROBLEM_INIT(NQ)                                                              \
   problem_t P = {B, Hq, Hkv, D, block_size, num_blocks, max_blocks_per_seq, q, k_cache, \
-                 v_cache, block_table, context_lens, scale}
+                 v_cache, block_table, context_lens, scale, NQ}
 
-/* All B*Hq rows; out is fp64 [B][Hq][D]. */
+/* All B*Hq rows of a decode step; out is fp64 [B][Hq][D]. */
 int pda_oracle_decode(PROBLEM_ARGS, double *out, int num_threads) {
-  PROBLEM_INIT;
+  PROBLEM_INIT(1);
   return run_rows(&P, NULL, B * Hq, out, num_threads);
 }
 
-/* Only the listed (b, h) pairs (rows[2r], rows[2r+1]); out is fp64 [n_rows][D]. */
-int pda_oracle_decode_rows(PROBLEM_ARGS, const int32_t *rows, int n_rows, double *out,
+/* All B*n*Hq rows with n new query tokens per sequence; q and out are
+ * [B][n][Hq][D] (out fp64). */
+int pda_oracle_decode_multi(PROBLEM_ARGS, int n, double *out, int num_threads) {
+  PROBLEM_INIT(n);
+  if (n <= 0) return -1;
+  return run_rows(&P, NULL, B * n * Hq, out, num_threads);
+}
+
+/* Only the listed (b, i, h) triples (rows[3r..3r+2]) with n new query tokens
+ * per sequence (n = 1: a decode step); out is fp64 [n_rows][D]. */
+int pda_oracle_decode_rows(PROBLEM_ARGS, int n, const int32_t *rows, int n_rows, double *out,
                            int num_threads) {
-  PROBLEM_INIT;
+  PROBLEM_INIT(n);
   if (n_rows > 0 && !rows) return -3;
   return run_rows(&P, rows, n_rows, out, num_threads);
 }
 
-/* The L softmax weights of (b, h) into w[0..L); returns L (>= 0) or an error. */
+/* The softmax weights of decode row (b, h) into w[0..L); returns L (>= 0) or
+ * an error. */
 int pda_oracle_weights(PROBLEM_ARGS, int b, int h, double *w) {
-  PROBLEM_INIT;
+  PROBLEM_INIT(1);
   int rc = check_problem(&P);
   if (rc) return rc;
   if (b < 0 || b >= B || h < 0 || h >= Hq) return -6;
-  return row_weights(&P, b, h, w);
+  return row_weights(&P, b, 0, h, w);
+}
+
+/* ---- KV-cache append ---- */
+
+/* Store the n new tokens of every sequence in the cache (in place).  All
+ * target block ids are checked before anything is written. */
+int pda_oracle_append(int B, int Hkv, int D, int block_size, int num_blocks, int max_blocks_per_seq,
+                      int n, const uint16_t *k_new, const uint16_t *v_new, const int32_t *block_table,
+                      const int32_t *context_lens, uint16_t *k_cache, uint16_t *v_cache) {
+  problem_t P = {B, Hkv, Hkv, D, block_size, num_blocks, max_blocks_per_seq, NULL, k_cache,
+                 v_cache, block_table, context_lens, 0.0, n};
+  if (B < 0 || Hkv <= 0 || D <= 0 || D % 8 != 0 || block_size <= 0 || num_blocks <= 0 ||
+      max_blocks_per_seq <= 0 || n <= 0)
+    return -1;
+  if (B > 0 && (!k_new || !v_new || !block_table || !context_lens || !k_cache || !v_cache)) return -3;
+  for (int b = 0; b < B; ++b) {
+    const int L = context_lens[b];
+    for (int i = 0; i < n; ++i) {
+      const int t = L - n + i;
+      if (t < 0) continue;
+      if (t / block_size >= max_blocks_per_seq) return -4;
+      const int32_t p = block_table[(size_t)b * max_blocks_per_seq + t / block_size];
+      if (p < 0 || p >= num_blocks) return -5;
+    }
+  }
+  for (int b = 0; b < B; ++b) {
+    const int L = context_lens[b];
+    const int32_t *bt = block_table + (size_t)b * max_blocks_per_seq;
+    for (int i = 0; i < n; ++i) {
+      const int t = L - n + i;
+      if (t < 0) continue;
+      const int32_t p = bt[t / block_size];
+      const int o = t % block_size;
+      for (int g = 0; g < Hkv; ++g) {
+        const size_t src = (((size_t)b * n + i) * Hkv + g) * D;
+        for (int d = 0; d < D; ++d) {
+          k_cache[k_elem(&P, p, g, o, d)] = k_new[src + d];
+          v_cache[v_row(&P, p, g, o) + d] = v_new[src + d];
+        }
+      }
+    }
+  }
+  return 0;
+}
+
+/* ---- token log-probabilities and entropy ---- */
+
+/* logits: B rows of V values, row r starting at element r * row_stride; bf16
+ * bit patterns when logits_are_f32 == 0, IEEE binary32 otherwise.  Writes
+ * logprob[b] and, when `entropy` is not NULL, entropy[b] (both fp64). */
+int pda_oracle_logprob(int B, int V, int64_t row_stride, const void *logits, int logits_are_f32,
+                       const int32_t *tokens, double inv_temperature, double *logprob, double *entropy) {
+  if (B < 0 || V <= 0 || row_stride < V) return -1;
+  if (B > 0 && (!logits || !tokens || !logprob)) return -3;
+  for (int b = 0; b < B; ++b)
+    if (tokens[b] < 0 || tokens[b] >= V) return -6;
+  for (int b = 0; b < B; ++b) {
+    const size_t base = (size_t)b * (size_t)row_stride;
+    double *x = (double *)malloc(sizeof(double) * (size_t)V);
+    if (!x) return -7;
+    for (int j = 0; j < V; ++j) {
+      double raw;
+      if (logits_are_f32) {
+        float f;
+        memcpy(&f, (const char *)logits + (base + j) * 4, 4);
+        raw = (double)f;
+      } else {
+        raw = bf16_to_double(((const uint16_t *)logits)[base + j]);
+      }
+      x[j] = raw * inv_temperature;
+    }
+    double m = -INFINITY;
+    for (int j = 0; j < V; ++j)
+      if (x[j] > m) m = x[j];
+    double Z = 0.0;
+    for (int j = 0; j < V; ++j) Z += exp(x[j] - m);
+    const double lse = m + log(Z);
+    logprob[b] = x[tokens[b]] - lse;
+    if (entropy) {
+      double mean_x = 0.0; /* sum_j softmax_j * x_j */
+      for (int j = 0; j < V; ++j) {
+        const double e = exp(x[j] - m);
+        if (e > 0.0) mean_x += e / Z * x[j]; /* a term of probability 0 adds 0, also at x = -inf */
+      }
+      entropy[b] = lse - mean_x;
+    }
+    free(x);
+  }
+  return 0;
 }

@@ -34,7 +34,8 @@ MUTANTS = {
     "K layout read as rows": ("((((size_t)p * P->Hkv + g) * (P->D / 8) + d / 8) * P->BS + o) * 8 + d % 8",
                               "(((size_t)p * P->Hkv + g) * P->BS + o) * P->D + d"),
     "K chunk element order": ("* P->BS + o) * 8 + d % 8", "* P->BS + o) * 8 + (7 - d % 8)"),
-    "q row of the kv head": ("((size_t)b * P->Hq + h) * P->D", "((size_t)b * P->Hq + g) * P->D"),
+    "q row of the kv head": ("(((size_t)b * P->nq + i) * P->Hq + h) * P->D",
+                             "(((size_t)b * P->nq + i) * P->Hq + g) * P->D"),
     "V read from K": ("const uint16_t *vrow = P->v +", "const uint16_t *vrow = P->k +"),
     "bf16 widened wrongly": ("(uint32_t)bits << 16", "(uint32_t)bits << 15"),
     "last token dropped from V sum": ("for (int t = 0; t < L; ++t) {\n    const uint16_t *vrow",
@@ -44,6 +45,32 @@ MUTANTS = {
                              "P->block_table + (size_t)b * P->B"),
     "zero length not zeroed": ("for (int d = 0; d < P->D; ++d) out_row[d] = 0.0;\n  int L",
                                "int L"),
+    # several query tokens per sequence
+    "visible length off by one": ("int n = L - P->nq + 1 + i;", "int n = L - P->nq + i;"),
+    "no causal mask": ("int n = L - P->nq + 1 + i;", "int n = L;"),
+    "same q row for every new token": ("(((size_t)b * P->nq + i) * P->Hq + h) * P->D",
+                                       "(((size_t)b * P->nq) * P->Hq + h) * P->D"),
+    "new-token index not decoded": ("i = (r / J->P->Hq) % J->P->nq;", "i = 0;"),
+    # KV-cache append
+    "append order reversed": ("const int t = L - n + i;\n      if (t < 0) continue;\n      const int32_t p = bt[",
+                              "const int t = L - 1 - i;\n      if (t < 0) continue;\n      const int32_t p = bt["),
+    "append K stored as rows": ("k_cache[k_elem(&P, p, g, o, d)] = k_new[src + d];",
+                                "k_cache[v_row(&P, p, g, o) + d] = k_new[src + d];"),
+    "append V taken from K": ("v_cache[v_row(&P, p, g, o) + d] = v_new[src + d];",
+                              "v_cache[v_row(&P, p, g, o) + d] = k_new[src + d];"),
+    "append source [b][g][i]": ("(((size_t)b * n + i) * Hkv + g) * D", "(((size_t)b * Hkv + g) * n + i) * D"),
+    "append no id check": ("if (p < 0 || p >= num_blocks) return -5;\n    }\n  }\n  for (int b = 0; b < B; ++b) {\n    const int L",
+                           "}\n  }\n  for (int b = 0; b < B; ++b) {\n    const int L"),
+    # log-probabilities
+    "temperature dropped": ("x[j] = raw * inv_temperature;", "x[j] = raw;"),
+    "lse without the max": ("const double lse = m + log(Z);", "const double lse = log(Z);"),
+    "no max subtraction in lse": [("Z += exp(x[j] - m);", "Z += exp(x[j]);"),
+                                  ("const double lse = m + log(Z);", "const double lse = log(Z);")],
+    "entropy sign": ("entropy[b] = lse - mean_x;", "entropy[b] = mean_x - lse;"),
+    "entropy unnormalised": ("mean_x += e / Z * x[j];", "mean_x += e * x[j];"),
+    "token off by one": ("logprob[b] = x[tokens[b]] - lse;", "logprob[b] = x[tokens[b] > 0 ? tokens[b] - 1 : 1] - lse;"),
+    "bf16 logits widened as f32 bits": ("raw = bf16_to_double(((const uint16_t *)logits)[base + j]);",
+                                        "raw = (double)((const uint16_t *)logits)[base + j];"),
 }
 
 RUNNER = textwrap.dedent("""
@@ -72,11 +99,15 @@ def run_pins_in_child(lib_path):
     return [f for f in lines[-1][len("FAILED:"):].split(",") if f]
 
 
-def build_variant(tmp_path, old, new):
+def build_variant(tmp_path, edits):
+    """`edits` is one (old, new) pair or a list of them (one mistake that
+    needs consistent edits in several places)."""
     src = open(SRC).read()
-    assert old in src, f"mutation anchor not found: {old!r}"
+    for old, new in ([edits] if isinstance(edits, tuple) else edits):
+        assert old in src, f"mutation anchor not found: {old!r}"
+        src = src.replace(old, new)
     path = tmp_path / "pda_oracle_mut.c"
-    path.write_text(src.replace(old, new))
+    path.write_text(src)
     lib = str(tmp_path / "libpda_oracle_mut.so")
     oracle.build(src=str(path), lib=lib)
     return lib
@@ -90,6 +121,5 @@ def test_unmodified_source_passes_all_pins(tmp_path):
 
 @pytest.mark.parametrize("name", list(MUTANTS))
 def test_mutant_is_caught(tmp_path, name):
-    old, new = MUTANTS[name]
-    failed = run_pins_in_child(build_variant(tmp_path, old, new))
+    failed = run_pins_in_child(build_variant(tmp_path, MUTANTS[name]))
     assert failed is None or len(failed) > 0, f"no pin caught mutant {name!r}"

@@ -20,7 +20,14 @@ stand in as Llama-3-shaped synthetic batches, since no model weights or
 datasets are available.
 
 Streams of the Philox generator (seed, stream):
-    1 lengths, 2 pool permutation, 3 q, 4 K, 5 V, 6 per-head K offset.
+    1 lengths, 2 pool permutation, 3 q, 4 K, 5 V, 6 per-head K offset,
+    7 multi-token q, 8 new K rows, 9 new V rows, 10 logits, 11 logit
+    structure (likely tokens, sampled tokens).
+
+Besides the attention inputs it draws the inputs of the steps around
+attention: the new tokens' K/V rows that a step stores in the cache, the
+queries of several new tokens per sequence, and LM-head logits with the
+sampled token of each row.
 Pool blocks that no sequence references, and the slots of a block beyond the
 longest context that references it, can be filled with bf16 NaN ("poison")
 so that any read of them shows up in the output.
@@ -40,6 +47,7 @@ import numpy as np
 
 BLOCK_SIZE = 16
 _STREAM_LENS, _STREAM_POOL, _STREAM_Q, _STREAM_K, _STREAM_V, _STREAM_KOFF = 1, 2, 3, 4, 5, 6
+_STREAM_QMULTI, _STREAM_KNEW, _STREAM_VNEW, _STREAM_LOGITS, _STREAM_LOGIT_STRUCT = 7, 8, 9, 10, 11
 _POOL_CHUNK_BLOCKS = 4096  # the value draw walks the pool in fixed chunks (deterministic)
 
 
@@ -332,3 +340,77 @@ def sample_rows(st: Structure, n: int, seed: int = 7) -> np.ndarray:
     while len(picks) < n:
         picks.append((int(r.integers(0, st.B)), int(r.integers(0, st.Hq))))
     return np.asarray(picks[:max(n, len(picks))], dtype=np.int32)
+
+
+def _torch_gen(seed: int, stream: int, device):
+    import torch
+
+    g = torch.Generator(device=torch.device(device))
+    g.manual_seed(_torch_seed(seed, stream))
+    return g
+
+
+def fill_multi_q(st: Structure, n: int, device="cpu"):
+    """Queries of n new tokens per sequence: bf16 [B][n][Hq][D], N(0, 1)."""
+    import torch
+
+    return torch.randn((st.B, n, st.Hq, st.D), generator=_torch_gen(st.seed, _STREAM_QMULTI, device),
+                       device=torch.device(device), dtype=torch.float32).to(torch.bfloat16)
+
+
+def fill_new_kv(st: Structure, n: int, device="cpu"):
+    """K and V rows of n new tokens per sequence: bf16 [B][n][Hkv][D] each, N(0, 1)."""
+    import torch
+
+    dev = torch.device(device)
+    shape = (st.B, n, st.Hkv, st.D)
+    k = torch.randn(shape, generator=_torch_gen(st.seed, _STREAM_KNEW, dev), device=dev, dtype=torch.float32)
+    v = torch.randn(shape, generator=_torch_gen(st.seed, _STREAM_VNEW, dev), device=dev, dtype=torch.float32)
+    return k.to(torch.bfloat16), v.to(torch.bfloat16)
+
+
+# LM-head outputs of one decode step (one row per sequence).  The paper's
+# rollouts use DeepSeek-R1-distilled Qwen models (Section 4.1); the
+# attention configurations above are Llama-3-shaped, so both vocabularies
+# appear.
+LOGIT_CONFIGS: Dict[str, dict] = {
+    "llama3_vocab": dict(index=10, B=256, V=128256,
+                         desc="LM-head logits of a Llama-3 decode step: B=256 rows x 128256 vocabulary"),
+    "qwen_vocab": dict(index=11, B=256, V=151936,
+                       desc="LM-head logits of a Qwen decode step: B=256 rows x 151936 vocabulary"),
+    "tiny_vocab": dict(index=12, B=5, V=1000, desc="tiny: 5 rows x 1000 vocabulary"),
+}
+
+
+def make_logits(B: int, V: int, seed: int, device="cpu", dtype=None, likely: int = 32,
+                background_std: float = 2.0, boost=(6.0, 14.0), p_likely: float = 0.7):
+    """Synthetic LM-head logits [B][V] and sampled tokens [B] (int32, host).
+
+    Each row is N(0, background_std^2) noise plus, on `likely` random tokens,
+    a boost drawn from U(boost): a peaked distribution with a long flat tail
+    like a language model's.  The sampled token is one of the likely tokens
+    with probability p_likely, else uniform over the vocabulary.  `dtype` is
+    torch.bfloat16 (default) or torch.float32."""
+    import torch
+
+    dtype = torch.bfloat16 if dtype is None else dtype
+    r = _rng(seed, _STREAM_LOGIT_STRUCT)
+    likely_ids = np.stack([r.choice(V, size=min(likely, V), replace=False) for _ in range(B)]) if B else \
+        np.zeros((0, min(likely, V)), dtype=np.int64)
+    boosts = r.uniform(boost[0], boost[1], size=likely_ids.shape)
+    pick_likely = r.random(B) < p_likely
+    tokens = np.where(pick_likely, likely_ids[np.arange(B), r.integers(0, likely_ids.shape[1], B)]
+                      if B else np.zeros(0, np.int64), r.integers(0, V, B)).astype(np.int32)
+    dev = torch.device(device)
+    x = torch.randn((B, V), generator=_torch_gen(seed, _STREAM_LOGITS, dev), device=dev,
+                    dtype=torch.float32) * background_std
+    if B:
+        rows = torch.arange(B, device=dev)[:, None].expand(B, likely_ids.shape[1])
+        x[rows, torch.from_numpy(likely_ids).to(dev)] += torch.from_numpy(boosts).float().to(dev)
+    return x.to(dtype), tokens
+
+
+def logits_for(name: str, device="cpu", dtype=None):
+    """make_logits for a named logit configuration (seed 2405 + index)."""
+    cfg = LOGIT_CONFIGS[name]
+    return make_logits(cfg["B"], cfg["V"], 2405 + cfg["index"], device, dtype)
