@@ -18,8 +18,15 @@
  *     s_t = scale * sum_d q[b][h][d] * K[p][g][d / 8][o][d % 8]
  *     out[b][h] = sum_t softmax(s)_t * V[p][g][o][:]
  *
+ * Several new tokens per sequence.  vLLM's speculative decoding and chunked
+ * prefill (Section 3.2) bring n > 1 new tokens of a sequence in one step.
+ * With num_query_tokens = n, q and out hold n rows per sequence; new token i
+ * (0 <= i < n) sits at position L - n + i of the context (L counts the new
+ * tokens) and attends causally, to tokens t < L - n + 1 + i.  n = 1 is the
+ * decode step above.
+ *
  * Layouts (row-major; all pointers below are DEVICE pointers):
- *   q            bf16  [num_seqs][num_q_heads][head_dim]
+ *   q            bf16  [num_seqs][n][num_q_heads][head_dim]
  *   k_cache      bf16  [num_blocks][num_kv_heads][head_dim/8][block_size][8]
  *                       each block's keys as head_dim/8 chunks of 16 slots x 8
  *                       consecutive elements (key element d of slot o at
@@ -29,33 +36,35 @@
  *   block_table  int32 [num_seqs][max_blocks_per_seq]  (entries past
  *                       ceil(L/16) are never read and may hold anything)
  *   context_lens int32 [num_seqs]
- *   out          fp32  [num_seqs][num_q_heads][head_dim]
- *   workspace    opaque, pda_workspace_bytes() bytes (split-K partials)
+ *   out          fp32  [num_seqs][n][num_q_heads][head_dim]
+ *   k_new, v_new bf16  [num_seqs][n][num_kv_heads][head_dim]  (pda_append_kv)
+ *   workspace    opaque, pda_workspace_bytes() bytes
  * Pool slots past a sequence's context (the tail of its last block) and pool
  * blocks no sequence references are never used, whatever they hold.
  *
  * Long contexts are split into partitions of `partition_tokens` tokens that
  * are processed independently; a second pass merges the partial softmax
- * states.  Pass 1 runs one workgroup per (partition, sequence, KV head),
- * largest partition first (a small kernel sorts the items by size on the
- * GPU).  The partition size depends only on the problem descriptor and the
- * arithmetic of an item only on its data, never on physical block ids,
- * timing or the order the items run in, so for a given descriptor the output
- * is bit-for-bit reproducible and independent of where blocks sit in the
- * pool.
+ * states.  Pass 1 runs one workgroup per (partition, sequence, KV head,
+ * chunk of at most 16 / G new tokens), largest partition first (a small
+ * kernel sorts the items by size on the GPU).  The partition size depends
+ * only on the problem descriptor and the arithmetic of an item only on its
+ * data, never on physical block ids, timing or the order the items run in,
+ * so for a given descriptor the output is bit-for-bit reproducible and
+ * independent of where blocks sit in the pool.
  *
- * Ownership and errors.  The caller owns every buffer; the library allocates
- * nothing and keeps no state, so concurrent calls (with separate workspaces)
- * are safe.
+ * Ownership and errors.  The caller owns every buffer; the per-step entry
+ * points allocate nothing and keep no state, so concurrent calls (with
+ * separate workspaces) are safe.  Only pda_step_graph_create allocates: the
+ * HIP graph objects it returns, freed by pda_step_graph_destroy.
  * Every entry point validates its scalar arguments and pointers on the host
  * and returns a pda_status without touching the GPU when they are invalid.
  * Work is enqueued asynchronously on `stream` (NULL = the null stream); a
  * failed launch returns PDA_ERR_HIP.  Device-resident contents are the
  * caller's contract (block ids in [0, num_blocks), lengths at most
  * max_context_len); the kernels clamp lengths to [0, max_context_len] and
- * never read outside the pool: a (b, kv head) whose block table holds an
- * out-of-range id gets NaN output rows.  pda_validate_host() checks host
- * copies of the contents.
+ * never read or write outside the pool: a (b, kv head) whose block table
+ * holds an out-of-range id gets NaN output rows, and the append skips that
+ * token.  pda_validate_host() checks host copies of the contents.
  */
 #ifndef PDA_H
 #define PDA_H
@@ -75,12 +84,12 @@ enum pda_status {
   PDA_ERR_SHAPE = 2,       /* a size is negative, zero where it must not be, too large, or inconsistent */
   PDA_ERR_UNSUPPORTED = 3, /* valid but not built: head_dim not 64/128, block_size not 16, G > 16 */
   PDA_ERR_WORKSPACE = 4,   /* workspace NULL or smaller than pda_workspace_bytes() */
-  PDA_ERR_ALIGNMENT = 5,   /* q, k_cache, v_cache or workspace not 16-byte aligned; out not 4-byte */
+  PDA_ERR_ALIGNMENT = 5,   /* q, k_cache, v_cache, k_new, v_new or workspace not 16-byte aligned; out not 4-byte */
   PDA_ERR_VALUE = 6,       /* non-finite scale, or a host-side content check failed */
-  PDA_ERR_HIP = 7          /* a HIP launch failed (hipGetLastError) */
+  PDA_ERR_HIP = 7          /* a HIP call failed (launch, graph capture or instantiation) */
 };
 
-/* Sizes of one decode step.  All fields are plain host integers. */
+/* Sizes of one step.  All fields are plain host integers. */
 typedef struct pda_problem {
   int32_t num_seqs;           /* B >= 0 */
   int32_t num_q_heads;        /* Hq >= 1 */
@@ -92,6 +101,7 @@ typedef struct pda_problem {
   int32_t max_context_len;    /* host-known bound on context_lens[]; 0 <= it <= 16*max_blocks_per_seq */
   int32_t partition_tokens;   /* split-K partition size: 0 lets the library choose, otherwise a
                                  positive multiple of 16 */
+  int32_t num_query_tokens;   /* n, new tokens per sequence: 0 or 1 = a decode step */
 } pda_problem;
 
 /* What pda_decode will do for a descriptor. */
@@ -109,17 +119,17 @@ int pda_plan(const pda_problem *prob, pda_plan_info *plan);
 /* Workspace bytes pda_decode needs for `prob` (0 only for an empty batch). */
 int pda_workspace_bytes(const pda_problem *prob, size_t *bytes);
 
-/* One decode-attention step for the whole batch: pda_partition_attention
- * followed by pda_merge_partitions on the same stream.  `scale` is the
- * softmax scale (usually 1/sqrt(head_dim)); it must be finite.  `workspace`
- * (any contents) must hold pda_workspace_bytes() bytes; it may be NULL for
- * an empty batch.  Calls that overlap on the GPU need separate workspaces. */
+/* One attention step for the whole batch: pda_partition_attention followed
+ * by pda_merge_partitions on the same stream.  `scale` is the softmax scale
+ * (usually 1/sqrt(head_dim)); it must be finite.  `workspace` (any contents)
+ * must hold pda_workspace_bytes() bytes; it may be NULL for an empty batch.
+ * Calls that overlap on the GPU need separate workspaces. */
 int pda_decode(const pda_problem *prob, const void *q, const void *k_cache, const void *v_cache,
                const int32_t *block_table, const int32_t *context_lens, float scale, float *out,
                void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Pass 1 alone (the work-order kernel, then one workgroup per partition):
- * rows of contexts that fit one partition, and of empty contexts, are final
+ * rows that see a single partition, and rows that see no token, are final
  * in `out` after this pass; the others are left as partial softmax states in
  * `workspace`. */
 int pda_partition_attention(const pda_problem *prob, const void *q, const void *k_cache,
@@ -128,10 +138,42 @@ int pda_partition_attention(const pda_problem *prob, const void *q, const void *
                             void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Pass 2 alone: merge the partial states that pass 1 left in `workspace` into
- * `out` for every context with more than one partition, in ascending
+ * `out` for every row that sees more than one partition, in ascending
  * partition order.  Must follow pass 1 for the same descriptor and lengths. */
 int pda_merge_partitions(const pda_problem *prob, const int32_t *context_lens, float *out,
                          const void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* KV-cache append, the step before attention (Appendix C: the rollout stage's
+ * KV-cache management): store the keys and values of the n new tokens of
+ * every sequence in the cache.  New token i of sequence b goes to position
+ * t = L - n + i (L = context_lens[b], clamped to [0, max_context_len], already
+ * counting the new tokens): block block_table[b][t / 16], slot t % 16, in the
+ * k_cache / v_cache layouts above.  Positions t < 0 are skipped, and so is a
+ * token whose block id is outside [0, num_blocks).  Nothing else in the
+ * cache changes.  k_new and v_new are 16-byte aligned device buffers of
+ * [B][n][Hkv][D] bf16; k_cache and v_cache are written in place. */
+int pda_append_kv(const pda_problem *prob, const void *k_new, const void *v_new,
+                  const int32_t *block_table, const int32_t *context_lens, void *k_cache,
+                  void *v_cache, hipStream_t stream);
+
+/* A whole step captured once as a HIP graph: pda_append_kv, then pda_decode,
+ * with the pointers given here (vLLM runs its decode steps as captured
+ * graphs, Section 3.2).  Each pda_step_graph_launch replays the step on
+ * `stream` and reads the buffers' CURRENT contents (new tokens, queries,
+ * block table, lengths), so a caller refills them and relaunches; the
+ * descriptor, in particular max_context_len, is fixed at creation.  The
+ * arguments are validated as for pda_append_kv and pda_decode.  Launches of
+ * one graph must not overlap on the GPU (they share the workspace).
+ * pda_step_graph_create allocates the graph objects; pda_step_graph_destroy
+ * frees them (NULL is accepted). */
+typedef struct pda_step_graph pda_step_graph;
+int pda_step_graph_create(const pda_problem *prob, const void *q, const void *k_new,
+                          const void *v_new, void *k_cache, void *v_cache,
+                          const int32_t *block_table, const int32_t *context_lens, float scale,
+                          float *out, void *workspace, size_t workspace_bytes,
+                          pda_step_graph **graph);
+int pda_step_graph_launch(pda_step_graph *graph, hipStream_t stream);
+int pda_step_graph_destroy(pda_step_graph *graph);
 
 /* Host-side check of device contents, on HOST copies: every context length
  * is at most max_context_len and every block id a sequence reads is in

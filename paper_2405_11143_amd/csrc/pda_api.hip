@@ -1,9 +1,12 @@
 // C ABI of the paged decode-attention library (declared in include/pda.h):
-// host-side validation, the plan (partition size, workspace), and the
-// launches.  Nothing here allocates memory or keeps state between calls.
+// host-side validation, the plan (partition size, query chunks, workspace),
+// the launches, and the captured step graph.  Apart from the graph objects
+// that pda_step_graph_create returns, nothing here allocates memory or keeps
+// state between calls.
 #include <math.h>
 
 #include <algorithm>
+#include <new>
 
 #include "pda.h"
 #include "pda_internal.h"
@@ -16,9 +19,9 @@ namespace {
 // each of the kConcurrentItems workgroups the GPU runs at once has to do;
 // longer items amortise each workgroup's start-up (order, length, block ids,
 // q) over more streamed tiles.  With only max_context_len on the host, the
-// work is estimated as B * Hkv * max_context_len / 2 tokens (the mean of
-// contexts spread up to the maximum), and the partition is that share rounded
-// up to kPartitionQuantum tokens, within [kMinPartitionTokens,
+// work is estimated as B * Hkv * chunks * max_context_len / 2 tokens (the
+// mean of contexts spread up to the maximum), and the partition is that
+// share rounded up to kPartitionQuantum tokens, within [kMinPartitionTokens,
 // kMaxPartitionTokens] and never longer than the longest context (then there
 // is one partition and no merge pass).  On MI355X this picks the fastest or
 // within 1% of the fastest of the sizes measured on the four Llama-3-shaped
@@ -28,14 +31,17 @@ constexpr int kMinPartitionTokens = 256;
 constexpr int kPartitionQuantum = 256;
 constexpr int64_t kConcurrentItems = 768;  // 256 compute units x 3 workgroups of 4 wavefronts
 
+int query_tokens(const pda_problem* p) { return p->num_query_tokens > 0 ? p->num_query_tokens : 1; }
+
 int check_problem(const pda_problem* p) {
   if (!p) return PDA_ERR_NULL;
   if (p->num_seqs < 0 || p->num_q_heads < 1 || p->num_kv_heads < 1 || p->num_blocks < 1 ||
-      p->max_blocks_per_seq < 1 || p->max_context_len < 0 || p->partition_tokens < 0)
+      p->max_blocks_per_seq < 1 || p->max_context_len < 0 || p->partition_tokens < 0 || p->num_query_tokens < 0)
     return PDA_ERR_SHAPE;
   if (p->num_q_heads % p->num_kv_heads != 0) return PDA_ERR_SHAPE;
   if (p->partition_tokens % pda::kBlockTokens != 0) return PDA_ERR_SHAPE;
   if ((int64_t)p->max_context_len > (int64_t)pda::kBlockTokens * p->max_blocks_per_seq) return PDA_ERR_SHAPE;
+  if ((int64_t)p->num_seqs * query_tokens(p) * p->num_q_heads > 0x7fffffff) return PDA_ERR_SHAPE;
   if (p->block_size != pda::kBlockTokens) return PDA_ERR_UNSUPPORTED;
   if (p->head_dim != 64 && p->head_dim != 128) return PDA_ERR_UNSUPPORTED;
   if (p->num_q_heads / p->num_kv_heads > pda::kMaxGroup) return PDA_ERR_UNSUPPORTED;
@@ -44,14 +50,20 @@ int check_problem(const pda_problem* p) {
 
 struct Plan {
   pda_plan_info info;
-  size_t items;           // P * B * Hkv work items (pass-1 workgroups)
-  size_t slots;           // partial states, one per (sequence, query head, partition); 0 when P == 1
+  int query_chunk;        // new tokens per work item: min(n, 16 / G)
+  int num_query_chunks;   // ceil(n / query_chunk)
+  size_t items;           // P * B * Hkv * chunks work items (pass-1 workgroups)
+  size_t slots;           // partial states, one per (sequence, new token, query head, partition); 0 when P == 1
 };
 
 int make_plan(const pda_problem* p, Plan* plan) {
   int rc = check_problem(p);
   if (rc != PDA_OK) return rc;
-  const int64_t units = (int64_t)p->num_seqs * p->num_kv_heads;
+  const int n = query_tokens(p);
+  const int G = p->num_q_heads / p->num_kv_heads;
+  const int qc = std::min(n, pda::kMaxGroup / G);
+  const int nqc = (n + qc - 1) / qc;
+  const int64_t units = (int64_t)p->num_seqs * p->num_kv_heads * nqc;
   int tp = p->partition_tokens;
   if (tp == 0) {
     const int64_t len = p->max_context_len > 0 ? p->max_context_len : 1;
@@ -66,9 +78,11 @@ int make_plan(const pda_problem* p, Plan* plan) {
   *plan = Plan{};
   plan->info.partition_tokens = tp;
   plan->info.num_partitions = (int32_t)parts;
+  plan->query_chunk = qc;
+  plan->num_query_chunks = nqc;
   if (p->num_seqs > 0) {
     plan->items = (size_t)(parts * units);
-    plan->slots = parts > 1 ? (size_t)p->num_seqs * p->num_q_heads * (size_t)parts : 0;
+    plan->slots = parts > 1 ? (size_t)p->num_seqs * n * p->num_q_heads * (size_t)parts : 0;
     // partial states (O, m, l) first, then the work order
     plan->info.workspace_bytes = plan->slots * (p->head_dim + 2) * sizeof(float) + plan->items * sizeof(int32_t);
   }
@@ -77,11 +91,11 @@ int make_plan(const pda_problem* p, Plan* plan) {
 
 bool aligned(const void* ptr, size_t a) { return ((uintptr_t)ptr % a) == 0; }
 
-// Sizes and workspace carving shared by both passes.
+// Sizes and workspace carving shared by every launch.
 void fill_args(const pda_problem* p, const Plan* plan, void* ws, pda::StepArgs* args) {
   *args = pda::StepArgs{};
   float* wsf = static_cast<float*>(ws);
-  if (plan->info.workspace_bytes > 0) {
+  if (plan->info.workspace_bytes > 0 && ws) {
     if (plan->slots > 0) {
       args->part_o = wsf;
       args->part_m = wsf + plan->slots * p->head_dim;
@@ -92,9 +106,13 @@ void fill_args(const pda_problem* p, const Plan* plan, void* ws, pda::StepArgs* 
   args->num_seqs = p->num_seqs;
   args->num_q_heads = p->num_q_heads;
   args->num_kv_heads = p->num_kv_heads;
+  args->group = p->num_q_heads / p->num_kv_heads;
   args->num_blocks = p->num_blocks;
   args->max_blocks_per_seq = p->max_blocks_per_seq;
   args->max_context_len = p->max_context_len;
+  args->num_query_tokens = query_tokens(p);
+  args->query_chunk = plan->query_chunk;
+  args->num_query_chunks = plan->num_query_chunks;
   args->partition_tokens = plan->info.partition_tokens;
   args->num_partitions = plan->info.num_partitions;
 }
@@ -103,7 +121,6 @@ void fill_args(const pda_problem* p, const Plan* plan, void* ws, pda::StepArgs* 
 int prepare_step(const pda_problem* p, const void* q, const void* k, const void* v, const int32_t* bt,
                  const int32_t* lens, float scale, float* out, void* ws, size_t ws_bytes, Plan* plan,
                  pda::StepArgs* args) {
-  // Everything that needs no device comes first; the plan may query the device.
   int rc = check_problem(p);
   if (rc != PDA_OK) return rc;
   if (p->num_seqs > 0 && (!q || !k || !v || !bt || !lens || !out)) return PDA_ERR_NULL;
@@ -126,7 +143,36 @@ int prepare_step(const pda_problem* p, const void* q, const void* k, const void*
   return PDA_OK;
 }
 
+// Validation of an append; fills `args` (no workspace is involved).
+int prepare_append(const pda_problem* p, const void* k_new, const void* v_new, const int32_t* bt,
+                   const int32_t* lens, void* k_cache, void* v_cache, pda::StepArgs* args) {
+  int rc = check_problem(p);
+  if (rc != PDA_OK) return rc;
+  if (p->num_seqs > 0 && (!k_new || !v_new || !bt || !lens || !k_cache || !v_cache)) return PDA_ERR_NULL;
+  if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16))
+    return PDA_ERR_ALIGNMENT;
+  Plan plan;
+  rc = make_plan(p, &plan);
+  if (rc != PDA_OK) return rc;
+  fill_args(p, &plan, nullptr, args);
+  args->table = bt;
+  args->lens = lens;
+  return PDA_OK;
+}
+
+hipError_t launch_append_of(const pda_problem* p, const pda::StepArgs& args, const void* k_new, const void* v_new,
+                            void* k_cache, void* v_cache, hipStream_t stream) {
+  return pda::launch_append(args, static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new),
+                            static_cast<uint16_t*>(k_cache), static_cast<uint16_t*>(v_cache), p->head_dim, stream);
+}
+
 }  // namespace
+
+struct pda_step_graph {
+  hipGraph_t graph;
+  hipGraphExec_t exec;
+  bool empty;  // an empty batch: nothing to launch
+};
 
 extern "C" {
 
@@ -157,9 +203,8 @@ int pda_partition_attention(const pda_problem* prob, const void* q, const void* 
                         workspace_bytes, &plan, &args);
   if (rc != PDA_OK) return rc;
   if (prob->num_seqs == 0) return PDA_OK;
-  const int group = prob->num_q_heads / prob->num_kv_heads;
   if (pda::launch_order(args, stream) != hipSuccess) return PDA_ERR_HIP;
-  if (pda::launch_partition(args, group, prob->head_dim, stream) != hipSuccess) return PDA_ERR_HIP;
+  if (pda::launch_partition(args, prob->head_dim, stream) != hipSuccess) return PDA_ERR_HIP;
   return PDA_OK;
 }
 
@@ -189,6 +234,77 @@ int pda_decode(const pda_problem* prob, const void* q, const void* k_cache, cons
                                    workspace_bytes, stream);
   if (rc != PDA_OK) return rc;
   return pda_merge_partitions(prob, context_lens, out, workspace, workspace_bytes, stream);
+}
+
+int pda_append_kv(const pda_problem* prob, const void* k_new, const void* v_new, const int32_t* block_table,
+                  const int32_t* context_lens, void* k_cache, void* v_cache, hipStream_t stream) {
+  pda::StepArgs args;
+  int rc = prepare_append(prob, k_new, v_new, block_table, context_lens, k_cache, v_cache, &args);
+  if (rc != PDA_OK) return rc;
+  if (prob->num_seqs == 0) return PDA_OK;
+  return launch_append_of(prob, args, k_new, v_new, k_cache, v_cache, stream) == hipSuccess ? PDA_OK : PDA_ERR_HIP;
+}
+
+int pda_step_graph_create(const pda_problem* prob, const void* q, const void* k_new, const void* v_new,
+                          void* k_cache, void* v_cache, const int32_t* block_table, const int32_t* context_lens,
+                          float scale, float* out, void* workspace, size_t workspace_bytes,
+                          pda_step_graph** graph) {
+  if (!graph) return PDA_ERR_NULL;
+  *graph = nullptr;
+  pda::StepArgs args, append_args;
+  Plan plan;
+  int rc = prepare_append(prob, k_new, v_new, block_table, context_lens, k_cache, v_cache, &append_args);
+  if (rc != PDA_OK) return rc;
+  rc = prepare_step(prob, q, k_cache, v_cache, block_table, context_lens, scale, out, workspace, workspace_bytes,
+                    &plan, &args);
+  if (rc != PDA_OK) return rc;
+  pda_step_graph* g = new (std::nothrow) pda_step_graph{nullptr, nullptr, prob->num_seqs == 0};
+  if (!g) return PDA_ERR_HIP;
+  if (g->empty) {
+    *graph = g;
+    return PDA_OK;
+  }
+  hipStream_t s = nullptr;
+  if (hipStreamCreateWithFlags(&s, hipStreamNonBlocking) != hipSuccess) {
+    delete g;
+    return PDA_ERR_HIP;
+  }
+  if (hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal) != hipSuccess) {
+    rc = PDA_ERR_HIP;
+  } else {
+    // the same launches as pda_append_kv + pda_decode
+    if (launch_append_of(prob, append_args, k_new, v_new, k_cache, v_cache, s) != hipSuccess ||
+        pda::launch_order(args, s) != hipSuccess || pda::launch_partition(args, prob->head_dim, s) != hipSuccess ||
+        (plan.slots > 0 && pda::launch_merge(args, prob->head_dim, s) != hipSuccess))
+      rc = PDA_ERR_HIP;
+    hipGraph_t captured = nullptr;
+    const hipError_t end = hipStreamEndCapture(s, &captured);  // always ends the capture
+    g->graph = captured;
+    if (rc == PDA_OK && (end != hipSuccess || !captured)) rc = PDA_ERR_HIP;
+    if (rc == PDA_OK && hipGraphInstantiate(&g->exec, captured, nullptr, nullptr, 0) != hipSuccess) rc = PDA_ERR_HIP;
+  }
+  (void)hipStreamDestroy(s);
+  if (rc != PDA_OK) {
+    pda_step_graph_destroy(g);
+    return rc;
+  }
+  *graph = g;
+  return PDA_OK;
+}
+
+int pda_step_graph_launch(pda_step_graph* graph, hipStream_t stream) {
+  if (!graph) return PDA_ERR_NULL;
+  if (graph->empty) return PDA_OK;
+  return hipGraphLaunch(graph->exec, stream) == hipSuccess ? PDA_OK : PDA_ERR_HIP;
+}
+
+int pda_step_graph_destroy(pda_step_graph* graph) {
+  if (!graph) return PDA_OK;
+  int rc = PDA_OK;
+  if (graph->exec && hipGraphExecDestroy(graph->exec) != hipSuccess) rc = PDA_ERR_HIP;
+  if (graph->graph && hipGraphDestroy(graph->graph) != hipSuccess) rc = PDA_ERR_HIP;
+  delete graph;
+  return rc;
 }
 
 int pda_validate_host(const pda_problem* prob, const int32_t* block_table, const int32_t* context_lens,
@@ -222,9 +338,10 @@ const char* pda_status_string(int status) {
     case PDA_ERR_SHAPE: return "PDA_ERR_SHAPE: sizes out of range or inconsistent";
     case PDA_ERR_UNSUPPORTED: return "PDA_ERR_UNSUPPORTED: head_dim must be 64 or 128, block_size 16, Hq/Hkv <= 16";
     case PDA_ERR_WORKSPACE: return "PDA_ERR_WORKSPACE: workspace missing or smaller than pda_workspace_bytes()";
-    case PDA_ERR_ALIGNMENT: return "PDA_ERR_ALIGNMENT: q/k_cache/v_cache/workspace need 16-byte alignment, out 4-byte";
+    case PDA_ERR_ALIGNMENT:
+      return "PDA_ERR_ALIGNMENT: q/k_cache/v_cache/k_new/v_new/workspace need 16-byte alignment, out 4-byte";
     case PDA_ERR_VALUE: return "PDA_ERR_VALUE: non-finite scale or invalid device contents";
-    case PDA_ERR_HIP: return "PDA_ERR_HIP: a HIP kernel launch failed";
+    case PDA_ERR_HIP: return "PDA_ERR_HIP: a HIP launch, graph capture or instantiation failed";
     default: return "unknown pda status";
   }
 }

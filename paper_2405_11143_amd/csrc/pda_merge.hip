@@ -2,12 +2,13 @@
 //
 // A context split into partitions k = 0..n-1 leaves, per query head, the
 // partition's reference maximum m_k (log2 domain), denominator l_k and
-// unnormalised output O_k.  Softmax over the whole context is recovered
+// unnormalised output O_k (a partition that the row does not reach has
+// m_k = -1e30, l_k = 0, O_k = 0).  Softmax over the whole context is recovered
 // exactly by rescaling every partition to the common maximum M = max_k m_k:
 //   out = sum_k 2^(m_k - M) O_k / sum_k 2^(m_k - M) l_k.
 // The output sum runs in ascending k and the denominator in a fixed
-// butterfly, so the result is reproducible.  One wavefront per (sequence,
-// query head); each lane owns D/64 output columns.
+// butterfly, so the result is reproducible.  One wavefront per output row
+// (sequence, new token, query head); each lane owns D/64 output columns.
 #include "pda_internal.h"
 
 namespace pda {
@@ -56,7 +57,7 @@ __device__ __forceinline__ void merge_partitions(const StepArgs& a, size_t first
   }
   const float lsum = wave_sum(lpart);
 #pragma unroll
-  for (int e = 0; e < PER; ++e) orow[lane * PER + e] = acc[e] / lsum;
+  for (int e = 0; e < PER; ++e) orow[lane * PER + e] = lsum > 0.f ? acc[e] / lsum : acc[e];  // 0: sees nothing
 }
 
 __device__ __forceinline__ int clamped_len(const StepArgs& a, int b) {
@@ -64,12 +65,16 @@ __device__ __forceinline__ int clamped_len(const StepArgs& a, int b) {
   return L < 0 ? 0 : (L > a.max_context_len ? a.max_context_len : L);
 }
 
-// Partition k of row (b, h) sits at slot row * P + k.
+// Partition k of output row (b, i, h) sits at slot row * P + k, with
+// row = (b * n + i) * Hq + h; the row has as many partitions as the query
+// chunk of new token i sees.
 template <int D>
 __global__ void __launch_bounds__(kWaveSize) merge_kernel(const StepArgs a) {
-  const int row = blockIdx.x;  // b * Hq + h
-  const int L = clamped_len(a, row / a.num_q_heads);
-  const int nparts = (L + a.partition_tokens - 1) / a.partition_tokens;
+  const int row = blockIdx.x;
+  const int i = (row / a.num_q_heads) % a.num_query_tokens;
+  const int L = clamped_len(a, row / (a.num_q_heads * a.num_query_tokens));
+  const int vis = chunk_visible(a, L, i / a.query_chunk);
+  const int nparts = vis > 0 ? (vis + a.partition_tokens - 1) / a.partition_tokens : 0;
   if (nparts <= 1) return;  // pass 1 wrote the final row
   merge_partitions<D>(a, (size_t)row * a.num_partitions, 1, nparts, a.out + (size_t)row * D);
 }
@@ -77,7 +82,7 @@ __global__ void __launch_bounds__(kWaveSize) merge_kernel(const StepArgs a) {
 }  // namespace
 
 hipError_t launch_merge(const StepArgs& a, int head_dim, hipStream_t stream) {
-  const unsigned grid = (unsigned)a.num_seqs * (unsigned)a.num_q_heads;
+  const unsigned grid = (unsigned)a.num_seqs * (unsigned)a.num_query_tokens * (unsigned)a.num_q_heads;
   if (head_dim == 64)
     hipLaunchKernelGGL(merge_kernel<64>, dim3(grid), dim3(kWaveSize), 0, stream, a);
   else if (head_dim == 128)

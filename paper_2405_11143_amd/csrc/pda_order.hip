@@ -1,5 +1,5 @@
-// Work order of pass 1: the (partition, sequence, KV head) items, largest
-// partition first.
+// Work order of pass 1: the (partition, sequence, KV head, query chunk)
+// items, largest partition first.
 //
 // Pass 1 launches one workgroup per item and the GPU starts workgroups in
 // index order, so the order of the items is the schedule.  Contexts are
@@ -13,7 +13,8 @@
 //
 // One workgroup does a counting sort of the B*P (sequence, partition) pairs
 // by size in blocks (classes capped at kOrderBuckets - 1 blocks) with LDS
-// atomics, then writes the Hkv items of each pair.  The order within a size
+// atomics, then writes the items of each pair (one per KV head and query
+// chunk).  The order within a size
 // class depends on atomic timing; no result does -- every item computes the
 // same values whichever workgroup runs it.
 #include "pda_internal.h"
@@ -63,12 +64,12 @@ __global__ void __launch_bounds__(kOrderThreads) order_kernel(const StepArgs a) 
     }
   }
   __syncthreads();
-  const int Hkv = a.num_kv_heads;
+  const int HC = a.num_kv_heads * a.num_query_chunks;  // items per pair
   for (int idx = tid; idx < pairs; idx += kOrderThreads) {
     const int pos = atomicAdd(&s_count[bucket(idx)], 1);
     const int b = idx % B;
     const int p = idx / B;
-    for (int g = 0; g < Hkv; ++g) a.order[(size_t)pos * Hkv + g] = (p * B + b) * Hkv + g;
+    for (int g = 0; g < HC; ++g) a.order[(size_t)pos * HC + g] = (p * B + b) * HC + g;
   }
 }
 

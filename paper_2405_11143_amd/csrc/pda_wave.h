@@ -1,42 +1,51 @@
-// One wavefront's share of paged decode attention on gfx950: single-query
-// attention of the G query heads of one KV head over a run of 16-token
-// blocks of one sequence (the rollout decode step the paper runs through
-// vLLM's PagedAttention: Section 3.2; Appendix C, rollout generation).  Both
-// schedules (pda_partition.hip, pda_stream.hip) are built from it.
+// One wavefront's share of paged attention on gfx950: up to 16 query rows --
+// the G query heads of one KV head, for one or several new tokens of one
+// sequence -- over a run of 16-token blocks of that sequence's context (the
+// rollout decode step the paper runs through vLLM's PagedAttention, and its
+// multi-token form for speculative decoding and chunked prefill: Section
+// 3.2; Appendix C, rollout generation).  The partition kernel
+// (pda_partition.hip) is built from it.
 //
-// Mapping onto CDNA4 (64-wide wavefronts, MFMA, LDS):
+// Mapping onto CDNA4 (64-wide wavefronts, MFMA):
+//  * Lanes.  Lane l = 16 kg + n works for query row n (rows past the last
+//    real one repeat real rows) and, in each block, for tokens 4kg .. 4kg+3.
+//    Everything a query row needs -- its running max, its denominator, its
+//    rescale factor and its output -- lives in the four lanes n, n+16, n+32,
+//    n+48, so the softmax needs no exchange through LDS.
 //  * Tiles.  A wavefront prefetches the next block's K and V tiles (16 x D
 //    bf16 each) into registers while it computes on the current one.  Every
 //    tile load is a buffer load (descriptor = the tile, so no read can leave
-//    it) whose instruction reads 1 KiB of contiguous memory (whole cache
-//    lines) with the non-temporal hint: the cache is streamed once, and on
+//    it) with the non-temporal hint: the cache is streamed once, and on
 //    MI355X the hint lifts a plain 4 KiB-tile gather from ~6.1 to ~6.9 TB/s.
-//    All K and V loads of a lane share one 32-bit offset register.
-//  * Scores.  S[G][16] = Q_g K^T is one small dense contraction per block:
-//    D/32 MFMA f32_16x16x32_bf16 with the G query heads (repeated to fill 16
-//    rows) as the A operand and the K tile as the B operand.  The K cache
-//    stores each block as D/8 chunks of [16 slots][8 elements], so the B
-//    fragment of lane l in k-step c -- 8 consecutive d of token l%16, chunk
-//    4c + l/16 -- is exactly the 16 bytes at offset 1024c + 16l of the tile.
-//    The A operand (q) uses the same assignment of d to (k-step, k-group,
-//    element), so the contraction is unchanged.
-//  * Softmax.  A lane holds the scores of 4 head rows for one token.  The
-//    running maximum is moved only when some score of the block exceeds it by
-//    more than 2^8 (a wavefront vote); then the block max of each row is a
-//    16-lane all-reduce of four DPP moves (quad swaps, half-row and row
-//    mirror) and the state is rescaled.  Otherwise probabilities are taken
-//    against the stale maximum (they stay below 2^8, far inside fp32), so
-//    most blocks need neither the reduction nor the O rescale; the result is
-//    the same softmax.  Each lane accumulates the denominator of its own
-//    token column; columns are summed once, at the end.
-//  * P V runs on the VALU in fp32: lane (phase, chunk) owns 8 consecutive d
-//    for all G heads and the tokens of its phase; the V tile offsets that hold
-//    those elements are the same 16l + 1024i as for K.  The probabilities and
-//    rescale factors of a block travel from the MFMA layout to this layout
-//    through LDS (double-buffered per wavefront; a wavefront barrier only).
-//  * Tokens past the context in the last block are removed by selection, not
-//    by multiplying with zero, so whatever those slots hold (NaN included)
-//    never reaches the result.
+//    A K load instruction reads 1 KiB of contiguous memory; a V load reads
+//    four whole 256-byte token rows (D = 128).
+//  * Scores, transposed.  S^T = K Q^T is D/32 MFMA f32_16x16x32_bf16 per
+//    block with the K tile as the A operand (16 token rows) and the query
+//    rows as the B operand.  The K cache stores each block as D/8 chunks of
+//    [16 slots][8 elements], so the A fragment of lane l in k-step c -- 8
+//    consecutive d of token l%16, chunk 4c + l/16 -- is exactly the 16 bytes
+//    at offset 1024c + 16l of the tile; q uses the same assignment of d to
+//    (k-step, k-group, element).  The result leaves lane (kg, n) with the
+//    scores of query row n for tokens 4kg .. 4kg+3.
+//  * Softmax.  The running maximum is moved only when some score of the block
+//    exceeds it by more than 2^8 (a wavefront vote); then each row's block
+//    max is reduced over its four lanes and the state is rescaled.
+//    Otherwise probabilities are taken against the stale maximum (they stay
+//    below 2^8, far inside fp32), so most blocks need neither the reduction
+//    nor the rescale; the result is the same softmax.
+//  * P V, transposed, on MFMA.  O^T = V^T P^T is D/16 MFMA f32_16x16x16_bf16
+//    per block and half: the probabilities of lane (kg, n) are already the B
+//    fragment (column n, k-group kg), and the A fragment of lane (kg, n) is
+//    4 tokens x 1 column of the V tile, picked out of the 16-byte row pieces
+//    the lane loaded.  Each probability p is split into bf16 hi = p with the
+//    low 16 bits cleared and lo = bf16(p - hi), and both halves go through
+//    the MFMA, so P keeps about 16 significant bits (relative error below
+//    2^-15) instead of bf16's 8.  The output of row n stays in the lanes of
+//    row n: D/16 accumulators of 4 floats each, whatever the row count.
+//  * Tokens a row must not see (past the context in the last block, or after
+//    the row's own position for multi-token queries) are removed by
+//    selection: score -inf, and V rows past the context set to zero, so
+//    whatever those slots hold (NaN included) never reaches the result.
 #pragma once
 
 #include "pda_internal.h"
@@ -44,29 +53,9 @@
 namespace pda {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short shortx4_t __attribute__((ext_vector_type(4)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
 typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
-
-template <int CTRL>
-__device__ __forceinline__ float dpp_move(float x) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
-}
-
-// All-reduce over each row of 16 lanes; every lane of the row gets the same bits.
-__device__ __forceinline__ float row16_max(float x) {
-  x = fmaxf(x, dpp_move<0xB1>(x));   // quad_perm(1,0,3,2)
-  x = fmaxf(x, dpp_move<0x4E>(x));   // quad_perm(2,3,0,1)
-  x = fmaxf(x, dpp_move<0x141>(x));  // row_half_mirror
-  x = fmaxf(x, dpp_move<0x140>(x));  // row_mirror
-  return x;
-}
-__device__ __forceinline__ float row16_sum(float x) {
-  x += dpp_move<0xB1>(x);
-  x += dpp_move<0x4E>(x);
-  x += dpp_move<0x141>(x);
-  x += dpp_move<0x140>(x);
-  return x;
-}
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -86,83 +75,67 @@ __device__ __forceinline__ uint4 load_stream(__amdgpu_buffer_rsrc_t r, int offse
   return make_uint4(t[0], t[1], t[2], t[3]);
 }
 
-// Widen 8 packed bf16 (a 16-byte load) to fp32: bf16 is the top half of fp32.
-__device__ __forceinline__ void unpack8(const uint4 u, float (&f)[8]) {
-  f[0] = __uint_as_float(u.x << 16);
-  f[1] = __uint_as_float(u.x & 0xffff0000u);
-  f[2] = __uint_as_float(u.y << 16);
-  f[3] = __uint_as_float(u.y & 0xffff0000u);
-  f[4] = __uint_as_float(u.z << 16);
-  f[5] = __uint_as_float(u.z & 0xffff0000u);
-  f[6] = __uint_as_float(u.w << 16);
-  f[7] = __uint_as_float(u.w & 0xffff0000u);
+// Two bf16 taken from the same half of two dwords, packed low-first:
+// hi_half ? (a >> 16) | (b & 0xffff0000) : (a & 0xffff) | (b << 16).
+__device__ __forceinline__ unsigned pack_halves(unsigned a, unsigned b, bool hi_half) {
+  return __builtin_amdgcn_perm(b, a, hi_half ? 0x07060302u : 0x05040100u);
 }
 
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-template <int G, int D>
+template <int D>
 struct WaveAttention {
-  static_assert(G >= 1 && G <= kMaxGroup, "query heads per KV head");
   static_assert(D == 64 || D == 128, "head_dim");
-  static constexpr int NC = D / 32;               // MFMA k-steps per block
-  static constexpr int CPR = D / 8;               // 16-byte chunks per V row
-  static constexpr int NPH = kWaveSize / CPR;     // token phases of the P.V layout
-  static constexpr int TPL = kBlockTokens / NPH;  // tokens per lane per block in P.V
-  static constexpr int GP = (G + 3) & ~3;         // head count padded to float4
-  static constexpr int kTileBytes = kBlockTokens * D * 2;
+  static constexpr int NC = D / 32;               // score MFMA k-steps per block
+  static constexpr int VT = D / 16;               // P.V MFMA output tiles (16 d each)
+  static constexpr int kRowBytes = D * 2;         // one token row of a V tile
+  static constexpr int kTileBytes = kBlockTokens * kRowBytes;
   static constexpr float kNegInf = -__builtin_huge_valf();
+  static constexpr float kFloor = -1e30f;         // running max of a row that has seen no token
   static constexpr float kRescaleSlack = 8.f;     // log2 of the largest unnormalised probability
 
-  // Per-wavefront LDS for the layout change MFMA -> P.V (double-buffered).
-  struct Exchange {
-    float p[2][kBlockTokens][GP];
-    float alpha[2][GP];
-  };
-
-  Exchange* x;
-  int lane, n, kg, tp;
+  int lane, n, kg;
+  int k_off, v_off;  // this lane's byte offsets in a K / V tile
+  int lim_off;       // this lane's query row sees tokens t < L - lim_off
   float scale_log2;
-  bool bad;  // a block id outside the pool was met (never dereferenced)
+  bool bad;          // a block id outside the pool was met (never dereferenced)
   bf16x8_t qa[NC];
-  float o[G][8];
-  float m_run[4], l_run[4];
+  floatx4_t o[VT];
+  float m_run, l_run;
 
-  __device__ __forceinline__ WaveAttention(Exchange* ex, float scale_log2_)
-      : x(ex), scale_log2(scale_log2_), bad(false) {
+  __device__ __forceinline__ explicit WaveAttention(float scale_log2_) : scale_log2(scale_log2_), bad(false) {
     lane = threadIdx.x & (kWaveSize - 1);
-    n = lane & 15;       // MFMA row of A (head) / column of B (token)
-    kg = lane >> 4;      // MFMA k-group: k-step c covers d = 8 * (4c + kg) + e
-    tp = lane / CPR;     // P.V: d in [8 * (lane % CPR), +8) for tokens tp, tp + NPH, ...
+    n = lane & 15;
+    kg = lane >> 4;
+    k_off = 16 * lane;
+    v_off = 4 * kg * kRowBytes + 16 * (n % (D / 8));
   }
 
-  // Load the G query rows starting at `q_rows` (A operand, d = 32c + 8kg + e)
-  // and clear the softmax state and the bad-id flag.
-  __device__ __forceinline__ void start(const uint16_t* q_rows) {
+  // The output element d of this lane's row held in accumulator t, register i.
+  // D = 128: A row r of tile t is column 8r + t, and C row 4kg + i is A row
+  // 4kg + i.  D = 64: lanes n and n + 8 load the same 8 columns, and A row r
+  // of tile t is column 8 (r % 8) + t + 4 (r / 8).
+  __device__ __forceinline__ int d_of(int i, int t) const {
+    const int r = 4 * kg + i;
+    return D == 128 ? 8 * r + t : 8 * (r & 7) + t + 4 * (r >> 3);
+  }
+
+  // Load this lane's query row (`q_row`: D bf16) and clear the state; the row
+  // sees context tokens t < L - lim_off_.
+  __device__ __forceinline__ void start(const uint16_t* q_row, int lim_off_) {
     bad = false;
-    const uint16_t* qrow = q_rows + (n % G) * D + kg * 8;
+    lim_off = lim_off_;
+    const uint16_t* p = q_row + kg * 8;
 #pragma unroll
-    for (int c = 0; c < NC; ++c)
-      qa[c] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(qrow + 32 * c));
+    for (int c = 0; c < NC; ++c) qa[c] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(p + 32 * c));
 #pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) o[h][e] = 0.f;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      m_run[i] = kNegInf;
-      l_run[i] = 0.f;
-    }
+    for (int t = 0; t < VT; ++t) o[t] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+    m_run = kFloor;
+    l_run = 0.f;
   }
 
   // Issue the K and V tile loads of one block (or, when !needed, loads through a
   // zero-length descriptor that the hardware drops without touching memory).
-  __device__ __forceinline__ void load_tiles(uint4 (&kr)[NC], uint4 (&vr)[TPL], const char* kpool,
-                                             const char* vpool, size_t block_bytes, int num_blocks, int phys,
-                                             bool needed) {
+  __device__ __forceinline__ void load_tiles(uint4 (&kr)[NC], uint4 (&vr)[4], const char* kpool, const char* vpool,
+                                             size_t block_bytes, int num_blocks, int phys, bool needed) {
     if ((unsigned)phys >= (unsigned)num_blocks) {  // contract violation: never read outside the pool
       bad = true;
       phys = 0;
@@ -171,91 +144,107 @@ struct WaveAttention {
     const int bytes = needed ? kTileBytes : 0;
     const __amdgpu_buffer_rsrc_t rk = tile_rsrc(kpool + off, bytes);
     const __amdgpu_buffer_rsrc_t rv = tile_rsrc(vpool + off, bytes);
-    const int lane_off = lane * 16;
 #pragma unroll
-    for (int c = 0; c < NC; ++c) kr[c] = load_stream(rk, lane_off + c * 1024);
+    for (int c = 0; c < NC; ++c) kr[c] = load_stream(rk, k_off + c * 1024);
 #pragma unroll
-    for (int i = 0; i < TPL; ++i) vr[i] = load_stream(rv, lane_off + i * 1024);
+    for (int e = 0; e < 4; ++e) vr[e] = load_stream(rv, v_off + e * kRowBytes);
   }
 
-  // Fold one block (logical tokens tok0 .. tok0+15, context length L) into the state.
-  __device__ __forceinline__ void process(const uint4 (&kr)[NC], const uint4 (&vr)[TPL], int tok0, int L, int par) {
-    // ---- scores: S = Q_g K^T on MFMA; lane holds rows 4*kg+i, column n ----
+  // Fold one block (logical tokens tok0 .. tok0+15) into the state.  `L` is
+  // the context length, `l_first` the limit of the chunk's first row (every
+  // row sees tokens below it) and `l_vis` the limit of its last row (no row
+  // sees a token at or above it).
+  __device__ __forceinline__ void process(const uint4 (&kr)[NC], uint4 (&vr)[4], int tok0, int L, int l_first,
+                                          int l_vis) {
+    // ---- scores S^T = K Q^T: lane (kg, n) gets row n, tokens 4kg + i ----
     floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int c = 0; c < NC; ++c)
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[c], __builtin_bit_cast(bf16x8_t, kr[c]), acc, 0, 0, 0);
-    const bool tail = tok0 + kBlockTokens > L;  // wave-uniform
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kr[c]), qa[c], acc, 0, 0, 0);
+    const bool tail = tok0 + kBlockTokens > l_first;  // wave-uniform
+    const int lim = L - lim_off;
     float sc[4];
     bool grow = false;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       sc[i] = acc[i] * scale_log2;
-      if (tail && tok0 + n >= L) sc[i] = kNegInf;
-      grow |= sc[i] > m_run[i] + kRescaleSlack;
+      if (tail && tok0 + 4 * kg + i >= lim) sc[i] = kNegInf;
+      grow |= sc[i] > m_run + kRescaleSlack;
     }
     // ---- move the running max only when a score outgrows it by 2^8 ----
-    const bool rescale = __builtin_amdgcn_ballot_w64(grow) != 0;  // wave-uniform
-    float al[4] = {1.f, 1.f, 1.f, 1.f};
-    if (rescale) {
+    if (__builtin_amdgcn_ballot_w64(grow) != 0) {  // wave-uniform
+      float mx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mn = fmaxf(m_run, mx);  // the same in the four lanes of the row
+      const float al = exp2_fast(m_run - mn);
+      m_run = mn;
+      l_run *= al;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float mn = fmaxf(m_run[i], row16_max(sc[i]));  // finite: the block has a valid token
-        al[i] = exp2_fast(m_run[i] - mn);
-        l_run[i] *= al[i];
-        m_run[i] = mn;
-      }
+      for (int t = 0; t < VT; ++t) o[t] *= al;
     }
     float pr[4];
 #pragma unroll
+    for (int i = 0; i < 4; ++i) pr[i] = exp2_fast(sc[i] - m_run);
+    l_run += (pr[0] + pr[1]) + (pr[2] + pr[3]);
+    // ---- P^T as two bf16 B fragments: hi = p truncated, lo = bf16(p - hi) ----
+    unsigned hb[4];
+    float lo[4];
+#pragma unroll
     for (int i = 0; i < 4; ++i) {
-      pr[i] = exp2_fast(sc[i] - m_run[i]);
-      l_run[i] += pr[i];
+      hb[i] = __float_as_uint(pr[i]) & 0xffff0000u;
+      lo[i] = pr[i] - __uint_as_float(hb[i]);
     }
-    if (4 * kg < G) {
-      *reinterpret_cast<float4*>(&x->p[par][n][4 * kg]) = make_float4(pr[0], pr[1], pr[2], pr[3]);
-      if (rescale && n == 0)
-        *reinterpret_cast<float4*>(&x->alpha[par][4 * kg]) = make_float4(al[0], al[1], al[2], al[3]);
+    const shortx4_t b_hi = __builtin_bit_cast(
+        shortx4_t, make_uint2(pack_halves(hb[0], hb[1], true), pack_halves(hb[2], hb[3], true)));
+    typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+    const bf16x4_t lo4 = {(__bf16)lo[0], (__bf16)lo[1], (__bf16)lo[2], (__bf16)lo[3]};
+    const shortx4_t b_lo = __builtin_bit_cast(shortx4_t, lo4);
+    // ---- V^T A fragments; rows past what the chunk sees are zeroed ----
+    if (tail) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (tok0 + 4 * kg + e >= l_vis) vr[e] = make_uint4(0u, 0u, 0u, 0u);
     }
-    wave_lds_sync();
-
-    // ---- O = alpha * O + P V on the VALU ----
-    if (rescale) {
-      float alpha[GP];
+    unsigned w[4][2];  // the 4 bf16 columns of this lane's tiles, per token row e
 #pragma unroll
-      for (int h4 = 0; h4 < GP; h4 += 4) {
-        const float4 t = *reinterpret_cast<const float4*>(&x->alpha[par][h4]);
-        alpha[h4] = t.x; alpha[h4 + 1] = t.y; alpha[h4 + 2] = t.z; alpha[h4 + 3] = t.w;
+    for (int e = 0; e < 4; ++e) {
+      if (D == 128) {
+        w[e][0] = 0;  // unused: tiles read vr directly below
+        w[e][1] = 0;
+      } else {
+        const bool upper = n >= 8;
+        w[e][0] = upper ? vr[e].z : vr[e].x;
+        w[e][1] = upper ? vr[e].w : vr[e].y;
       }
-#pragma unroll
-      for (int h = 0; h < G; ++h)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o[h][e] *= alpha[h];
     }
 #pragma unroll
-    for (int i = 0; i < TPL; ++i) {
-      const int row = i * NPH + tp;
-      float f[8];
-      unpack8(vr[i], f);
-      if (tail && tok0 + row >= L) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) f[e] = 0.f;
+    for (int t = 0; t < VT; ++t) {
+      unsigned r0, r1, r2, r3;  // dword holding column t of token rows 0..3
+      if (D == 128) {
+        const int dw = t >> 1;
+        r0 = dw == 0 ? vr[0].x : dw == 1 ? vr[0].y : dw == 2 ? vr[0].z : vr[0].w;
+        r1 = dw == 0 ? vr[1].x : dw == 1 ? vr[1].y : dw == 2 ? vr[1].z : vr[1].w;
+        r2 = dw == 0 ? vr[2].x : dw == 1 ? vr[2].y : dw == 2 ? vr[2].z : vr[2].w;
+        r3 = dw == 0 ? vr[3].x : dw == 1 ? vr[3].y : dw == 2 ? vr[3].z : vr[3].w;
+      } else {
+        const int dw = t >> 1;
+        r0 = w[0][dw];
+        r1 = w[1][dw];
+        r2 = w[2][dw];
+        r3 = w[3][dw];
       }
-      float ph[GP];
-#pragma unroll
-      for (int h4 = 0; h4 < GP; h4 += 4) {
-        const float4 t = *reinterpret_cast<const float4*>(&x->p[par][row][h4]);
-        ph[h4] = t.x; ph[h4 + 1] = t.y; ph[h4 + 2] = t.z; ph[h4 + 3] = t.w;
-      }
-#pragma unroll
-      for (int h = 0; h < G; ++h)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o[h][e] = fmaf(ph[h], f[e], o[h][e]);
+      const bool hi_half = t & 1;
+      const shortx4_t a = __builtin_bit_cast(
+          shortx4_t, make_uint2(pack_halves(r0, r1, hi_half), pack_halves(r2, r3, hi_half)));
+      o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b_hi, o[t], 0, 0, 0);
+      o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b_lo, o[t], 0, 0, 0);
     }
   }
 
   // Stream blocks [j0, j1) of one sequence: block ids in `table_row`, tiles of
-  // this KV head at kpool/vpool + id * block_bytes, context length L.
+  // this KV head at kpool/vpool + id * block_bytes; L, l_first, l_vis as in
+  // process().
   //
   // Two register buffers: the tiles of block i+1 are in flight while block i
   // is computed.  Every load is unconditional, so the compiler counts
@@ -264,10 +253,10 @@ struct WaveAttention {
   // the current tiles.  Past the end of the run the prefetch gets a
   // zero-length descriptor.  Block ids come 64 at a time, one per lane, and
   // are read with readlane, so no tile load waits on a scalar load.
-  __device__ __forceinline__ void run(const int32_t* table_row, int j0, int j1, int L, const char* kpool,
-                                      const char* vpool, size_t block_bytes, int num_blocks) {
+  __device__ __forceinline__ void run(const int32_t* table_row, int j0, int j1, int L, int l_first, int l_vis,
+                                      const char* kpool, const char* vpool, size_t block_bytes, int num_blocks) {
     const int cnt = j1 - j0;
-    uint4 k0[NC], v0[TPL], k1[NC], v1[TPL];
+    uint4 k0[NC], v0[4], k1[NC], v1[4];
     for (int c0 = 0; c0 < cnt; c0 += kWaveSize) {
       const int cn = min(kWaveSize, cnt - c0);
       const int jc = j0 + c0;
@@ -277,34 +266,21 @@ struct WaveAttention {
       for (int i = 0; i < cn; i += 2) {
         load_tiles(k1, v1, kpool, vpool, block_bytes, num_blocks, id(min(i + 1, cn - 1)), i + 1 < cn);
         __builtin_amdgcn_sched_barrier(0);
-        process(k0, v0, (jc + i) * kBlockTokens, L, 0);
+        process(k0, v0, (jc + i) * kBlockTokens, L, l_first, l_vis);
         if (i + 1 >= cn) break;
         load_tiles(k0, v0, kpool, vpool, block_bytes, num_blocks, id(min(i + 2, cn - 1)), i + 2 < cn);
         __builtin_amdgcn_sched_barrier(0);
-        process(k1, v1, (jc + i + 1) * kBlockTokens, L, 1);
+        process(k1, v1, (jc + i + 1) * kBlockTokens, L, l_first, l_vis);
       }
     }
   }
 
-  // Reduce the per-lane state: denominators over the 16 token columns of each
-  // row, O over the token phases.  Afterwards lanes < CPR hold O[h][8*lane + e]
-  // for every head h < G, and every lane holds each head's max mh[h] and
-  // denominator lh[h] (head h sits in MFMA row h: k-group h/4, register h%4).
-  float mh[G], lh[G];
+  // Sum each row's denominator over its four lanes (a fixed butterfly, so the
+  // four lanes hold the same bits).  The running max is already the same in
+  // the four lanes, and the output of row n is complete in them.
   __device__ __forceinline__ void finish() {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) l_run[i] = row16_sum(l_run[i]);
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      mh[h] = readlane_f(m_run[h & 3], 16 * (h >> 2));
-      lh[h] = readlane_f(l_run[h & 3], 16 * (h >> 2));
-    }
-#pragma unroll
-    for (int h = 0; h < G; ++h)
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-#pragma unroll
-        for (int s = CPR; s < kWaveSize; s <<= 1) o[h][e] += __shfl_xor(o[h][e], s);
+    l_run += __shfl_xor(l_run, 16);
+    l_run += __shfl_xor(l_run, 32);
   }
 };
 

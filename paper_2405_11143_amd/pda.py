@@ -10,7 +10,7 @@ from __future__ import annotations
 
 import ctypes
 import os
-from typing import Optional, Tuple
+from typing import Tuple
 
 import numpy as np
 
@@ -20,15 +20,16 @@ LIB_PATH = os.path.join(_PKG, "libpda.so")
 PDA_OK, PDA_ERR_NULL, PDA_ERR_SHAPE, PDA_ERR_UNSUPPORTED = 0, 1, 2, 3
 PDA_ERR_WORKSPACE, PDA_ERR_ALIGNMENT, PDA_ERR_VALUE, PDA_ERR_HIP = 4, 5, 6, 7
 
-# Every symbol include/pda.h declares.
+# Every function include/pda.h declares.
 EXPORTED = ("pda_plan", "pda_workspace_bytes", "pda_decode", "pda_partition_attention",
-            "pda_merge_partitions", "pda_validate_host", "pda_status_string")
+            "pda_merge_partitions", "pda_append_kv", "pda_step_graph_create", "pda_step_graph_launch",
+            "pda_step_graph_destroy", "pda_validate_host", "pda_status_string")
 
 
 class pda_problem(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int32) for name in (
         "num_seqs", "num_q_heads", "num_kv_heads", "head_dim", "block_size", "num_blocks",
-        "max_blocks_per_seq", "max_context_len", "partition_tokens")]
+        "max_blocks_per_seq", "max_context_len", "partition_tokens", "num_query_tokens")]
 
 
 class pda_plan_info(ctypes.Structure):
@@ -65,6 +66,11 @@ def load_library(path: str = LIB_PATH):
     lib.pda_decode.argtypes = step
     lib.pda_partition_attention.argtypes = step
     lib.pda_merge_partitions.argtypes = [P, vp, vp, vp, sz, vp]
+    lib.pda_append_kv.argtypes = [P, vp, vp, vp, vp, vp, vp, vp]
+    lib.pda_step_graph_create.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, ctypes.c_float, vp, vp, sz,
+                                          ctypes.POINTER(vp)]
+    lib.pda_step_graph_launch.argtypes = [vp, vp]
+    lib.pda_step_graph_destroy.argtypes = [vp]
     lib.pda_validate_host.argtypes = [P, vp, vp, ctypes.POINTER(ctypes.c_int64)]
     lib.pda_status_string.argtypes = [i32]
     lib.pda_status_string.restype = ctypes.c_char_p
@@ -80,9 +86,10 @@ def pda_status_string(status: int) -> str:
 
 
 def make_problem(num_seqs, num_q_heads, num_kv_heads, head_dim, num_blocks, max_blocks_per_seq,
-                 max_context_len, partition_tokens=0, block_size=16) -> pda_problem:
+                 max_context_len, partition_tokens=0, block_size=16, num_query_tokens=1) -> pda_problem:
     return pda_problem(int(num_seqs), int(num_q_heads), int(num_kv_heads), int(head_dim), int(block_size),
-                       int(num_blocks), int(max_blocks_per_seq), int(max_context_len), int(partition_tokens))
+                       int(num_blocks), int(max_blocks_per_seq), int(max_context_len), int(partition_tokens),
+                       int(num_query_tokens))
 
 
 def pda_plan(prob: pda_problem) -> dict:
@@ -112,18 +119,34 @@ def pda_validate_host(prob: pda_problem, block_table, context_lens) -> Tuple[int
     return rc, bad.value
 
 
-def _problem_from(q, k_cache, block_table, max_context_len, partition_tokens) -> pda_problem:
-    import torch
+def _query_shape(q):
+    """(B, n, Hq, D) of q [B][Hq][D] (n = 1) or [B][n][Hq][D]."""
+    if q.dim() == 3:
+        return q.shape[0], 1, q.shape[1], q.shape[2]
+    if q.dim() == 4:
+        return tuple(q.shape)
+    raise ValueError("q must be [B][Hq][D] or [B][n][Hq][D]")
 
-    if q.dim() != 3 or k_cache.dim() != 5 or block_table.dim() != 2:
-        raise ValueError("q [B][Hq][D], k_cache [num_blocks][Hkv][D/8][16][8], block_table [B][max_blocks]")
-    B, Hq, D = q.shape
+
+def _problem_from(q, k_cache, block_table, max_context_len, partition_tokens) -> pda_problem:
+    if k_cache.dim() != 5 or block_table.dim() != 2:
+        raise ValueError("k_cache [num_blocks][Hkv][D/8][16][8], block_table [B][max_blocks]")
+    B, n, Hq, D = _query_shape(q)
     NB, Hkv, C, BS, E = k_cache.shape
     if C * E != D or E != 8 or block_table.shape[0] != B:
         raise ValueError("q, k_cache and block_table shapes disagree")
     if max_context_len is None:
         raise ValueError("max_context_len must be given (the host bound on context_lens)")
-    return make_problem(B, Hq, Hkv, D, NB, block_table.shape[1], max_context_len, partition_tokens, BS)
+    return make_problem(B, Hq, Hkv, D, NB, block_table.shape[1], max_context_len, partition_tokens, BS, n)
+
+
+def _require(name, t, dtype):
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
 
 
 def _check_tensors(q, k_cache, v_cache, block_table, context_lens, out):
@@ -132,12 +155,7 @@ def _check_tensors(q, k_cache, v_cache, block_table, context_lens, out):
     for name, t, dt in (("q", q, torch.bfloat16), ("k_cache", k_cache, torch.bfloat16),
                         ("v_cache", v_cache, torch.bfloat16), ("block_table", block_table, torch.int32),
                         ("context_lens", context_lens, torch.int32), ("out", out, torch.float32)):
-        if t.dtype != dt:
-            raise TypeError(f"{name} must be {dt}, got {t.dtype}")
-        if not t.is_cuda:
-            raise ValueError(f"{name} must be a device tensor")
-        if not t.is_contiguous():
-            raise ValueError(f"{name} must be contiguous")
+        _require(name, t, dt)
     NB, Hkv, C, BS, E = k_cache.shape
     if tuple(v_cache.shape) != (NB, Hkv, BS, C * E):
         raise ValueError("v_cache must be [num_blocks][Hkv][16][D] (k_cache is [num_blocks][Hkv][D/8][16][8])")
@@ -145,6 +163,17 @@ def _check_tensors(q, k_cache, v_cache, block_table, context_lens, out):
         raise ValueError("out must have the shape of q")
     if context_lens.shape != (q.shape[0],):
         raise ValueError("context_lens must be [B]")
+
+
+def _check_new_kv(k_new, v_new, q_shape, k_cache):
+    import torch
+
+    _require("k_new", k_new, torch.bfloat16)
+    _require("v_new", v_new, torch.bfloat16)
+    B, n, _, D = q_shape
+    Hkv = k_cache.shape[1]
+    if tuple(k_new.shape) != (B, n, Hkv, D) or tuple(v_new.shape) != (B, n, Hkv, D):
+        raise ValueError(f"k_new and v_new must be [B][n][Hkv][D] = {(B, n, Hkv, D)}")
 
 
 def _stream_handle(stream, device):
@@ -155,6 +184,17 @@ def _stream_handle(stream, device):
     return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
 
 
+def _workspace(prob, workspace, device):
+    import torch
+
+    need = pda_workspace_bytes(prob)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=device)
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    return workspace, ws_ptr, ws_bytes
+
+
 def _step(fn_name, q, k_cache, v_cache, block_table, context_lens, scale, out, max_context_len,
           partition_tokens, workspace, stream):
     import torch
@@ -163,11 +203,7 @@ def _step(fn_name, q, k_cache, v_cache, block_table, context_lens, scale, out, m
         out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
     _check_tensors(q, k_cache, v_cache, block_table, context_lens, out)
     prob = _problem_from(q, k_cache, block_table, max_context_len, partition_tokens)
-    need = pda_workspace_bytes(prob)
-    if workspace is None and need > 0:
-        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
-    ws_ptr = workspace.data_ptr() if workspace is not None else None
-    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    workspace, ws_ptr, ws_bytes = _workspace(prob, workspace, q.device)
     rc = getattr(load_library(), fn_name)(
         ctypes.byref(prob), q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(),
         context_lens.data_ptr(), ctypes.c_float(scale), out.data_ptr(), ws_ptr, ws_bytes,
@@ -179,10 +215,12 @@ def _step(fn_name, q, k_cache, v_cache, block_table, context_lens, scale, out, m
 
 def pda_decode(q, k_cache, v_cache, block_table, context_lens, scale: float, out=None, *,
                max_context_len: int, partition_tokens: int = 0, workspace=None, stream=None):
-    """One decode-attention step (both passes).  Tensors on the GPU:
-    q bf16 [B][Hq][D], k_cache bf16 [num_blocks][Hkv][D/8][16][8] (each block's
-    keys as D/8 chunks of 16 slots x 8 elements), v_cache bf16 [num_blocks][Hkv][16][D],
-    block_table int32 [B][max_blocks], context_lens int32 [B], out fp32 [B][Hq][D].
+    """One attention step (both passes).  Tensors on the GPU: q bf16
+    [B][Hq][D] (a decode step) or [B][n][Hq][D] (n new tokens per sequence,
+    the last n of its context, attending causally), k_cache bf16
+    [num_blocks][Hkv][D/8][16][8] (each block's keys as D/8 chunks of 16 slots
+    x 8 elements), v_cache bf16 [num_blocks][Hkv][16][D], block_table int32
+    [B][max_blocks], context_lens int32 [B], out fp32 shaped like q.
     `workspace` (uint8, >= pda_workspace_bytes) is allocated when not given;
     partition_tokens > 0 fixes the split-K partition size."""
     return _step("pda_decode", q, k_cache, v_cache, block_table, context_lens, scale, out, max_context_len,
@@ -205,3 +243,76 @@ def pda_merge_partitions(prob: pda_problem, context_lens, out, workspace, stream
     if rc != PDA_OK:
         raise PdaError(rc, "pda_merge_partitions")
     return out
+
+
+def pda_append_kv(k_new, v_new, block_table, context_lens, k_cache, v_cache, *, max_context_len: int,
+                  num_q_heads: int = None, stream=None):
+    """Store the K/V rows of each sequence's n new tokens (bf16 [B][n][Hkv][D])
+    at positions L - n .. L - 1 of its paged cache, in place."""
+    import torch
+
+    if k_new.dim() != 4:
+        raise ValueError("k_new must be [B][n][Hkv][D]")
+    B, n, Hkv, D = k_new.shape
+    for name, t, dt in (("k_cache", k_cache, torch.bfloat16), ("v_cache", v_cache, torch.bfloat16),
+                        ("block_table", block_table, torch.int32), ("context_lens", context_lens, torch.int32)):
+        _require(name, t, dt)
+    q_shape = (B, n, Hkv if num_q_heads is None else num_q_heads, D)
+    _check_new_kv(k_new, v_new, q_shape, k_cache)
+    NB, Hkv_c, C, BS, E = k_cache.shape
+    if Hkv_c != Hkv or C * E != D or tuple(v_cache.shape) != (NB, Hkv, BS, D):
+        raise ValueError("k_new/v_new and the caches disagree")
+    if block_table.dim() != 2 or block_table.shape[0] != B or context_lens.shape != (B,):
+        raise ValueError("block_table [B][max_blocks], context_lens [B]")
+    prob = make_problem(B, q_shape[2], Hkv, D, NB, block_table.shape[1], max_context_len, 0, BS, n)
+    rc = load_library().pda_append_kv(ctypes.byref(prob), k_new.data_ptr(), v_new.data_ptr(),
+                                      block_table.data_ptr(), context_lens.data_ptr(), k_cache.data_ptr(),
+                                      v_cache.data_ptr(), _stream_handle(stream, k_cache.device))
+    if rc != PDA_OK:
+        raise PdaError(rc, "pda_append_kv")
+
+
+class StepGraph:
+    """pda_step_graph: append + attention captured once as a HIP graph over
+    fixed buffers.  launch() replays it on a stream and reads the buffers'
+    current contents.  The tensors are kept alive for the graph's lifetime."""
+
+    def __init__(self, q, k_new, v_new, k_cache, v_cache, block_table, context_lens, scale: float, out=None, *,
+                 max_context_len: int, partition_tokens: int = 0, workspace=None):
+        import torch
+
+        if out is None:
+            out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+        _check_tensors(q, k_cache, v_cache, block_table, context_lens, out)
+        _check_new_kv(k_new, v_new, _query_shape(q), k_cache)
+        self.prob = _problem_from(q, k_cache, block_table, max_context_len, partition_tokens)
+        workspace, ws_ptr, ws_bytes = _workspace(self.prob, workspace, q.device)
+        self.out, self.workspace = out, workspace
+        self._keep = (q, k_new, v_new, k_cache, v_cache, block_table, context_lens)
+        handle = ctypes.c_void_p()
+        rc = load_library().pda_step_graph_create(
+            ctypes.byref(self.prob), q.data_ptr(), k_new.data_ptr(), v_new.data_ptr(), k_cache.data_ptr(),
+            v_cache.data_ptr(), block_table.data_ptr(), context_lens.data_ptr(), ctypes.c_float(scale),
+            out.data_ptr(), ws_ptr, ws_bytes, ctypes.byref(handle))
+        if rc != PDA_OK:
+            raise PdaError(rc, "pda_step_graph_create")
+        self._handle = handle
+
+    def launch(self, stream=None):
+        rc = load_library().pda_step_graph_launch(self._handle, _stream_handle(stream, self.out.device))
+        if rc != PDA_OK:
+            raise PdaError(rc, "pda_step_graph_launch")
+        return self.out
+
+    def close(self):
+        if getattr(self, "_handle", None) is not None:
+            rc = load_library().pda_step_graph_destroy(self._handle)
+            self._handle = None
+            if rc != PDA_OK:
+                raise PdaError(rc, "pda_step_graph_destroy")
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,107 @@
+"""GPU parity of the KV-cache append and of the captured step graph.
+
+The append is byte work: the GPU caches must equal the oracle's bit for bit
+(NaN poison included) after storing each sequence's n new tokens at positions
+L - n .. L - 1.  The step graph (append + attention captured once) is replayed
+several times with fresh inputs written between replays by ordinary eager
+work; every replay must equal the same step run eagerly through the C ABI,
+bit for bit, and the oracle within the attention tolerance.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from paper_2405_11143_amd import StepGraph, pda_append_kv, pda_decode
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS, MEAN_ABS = 8e-3, 1e-3
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return torch.device("cuda:0")
+
+
+def bits16(t):
+    return W.bf16_bits(t)
+
+
+@pytest.mark.parametrize("Hq,Hkv,D", [(32, 8, 128), (8, 2, 64), (16, 1, 128)], ids=str)
+@pytest.mark.parametrize("n", [1, 3, 16])
+def test_append_bit_exact(dev, Hq, Hkv, D, n):
+    lens = [0, 1, 2, 15, 16, 17, 31, 32, 33, 200, -3, 1000]
+    st = W.custom_structure(len(lens), Hq, Hkv, D, lens, seed=40 + n)
+    _, k, v = W.fill_values(st, dev, fill="nan")
+    kn, vn = W.fill_new_kv(st, n, dev)
+    k_ref, v_ref = oracle.append(bits16(kn), bits16(vn), st.block_table, st.context_lens, bits16(k), bits16(v))
+    bt = torch.from_numpy(st.block_table).to(dev)
+    ln = torch.from_numpy(st.context_lens).to(dev)
+    pda_append_kv(kn, vn, bt, ln, k, v, max_context_len=st.max_context_len, num_q_heads=Hq)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits16(k), k_ref), "K cache"
+    assert np.array_equal(bits16(v), v_ref), "V cache"
+
+
+def test_append_full_size(dev):
+    """The Llama-3-8B step's append (one new token per sequence) at full size."""
+    st = W.make_structure("llama3_8b")
+    _, k, v = W.fill_values(st, dev, fill="nan")
+    kn, vn = W.fill_new_kv(st, 1, dev)
+    k_ref, v_ref = oracle.append(bits16(kn), bits16(vn), st.block_table, st.context_lens, bits16(k), bits16(v))
+    pda_append_kv(kn, vn, torch.from_numpy(st.block_table).to(dev), torch.from_numpy(st.context_lens).to(dev),
+                  k, v, max_context_len=st.max_context_len, num_q_heads=st.Hq)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits16(k), k_ref) and np.array_equal(bits16(v), v_ref)
+
+
+def check(got, ref, what):
+    err = np.abs(got.astype(np.float64) - ref)
+    print(f"{what}: max-abs {err.max():.3e} mean-abs {err.mean():.3e}", flush=True)
+    assert np.isfinite(got).all() and err.max() <= MAX_ABS and err.mean() <= MEAN_ABS, what
+
+
+@pytest.mark.parametrize("n", [1, 4])
+def test_step_graph_replays(dev, n):
+    """Replays of one captured step, each after new queries, new K/V rows and
+    longer contexts were written by eager torch work, against the eager step
+    (bitwise) and the oracle."""
+    growth = np.array([[s % 2, 1, 2, 3] for s in range(4)], dtype=np.int32)  # per replay and sequence
+    final = [50, 100, 17, 230]
+    st = W.custom_structure(4, 8, 2, 64, final, seed=77)
+    B = st.B
+    lens0 = (np.asarray(final) - growth.sum(axis=0)).astype(np.int32)  # every context stays in its blocks
+    bt = torch.from_numpy(st.block_table).to(dev)
+    lens = torch.from_numpy(lens0).to(dev)
+    _, k_g, v_g = W.fill_values(st, dev, fill="nan")
+    k_e, v_e = k_g.clone(), v_g.clone()
+    q = torch.empty((B, n, st.Hq, st.D), dtype=torch.bfloat16, device=dev)
+    kn = torch.empty((B, n, st.Hkv, st.D), dtype=torch.bfloat16, device=dev)
+    vn = torch.empty_like(kn)
+    graph = StepGraph(q, kn, vn, k_g, v_g, bt, lens, st.scale, max_context_len=st.max_context_len)
+    try:
+        for step in range(4):
+            # eager work between replays: new inputs, one more token per sequence
+            torch.manual_seed(step)
+            q.copy_(torch.randn(q.shape, device=dev).to(torch.bfloat16))
+            kn.copy_(torch.randn(kn.shape, device=dev).to(torch.bfloat16))
+            vn.copy_(torch.randn(vn.shape, device=dev).to(torch.bfloat16))
+            lens.add_(torch.from_numpy(growth[step]).to(dev))
+            torch.cuda.synchronize()
+            out_g = graph.launch().clone()
+            torch.cuda.synchronize()
+            # the same step eagerly
+            pda_append_kv(kn, vn, bt, lens, k_e, v_e, max_context_len=st.max_context_len, num_q_heads=st.Hq)
+            out_e = pda_decode(q, k_e, v_e, bt, lens, st.scale, max_context_len=st.max_context_len)
+            torch.cuda.synchronize()
+            assert torch.equal(k_g.view(torch.int16), k_e.view(torch.int16)), f"replay {step}: K cache"
+            assert torch.equal(v_g.view(torch.int16), v_e.view(torch.int16)), f"replay {step}: V cache"
+            assert torch.equal(out_g, out_e), f"replay {step}: output differs from the eager step"
+            lens_h = lens.cpu().numpy()
+            ref = oracle.decode_multi(bits16(q), bits16(k_g), bits16(v_g), st.block_table, lens_h, st.scale)
+            check(out_g.cpu().numpy(), ref, f"graph replay {step} n={n}")
+    finally:
+        graph.close()

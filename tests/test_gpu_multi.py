@@ -1,0 +1,120 @@
+"""GPU parity of several new query tokens per sequence (speculative decoding,
+chunked prefill: Section 3.2) through the C ABI, against the fp64 oracle.
+
+New token i of a sequence with n new tokens and context length L sits at
+position L - n + i and attends to tokens t < L - n + 1 + i.  Bar as for the
+decode step: max-abs <= 8e-3 and mean-abs <= 1e-3 over every compared
+element.  Small problems are compared on every element; a Llama-3-8B-shaped
+step with 4 draft tokens per sequence runs at full size and is compared on
+sampled rows.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from paper_2405_11143_amd import make_problem, pda_decode, pda_plan
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS, MEAN_ABS = 8e-3, 1e-3
+THREADS = max(1, min(16, os.cpu_count() or 1))
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return torch.device("cuda:0")
+
+
+def run_multi(st, q, k, v, dev, partition_tokens=0):
+    bt = torch.from_numpy(st.block_table).to(dev)
+    lens = torch.from_numpy(st.context_lens).to(dev)
+    out = pda_decode(q, k, v, bt, lens, st.scale, max_context_len=st.max_context_len,
+                     partition_tokens=partition_tokens)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def check(got, ref, what):
+    got = got.astype(np.float64)
+    assert np.isfinite(got).all(), f"{what}: non-finite output"
+    err = np.abs(got - ref)
+    print(f"{what}: max-abs {err.max():.3e} mean-abs {err.mean():.3e} over {err.size} elements", flush=True)
+    assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS, what
+
+
+LENS = [1, 2, 3, 4, 5, 15, 16, 17, 33, 64, 65, 300, 1000, 2049]
+CASES = [  # (Hq, Hkv, D, n): rows per work item = min(n, 16 // G) * G
+    (32, 8, 128, 4),   # G=4: one 16-row chunk
+    (32, 8, 128, 7),   # two chunks (4 + 3 tokens)
+    (8, 1, 128, 2),    # G=8
+    (8, 8, 128, 16),   # G=1: 16 tokens in one chunk
+    (16, 1, 64, 3),    # G=16: one token per chunk
+    (12, 4, 64, 5),    # G=3: chunks of 5 tokens, 15 rows
+    (8, 2, 64, 1),     # a decode step given as [B][1][Hq][D]
+]
+
+
+@pytest.mark.parametrize("Hq,Hkv,D,n", CASES, ids=lambda x: str(x))
+@pytest.mark.parametrize("partition_tokens", [0, 16, 64])
+def test_multi_token_parity(dev, Hq, Hkv, D, n, partition_tokens):
+    st = W.custom_structure(len(LENS), Hq, Hkv, D, LENS, seed=100 + Hq + n)
+    _, k, v = W.fill_values(st, dev, fill="nan")
+    q = W.fill_multi_q(st, n, dev)
+    ref = oracle.decode_multi(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
+                              st.context_lens, st.scale, threads=THREADS)
+    got = run_multi(st, q, k, v, dev, partition_tokens)
+    # rows of tokens that see nothing (L < n) are zero
+    for b, L in enumerate(LENS):
+        for i in range(n):
+            if L - n + 1 + i <= 0:
+                assert np.all(got[b, i] == 0), (b, i)
+    check(got, ref, f"multi Hq={Hq} Hkv={Hkv} D={D} n={n} Tp={partition_tokens}")
+
+
+def test_one_token_equals_decode_step(dev):
+    """q as [B][1][Hq][D] runs the same arithmetic as the decode step: bitwise."""
+    lens = [1, 17, 300, 2049, 4096, 0]
+    st = W.custom_structure(len(lens), 32, 8, 128, lens, seed=7)
+    q, k, v = W.fill_values(st, dev, fill="nan")
+    a = run_multi(st, q, k, v, dev)
+    b = run_multi(st, q[:, None].contiguous(), k, v, dev)
+    assert np.array_equal(a, b[:, 0])
+
+
+def test_multi_token_poison_and_shuffle_bit_identical(dev):
+    lens = [40, 7, 900, 2047]
+    st = W.custom_structure(len(lens), 32, 8, 128, lens, seed=9)
+    q = W.fill_multi_q(st, 4, dev)
+    _, k, v = W.fill_values(st, dev, fill="nan")
+    base = run_multi(st, q, k, v, dev)
+    assert np.array_equal(base, run_multi(st, q, k, v, dev)), "run-to-run"
+    st2, k2, v2 = W.permute_pool(st, k, v, seed=3)
+    assert np.array_equal(base, run_multi(st2, q, k2, v2, dev)), "block shuffle"
+    _, kz, vz = W.fill_values(st, dev, fill="zero")
+    assert np.array_equal(base, run_multi(st, q, kz, vz, dev)), "NaN poison vs zero fill"
+
+
+def test_multi_token_full_size_sampled(dev):
+    """The Llama-3-8B decode step with 4 draft tokens per sequence to verify
+    (speculative decoding), in the launch configuration the benchmark times."""
+    st = W.make_structure("llama3_8b")
+    n = 4
+    plan = pda_plan(make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq,
+                                 st.max_context_len, num_query_tokens=n))
+    print(f"llama3_8b x {n} tokens: plan={plan}", flush=True)
+    _, k, v = W.fill_values(st, dev, fill="nan")
+    q = W.fill_multi_q(st, n, dev)
+    got = run_multi(st, q, k, v, dev)
+    assert np.isfinite(got).all()
+    r = np.random.default_rng(5)
+    rows = np.stack([r.integers(0, st.B, 64), r.integers(0, n, 64), r.integers(0, st.Hq, 64)], axis=1)
+    rows[0] = [int(np.argmax(st.context_lens)), n - 1, st.Hq - 1]
+    rows[1] = [int(np.argmin(st.context_lens)), 0, 0]
+    ref = oracle.decode_multi_rows(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
+                                   st.context_lens, st.scale, rows.astype(np.int32), threads=THREADS)
+    check(got[rows[:, 0], rows[:, 1], rows[:, 2]], ref, "llama3_8b 4 draft tokens, sampled rows")

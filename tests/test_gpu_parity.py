@@ -142,9 +142,13 @@ def test_constant_v_gives_constant(dev):
     q, k, v = W.fill_values(st, dev, fill="nan")
     mask = torch.from_numpy(W.unread_slot_mask(st)).to(dev)[:, None, :, None]
     v = torch.ones_like(v).masked_fill_(mask, float("nan"))
+    # The P.V product takes each probability p as two bf16 halves, hi = p
+    # truncated to bf16 and lo = bf16(p - hi), so every weight carries a
+    # relative error below 2^-16 against the fp32 denominator; the output, a
+    # convex combination of ones, is 1 within that bound (plus fp32 rounding).
     for tp in (0, 64):
         got = run(st, q, k, v, dev, tp)
-        assert np.abs(got - 1.0).max() <= 1e-6
+        assert np.abs(got - 1.0).max() <= 2.0 ** -16 + 1e-6
 
 
 def test_gqa_mapping(dev):
@@ -156,7 +160,8 @@ def test_gqa_mapping(dev):
         got = run(st, q, k, v, dev, 64)
         G = Hq // Hkv
         for h in range(Hq):
-            assert np.abs(got[:, h] - (h // G + 1)).max() <= 1e-5, (Hq, Hkv, h)
+            # weights carry a relative error below 2^-16 (bf16 hi/lo probabilities)
+            assert np.abs(got[:, h] - (h // G + 1)).max() <= (h // G + 1) * (2.0 ** -16 + 1e-6), (Hq, Hkv, h)
 
 
 def test_block_shuffle_and_poison_bit_identical(dev):
