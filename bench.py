@@ -1,11 +1,12 @@
-"""Benchmark of one paged decode-attention step on one MI355X.
+"""Benchmark of the rollout decode step's hot path on one MI355X.
 
-A step is one pda_decode call (pass 1 + merge pass) over a whole
-batch: every sequence's new query token attends over its paged KV cache.
-The default workload is the Llama-3-8B-shaped rollout step (B=256, 32 query
-/ 8 KV heads, head_dim 128, contexts uniform in [512, 4096], random block
-placement in a pool of the used blocks + 10%); inputs are synthetic and
-already resident in HBM when the timed region starts.
+Default (--op decode): a step is one pda_decode call (work order + pass 1 +
+merge pass) over a whole batch: every sequence's new query token attends over
+its paged KV cache.  The default workload is the Llama-3-8B-shaped rollout
+step (B=256, 32 query / 8 KV heads, head_dim 128, contexts uniform in
+[512, 4096], random block placement in a pool of the used blocks + 10%);
+inputs are synthetic and already resident in HBM when the timed region
+starts.
 
 Prints one JSON line:
   value      algorithmic HBM bytes per step / step time, in GB/s
@@ -17,6 +18,14 @@ Prints one JSON line:
              `traffic` is the measured HBM bytes per launch from rocprofv3
              counters when they were taken on this kernel source
   cpu_baseline  the fp64 oracle on the host cores, same workload
+
+Other steps around attention (--op):
+  multi    n new query tokens per sequence (--tokens, default 4: verifying
+           speculative-decoding drafts), same KV bytes, n times the rows
+  append   the KV-cache append of the step's new tokens alone
+  graph    append + attention as one captured HIP graph against the same
+           calls issued eagerly (default workload: the tiny batch, where
+           launch overhead dominates)
 """
 from __future__ import annotations
 
@@ -39,6 +48,7 @@ CSRC = "paper_2405_11143_amd/csrc/"
 KERNEL = "partition_kernel"
 KERNEL_SOURCES = {
     "partition_kernel": [CSRC + "pda_partition.hip", CSRC + "pda_wave.h", CSRC + "pda_internal.h"],
+    "append_kernel": [CSRC + "pda_append.hip", CSRC + "pda_internal.h"],
 }
 
 
@@ -65,8 +75,6 @@ def measured_traffic(kernel: str, workload: str):
 
 
 def cpu_baseline(st, q, k, v, min_seconds: float, max_reps: int):
-    import numpy as np
-
     import oracle
     import workloads as W
 
@@ -86,19 +94,203 @@ def cpu_baseline(st, q, k, v, min_seconds: float, max_reps: int):
                       f"{reps} repetition(s), {t_total:.1f} s total, fp64, {threads} threads"}
 
 
+def timed(fn, n, stream):
+    """Average ms per call of fn over n calls, HIP events on `stream`."""
+    import torch
+
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(n):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / n
+
+
+def base_result(args, value, unit, ms_step, metric, config, dtype="bf16"):
+    return {"metric": metric, "value": round(value, 2), "unit": unit, "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": round(ms_step, 5), "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": dtype,
+            "data": "synthetic (seeded N(0,1) bf16 q/K/V, random block placement)", "config": config}
+
+
+def roofline(achieved_gbs, ms, kernel, workload):
+    return {"bound": "hbm", "kernel": kernel, "achieved": round(achieved_gbs, 2), "peak": PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved_gbs / PEAK_GBS, 4), "traffic": measured_traffic(kernel, workload),
+            "ms_per_launch": round(ms, 5)}
+
+
+def config_of(st, cfg_desc, name, plan=None, **extra):
+    c = {"workload": cfg_desc, "name": name, "batch": st.B, "q_heads": st.Hq, "kv_heads": st.Hkv,
+         "head_dim": st.D, "block_size": st.block_size, "pool_blocks": st.num_blocks,
+         "context_tokens": st.logical_tokens, "unique_context_tokens": st.unique_tokens}
+    if plan is not None:
+        c.update(partition_tokens=plan["partition_tokens"], partitions=plan["num_partitions"])
+    c.update(extra)
+    return c
+
+
+def setup(args, n_tokens=1):
+    import torch
+
+    import workloads as W
+    from paper_2405_11143_amd import make_problem, pda_plan
+
+    dev = torch.device("cuda:0")
+    st = W.make_structure(args.config)
+    q, k, v = W.fill_values(st, dev, fill="nan")
+    if n_tokens > 1:
+        q = W.fill_multi_q(st, n_tokens, dev)
+    bt = torch.from_numpy(st.block_table).to(dev)
+    lens = torch.from_numpy(st.context_lens).to(dev)
+    prob = make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq, st.max_context_len,
+                        args.partition_tokens, num_query_tokens=n_tokens)
+    plan = pda_plan(prob)
+    out = torch.empty(q.shape, dtype=torch.float32, device=dev)
+    ws = torch.empty(max(plan["workspace_bytes"], 16), dtype=torch.uint8, device=dev)
+    return dev, st, q, k, v, bt, lens, plan, out, ws
+
+
+def op_decode(args, n_tokens=1):
+    import torch
+
+    import workloads as W
+    from paper_2405_11143_amd import pda_decode, pda_partition_attention
+
+    dev, st, q, k, v, bt, lens, plan, out, ws = setup(args, n_tokens)
+    stream = torch.cuda.current_stream(dev)
+    kw = dict(max_context_len=st.max_context_len, partition_tokens=args.partition_tokens, workspace=ws,
+              stream=stream)
+
+    def step():
+        pda_decode(q, k, v, bt, lens, st.scale, out, **kw)
+
+    def pass1():
+        pda_partition_attention(q, k, v, bt, lens, st.scale, out, **kw)
+
+    fn = pass1 if args.pass1_only else step
+    for _ in range(args.warmup):
+        fn()
+    torch.cuda.synchronize()
+    ms_step = timed(fn, args.steps, stream)
+    ms_pass1 = ms_step if args.pass1_only else timed(pass1, args.steps, stream)
+    alg = st.algorithmic_bytes(query_tokens=n_tokens)
+    value = alg / (ms_step * 1e-3) / 1e9
+    cfg = W.CONFIGS[args.config]
+    if n_tokens == 1:
+        metric, desc = METRIC, cfg["desc"]
+    else:
+        metric = f"multi-token attention HBM GB/s ({n_tokens} new tokens per sequence), {args.config} shape"
+        desc = f"{cfg['desc']}; {n_tokens} new query tokens per sequence (causal)"
+    result = base_result(args, value, "GB/s", ms_step, metric,
+                         config_of(st, desc, args.config, plan, query_tokens=n_tokens,
+                                   timed="pass1 only" if args.pass1_only else "full step"))
+    result.update({"seq_steps_per_s": round(st.B / (ms_step * 1e-3), 1),
+                   "pct_of_peak": round(100.0 * value / PEAK_GBS, 2), "algorithmic_bytes_per_step": alg,
+                   "roofline": roofline(alg / (ms_pass1 * 1e-3) / 1e9, ms_pass1, KERNEL,
+                                        args.config if n_tokens == 1 else f"{args.config}_x{n_tokens}"),
+                   "cpu_baseline": None})
+    if n_tokens > 1:
+        result["query_tokens_per_s"] = round(st.B * n_tokens / (ms_step * 1e-3), 1)
+    if n_tokens == 1 and not args.no_cpu_baseline and not args.pass1_only:
+        result["cpu_baseline"] = cpu_baseline(st, q, k, v, args.cpu_min_seconds, args.cpu_max_reps)
+    return result
+
+
+def op_append(args):
+    import torch
+
+    import workloads as W
+    from paper_2405_11143_amd import pda_append_kv
+
+    n = args.tokens
+    dev = torch.device("cuda:0")
+    st = W.make_structure(args.config)
+    _, k, v = W.fill_values(st, dev, fill="nan")
+    kn, vn = W.fill_new_kv(st, n, dev)
+    bt = torch.from_numpy(st.block_table).to(dev)
+    lens = torch.from_numpy(st.context_lens).to(dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step():  # rewrites the same slots every time
+        pda_append_kv(kn, vn, bt, lens, k, v, max_context_len=st.max_context_len, num_q_heads=st.Hq, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ms = timed(step, args.steps, stream)
+    alg = st.append_bytes(n)
+    value = alg / (ms * 1e-3) / 1e9
+    cfg = W.CONFIGS[args.config]
+    result = base_result(args, value, "GB/s", ms, f"KV-cache append HBM GB/s ({n} new tokens per sequence)",
+                         config_of(st, f"{cfg['desc']}; append of {n} new token(s) per sequence", args.config,
+                                   new_tokens=n))
+    result.update({"seq_steps_per_s": round(st.B / (ms * 1e-3), 1), "algorithmic_bytes_per_step": alg,
+                   "roofline": roofline(value, ms, "append_kernel", args.config), "cpu_baseline": None})
+    return result
+
+
+def op_graph(args):
+    import torch
+
+    import workloads as W
+    from paper_2405_11143_amd import StepGraph, pda_append_kv, pda_decode
+
+    n = args.tokens
+    dev, st, q, k, v, bt, lens, plan, out, ws = setup(args, n)
+    kn, vn = W.fill_new_kv(st, n, dev)
+    stream = torch.cuda.current_stream(dev)
+    graph = StepGraph(q, kn, vn, k, v, bt, lens, st.scale, out, max_context_len=st.max_context_len,
+                      partition_tokens=args.partition_tokens, workspace=ws)
+
+    def eager():
+        pda_append_kv(kn, vn, bt, lens, k, v, max_context_len=st.max_context_len, num_q_heads=st.Hq, stream=stream)
+        pda_decode(q, k, v, bt, lens, st.scale, out, max_context_len=st.max_context_len,
+                   partition_tokens=args.partition_tokens, workspace=ws, stream=stream)
+
+    def replay():
+        graph.launch(stream)
+
+    try:
+        for f in (eager, replay):
+            for _ in range(args.warmup):
+                f()
+        torch.cuda.synchronize()
+        ms_eager = timed(eager, args.steps, stream)
+        ms_graph = timed(replay, args.steps, stream)
+    finally:
+        graph.close()
+    alg = st.algorithmic_bytes(query_tokens=n) + st.append_bytes(n)
+    value = st.B / (ms_graph * 1e-3)
+    cfg = W.CONFIGS[args.config]
+    result = base_result(args, value, "seq-steps/s", ms_graph,
+                         "decode step (append + attention) as one HIP graph, seq-steps/s",
+                         config_of(st, f"{cfg['desc']}; append + attention of {n} new token(s)", args.config, plan,
+                                   query_tokens=n))
+    result.update({"ms_per_step_eager": round(ms_eager, 5), "graph_speedup": round(ms_eager / ms_graph, 3),
+                   "algorithmic_bytes_per_step": alg,
+                   "roofline": roofline(alg / (ms_graph * 1e-3) / 1e9, ms_graph, KERNEL, args.config),
+                   "cpu_baseline": None})
+    return result
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", default="llama3_8b")
+    ap.add_argument("--op", default="decode", choices=["decode", "multi", "append", "graph"])
+    ap.add_argument("--config", default=None, help="workload (default: llama3_8b; tiny for --op graph)")
+    ap.add_argument("--tokens", type=int, default=None,
+                    help="new tokens per sequence (--op multi: 4; append, graph: 1)")
     ap.add_argument("--partition-tokens", type=int, default=0,
                     help="> 0: split-K partition size in tokens (0: the library's choice)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-min-seconds", type=float, default=10.0)
     ap.add_argument("--cpu-max-reps", type=int, default=20)
     ap.add_argument("--pass1-only", action="store_true",
-                    help="time and launch only the pass-1 kernel (for counter runs)")
+                    help="time and launch only the pass-1 kernels (for counter runs)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a device copy of this many MiB (counter calibration) and exit")
     args = ap.parse_args(argv)
@@ -108,11 +300,12 @@ def main(argv=None):
               "sequence or KV head with no exchange, and this build runs on a single MI355X.",
               file=sys.stderr)
         return 2
+    if args.config is None:
+        args.config = "tiny" if args.op == "graph" else "llama3_8b"
+    if args.tokens is None:
+        args.tokens = 4 if args.op == "multi" else 1
 
     import torch
-
-    import workloads as W
-    from paper_2405_11143_amd import make_problem, pda_decode, pda_partition_attention, pda_plan
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -128,79 +321,14 @@ def main(argv=None):
         print(json.dumps({"copy_calibration_bytes": n, "copies": 3}))
         return 0
 
-    st = W.make_structure(args.config)
-    q, k, v = W.fill_values(st, dev, fill="nan")
-    bt = torch.from_numpy(st.block_table).to(dev)
-    lens = torch.from_numpy(st.context_lens).to(dev)
-    prob = make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq,
-                        st.max_context_len, args.partition_tokens)
-    plan = pda_plan(prob)
-    ws_bytes = plan["workspace_bytes"]
-    out = torch.empty((st.B, st.Hq, st.D), dtype=torch.float32, device=dev)
-    ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=dev)
-    stream = torch.cuda.current_stream(dev)
-    kw = dict(max_context_len=st.max_context_len, partition_tokens=args.partition_tokens,
-              workspace=ws, stream=stream)
-
-    def step():
-        pda_decode(q, k, v, bt, lens, st.scale, out, **kw)
-
-    def pass1():
-        pda_partition_attention(q, k, v, bt, lens, st.scale, out, **kw)
-
-    fn = pass1 if args.pass1_only else step
-    for _ in range(args.warmup):
-        fn()
-    torch.cuda.synchronize()
-
-    def timed(f, n):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        e0.record(stream)
-        for _ in range(n):
-            f()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / n  # ms
-
-    ms_step = timed(fn, args.steps)
-    ms_pass1 = ms_step if args.pass1_only else timed(pass1, args.steps)
-
-    alg = st.algorithmic_bytes()
-    value = alg / (ms_step * 1e-3) / 1e9
-    achieved = alg / (ms_pass1 * 1e-3) / 1e9
-    kernel = KERNEL
-    traffic = measured_traffic(kernel, args.config)
-    cfg = W.CONFIGS[args.config]
-    result = {
-        "metric": METRIC,
-        "value": round(value, 2),
-        "unit": "GB/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic (seeded N(0,1) bf16 q/K/V, random block placement)",
-        "config": {"workload": cfg["desc"], "name": args.config, "batch": st.B, "q_heads": st.Hq,
-                   "kv_heads": st.Hkv, "head_dim": st.D, "block_size": st.block_size,
-                   "pool_blocks": st.num_blocks, "context_tokens": st.logical_tokens,
-                   "unique_context_tokens": st.unique_tokens,
-                   "partition_tokens": plan["partition_tokens"], "partitions": plan["num_partitions"],
-                   "timed": "pass1 only" if args.pass1_only else "full step"},
-        "seq_steps_per_s": round(st.B / (ms_step * 1e-3), 1),
-        "pct_of_peak": round(100.0 * value / PEAK_GBS, 2),
-        "algorithmic_bytes_per_step": alg,
-        "roofline": {"bound": "hbm", "kernel": kernel, "achieved": round(achieved, 2),
-                     "peak": PEAK_GBS, "unit": "GB/s", "frac": round(achieved / PEAK_GBS, 4),
-                     "traffic": traffic, "ms_per_launch": round(ms_pass1, 5)},
-        "cpu_baseline": None,
-    }
-    if not args.no_cpu_baseline and not args.pass1_only:
-        result["cpu_baseline"] = cpu_baseline(st, q, k, v, args.cpu_min_seconds, args.cpu_max_reps)
+    if args.op == "decode":
+        result = op_decode(args, 1)
+    elif args.op == "multi":
+        result = op_decode(args, args.tokens)
+    elif args.op == "append":
+        result = op_append(args)
+    else:
+        result = op_graph(args)
     print(json.dumps(result), flush=True)
     return 0
 

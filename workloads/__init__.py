@@ -138,16 +138,23 @@ class Structure:
     def unique_tokens(self) -> int:
         return int(self.valid_slots().sum())
 
-    def algorithmic_bytes(self, unique: bool = True) -> int:
-        """Bytes a decode step must move: K and V rows of the context (each
-        shared physical row once when ``unique``), q, the fp32 output, the
-        block-table entries read and the context lengths."""
+    def algorithmic_bytes(self, unique: bool = True, query_tokens: int = 1) -> int:
+        """Bytes an attention step must move: K and V rows of the context (each
+        shared physical row once when ``unique``), q and the fp32 output of
+        ``query_tokens`` new tokens per sequence, the block-table entries read
+        and the context lengths."""
         tokens = self.unique_tokens if unique else self.logical_tokens
         kv = tokens * self.Hkv * self.D * 2 * 2
-        q = self.B * self.Hq * self.D * 2
-        out = self.B * self.Hq * self.D * 4
+        q = self.B * query_tokens * self.Hq * self.D * 2
+        out = self.B * query_tokens * self.Hq * self.D * 4
         bt = int(self.blocks_used().sum()) * 4
         return int(kv + q + out + bt + self.B * 4)
+
+    def append_bytes(self, new_tokens: int = 1) -> int:
+        """Bytes a KV-cache append must move: the new K and V rows read and
+        written once, the block-table entry of each new token, the lengths."""
+        rows = self.B * new_tokens * self.Hkv * self.D * 2
+        return int(2 * 2 * rows + self.B * new_tokens * 4 + self.B * 4)
 
 
 def _draw_lens(rng: np.random.Generator, kind: str, lo: int, hi: int, n: int) -> np.ndarray:
