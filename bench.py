@@ -26,6 +26,9 @@ Other steps around attention (--op):
   graph    append + attention as one captured HIP graph against the same
            calls issued eagerly (default workload: the tiny batch, where
            launch overhead dominates)
+  logprob  log-probability of each sampled token and the entropy over the
+           LM-head logits of one decode step (256 rows x 128256 Llama-3
+           vocabulary, bf16; --logits-f32, --config qwen_vocab)
 """
 from __future__ import annotations
 
@@ -49,6 +52,7 @@ KERNEL = "partition_kernel"
 KERNEL_SOURCES = {
     "partition_kernel": [CSRC + "pda_partition.hip", CSRC + "pda_wave.h", CSRC + "pda_internal.h"],
     "append_kernel": [CSRC + "pda_append.hip", CSRC + "pda_internal.h"],
+    "logprob_kernel": [CSRC + "pda_logprob.hip", CSRC + "pda_internal.h"],
 }
 
 
@@ -275,12 +279,48 @@ def op_graph(args):
     return result
 
 
+def op_logprob(args):
+    import torch
+
+    import workloads as W
+    from paper_2405_11143_amd import pda_token_logprobs
+
+    name = args.config if args.config in W.LOGIT_CONFIGS else "llama3_vocab"
+    dtype = torch.float32 if args.logits_f32 else torch.bfloat16
+    dev = torch.device("cuda:0")
+    x, tok = W.logits_for(name, dev, dtype)
+    tokens = torch.from_numpy(tok).to(dev)
+    B, V = x.shape
+    lp = torch.empty(B, dtype=torch.float32, device=dev)
+    ent = torch.empty(B, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step():
+        pda_token_logprobs(x, tokens, 1.0, logprobs=lp, entropies=ent, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ms = timed(step, args.steps, stream)
+    alg = B * V * x.element_size() + B * 4 + B * 8
+    value = alg / (ms * 1e-3) / 1e9
+    cfg = W.LOGIT_CONFIGS[name]
+    result = base_result(args, value, "GB/s", ms, "token log-prob + entropy HBM GB/s over the LM-head logits",
+                         {"workload": cfg["desc"] + f", {str(dtype).split('.')[-1]} logits", "name": name,
+                          "rows": B, "vocab": V}, dtype="bf16" if dtype == torch.bfloat16 else "f32")
+    result.update({"rows_per_s": round(B / (ms * 1e-3), 1), "algorithmic_bytes_per_step": alg,
+                   "pct_of_peak": round(100.0 * value / PEAK_GBS, 2),
+                   "roofline": roofline(value, ms, "logprob_kernel", name), "cpu_baseline": None})
+    return result
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--op", default="decode", choices=["decode", "multi", "append", "graph"])
+    ap.add_argument("--op", default="decode", choices=["decode", "multi", "append", "graph", "logprob"])
+    ap.add_argument("--logits-f32", action="store_true", help="--op logprob: float32 logits (default bf16)")
     ap.add_argument("--config", default=None, help="workload (default: llama3_8b; tiny for --op graph)")
     ap.add_argument("--tokens", type=int, default=None,
                     help="new tokens per sequence (--op multi: 4; append, graph: 1)")
@@ -301,7 +341,7 @@ def main(argv=None):
               file=sys.stderr)
         return 2
     if args.config is None:
-        args.config = "tiny" if args.op == "graph" else "llama3_8b"
+        args.config = {"graph": "tiny", "logprob": "llama3_vocab"}.get(args.op, "llama3_8b")
     if args.tokens is None:
         args.tokens = 4 if args.op == "multi" else 1
 
@@ -327,6 +367,8 @@ def main(argv=None):
         result = op_decode(args, args.tokens)
     elif args.op == "append":
         result = op_append(args)
+    elif args.op == "logprob":
+        result = op_logprob(args)
     else:
         result = op_graph(args)
     print(json.dumps(result), flush=True)

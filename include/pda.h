@@ -175,6 +175,23 @@ int pda_step_graph_create(const pda_problem *prob, const void *q, const void *k_
 int pda_step_graph_launch(pda_step_graph *graph, hipStream_t stream);
 int pda_step_graph_destroy(pda_step_graph *graph);
 
+/* Token log-probabilities and entropies of one step's LM-head logits: the
+ * rollout records the log-probability of every sampled token, and the policy
+ * loss uses the entropy of the same distribution (Appendix C).  With
+ * x_j = logits[r][j] * inv_temperature over j in [0, vocab):
+ *   logprobs[r]  = x_{tokens[r]} - log sum_j exp(x_j)
+ *   entropies[r] = -sum_j p_j log p_j,  p = softmax(x)      (skipped if NULL)
+ * in natural-log units.  logits: device rows of `vocab` values (bf16 for
+ * PDA_DTYPE_BF16, fp32 for PDA_DTYPE_F32), row r starting at element
+ * r * row_stride (row_stride >= vocab); the buffer holds num_rows * row_stride
+ * elements and every row must be 16-byte aligned.  -inf logits have probability 0; a token id outside
+ * [0, vocab) gives a NaN log-probability.  inv_temperature must be finite
+ * and >= 0 (0: the uniform distribution). */
+enum pda_dtype { PDA_DTYPE_BF16 = 0, PDA_DTYPE_F32 = 1 };
+int pda_token_logprobs(int32_t num_rows, int32_t vocab, int64_t row_stride, int32_t logits_dtype,
+                       const void *logits, const int32_t *tokens, float inv_temperature,
+                       float *logprobs, float *entropies, hipStream_t stream);
+
 /* Host-side check of device contents, on HOST copies: every context length
  * is at most max_context_len and every block id a sequence reads is in
  * [0, num_blocks).  Returns PDA_OK or PDA_ERR_VALUE; on error *first_bad (if

@@ -307,6 +307,31 @@ int pda_step_graph_destroy(pda_step_graph* graph) {
   return rc;
 }
 
+int pda_token_logprobs(int32_t num_rows, int32_t vocab, int64_t row_stride, int32_t logits_dtype, const void* logits,
+                       const int32_t* tokens, float inv_temperature, float* logprobs, float* entropies,
+                       hipStream_t stream) {
+  if (num_rows < 0 || vocab < 1 || row_stride < vocab) return PDA_ERR_SHAPE;
+  if (logits_dtype != PDA_DTYPE_BF16 && logits_dtype != PDA_DTYPE_F32) return PDA_ERR_UNSUPPORTED;
+  const int esize = logits_dtype == PDA_DTYPE_BF16 ? 2 : 4;
+  if ((int64_t)vocab * esize + 64 > 0x7fffffff) return PDA_ERR_SHAPE;  // one row must fit a buffer descriptor
+  if (num_rows == 0) return PDA_OK;
+  if (!logits || !tokens || !logprobs) return PDA_ERR_NULL;
+  if (!isfinite(inv_temperature) || inv_temperature < 0.f) return PDA_ERR_VALUE;
+  if (!aligned(logits, 16) || (row_stride * esize) % 16 != 0 || !aligned(logprobs, 4) || !aligned(entropies, 4))
+    return PDA_ERR_ALIGNMENT;
+  pda::LogprobArgs a;
+  a.logits = logits;
+  a.tokens = tokens;
+  a.logprobs = logprobs;
+  a.entropies = entropies;
+  a.inv_temperature = inv_temperature;
+  a.num_rows = num_rows;
+  a.vocab = vocab;
+  a.row_stride = row_stride;
+  a.elem_bytes = esize;
+  return pda::launch_logprob(a, stream) == hipSuccess ? PDA_OK : PDA_ERR_HIP;
+}
+
 int pda_validate_host(const pda_problem* prob, const int32_t* block_table, const int32_t* context_lens,
                       int64_t* first_bad) {
   int rc = check_problem(prob);

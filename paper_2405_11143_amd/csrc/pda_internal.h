@@ -50,7 +50,23 @@ __device__ __forceinline__ int chunk_visible(const StepArgs& a, int L, int chunk
   return L - a.num_query_tokens + i0 + nv;
 }
 
+// Arguments of the token log-probability kernel (passed by value).
+struct LogprobArgs {
+  const void* logits;      // [num_rows][row_stride] bf16 or fp32, the first `vocab` of each row used
+  const int32_t* tokens;   // int32 [num_rows]
+  float* logprobs;         // fp32 [num_rows]
+  float* entropies;        // fp32 [num_rows], or null
+  float inv_temperature;   // 1 / T
+  int32_t num_rows;
+  int32_t vocab;
+  int64_t row_stride;      // elements
+  int32_t elem_bytes;      // 2 (bf16) or 4 (fp32)
+};
+
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+
 // Launchers (asynchronous; return the hipGetLastError() of the launch).
+hipError_t launch_logprob(const LogprobArgs& a, hipStream_t stream);
 hipError_t launch_append(const StepArgs& a, const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_cache,
                          uint16_t* v_cache, int head_dim, hipStream_t stream);
 hipError_t launch_order(const StepArgs& a, hipStream_t stream);

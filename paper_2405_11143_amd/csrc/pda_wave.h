@@ -55,7 +55,6 @@ namespace pda {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef short shortx4_t __attribute__((ext_vector_type(4)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
-typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 

@@ -23,7 +23,8 @@ PDA_ERR_WORKSPACE, PDA_ERR_ALIGNMENT, PDA_ERR_VALUE, PDA_ERR_HIP = 4, 5, 6, 7
 # Every function include/pda.h declares.
 EXPORTED = ("pda_plan", "pda_workspace_bytes", "pda_decode", "pda_partition_attention",
             "pda_merge_partitions", "pda_append_kv", "pda_step_graph_create", "pda_step_graph_launch",
-            "pda_step_graph_destroy", "pda_validate_host", "pda_status_string")
+            "pda_step_graph_destroy", "pda_token_logprobs", "pda_validate_host", "pda_status_string")
+PDA_DTYPE_BF16, PDA_DTYPE_F32 = 0, 1
 
 
 class pda_problem(ctypes.Structure):
@@ -71,6 +72,8 @@ def load_library(path: str = LIB_PATH):
                                           ctypes.POINTER(vp)]
     lib.pda_step_graph_launch.argtypes = [vp, vp]
     lib.pda_step_graph_destroy.argtypes = [vp]
+    lib.pda_token_logprobs.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, vp, vp,
+                                       ctypes.c_float, vp, vp, vp]
     lib.pda_validate_host.argtypes = [P, vp, vp, ctypes.POINTER(ctypes.c_int64)]
     lib.pda_status_string.argtypes = [i32]
     lib.pda_status_string.restype = ctypes.c_char_p
@@ -316,3 +319,39 @@ class StepGraph:
             self.close()
         except Exception:
             pass
+
+
+def pda_token_logprobs(logits, tokens, inv_temperature: float = 1.0, entropy: bool = True, vocab: int = None,
+                       logprobs=None, entropies=None, stream=None):
+    """Log-probability of tokens[r] under softmax(logits[r][:vocab] * inv_temperature),
+    and the entropy of that distribution (natural-log units).  logits: a device
+    tensor [rows][row_stride] of bf16 or float32 (16-byte aligned rows); tokens
+    int32 [rows].  Returns (logprobs fp32 [rows], entropies fp32 [rows] or None)."""
+    import torch
+
+    if logits.dim() != 2 or logits.stride(1) != 1:
+        raise ValueError("logits must be [rows][row_stride] with unit element stride")
+    if logits.dtype == torch.bfloat16:
+        dtype = PDA_DTYPE_BF16
+    elif logits.dtype == torch.float32:
+        dtype = PDA_DTYPE_F32
+    else:
+        raise TypeError("logits must be bfloat16 or float32")
+    _require("tokens", tokens, torch.int32)
+    if not logits.is_cuda:
+        raise ValueError("logits must be a device tensor")
+    rows = logits.shape[0]
+    vocab = logits.shape[1] if vocab is None else int(vocab)
+    if tokens.shape != (rows,):
+        raise ValueError("tokens must be [rows]")
+    if logprobs is None:
+        logprobs = torch.empty(rows, dtype=torch.float32, device=logits.device)
+    if entropy and entropies is None:
+        entropies = torch.empty(rows, dtype=torch.float32, device=logits.device)
+    rc = load_library().pda_token_logprobs(rows, vocab, logits.stride(0), dtype, logits.data_ptr(), tokens.data_ptr(),
+                                           ctypes.c_float(inv_temperature), logprobs.data_ptr(),
+                                           entropies.data_ptr() if entropy else None,
+                                           _stream_handle(stream, logits.device))
+    if rc != PDA_OK:
+        raise PdaError(rc, "pda_token_logprobs")
+    return logprobs, (entropies if entropy else None)

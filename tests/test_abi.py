@@ -149,6 +149,66 @@ def test_merge_validation():
     assert f(ctypes.byref(single), 0x1000, 0x1000, None, 0, None) == pda.pda.PDA_OK
 
 
+def test_logprob_validation():
+    """Host validation of pda_token_logprobs (no launch)."""
+    f = pda.load_library().pda_token_logprobs
+    ok = dict(rows=4, vocab=1000, stride=1000, dtype=pda.pda.PDA_DTYPE_BF16, logits=0x1000, tokens=0x1000,
+              inv_t=1.0, lp=0x1000, ent=0x1000)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(a["rows"], a["vocab"], a["stride"], a["dtype"], a["logits"], a["tokens"],
+                 ctypes.c_float(a["inv_t"]), a["lp"], a["ent"], None)
+    assert call(rows=-1) == pda.pda.PDA_ERR_SHAPE
+    assert call(vocab=0) == pda.pda.PDA_ERR_SHAPE
+    assert call(stride=999) == pda.pda.PDA_ERR_SHAPE
+    assert call(vocab=2**30, stride=2**30) == pda.pda.PDA_ERR_SHAPE  # a row beyond one buffer descriptor
+    assert call(dtype=7) == pda.pda.PDA_ERR_UNSUPPORTED
+    assert call(logits=None) == pda.pda.PDA_ERR_NULL
+    assert call(tokens=None) == pda.pda.PDA_ERR_NULL
+    assert call(lp=None) == pda.pda.PDA_ERR_NULL
+    assert call(inv_t=float("nan")) == pda.pda.PDA_ERR_VALUE
+    assert call(inv_t=-1.0) == pda.pda.PDA_ERR_VALUE
+    assert call(logits=0x1008) == pda.pda.PDA_ERR_ALIGNMENT
+    assert call(stride=1004) == pda.pda.PDA_ERR_ALIGNMENT          # rows of 2008 bytes
+    assert call(stride=1002, dtype=pda.pda.PDA_DTYPE_F32) == pda.pda.PDA_ERR_ALIGNMENT
+    assert call(rows=0, logits=None, tokens=None, lp=None) == pda.pda.PDA_OK  # nothing to do
+
+
+def test_append_and_graph_validation():
+    lib = pda.load_library()
+    p = prob()
+    args = [0x1000] * 6
+    f = lib.pda_append_kv
+    assert f(ctypes.byref(p), None, *args[1:], None) == pda.pda.PDA_ERR_NULL
+    assert f(ctypes.byref(p), 0x1008, *args[1:], None) == pda.pda.PDA_ERR_ALIGNMENT
+    assert f(ctypes.byref(prob(num_query_tokens=-1)), *args, None) == pda.pda.PDA_ERR_SHAPE
+    assert f(ctypes.byref(prob(head_dim=96)), *args, None) == pda.pda.PDA_ERR_UNSUPPORTED
+    assert f(ctypes.byref(prob(num_seqs=0)), *([None] * 6), None) == pda.pda.PDA_OK
+    g = ctypes.c_void_p()
+    c = lib.pda_step_graph_create
+    assert c(ctypes.byref(p), *([0x1000] * 7), ctypes.c_float(0.1), 0x1000, None, 0,
+             ctypes.byref(g)) == pda.pda.PDA_ERR_WORKSPACE
+    assert c(ctypes.byref(p), None, *([0x1000] * 6), ctypes.c_float(0.1), 0x1000, None, 0,
+             ctypes.byref(g)) == pda.pda.PDA_ERR_NULL
+    assert c(ctypes.byref(p), *([0x1000] * 7), ctypes.c_float(0.1), 0x1000, None, 0, None) == pda.pda.PDA_ERR_NULL
+    assert g.value is None
+    assert lib.pda_step_graph_launch(None, None) == pda.pda.PDA_ERR_NULL
+    assert lib.pda_step_graph_destroy(None) == pda.pda.PDA_OK
+
+
+def test_multi_token_plan():
+    # n new tokens per sequence: query chunks of min(n, 16 // G) tokens; one
+    # work item per (partition, sequence, KV head, chunk)
+    d = pda.pda_plan(llama(num_query_tokens=4, partition_tokens=4096))     # G = 4: one chunk
+    assert d["workspace_bytes"] == 256 * 8 * 4
+    d = pda.pda_plan(llama(num_query_tokens=7, partition_tokens=4096))     # two chunks
+    assert d["workspace_bytes"] == 256 * 8 * 2 * 4
+    d = pda.pda_plan(llama(num_query_tokens=4, partition_tokens=2048))     # 2 partitions: partials per row
+    assert d["workspace_bytes"] == 256 * 4 * 32 * 2 * (128 + 2) * 4 + 2 * 256 * 8 * 4
+    assert pda.pda_plan(llama(num_query_tokens=0)) == pda.pda_plan(llama(num_query_tokens=1))
+
+
 def test_validate_host():
     st = W.make_structure("tiny")
     p = prob(num_blocks=st.num_blocks, max_blocks_per_seq=st.max_blocks_per_seq,

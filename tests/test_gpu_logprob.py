@@ -1,0 +1,112 @@
+"""GPU parity of the token log-probability / entropy kernel against the fp64
+oracle, through the C ABI.
+
+Bar: max-abs error <= 1e-4 on both log-probabilities and entropies (natural
+log units).  The kernel works in fp32 on d = (logit - m) / T * log2(e), m the running
+max of the raw logits:
+- the difference is taken on the raw values, so a large common offset costs
+  nothing; rounding d costs at most |d| * 2^-24 (< 3e-6 here);
+- each thread sums about 130 terms in order and 16 + 64 partial states are
+  merged, so the relative error of the sums stays below ~1e-5, i.e. ~1e-5
+  after the logarithm;
+- the entropy is formed from sum p (y - m) relative to the running max, so
+  its error scales with the entropy (< 12 nats here), not with |y|.
+1e-4 leaves several times that margin.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from paper_2405_11143_amd import pda_token_logprobs
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return torch.device("cuda:0")
+
+
+def host_values(x):
+    """What the oracle reads: bf16 bit patterns or float32 values."""
+    return W.bf16_bits(x) if x.dtype == torch.bfloat16 else x.float().cpu().numpy()
+
+
+def compare(lp, ent, ref_lp, ref_ent, what):
+    lp, ent = lp.cpu().numpy().astype(np.float64), ent.cpu().numpy().astype(np.float64)
+    e1, e2 = np.abs(lp - ref_lp).max(), np.abs(ent - ref_ent).max()
+    print(f"{what}: logprob max-abs {e1:.2e}, entropy max-abs {e2:.2e}", flush=True)
+    assert e1 <= TOL and e2 <= TOL, what
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32], ids=["bf16", "f32"])
+@pytest.mark.parametrize("inv_t", [1.0, 1 / 0.7, 0.5, 0.0])
+def test_small_vocab(dev, dtype, inv_t):
+    x, tok = W.make_logits(5, 1000, seed=3, device=dev, dtype=dtype)
+    lp, ent = pda_token_logprobs(x, torch.from_numpy(tok).to(dev), inv_t)
+    torch.cuda.synchronize()
+    ref_lp, ref_ent = oracle.logprob(host_values(x), tok, np.float32(inv_t))
+    compare(lp, ent, ref_lp, ref_ent, f"V=1000 {dtype} 1/T={inv_t:.3f}")
+
+
+@pytest.mark.parametrize("name", ["llama3_vocab", "qwen_vocab"])
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32], ids=["bf16", "f32"])
+def test_full_size(dev, name, dtype):
+    """One decode step's LM-head logits (256 rows x the full vocabulary)."""
+    x, tok = W.logits_for(name, dev, dtype)
+    lp, ent = pda_token_logprobs(x, torch.from_numpy(tok).to(dev), 1.0)
+    torch.cuda.synchronize()
+    ref_lp, ref_ent = oracle.logprob(host_values(x), tok, 1.0)
+    compare(lp, ent, ref_lp, ref_ent, f"{name} {dtype}")
+    lp2, ent2 = pda_token_logprobs(x, torch.from_numpy(tok).to(dev), 1.0)
+    assert torch.equal(lp, lp2) and torch.equal(ent, ent2), "run-to-run"
+
+
+@pytest.mark.parametrize("V,stride", [(1001, 1008), (7, 8), (1, 8), (33000, 33024)])
+def test_ragged_vocab_and_padded_rows(dev, V, stride):
+    """Vocabularies that are not a multiple of the 16-byte load, and rows with
+    padding past the vocabulary that holds NaN (never read into the result)."""
+    x, tok = W.make_logits(6, V, seed=V, device=dev, dtype=torch.bfloat16)
+    padded = torch.full((6, stride), float("nan"), dtype=torch.bfloat16, device=dev)
+    padded[:, :V] = x
+    lp, ent = pda_token_logprobs(padded, torch.from_numpy(tok).to(dev), 1.0, vocab=V)
+    torch.cuda.synchronize()
+    ref_lp, ref_ent = oracle.logprob(W.bf16_bits(x), tok, 1.0)
+    compare(lp, ent, ref_lp, ref_ent, f"V={V} stride={stride}")
+
+
+def test_masked_huge_and_bad_tokens(dev):
+    """-inf logits drop out; logits of +-30000 do not overflow; a token id
+    outside the vocabulary gives NaN for its row only."""
+    x, tok = W.make_logits(4, 4096, seed=9, device=dev, dtype=torch.float32)
+    x[0, 2048:] = float("-inf")
+    tok[0] = min(int(tok[0]), 2047)
+    x[1] = x[1] * 0
+    x[1, 5], x[1, 6], x[1, 7] = 30000.0, 29990.0, -30000.0
+    tok[1] = 6
+    lp, ent = pda_token_logprobs(x, torch.from_numpy(tok).to(dev), 1.0)
+    torch.cuda.synchronize()
+    ref_lp, ref_ent = oracle.logprob(x.cpu().numpy(), tok, 1.0)
+    compare(lp, ent, ref_lp, ref_ent, "masked / huge logits")
+    bad = tok.copy()
+    bad[2] = 4096
+    bad[3] = -1
+    lp_b, ent_b = pda_token_logprobs(x, torch.from_numpy(bad).to(dev), 1.0)
+    torch.cuda.synchronize()
+    lp_b = lp_b.cpu().numpy()
+    assert np.isnan(lp_b[2]) and np.isnan(lp_b[3]) and np.isfinite(lp_b[:2]).all()
+    assert np.array_equal(ent_b.cpu().numpy(), ent.cpu().numpy())  # the entropy does not depend on the token
+
+
+def test_no_entropy_output(dev):
+    x, tok = W.make_logits(3, 5000, seed=11, device=dev)
+    lp, ent = pda_token_logprobs(x, torch.from_numpy(tok).to(dev), 1.0, entropy=False)
+    torch.cuda.synchronize()
+    assert ent is None
+    ref_lp, _ = oracle.logprob(W.bf16_bits(x), tok, 1.0, entropy=False)
+    assert np.abs(lp.cpu().numpy() - ref_lp).max() <= TOL
