@@ -8,19 +8,22 @@
 // One 1024-thread workgroup streams one row once; the row (250-300 KB for
 // Llama-3 / Qwen vocabularies in bf16) is read with 16-byte non-temporal
 // buffer loads (descriptor = the row, so no read leaves it), four in flight
-// per thread.  Each thread keeps an online state:
-//   m   running max of the raw logits,
-//   s = sum 2^{d},  t = sum 2^{d} d,  d = (logit - m) * log2(e) / T <= 0,
-// rescaled when m grows.  Differences are taken on the raw logits and only
-// then scaled, so a large common offset (logits of +-30000, say) costs no
-// precision; t is relative to m, so t / s stays small and the entropy keeps
-// its precision in fp32.  The states are combined over the workgroup in a
-// fixed order (a wavefront butterfly, then the 16 wavefronts in index
-// order), so results are reproducible.  Finally
-//   logprob = ln2 ((logit_tok - m) log2(e) / T - log2 s),  entropy = ln2 (log2 s - t / s).
-// Elements past the vocabulary have probability 0 by selection; -inf logits
-// get 2^{-inf} = 0 and add nothing to t.  A token id outside [0, vocab) gives
-// NaN.  The inverse temperature must be >= 0 (the host checks it).
+// per thread.  With k = log2(e) / T, each thread keeps an online state:
+//   m    running max of the raw logits, and mk = fp32(m * k),
+//   s = sum 2^d,  t = sum 2^d d,  d = fma(logit, k, -mk)   (<= ~0),
+// rescaled when m grows.  The fused multiply-add rounds d once, so a large
+// common offset of the logits (+-30000, say) costs no precision, and the
+// rounding of mk shifts every d of the state by the same amount, which
+// cancels in both results below.  t is relative to mk, so t / s stays small
+// and the entropy keeps its precision in fp32.  The states are combined over
+// the workgroup in a fixed order (a wavefront butterfly, then the 16
+// wavefronts in index order), so results are reproducible.  Finally
+//   logprob = ln2 (fma(logit_tok, k, -mk) - log2 s),  entropy = ln2 (log2 s - t / s).
+// The hot loop covers whole 16-byte chunks of the vocabulary; the one partial
+// chunk at its end is handled after it, with elements past the vocabulary at
+// probability 0.  -inf logits get 2^-inf = 0 and add nothing to t.  A token
+// id outside [0, vocab) gives NaN.  The inverse temperature must be >= 0 (the
+// host checks it), so the max of the logits is the max of the scaled values.
 #include "pda_internal.h"
 
 namespace pda {
@@ -33,18 +36,20 @@ constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kFloorMax = -1e30f;  // running max (raw logit units) before any finite logit
 
 struct LpState {
-  float m, s, t;
+  float m, mk, s, t;  // max of the raw logits, fp32(m * k), sum 2^d, sum 2^d d
 };
 
-// Merge two states; k = log2(e) / T converts raw logit differences.
-__device__ __forceinline__ LpState lp_merge(LpState a, LpState b, float k) {
-  const float M = fmaxf(a.m, b.m);
-  const float da = (a.m - M) * k, db = (b.m - M) * k;  // <= 0
+// Merge two states (both relative to their own mk).
+__device__ __forceinline__ LpState lp_merge(LpState a, LpState b) {
+  const bool a_big = a.m >= b.m;
+  const float MK = a_big ? a.mk : b.mk;
+  const float da = a.mk - MK, db = b.mk - MK;  // <= 0
   const float fa = __builtin_amdgcn_exp2f(da);
   const float fb = __builtin_amdgcn_exp2f(db);
-  // sum p (d relative to M) = sum p (d relative to m) + (m - M) k sum p, rescaled to M
+  // sum p (d relative to MK) = sum p (d relative to mk) + (mk - MK) sum p, rescaled
   LpState r;
-  r.m = M;
+  r.m = a_big ? a.m : b.m;
+  r.mk = MK;
   r.s = a.s * fa + b.s * fb;
   r.t = (a.s > 0.f ? (a.t + da * a.s) * fa : 0.f) + (b.s > 0.f ? (b.t + db * b.s) * fb : 0.f);
   return r;
@@ -85,52 +90,71 @@ __global__ void __launch_bounds__(kLpThreads) logprob_kernel(const LogprobArgs a
   const int row_bytes = (a.vocab * ESIZE + 15) / 16 * 16;
   const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base), 0, row_bytes, 0x00020000);
   const float k = a.inv_temperature * kLog2e;
-  const int nchunks = (a.vocab + E - 1) / E;
 
-  LpState st = {kFloorMax, 0.f, 0.f};
-  for (int c0 = tid; c0 < nchunks; c0 += kLpThreads * kLpUnroll) {
-    uint4 u[kLpUnroll];
+  LpState st = {kFloorMax, kFloorMax * k, 0.f, 0.f};
+  // Fold one chunk of E logits into the state; `valid` elements past the
+  // vocabulary (only in the last, partial chunk) get probability 0.
+  auto fold = [&](float (&x)[E], int valid) {
+    float mx = kFloorMax;
 #pragma unroll
-    for (int j = 0; j < kLpUnroll; ++j) {  // loads past the row come back as zeros (masked below)
-      const u32x4_t t = __builtin_amdgcn_raw_buffer_load_b128(rsrc, (c0 + j * kLpThreads) * 16, 0, 2);
-      u[j] = make_uint4(t[0], t[1], t[2], t[3]);
+    for (int e = 0; e < E; ++e)
+      if (e < valid) mx = fmaxf(mx, x[e]);
+    if (mx > st.m) {  // the max grows: rescale the state to the new mk
+      const float mk = mx * k;
+      const float dm = st.mk - mk;
+      const float sc = __builtin_amdgcn_exp2f(dm);
+      st.t = st.s > 0.f ? (st.t + dm * st.s) * sc : 0.f;
+      st.s *= sc;
+      st.m = mx;
+      st.mk = mk;
     }
 #pragma unroll
-    for (int j = 0; j < kLpUnroll; ++j) {
-      const int c = c0 + j * kLpThreads;
-      float x[E];
-      unpack<ESIZE>(u[j], x);
-      float mx = kFloorMax;
-#pragma unroll
-      for (int e = 0; e < E; ++e)
-        if (c * E + e < a.vocab) mx = fmaxf(mx, x[e]);
-      if (mx > st.m) {  // the max grows: rescale the state
-        const float dm = (st.m - mx) * k;
-        const float sc = __builtin_amdgcn_exp2f(dm);
-        st.t = st.s > 0.f ? (st.t + dm * st.s) * sc : 0.f;
-        st.s *= sc;
-        st.m = mx;
-      }
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const float d = (x[e] - st.m) * k;
-        const float p = c * E + e < a.vocab ? __builtin_amdgcn_exp2f(d) : 0.f;
+    for (int e = 0; e < E; ++e) {
+      if (e < valid) {
+        const float d = fmaf(x[e], k, -st.mk);
+        const float p = __builtin_amdgcn_exp2f(d);
         st.s += p;
-        st.t += p > 0.f ? p * d : 0.f;  // a zero-probability term adds nothing, also at -inf
+        st.t = fmaf(p, fmaxf(d, kFloorMax), st.t);  // p = 0 exactly where d = -inf: adds 0
+      }
+    }
+  };
+  auto load = [&](int c) {
+    const u32x4_t t = __builtin_amdgcn_raw_buffer_load_b128(rsrc, c * 16, 0, 2);
+    return make_uint4(t[0], t[1], t[2], t[3]);
+  };
+  const int nfull = a.vocab / E;  // whole chunks
+  // Every pass issues all its loads first (those past the row return zeros
+  // and are skipped), so the last, partly filled pass costs one round trip
+  // like the others.
+  for (int c = tid; c < nfull; c += kLpUnroll * kLpThreads) {
+    uint4 u[kLpUnroll];
+#pragma unroll
+    for (int j = 0; j < kLpUnroll; ++j) u[j] = load(c + j * kLpThreads);
+#pragma unroll
+    for (int j = 0; j < kLpUnroll; ++j) {
+      if (c + j * kLpThreads < nfull) {
+        float x[E];
+        unpack<ESIZE>(u[j], x);
+        fold(x, E);
       }
     }
   }
+  if (tid == nfull % kLpThreads && nfull * E < a.vocab) {  // the partial chunk (the descriptor covers it)
+    float x[E];
+    unpack<ESIZE>(load(nfull), x);
+    fold(x, a.vocab - nfull * E);
+  }
   // ---- combine: wavefront butterfly, then the wavefronts in index order ----
   for (int o = 1; o < kWaveSize; o <<= 1) {
-    LpState other = {__shfl_xor(st.m, o), __shfl_xor(st.s, o), __shfl_xor(st.t, o)};
-    st = (tid & o) ? lp_merge(other, st, k) : lp_merge(st, other, k);  // the same order in both lanes
+    LpState other = {__shfl_xor(st.m, o), __shfl_xor(st.mk, o), __shfl_xor(st.s, o), __shfl_xor(st.t, o)};
+    st = (tid & o) ? lp_merge(other, st) : lp_merge(st, other);  // the same order in both lanes
   }
   const int w = tid / kWaveSize;
   if ((tid & (kWaveSize - 1)) == 0) s_state[w] = st;
   __syncthreads();
   if (tid == 0) {
     LpState r = s_state[0];
-    for (int x = 1; x < kLpThreads / kWaveSize; ++x) r = lp_merge(r, s_state[x], k);
+    for (int x = 1; x < kLpThreads / kWaveSize; ++x) r = lp_merge(r, s_state[x]);
     const float log2s = __builtin_amdgcn_logf(r.s);  // log2
     const int tok = a.tokens[row];
     float lp;
@@ -138,7 +162,7 @@ __global__ void __launch_bounds__(kLpThreads) logprob_kernel(const LogprobArgs a
       const char* p = base + (size_t)tok * ESIZE;
       const float raw = ESIZE == 2 ? __uint_as_float((unsigned)*reinterpret_cast<const uint16_t*>(p) << 16)
                                    : *reinterpret_cast<const float*>(p);
-      lp = kLn2 * ((raw - r.m) * k - log2s);
+      lp = kLn2 * (fmaf(raw, k, -r.mk) - log2s);
     } else {
       lp = __builtin_nanf("");
     }
