@@ -26,6 +26,9 @@ Other steps around attention (--op):
   graph    append + attention as one captured HIP graph against the same
            calls issued eagerly (default workload: the tiny batch, where
            launch overhead dominates)
+  prefix   the shared-prefix workload (32 prompts x 8 samples) with each
+           prompt's prefix attended once for its samples, against the plain
+           decode step
   logprob  log-probability of each sampled token and the entropy over the
            LM-head logits of one decode step (256 rows x 128256 Llama-3
            vocabulary, bf16; --logits-f32, --config qwen_vocab)
@@ -308,6 +311,55 @@ def op_graph(args):
     return result
 
 
+def op_prefix(args):
+    """The shared-prefix workload with each prompt's prefix attended once
+    (pda_decode_shared_prefix), against the plain decode step on the same
+    inputs."""
+    import torch
+
+    import workloads as W
+    from paper_2405_11143_amd import pda_decode, pda_decode_shared_prefix
+
+    args.config = args.config if W.CONFIGS.get(args.config, {}).get("prompts") else "shared_prefix"
+    dev, st, q, k, v, bt, lens, plan, out, ws = setup(args, 1)
+    gs = torch.from_numpy(st.group_start).to(dev)
+    gp = torch.from_numpy(st.group_prefix_len).to(dev)
+    cfg = W.CONFIGS[args.config]
+    stream = torch.cuda.current_stream(dev)
+    kw = dict(max_context_len=st.max_context_len, partition_tokens=args.partition_tokens, stream=stream)
+    out2 = torch.empty_like(out)
+
+    def shared():
+        pda_decode_shared_prefix(q, k, v, bt, lens, st.scale, gs, gp, out2, max_group_size=cfg["samples"],
+                                 max_prefix_len=cfg["prefix_len"], workspace=ws_sp, **kw)
+
+    def plain():
+        pda_decode(q, k, v, bt, lens, st.scale, out, workspace=ws, **kw)
+
+    from paper_2405_11143_amd import make_prefix_groups, make_problem, pda_plan_shared_prefix
+    prob = make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq, st.max_context_len,
+                        args.partition_tokens)
+    need = pda_plan_shared_prefix(prob, make_prefix_groups(len(gp), cfg["samples"], cfg["prefix_len"]))
+    ws_sp = torch.empty(max(need["workspace_bytes"], 16), dtype=torch.uint8, device=dev)
+    for f in (shared, plain):
+        for _ in range(args.warmup):
+            f()
+    torch.cuda.synchronize()
+    ms = timed(shared, args.steps, stream)
+    ms_plain = timed(plain, args.steps, stream)
+    alg = st.algorithmic_bytes()
+    value = alg / (ms * 1e-3) / 1e9
+    result = base_result(args, value, "GB/s", ms, "shared-prefix decode HBM GB/s (unique bytes), "
+                         "each prompt's prefix attended once",
+                         config_of(st, cfg["desc"], args.config, need, prompts=cfg["prompts"], samples=cfg["samples"],
+                                   prefix_len=cfg["prefix_len"]))
+    result.update({"seq_steps_per_s": round(st.B / (ms * 1e-3), 1), "pct_of_peak": round(100.0 * value / PEAK_GBS, 2),
+                   "algorithmic_bytes_per_step": alg, "ms_per_step_plain_decode": round(ms_plain, 5),
+                   "speedup_vs_plain_decode": round(ms_plain / ms, 3),
+                   "roofline": roofline(value, ms, KERNEL, args.config + "_shared"), "cpu_baseline": None})
+    return result
+
+
 def op_logprob(args):
     import torch
 
@@ -351,7 +403,7 @@ def main(argv=None):
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--op", default="decode", choices=["decode", "multi", "append", "graph", "logprob"])
+    ap.add_argument("--op", default="decode", choices=["decode", "multi", "append", "graph", "logprob", "prefix"])
     ap.add_argument("--logits-f32", action="store_true", help="--op logprob: float32 logits (default bf16)")
     ap.add_argument("--config", default=None, help="workload (default: llama3_8b; tiny for --op graph)")
     ap.add_argument("--tokens", type=int, default=None,
@@ -373,7 +425,7 @@ def main(argv=None):
               file=sys.stderr)
         return 2
     if args.config is None:
-        args.config = {"graph": "tiny", "logprob": "llama3_vocab"}.get(args.op, "llama3_8b")
+        args.config = {"graph": "tiny", "logprob": "llama3_vocab", "prefix": "shared_prefix"}.get(args.op, "llama3_8b")
     if args.tokens is None:
         args.tokens = 4 if args.op == "multi" else 1
 
@@ -401,6 +453,8 @@ def main(argv=None):
         result = op_append(args)
     elif args.op == "logprob":
         result = op_logprob(args)
+    elif args.op == "prefix":
+        result = op_prefix(args)
     else:
         result = op_graph(args)
     print(json.dumps(result), flush=True)

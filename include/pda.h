@@ -143,6 +143,40 @@ int pda_partition_attention(const pda_problem *prob, const void *q, const void *
 int pda_merge_partitions(const pda_problem *prob, const int32_t *context_lens, float *out,
                          const void *workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* Shared-prefix groups for parallel sampling (Section 3.2: PagedAttention
+ * lets the samples of one prompt share the prompt's KV blocks).  The members
+ * of group i are the sequences [group_start[i], group_start[i+1]) -- a
+ * prompt's samples sit next to each other in the batch -- and their first
+ * group_prefix_len[i] tokens (a multiple of 16, at most every member's
+ * context length) live in the same physical blocks, i.e. entries
+ * 0 .. group_prefix_len[i]/16 - 1 of their block-table rows are equal.
+ * Sequences in no group attend as in pda_decode.  The host bounds size the
+ * launch; the two arrays are device data (their contents are clamped to the
+ * bounds, never trusted for memory safety). */
+typedef struct pda_prefix_groups {
+  int32_t num_groups;               /* >= 0 */
+  int32_t max_group_size;           /* bound on members per group: 1 .. 64 / G */
+  int32_t max_prefix_len;           /* bound on group_prefix_len[]: a multiple of 16, <= max_context_len */
+  const int32_t *group_start;       /* device int32 [num_groups + 1], non-decreasing, within [0, num_seqs] */
+  const int32_t *group_prefix_len;  /* device int32 [num_groups] */
+} pda_prefix_groups;
+
+/* Plan of pda_decode_shared_prefix (the workspace is larger than pda_decode's);
+ * only the host bounds of `groups` are read. */
+int pda_plan_shared_prefix(const pda_problem *prob, const pda_prefix_groups *groups, pda_plan_info *plan);
+
+/* The decode step of pda_decode (one new token per sequence: num_query_tokens
+ * 0 or 1) with each group's shared prefix attended once for all its members:
+ * a work item reads the prefix blocks and computes all members x G query
+ * rows of a KV head on one 16-row MFMA tile per wavefront, and every member
+ * row then merges the prefix's partial softmax state with those of its own
+ * tokens.  The result is the same attention as pda_decode (up to rounding).
+ * `workspace` must hold pda_plan_shared_prefix()'s workspace_bytes. */
+int pda_decode_shared_prefix(const pda_problem *prob, const pda_prefix_groups *groups, const void *q,
+                             const void *k_cache, const void *v_cache, const int32_t *block_table,
+                             const int32_t *context_lens, float scale, float *out, void *workspace,
+                             size_t workspace_bytes, hipStream_t stream);
+
 /* KV-cache append, the step before attention (Appendix C: the rollout stage's
  * KV-cache management): store the keys and values of the n new tokens of
  * every sequence in the cache.  New token i of sequence b goes to position

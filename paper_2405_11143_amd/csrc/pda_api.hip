@@ -52,13 +52,28 @@ struct Plan {
   pda_plan_info info;
   int query_chunk;        // new tokens per work item: min(n, 16 / G)
   int num_query_chunks;   // ceil(n / query_chunk)
-  size_t items;           // P * B * Hkv * chunks work items (pass-1 workgroups)
-  size_t slots;           // partial states, one per (sequence, new token, query head, partition); 0 when P == 1
+  int prefix_partitions;  // Pp: partitions of the longest shared prefix (0 without groups)
+  size_t regular_items;   // P * B * Hkv * chunks (pass-1 workgroups of the sequences' own tokens)
+  size_t items;           // regular items + num_groups * Pp * Hkv prefix items
+  size_t slots;           // partial states: (Pp + P) per output row; 0 when nothing is split
 };
 
-int make_plan(const pda_problem* p, Plan* plan) {
+// Shared-prefix groups: host bounds checked here (the plan needs no more);
+// the arrays are device data, required by the step itself.
+int check_groups(const pda_problem* p, const pda_prefix_groups* g) {
+  if (!g) return PDA_ERR_NULL;
+  if (g->num_groups < 0 || g->max_group_size < 1 || g->max_prefix_len < 0 ||
+      g->max_prefix_len % pda::kBlockTokens != 0 || g->max_prefix_len > p->max_context_len)
+    return PDA_ERR_SHAPE;
+  if (p->num_query_tokens > 1) return PDA_ERR_UNSUPPORTED;  // one new token per sequence
+  if (g->max_group_size * (p->num_q_heads / p->num_kv_heads) > 64) return PDA_ERR_UNSUPPORTED;
+  return PDA_OK;
+}
+
+int make_plan(const pda_problem* p, const pda_prefix_groups* groups, Plan* plan) {
   int rc = check_problem(p);
   if (rc != PDA_OK) return rc;
+  if (groups && (rc = check_groups(p, groups)) != PDA_OK) return rc;
   const int n = query_tokens(p);
   const int G = p->num_q_heads / p->num_kv_heads;
   const int qc = std::min(n, pda::kMaxGroup / G);
@@ -74,17 +89,27 @@ int make_plan(const pda_problem* p, Plan* plan) {
     if (rounded < tp) tp = rounded;  // the whole context fits one partition
   }
   const int64_t parts = p->max_context_len > 0 ? ((int64_t)p->max_context_len + tp - 1) / tp : 1;
-  if (parts * units > 0x7fffffff || parts * p->num_seqs > 0x7fffffff) return PDA_ERR_SHAPE;
+  const int num_groups = groups ? groups->num_groups : 0;
+  const int64_t pparts = num_groups > 0 ? ((int64_t)groups->max_prefix_len + tp - 1) / tp : 0;
+  const int64_t prefix_items = (int64_t)num_groups * pparts * p->num_kv_heads;
+  if (parts * units + prefix_items > 0x7fffffff || parts * p->num_seqs + num_groups * pparts > 0x7fffffff)
+    return PDA_ERR_SHAPE;
   *plan = Plan{};
   plan->info.partition_tokens = tp;
   plan->info.num_partitions = (int32_t)parts;
   plan->query_chunk = qc;
   plan->num_query_chunks = nqc;
+  plan->prefix_partitions = (int)pparts;
   if (p->num_seqs > 0) {
-    plan->items = (size_t)(parts * units);
-    plan->slots = parts > 1 ? (size_t)p->num_seqs * n * p->num_q_heads * (size_t)parts : 0;
-    // partial states (O, m, l) first, then the work order
-    plan->info.workspace_bytes = plan->slots * (p->head_dim + 2) * sizeof(float) + plan->items * sizeof(int32_t);
+    plan->regular_items = (size_t)(parts * units);
+    plan->items = plan->regular_items + (size_t)prefix_items;
+    // with groups every member row is merged from its prefix and own partitions
+    const bool split = parts > 1 || groups != nullptr;
+    plan->slots = split ? (size_t)p->num_seqs * n * p->num_q_heads * (size_t)(pparts + parts) : 0;
+    // partial states (O, m, l), then the work order, then (with groups) the
+    // per-sequence prefix lengths
+    plan->info.workspace_bytes = plan->slots * (p->head_dim + 2) * sizeof(float) + plan->items * sizeof(int32_t) +
+                                 (groups ? (size_t)p->num_seqs * sizeof(int32_t) : 0);
   }
   return PDA_OK;
 }
@@ -103,6 +128,9 @@ void fill_args(const pda_problem* p, const Plan* plan, void* ws, pda::StepArgs* 
     }
     args->order = reinterpret_cast<int32_t*>(wsf + plan->slots * (p->head_dim + 2));
   }
+  args->slots_per_row = plan->prefix_partitions + plan->info.num_partitions;
+  args->prefix_partitions = plan->prefix_partitions;
+  args->num_regular_items = (int32_t)plan->regular_items;
   args->num_seqs = p->num_seqs;
   args->num_q_heads = p->num_q_heads;
   args->num_kv_heads = p->num_kv_heads;
@@ -118,21 +146,31 @@ void fill_args(const pda_problem* p, const Plan* plan, void* ws, pda::StepArgs* 
 }
 
 // Validation shared by the entry points that launch pass 1; fills `args`.
-int prepare_step(const pda_problem* p, const void* q, const void* k, const void* v, const int32_t* bt,
-                 const int32_t* lens, float scale, float* out, void* ws, size_t ws_bytes, Plan* plan,
-                 pda::StepArgs* args) {
+int prepare_step(const pda_problem* p, const pda_prefix_groups* groups, const void* q, const void* k, const void* v,
+                 const int32_t* bt, const int32_t* lens, float scale, float* out, void* ws, size_t ws_bytes,
+                 Plan* plan, pda::StepArgs* args) {
   int rc = check_problem(p);
   if (rc != PDA_OK) return rc;
   if (p->num_seqs > 0 && (!q || !k || !v || !bt || !lens || !out)) return PDA_ERR_NULL;
   if (!isfinite(scale)) return PDA_ERR_VALUE;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 4)) return PDA_ERR_ALIGNMENT;
-  rc = make_plan(p, plan);
+  rc = make_plan(p, groups, plan);
   if (rc != PDA_OK) return rc;
   if (plan->info.workspace_bytes > 0) {
     if (!ws || ws_bytes < plan->info.workspace_bytes) return PDA_ERR_WORKSPACE;
     if (!aligned(ws, 16)) return PDA_ERR_ALIGNMENT;
   }
+  if (groups && groups->num_groups > 0 && p->num_seqs > 0 && (!groups->group_start || !groups->group_prefix_len))
+    return PDA_ERR_NULL;
   fill_args(p, plan, ws, args);
+  if (groups && groups->num_groups > 0 && p->num_seqs > 0) {
+    args->group_start = groups->group_start;
+    args->group_prefix_len = groups->group_prefix_len;
+    args->num_groups = groups->num_groups;
+    args->max_group_size = groups->max_group_size;
+    args->max_prefix_len = groups->max_prefix_len;
+    args->seq_prefix = args->order + plan->items;
+  }
   args->q = static_cast<const uint16_t*>(q);
   args->k = static_cast<const uint16_t*>(k);
   args->v = static_cast<const uint16_t*>(v);
@@ -152,11 +190,20 @@ int prepare_append(const pda_problem* p, const void* k_new, const void* v_new, c
   if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16))
     return PDA_ERR_ALIGNMENT;
   Plan plan;
-  rc = make_plan(p, &plan);
+  rc = make_plan(p, nullptr, &plan);
   if (rc != PDA_OK) return rc;
   fill_args(p, &plan, nullptr, args);
   args->table = bt;
   args->lens = lens;
+  return PDA_OK;
+}
+
+// The launches of one attention step (work order, pass 1, merge).
+int launch_attention(const pda_problem* p, const Plan& plan, const pda::StepArgs& args, hipStream_t stream) {
+  if (p->num_seqs == 0) return PDA_OK;
+  if (pda::launch_order(args, stream) != hipSuccess) return PDA_ERR_HIP;
+  if (pda::launch_partition(args, p->head_dim, stream) != hipSuccess) return PDA_ERR_HIP;
+  if (plan.slots > 0 && pda::launch_merge(args, p->head_dim, stream) != hipSuccess) return PDA_ERR_HIP;
   return PDA_OK;
 }
 
@@ -179,7 +226,7 @@ extern "C" {
 int pda_plan(const pda_problem* prob, pda_plan_info* info) {
   if (!info) return PDA_ERR_NULL;
   Plan plan;
-  int rc = make_plan(prob, &plan);
+  int rc = make_plan(prob, nullptr, &plan);
   if (rc != PDA_OK) return rc;
   *info = plan.info;
   return PDA_OK;
@@ -188,7 +235,7 @@ int pda_plan(const pda_problem* prob, pda_plan_info* info) {
 int pda_workspace_bytes(const pda_problem* prob, size_t* bytes) {
   if (!bytes) return PDA_ERR_NULL;
   Plan plan;
-  int rc = make_plan(prob, &plan);
+  int rc = make_plan(prob, nullptr, &plan);
   if (rc != PDA_OK) return rc;
   *bytes = plan.info.workspace_bytes;
   return PDA_OK;
@@ -199,7 +246,7 @@ int pda_partition_attention(const pda_problem* prob, const void* q, const void* 
                             void* workspace, size_t workspace_bytes, hipStream_t stream) {
   Plan plan;
   pda::StepArgs args;
-  int rc = prepare_step(prob, q, k_cache, v_cache, block_table, context_lens, scale, out, workspace,
+  int rc = prepare_step(prob, nullptr, q, k_cache, v_cache, block_table, context_lens, scale, out, workspace,
                         workspace_bytes, &plan, &args);
   if (rc != PDA_OK) return rc;
   if (prob->num_seqs == 0) return PDA_OK;
@@ -216,7 +263,7 @@ int pda_merge_partitions(const pda_problem* prob, const int32_t* context_lens, f
   if (!context_lens || !out) return PDA_ERR_NULL;
   if (!aligned(workspace, 16) || !aligned(out, 4)) return PDA_ERR_ALIGNMENT;
   Plan plan;
-  rc = make_plan(prob, &plan);
+  rc = make_plan(prob, nullptr, &plan);
   if (rc != PDA_OK) return rc;
   if (plan.slots == 0) return PDA_OK;  // nothing was split
   if (!workspace || workspace_bytes < plan.info.workspace_bytes) return PDA_ERR_WORKSPACE;
@@ -255,8 +302,8 @@ int pda_step_graph_create(const pda_problem* prob, const void* q, const void* k_
   Plan plan;
   int rc = prepare_append(prob, k_new, v_new, block_table, context_lens, k_cache, v_cache, &append_args);
   if (rc != PDA_OK) return rc;
-  rc = prepare_step(prob, q, k_cache, v_cache, block_table, context_lens, scale, out, workspace, workspace_bytes,
-                    &plan, &args);
+  rc = prepare_step(prob, nullptr, q, k_cache, v_cache, block_table, context_lens, scale, out, workspace,
+                    workspace_bytes, &plan, &args);
   if (rc != PDA_OK) return rc;
   pda_step_graph* g = new (std::nothrow) pda_step_graph{nullptr, nullptr, prob->num_seqs == 0};
   if (!g) return PDA_ERR_HIP;
@@ -305,6 +352,28 @@ int pda_step_graph_destroy(pda_step_graph* graph) {
   if (graph->graph && hipGraphDestroy(graph->graph) != hipSuccess) rc = PDA_ERR_HIP;
   delete graph;
   return rc;
+}
+
+int pda_plan_shared_prefix(const pda_problem* prob, const pda_prefix_groups* groups, pda_plan_info* info) {
+  if (!info) return PDA_ERR_NULL;
+  Plan plan;
+  int rc = make_plan(prob, groups, &plan);
+  if (rc != PDA_OK) return rc;
+  *info = plan.info;
+  return PDA_OK;
+}
+
+int pda_decode_shared_prefix(const pda_problem* prob, const pda_prefix_groups* groups, const void* q,
+                             const void* k_cache, const void* v_cache, const int32_t* block_table,
+                             const int32_t* context_lens, float scale, float* out, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream) {
+  if (!groups) return PDA_ERR_NULL;
+  Plan plan;
+  pda::StepArgs args;
+  int rc = prepare_step(prob, groups, q, k_cache, v_cache, block_table, context_lens, scale, out, workspace,
+                        workspace_bytes, &plan, &args);
+  if (rc != PDA_OK) return rc;
+  return launch_attention(prob, plan, args, stream);
 }
 
 int pda_token_logprobs(int32_t num_rows, int32_t vocab, int64_t row_stride, int32_t logits_dtype, const void* logits,

@@ -24,10 +24,10 @@ struct StepArgs {
   const int32_t* table;    // int32 [B][max_blocks_per_seq]
   const int32_t* lens;     // int32 [B]
   float* out;              // fp32 [B][n][Hq][D]
-  int32_t* order;          // int32 [P*B*Hkv*NQC]: work items, largest partition first
-  float* part_o;           // fp32 [B*n*Hq*P][D]  unnormalised partition outputs (P > 1)
-  float* part_m;           // fp32 [B*n*Hq*P]     partition reference max, log2 domain
-  float* part_l;           // fp32 [B*n*Hq*P]     partition softmax denominators
+  int32_t* order;          // int32 [items]: work items, largest partition first
+  float* part_o;           // fp32 [B*n*Hq*slots_per_row][D]  unnormalised partition outputs
+  float* part_m;           // fp32 [B*n*Hq*slots_per_row]     partition reference max, log2 domain
+  float* part_l;           // fp32 [B*n*Hq*slots_per_row]     partition softmax denominators
   float scale_log2;        // softmax scale * log2(e)
   int32_t num_seqs;        // B
   int32_t num_q_heads;     // Hq
@@ -41,7 +41,25 @@ struct StepArgs {
   int32_t num_query_chunks;  // NQC = ceil(n / query_chunk)
   int32_t partition_tokens;  // T_p, multiple of 16
   int32_t num_partitions;    // P = max(1, ceil(max_context_len / T_p))
+  // Shared-prefix groups (num_groups == 0: none).  The members of group i are
+  // sequences [group_start[i], group_start[i+1]); their first
+  // group_prefix_len[i] tokens sit in the same blocks.
+  const int32_t* group_start;       // int32 [num_groups + 1]
+  const int32_t* group_prefix_len;  // int32 [num_groups], multiples of 16
+  int32_t* seq_prefix;              // int32 [B] (workspace): prefix tokens of each sequence's group
+  int32_t num_groups;
+  int32_t max_group_size;           // members of one group, <= 64 / G
+  int32_t max_prefix_len;           // bound on group_prefix_len, multiple of 16
+  int32_t prefix_partitions;        // Pp = ceil(max_prefix_len / T_p)
+  int32_t slots_per_row;            // Pp + P partial states per output row (P when no groups)
+  int32_t num_regular_items;        // items below this index are (partition, sequence, KV head, chunk)
 };
+
+// Prefix tokens of sequence b's group (0 without groups); pass 1 and the
+// merge treat tokens [0, prefix) as covered by the group's prefix items.
+__device__ __forceinline__ int seq_prefix_len(const StepArgs& a, int b) {
+  return a.seq_prefix ? a.seq_prefix[b] : 0;
+}
 
 // Tokens that the last row of query chunk `chunk` sees (<= 0: none).
 __device__ __forceinline__ int chunk_visible(const StepArgs& a, int L, int chunk) {

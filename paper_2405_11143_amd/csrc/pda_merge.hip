@@ -26,17 +26,21 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
-// Merge n partitions whose states sit at index first + k * step (k < n) of
-// part_m / part_l, with outputs at (first + k * step) * D of part_o.
+// Merge n partitions of one row: partition k (k < n) sits at state index
+// first + k for k < n_pre (the group's prefix partitions) and at
+// first + gap + k after them (the row's own partitions); the outputs sit at
+// D times those indices in part_o.
 template <int D>
-__device__ __forceinline__ void merge_partitions(const StepArgs& a, size_t first, size_t step, int n, float* orow) {
+__device__ __forceinline__ void merge_partitions(const StepArgs& a, size_t first, int n_pre, int gap, int n,
+                                                 float* orow) {
   constexpr int PER = D / kWaveSize;
   const int lane = threadIdx.x;
+  auto slot = [&](int k) { return first + (size_t)k + (k >= n_pre ? gap : 0); };
   // States are read lane-parallel (lane x holds partition p0 + x), so the
   // dependent chain is states -> outputs, whatever n is.
   float M = -__builtin_huge_valf();
   for (int p0 = 0; p0 < n; p0 += kWaveSize)
-    if (p0 + lane < n) M = fmaxf(M, a.part_m[first + (p0 + lane) * step]);
+    if (p0 + lane < n) M = fmaxf(M, a.part_m[slot(p0 + lane)]);
   M = wave_max(M);
   float acc[PER];
 #pragma unroll
@@ -44,13 +48,12 @@ __device__ __forceinline__ void merge_partitions(const StepArgs& a, size_t first
   float lpart = 0.f;
   for (int p0 = 0; p0 < n; p0 += kWaveSize) {
     const int p = p0 + lane;
-    const size_t idx = first + (size_t)p * step;
-    const float wgt = p < n ? __builtin_amdgcn_exp2f(a.part_m[idx] - M) : 0.f;  // 2^(m_p - M)
-    if (p < n) lpart = fmaf(wgt, a.part_l[idx], lpart);
+    const float wgt = p < n ? __builtin_amdgcn_exp2f(a.part_m[slot(p)] - M) : 0.f;  // 2^(m_p - M)
+    if (p < n) lpart = fmaf(wgt, a.part_l[slot(p)], lpart);
     const int cnt = min(kWaveSize, n - p0);
     for (int x = 0; x < cnt; ++x) {
       const float sc = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, wgt), x));
-      const float* src = a.part_o + (first + (size_t)(p0 + x) * step) * D + lane * PER;
+      const float* src = a.part_o + slot(p0 + x) * D + lane * PER;
 #pragma unroll
       for (int e = 0; e < PER; ++e) acc[e] = fmaf(sc, src[e], acc[e]);
     }
@@ -65,18 +68,25 @@ __device__ __forceinline__ int clamped_len(const StepArgs& a, int b) {
   return L < 0 ? 0 : (L > a.max_context_len ? a.max_context_len : L);
 }
 
-// Partition k of output row (b, i, h) sits at slot row * P + k, with
-// row = (b * n + i) * Hq + h; the row has as many partitions as the query
-// chunk of new token i sees.
+// Output row (b, i, h), row = (b * n + i) * Hq + h, has its partial states
+// at slots row * S .. row * S + S - 1 (S = slots_per_row): first the prefix
+// partitions of its group, then, from slot row * S + Pp, its own partitions
+// (as many as the query chunk of new token i sees after the prefix).
 template <int D>
 __global__ void __launch_bounds__(kWaveSize) merge_kernel(const StepArgs a) {
   const int row = blockIdx.x;
   const int i = (row / a.num_q_heads) % a.num_query_tokens;
-  const int L = clamped_len(a, row / (a.num_q_heads * a.num_query_tokens));
+  const int b = row / (a.num_q_heads * a.num_query_tokens);
+  const int L = clamped_len(a, b);
   const int vis = chunk_visible(a, L, i / a.query_chunk);
-  const int nparts = vis > 0 ? (vis + a.partition_tokens - 1) / a.partition_tokens : 0;
-  if (nparts <= 1) return;  // pass 1 wrote the final row
-  merge_partitions<D>(a, (size_t)row * a.num_partitions, 1, nparts, a.out + (size_t)row * D);
+  if (vis <= 0) return;  // pass 1 wrote zeros
+  const int Tp = a.partition_tokens;
+  const int t0 = min(seq_prefix_len(a, b), vis);
+  const int n_pre = (t0 + Tp - 1) / Tp;
+  const int n_own = (vis - t0 + Tp - 1) / Tp;
+  if (n_pre == 0 && n_own <= 1) return;  // pass 1 wrote the final row
+  merge_partitions<D>(a, (size_t)row * a.slots_per_row, n_pre, a.prefix_partitions - n_pre, n_pre + n_own,
+                      a.out + (size_t)row * D);
 }
 
 }  // namespace

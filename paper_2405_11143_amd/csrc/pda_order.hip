@@ -1,5 +1,4 @@
-// Work order of pass 1: the (partition, sequence, KV head, query chunk)
-// items, largest partition first.
+// Work order of pass 1: every item, largest first.
 //
 // Pass 1 launches one workgroup per item and the GPU starts workgroups in
 // index order, so the order of the items is the schedule.  Contexts are
@@ -9,14 +8,20 @@
 // Sorting the items by size, largest first (a greedy longest-processing-
 // time schedule), leaves only short items for the end: on MI355X it raised
 // pass 1 by 3-10% on the Llama-3-shaped decode steps.  Items of size zero
-// (partitions past a context's end) come last and exit at once.
+// (partitions past what a context needs) come last and exit at once.
 //
-// One workgroup does a counting sort of the B*P (sequence, partition) pairs
-// by size in blocks (classes capped at kOrderBuckets - 1 blocks) with LDS
-// atomics, then writes the items of each pair (one per KV head and query
-// chunk).  The order within a size
-// class depends on atomic timing; no result does -- every item computes the
-// same values whichever workgroup runs it.
+// The items come in pairs of equal size: a regular pair (sequence, partition)
+// stands for its items of every KV head and query chunk, a prefix pair
+// (shared-prefix group, prefix partition) for its items of every KV head.
+// One workgroup counting-sorts the pairs by size in blocks (classes capped
+// at kOrderBuckets - 1 blocks) with LDS atomics, then writes the items of
+// each pair.  The order within a size class depends on atomic timing; no
+// result does -- every item computes the same values whichever workgroup
+// runs it.
+//
+// With shared-prefix groups the same workgroup first writes, for every
+// sequence, the prefix length of its group (0 outside any group) into the
+// workspace; the sizes of the regular pairs, pass 1 and the merge read it.
 #include "pda_internal.h"
 
 namespace pda {
@@ -27,15 +32,43 @@ __global__ void __launch_bounds__(kOrderThreads) order_kernel(const StepArgs a) 
   const int tid = threadIdx.x;
   const int B = a.num_seqs;
   const int P = a.num_partitions;
+  const int Pp = a.prefix_partitions;
   const int Tp = a.partition_tokens;
-  const int pairs = B * P;
-  // size class of pair (b, p): kOrderBuckets - 1 - blocks, so larger first
+  const int regular_pairs = B * P;
+  const int pairs = regular_pairs + a.num_groups * Pp;
+
+  if (a.seq_prefix) {  // per-sequence prefix length (group contents clamped: device data)
+    for (int b = tid; b < B; b += kOrderThreads) a.seq_prefix[b] = 0;
+    __threadfence_block();
+    __syncthreads();
+    for (int grp = tid; grp < a.num_groups; grp += kOrderThreads) {
+      const int first = min(max(a.group_start[grp], 0), B);
+      const int last = min(min(a.group_start[grp + 1], B), first + a.max_group_size);
+      int plen = a.group_prefix_len[grp];
+      plen = plen < 0 ? 0 : (plen > a.max_prefix_len ? a.max_prefix_len : plen) / kBlockTokens * kBlockTokens;
+      for (int b = first; b < last; ++b) a.seq_prefix[b] = plen;
+    }
+    __threadfence_block();
+    __syncthreads();
+  }
+
+  // size class of pair idx: kOrderBuckets - 1 - blocks, so larger first
   auto bucket = [&](int idx) {
-    const int b = idx % B;
-    const int p = idx / B;
-    int L = a.lens[b];
-    L = L < 0 ? 0 : (L > a.max_context_len ? a.max_context_len : L);
-    const int tok = max(0, min(L, (p + 1) * Tp) - p * Tp);
+    int tok;
+    if (idx < regular_pairs) {
+      const int b = idx % B;
+      const int p = idx / B;
+      int L = a.lens[b];
+      L = L < 0 ? 0 : (L > a.max_context_len ? a.max_context_len : L);
+      const int t0 = min(seq_prefix_len(a, b), L);
+      tok = max(0, min(L, t0 + (p + 1) * Tp) - (t0 + p * Tp));
+    } else {
+      const int grp = (idx - regular_pairs) / Pp;
+      const int pp = (idx - regular_pairs) % Pp;
+      int plen = a.group_prefix_len[grp];
+      plen = plen < 0 ? 0 : (plen > a.max_prefix_len ? a.max_prefix_len : plen);
+      tok = max(0, min(plen, (pp + 1) * Tp) - pp * Tp);
+    }
     const int blocks = min((tok + kBlockTokens - 1) / kBlockTokens, kOrderBuckets - 1);
     return kOrderBuckets - 1 - blocks;
   };
@@ -64,12 +97,19 @@ __global__ void __launch_bounds__(kOrderThreads) order_kernel(const StepArgs a) 
     }
   }
   __syncthreads();
-  const int HC = a.num_kv_heads * a.num_query_chunks;  // items per pair
+  // Position pos of the sorted pairs holds items pos * HC .. pos * HC + HC - 1;
+  // prefix pairs (which come with groups only, where HC = Hkv) use the same stride.
+  const int HC = a.num_kv_heads * a.num_query_chunks;
   for (int idx = tid; idx < pairs; idx += kOrderThreads) {
     const int pos = atomicAdd(&s_count[bucket(idx)], 1);
-    const int b = idx % B;
-    const int p = idx / B;
-    for (int g = 0; g < HC; ++g) a.order[(size_t)pos * HC + g] = (p * B + b) * HC + g;
+    if (idx < regular_pairs) {
+      const int b = idx % B;
+      const int p = idx / B;
+      for (int g = 0; g < HC; ++g) a.order[(size_t)pos * HC + g] = (p * B + b) * HC + g;
+    } else {
+      const int q = idx - regular_pairs;  // = grp * Pp + pp
+      for (int g = 0; g < HC; ++g) a.order[(size_t)pos * HC + g] = a.num_regular_items + q * HC + g;
+    }
   }
 }
 

@@ -1,50 +1,106 @@
-// Pass 1: one workgroup per (partition of a context, sequence, KV head,
-// chunk of new query tokens), taken in the order pda_order.hip computed
-// (largest partition first).
+// Pass 1: one workgroup per work item, taken in the order pda_order.hip
+// computed (largest first).  Two kinds of items share the launch:
 //
-// A chunk holds up to 16 / G consecutive new tokens of the sequence, so its
-// query rows (token-major, then the G heads of the KV head) fill at most one
-// 16-row MFMA tile; a decode step has one token, i.e. one chunk of G rows.
-// New token i of a sequence with n new tokens and context length L sits at
-// position L - n + i and sees tokens t < L - n + 1 + i.
+// Regular items: (partition of a context, sequence, KV head, chunk of new
+// query tokens).  A chunk holds up to 16 / G consecutive new tokens of the
+// sequence, so its query rows (token-major, then the G heads of the KV head)
+// fill at most one 16-row MFMA tile; a decode step has one token, i.e. one
+// chunk of G rows.  New token i of a sequence with n new tokens and context
+// length L sits at position L - n + i and sees tokens t < L - n + 1 + i.
+// With shared-prefix groups, a sequence's regular items cover only the
+// tokens after its group's prefix.
 //
-// The partition's 16-token blocks that the chunk can see are split into 4
-// contiguous runs, one per wavefront; each wavefront streams its run with
-// WaveAttention (pda_wave.h) and the 4 states are merged through LDS in a
-// fixed order.  The workgroup leaves the final output rows (the chunk sees a
-// single partition) or a partial softmax state (max, denominator,
-// unnormalised output) for the merge pass.  Nothing depends on physical
-// block ids or on timing, so results are bit-for-bit reproducible and
-// independent of block placement.
+// Prefix items: (shared-prefix group, prefix partition, KV head).  All
+// members of a group read the same prefix blocks (parallel sampling, Section
+// 3.2), so the prefix is attended once for all members x G heads (up to 64
+// query rows): the 4 wavefronts take 16-row tiles first and runs of blocks
+// second, and every block's tiles reach the compute unit once.
+//
+// Each wavefront streams its run of 16-token blocks with WaveAttention
+// (pda_wave.h); the states of the wavefronts that share a row are merged
+// through LDS in a fixed order.  A regular item with no prefix that sees a
+// single partition writes its final output rows; every other item leaves a
+// partial softmax state (max, denominator, unnormalised output) for the
+// merge pass.  Nothing depends on physical block ids or on timing, so results
+// are bit-for-bit reproducible and independent of block placement.
 #include "pda_wave.h"
 
 namespace pda {
 namespace {
 
-// Occupancy: 3 wavefronts per SIMD (12 per compute unit) at most 168 VGPRs.
-template <int D>
-__global__ void __launch_bounds__(kWaves * kWaveSize) __attribute__((amdgpu_waves_per_eu(3)))
-partition_kernel(const StepArgs a) {
-  using WA = WaveAttention<D>;
-  constexpr int kRows = 16;
-  __shared__ __align__(16) float s_o[kWaves][kRows][D];
-  __shared__ float s_m[kWaves][kRows];
-  __shared__ float s_l[kWaves][kRows];
-  __shared__ int s_bad[kWaves];
+constexpr int kRows = 16;           // rows of one wavefront (one MFMA tile)
 
+template <int D>
+struct PassShared {
+  float o[kWaves][kRows][D];
+  float m[kWaves][kRows];
+  float l[kWaves][kRows];
+  int bad[kWaves];
+};
+
+// Publish a finished wavefront's state: rows n < rows of the tile.
+template <int D>
+__device__ __forceinline__ void publish(PassShared<D>& sh, const WaveAttention<D>& wave, int w, int lane, int rows) {
+  const int n = lane & 15;
+  if (n < rows) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int d0 = wave.d_of(i, 0);  // D = 128: 8 consecutive columns; D = 64: 4
+      *reinterpret_cast<float4*>(&sh.o[w][n][d0]) =
+          make_float4(wave.o[0][i], wave.o[1][i], wave.o[2][i], wave.o[3][i]);
+      if (D == 128)
+        *reinterpret_cast<float4*>(&sh.o[w][n][d0 + 4]) =
+            make_float4(wave.o[4][i], wave.o[5][i], wave.o[6][i], wave.o[7][i]);
+    }
+    if (lane < 16) {
+      sh.m[w][n] = wave.m_run;
+      sh.l[w][n] = wave.l_run;
+    }
+  }
+  if (lane == 0) sh.bad[w] = wave.bad ? 1 : 0;
+}
+
+// Combine, for one output element, the states of wavefronts w0, w0 + step,
+// ... (count of them) at tile row n: returns (acc, M, lsum).
+template <int D>
+__device__ __forceinline__ void combine(const PassShared<D>& sh, int w0, int step, int count, int n, int d,
+                                        float& acc, float& M, float& lsum) {
+  M = WaveAttention<D>::kFloor;
+  for (int x = 0; x < count; ++x) M = fmaxf(M, sh.m[w0 + x * step][n]);
+  acc = 0.f;
+  lsum = 0.f;
+  for (int x = 0; x < count; ++x) {
+    const int w = w0 + x * step;
+    const float sc = exp2_fast(sh.m[w][n] - M);  // 0 for a wavefront without tokens of this row
+    acc = fmaf(sc, sh.o[w][n][d], acc);
+    lsum = fmaf(sc, sh.l[w][n], lsum);
+  }
+}
+
+__device__ __forceinline__ void store_partial(const StepArgs& a, size_t slot, int d, int D, float acc, float M,
+                                              float lsum) {
+  a.part_o[slot * D + d] = acc;
+  if (d == 0) {
+    a.part_m[slot] = M;
+    a.part_l[slot] = lsum;
+  }
+}
+
+template <int D>
+__device__ void regular_item(const StepArgs& a, PassShared<D>& sh, int item) {
+  using WA = WaveAttention<D>;
   const int Hq = a.num_q_heads;
   const int G = a.group;
   const int HC = a.num_kv_heads * a.num_query_chunks;
-  const int item = a.order[blockIdx.x];  // (p * B + b) * HC + g * NQC + chunk
-  const int gc = item % HC;
+  const int gc = item % HC;  // item = (p * B + b) * HC + g * NQC + chunk
   const int b = (item / HC) % a.num_seqs;
   const int p = item / (HC * a.num_seqs);
   const int g = gc / a.num_query_chunks;
   const int chunk = gc % a.num_query_chunks;
   const int nq = a.num_query_tokens;
-  const int i0 = chunk * a.query_chunk;                // first new token of the chunk
-  const int nv = min(a.query_chunk, nq - i0);          // its tokens
-  const int rows = nv * G;                             // its query rows, token-major
+  const int i0 = chunk * a.query_chunk;        // first new token of the chunk
+  const int nv = min(a.query_chunk, nq - i0);  // its tokens
+  const int rows = nv * G;                     // its query rows, token-major
   const int tid = threadIdx.x;
   const int lane = tid & (kWaveSize - 1);
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -55,17 +111,18 @@ partition_kernel(const StepArgs a) {
   int L = a.lens[b];
   L = L < 0 ? 0 : (L > a.max_context_len ? a.max_context_len : L);
   const int l_vis = chunk_visible(a, L, chunk);  // the chunk's last row sees tokens below this
-  const int l_first = l_vis - nv + 1;  // its first row sees tokens below this
+  const int l_first = l_vis - nv + 1;            // its first row sees tokens below this
   if (l_vis <= 0) {
     if (p == 0)
       for (int i = tid; i < rows * D; i += kWaves * kWaveSize) a.out[out_row(i / D) * D + i % D] = 0.f;
     return;
   }
+  const int t0 = min(seq_prefix_len(a, b), l_vis);  // tokens before t0 belong to the group's prefix items
   const int Tp = a.partition_tokens;
-  const int nparts = (l_vis + Tp - 1) / Tp;
+  const int nparts = (l_vis - t0 + Tp - 1) / Tp;
   if (p >= nparts) return;
-  const int t_end = min(l_vis, (p + 1) * Tp);
-  const int j_begin = (p * Tp) / kBlockTokens;
+  const int t_end = min(l_vis, t0 + (p + 1) * Tp);
+  const int j_begin = (t0 + p * Tp) / kBlockTokens;
   const int j_end = (t_end + kBlockTokens - 1) / kBlockTokens;
   const int per_wave = (j_end - j_begin + kWaves - 1) / kWaves;
   const int wj0 = min(j_end, j_begin + w * per_wave);
@@ -81,68 +138,105 @@ partition_kernel(const StepArgs a) {
   wave.run(a.table + (size_t)b * a.max_blocks_per_seq, wj0, wj1, L, l_first, l_vis, kpool, vpool,
            (size_t)a.num_kv_heads * WA::kTileBytes, a.num_blocks);
   wave.finish();
-
-  const int n = lane & 15;
-  if (n < rows) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      if (D == 128) {
-        const int d0 = wave.d_of(i, 0);  // 8 consecutive columns
-        *reinterpret_cast<float4*>(&s_o[w][n][d0]) =
-            make_float4(wave.o[0][i], wave.o[1][i], wave.o[2][i], wave.o[3][i]);
-        *reinterpret_cast<float4*>(&s_o[w][n][d0 + 4]) =
-            make_float4(wave.o[4][i], wave.o[5][i], wave.o[6][i], wave.o[7][i]);
-      } else {
-        const int d0 = wave.d_of(i, 0);  // 4 consecutive columns
-        *reinterpret_cast<float4*>(&s_o[w][n][d0]) =
-            make_float4(wave.o[0][i], wave.o[1][i], wave.o[2][i], wave.o[3][i]);
-      }
-    }
-    if (lane < 16) {
-      s_m[w][n] = wave.m_run;
-      s_l[w][n] = wave.l_run;
-    }
-  }
-  if (lane == 0) s_bad[w] = wave.bad ? 1 : 0;
+  publish(sh, wave, w, lane, rows);
   __syncthreads();
 
   // ---- merge the 4 wavefront states in a fixed order ----
   int any_bad = 0;
 #pragma unroll
-  for (int x = 0; x < kWaves; ++x) any_bad |= s_bad[x];
-  const bool single = nparts == 1;
+  for (int x = 0; x < kWaves; ++x) any_bad |= sh.bad[x];
+  const bool single = nparts == 1 && t0 == 0;
   for (int idx = tid; idx < rows * D; idx += kWaves * kWaveSize) {
     const int h = idx / D;
     const int d = idx % D;
-    float M = WA::kFloor;
-#pragma unroll
-    for (int x = 0; x < kWaves; ++x) M = fmaxf(M, s_m[x][h]);
-    float acc = 0.f, lsum = 0.f;
-#pragma unroll
-    for (int x = 0; x < kWaves; ++x) {
-      const float sc = exp2_fast(s_m[x][h] - M);  // 0 for a wavefront without tokens of this row
-      acc = fmaf(sc, s_o[x][h][d], acc);
-      lsum = fmaf(sc, s_l[x][h], lsum);
-    }
+    float acc, M, lsum;
+    combine(sh, 0, 1, kWaves, h, d, acc, M, lsum);
     if (any_bad) acc = __builtin_nanf("");
     const size_t row = out_row(h);
-    if (single) {
+    if (single)
       a.out[row * D + d] = lsum > 0.f ? acc / lsum : acc;  // acc is 0 (or NaN) for a row that sees nothing
-    } else {
-      const size_t slot = row * a.num_partitions + p;
-      a.part_o[slot * D + d] = acc;
-      if (d == 0) {
-        a.part_m[slot] = M;
-        a.part_l[slot] = lsum;
-      }
-    }
+    else
+      store_partial(a, row * a.slots_per_row + a.prefix_partitions + p, d, D, acc, M, lsum);
   }
 }
 
 template <int D>
+__device__ void prefix_item(const StepArgs& a, PassShared<D>& sh, int pitem) {
+  using WA = WaveAttention<D>;
+  const int Hq = a.num_q_heads;
+  const int G = a.group;
+  const int g = pitem % a.num_kv_heads;  // pitem = (group * Pp + pp) * Hkv + g
+  const int pp = (pitem / a.num_kv_heads) % a.prefix_partitions;
+  const int grp = pitem / (a.num_kv_heads * a.prefix_partitions);
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWaveSize - 1);
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  // group contents are device data: clamp so that nothing is read or written out of bounds
+  const int first = min(max(a.group_start[grp], 0), a.num_seqs);
+  const int members = min(min(a.group_start[grp + 1], a.num_seqs) - first, a.max_group_size);
+  int plen = a.group_prefix_len[grp];
+  plen = plen < 0 ? 0 : (plen > a.max_prefix_len ? a.max_prefix_len : plen) / kBlockTokens * kBlockTokens;
+  const int Tp = a.partition_tokens;
+  if (members <= 0 || pp * Tp >= plen) return;
+  const int rows = members * G;                    // member-major, then the G heads
+  const int ntile = (rows + kRows - 1) / kRows;    // 16-row tiles: 1 .. 4
+  const int slices = kWaves / ntile;               // runs of blocks per tile
+  const int tile = w % ntile;
+  const int slice = w / ntile;
+  const int t_end = min(plen, (pp + 1) * Tp);
+  const int j_begin = (pp * Tp) / kBlockTokens;
+  const int j_end = t_end / kBlockTokens;
+  const int per_slice = (j_end - j_begin + slices - 1) / slices;
+  const int wj0 = slice < slices ? min(j_end, j_begin + slice * per_slice) : j_end;
+  const int wj1 = min(j_end, wj0 + per_slice);
+  const int tile_rows = min(kRows, rows - tile * kRows);
+
+  // lane row n of this tile repeats real rows past the tile's last one
+  const int r = tile * kRows + (lane & 15) % tile_rows;
+  const int b = first + r / G;
+  WA wave(a.scale_log2);
+  wave.start(a.q + ((size_t)b * Hq + (size_t)g * G + r % G) * D, 0);
+  const char* kpool = reinterpret_cast<const char*>(a.k) + (size_t)g * WA::kTileBytes;
+  const char* vpool = reinterpret_cast<const char*>(a.v) + (size_t)g * WA::kTileBytes;
+  // the prefix blocks are those of the group's first member (shared by contract)
+  wave.run(a.table + (size_t)first * a.max_blocks_per_seq, wj0, wj1, plen, plen, plen, kpool, vpool,
+           (size_t)a.num_kv_heads * WA::kTileBytes, a.num_blocks);
+  wave.finish();
+  publish(sh, wave, w, lane, tile_rows);
+  __syncthreads();
+
+  // ---- merge the slices of each tile in a fixed order; every member row gets a partial state ----
+  int any_bad = 0;
+#pragma unroll
+  for (int x = 0; x < kWaves; ++x) any_bad |= sh.bad[x];
+  for (int idx = tid; idx < rows * D; idx += kWaves * kWaveSize) {
+    const int rr = idx / D;
+    const int d = idx % D;
+    float acc, M, lsum;
+    combine(sh, rr / kRows, ntile, slices, rr % kRows, d, acc, M, lsum);
+    if (any_bad) acc = __builtin_nanf("");
+    const size_t row = (size_t)(first + rr / G) * Hq + (size_t)g * G + rr % G;
+    store_partial(a, row * a.slots_per_row + pp, d, D, acc, M, lsum);
+  }
+}
+
+// Occupancy: 3 wavefronts per SIMD (12 per compute unit) at most 168 VGPRs.
+template <int D>
+__global__ void __launch_bounds__(kWaves * kWaveSize) __attribute__((amdgpu_waves_per_eu(3)))
+partition_kernel(const StepArgs a) {
+  __shared__ __align__(16) PassShared<D> sh;
+  const int item = a.order[blockIdx.x];
+  if (item < a.num_regular_items)
+    regular_item<D>(a, sh, item);
+  else
+    prefix_item<D>(a, sh, item - a.num_regular_items);
+}
+
+template <int D>
 hipError_t launch_d(const StepArgs& a, hipStream_t stream) {
-  const unsigned grid = (unsigned)a.num_partitions * (unsigned)a.num_seqs * (unsigned)a.num_kv_heads *
-                        (unsigned)a.num_query_chunks;
+  const unsigned grid = (unsigned)a.num_regular_items +
+                        (unsigned)a.num_groups * (unsigned)a.prefix_partitions * (unsigned)a.num_kv_heads;
   hipLaunchKernelGGL((partition_kernel<D>), dim3(grid), dim3(kWaves * kWaveSize), 0, stream, a);
   return hipGetLastError();
 }

@@ -22,8 +22,9 @@ PDA_ERR_WORKSPACE, PDA_ERR_ALIGNMENT, PDA_ERR_VALUE, PDA_ERR_HIP = 4, 5, 6, 7
 
 # Every function include/pda.h declares.
 EXPORTED = ("pda_plan", "pda_workspace_bytes", "pda_decode", "pda_partition_attention",
-            "pda_merge_partitions", "pda_append_kv", "pda_step_graph_create", "pda_step_graph_launch",
-            "pda_step_graph_destroy", "pda_token_logprobs", "pda_validate_host", "pda_status_string")
+            "pda_merge_partitions", "pda_plan_shared_prefix", "pda_decode_shared_prefix", "pda_append_kv",
+            "pda_step_graph_create", "pda_step_graph_launch", "pda_step_graph_destroy", "pda_token_logprobs",
+            "pda_validate_host", "pda_status_string")
 PDA_DTYPE_BF16, PDA_DTYPE_F32 = 0, 1
 
 
@@ -39,6 +40,12 @@ class pda_plan_info(ctypes.Structure):
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+class pda_prefix_groups(ctypes.Structure):
+    _fields_ = [("num_groups", ctypes.c_int32), ("max_group_size", ctypes.c_int32),
+                ("max_prefix_len", ctypes.c_int32), ("group_start", ctypes.c_void_p),
+                ("group_prefix_len", ctypes.c_void_p)]
 
 
 class PdaError(RuntimeError):
@@ -67,6 +74,9 @@ def load_library(path: str = LIB_PATH):
     lib.pda_decode.argtypes = step
     lib.pda_partition_attention.argtypes = step
     lib.pda_merge_partitions.argtypes = [P, vp, vp, vp, sz, vp]
+    G = ctypes.POINTER(pda_prefix_groups)
+    lib.pda_plan_shared_prefix.argtypes = [P, G, ctypes.POINTER(pda_plan_info)]
+    lib.pda_decode_shared_prefix.argtypes = [P, G, vp, vp, vp, vp, vp, ctypes.c_float, vp, vp, sz, vp]
     lib.pda_append_kv.argtypes = [P, vp, vp, vp, vp, vp, vp, vp]
     lib.pda_step_graph_create.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, ctypes.c_float, vp, vp, sz,
                                           ctypes.POINTER(vp)]
@@ -101,6 +111,22 @@ def pda_plan(prob: pda_problem) -> dict:
     rc = load_library().pda_plan(ctypes.byref(prob), ctypes.byref(info))
     if rc != PDA_OK:
         raise PdaError(rc, "pda_plan")
+    return info.as_dict()
+
+
+def make_prefix_groups(num_groups, max_group_size, max_prefix_len, group_start=None,
+                       group_prefix_len=None) -> pda_prefix_groups:
+    """Host bounds plus the two device arrays (torch int32 tensors or raw pointers)."""
+    ptr = lambda t: (t.data_ptr() if hasattr(t, "data_ptr") else t)
+    return pda_prefix_groups(int(num_groups), int(max_group_size), int(max_prefix_len), ptr(group_start),
+                             ptr(group_prefix_len))
+
+
+def pda_plan_shared_prefix(prob: pda_problem, groups: pda_prefix_groups) -> dict:
+    info = pda_plan_info()
+    rc = load_library().pda_plan_shared_prefix(ctypes.byref(prob), ctypes.byref(groups), ctypes.byref(info))
+    if rc != PDA_OK:
+        raise PdaError(rc, "pda_plan_shared_prefix")
     return info.as_dict()
 
 
@@ -355,3 +381,36 @@ def pda_token_logprobs(logits, tokens, inv_temperature: float = 1.0, entropy: bo
     if rc != PDA_OK:
         raise PdaError(rc, "pda_token_logprobs")
     return logprobs, (entropies if entropy else None)
+
+
+def pda_decode_shared_prefix(q, k_cache, v_cache, block_table, context_lens, scale: float, group_start,
+                             group_prefix_len, out=None, *, max_context_len: int, max_group_size: int,
+                             max_prefix_len: int, partition_tokens: int = 0, workspace=None, stream=None):
+    """The decode step with each shared-prefix group's prefix attended once for
+    all its members.  group_start int32 [num_groups + 1] and group_prefix_len
+    int32 [num_groups] are device tensors; max_group_size and max_prefix_len
+    are their host bounds.  Other arguments as pda_decode (q [B][Hq][D])."""
+    import torch
+
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    _check_tensors(q, k_cache, v_cache, block_table, context_lens, out)
+    _require("group_start", group_start, torch.int32)
+    _require("group_prefix_len", group_prefix_len, torch.int32)
+    num_groups = group_prefix_len.shape[0]
+    if group_start.shape != (num_groups + 1,):
+        raise ValueError("group_start must be [num_groups + 1]")
+    prob = _problem_from(q, k_cache, block_table, max_context_len, partition_tokens)
+    groups = make_prefix_groups(num_groups, max_group_size, max_prefix_len, group_start, group_prefix_len)
+    need = pda_plan_shared_prefix(prob, groups)["workspace_bytes"]
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    rc = load_library().pda_decode_shared_prefix(
+        ctypes.byref(prob), ctypes.byref(groups), q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
+        block_table.data_ptr(), context_lens.data_ptr(), ctypes.c_float(scale), out.data_ptr(), ws_ptr, ws_bytes,
+        _stream_handle(stream, q.device))
+    if rc != PDA_OK:
+        raise PdaError(rc, "pda_decode_shared_prefix")
+    return out

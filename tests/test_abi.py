@@ -209,6 +209,34 @@ def test_multi_token_plan():
     assert pda.pda_plan(llama(num_query_tokens=0)) == pda.pda_plan(llama(num_query_tokens=1))
 
 
+def test_shared_prefix_validation():
+    G = pda.pda.make_prefix_groups
+    ok = dict(num_groups=3, max_group_size=8, max_prefix_len=256, group_start=0x1000, group_prefix_len=0x1000)
+
+    def plan(p=None, **kw):
+        return pda.pda.load_library().pda_plan_shared_prefix(
+            ctypes.byref(p or llama()), ctypes.byref(G(**dict(ok, **kw))), ctypes.byref(pda.pda_plan_info()))
+    assert plan() == pda.pda.PDA_OK
+    assert plan(num_groups=-1) == pda.pda.PDA_ERR_SHAPE
+    assert plan(max_group_size=0) == pda.pda.PDA_ERR_SHAPE
+    assert plan(max_prefix_len=100) == pda.pda.PDA_ERR_SHAPE        # not a multiple of 16
+    assert plan(max_prefix_len=8192) == pda.pda.PDA_ERR_SHAPE       # beyond max_context_len
+    assert plan(max_group_size=17) == pda.pda.PDA_ERR_UNSUPPORTED   # 17 x G=4 > 64 rows
+    assert plan(llama(num_query_tokens=2)) == pda.pda.PDA_ERR_UNSUPPORTED
+    assert plan(group_start=None) == pda.pda.PDA_OK  # planning reads the host bounds only
+    assert plan(num_groups=0, group_start=None, group_prefix_len=None) == pda.pda.PDA_OK
+    # workspace: (Pp + P) partial states per row, the work order (regular +
+    # prefix items) and one int per sequence
+    d = pda.pda_plan_shared_prefix(llama(partition_tokens=1024), G(**ok))
+    assert d["workspace_bytes"] == (256 * 32 * (1 + 4) * (128 + 2) * 4 + (4 * 256 * 8 + 3 * 1 * 8) * 4 + 256 * 4)
+    f = pda.pda.load_library().pda_decode_shared_prefix
+    assert f(ctypes.byref(llama()), None, *([0x1000] * 5), ctypes.c_float(1), 0x1000, None, 0,
+             None) == pda.pda.PDA_ERR_NULL
+    no_arrays = G(**dict(ok, group_start=None))
+    assert f(ctypes.byref(llama()), ctypes.byref(no_arrays), *([0x1000] * 5), ctypes.c_float(1), 0x1000, 0x1000,
+             1 << 40, None) == pda.pda.PDA_ERR_NULL
+
+
 def test_validate_host():
     st = W.make_structure("tiny")
     p = prob(num_blocks=st.num_blocks, max_blocks_per_seq=st.max_blocks_per_seq,

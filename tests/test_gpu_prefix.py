@@ -1,0 +1,123 @@
+"""GPU parity of the shared-prefix decode step (parallel sampling: the
+samples of one prompt share its KV blocks, Section 3.2) through the C ABI.
+
+The operation is the same attention as the decode step, only scheduled so
+that each group's prefix is attended once for all members; the fp64 oracle
+is the plain decode definition.  Bar: max-abs <= 8e-3, mean-abs <= 1e-3 over
+every compared element; bitwise run-to-run and under block shuffles.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from paper_2405_11143_amd import make_prefix_groups, make_problem, pda_decode_shared_prefix, pda_plan_shared_prefix
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS, MEAN_ABS = 8e-3, 1e-3
+THREADS = max(1, min(16, os.cpu_count() or 1))
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return torch.device("cuda:0")
+
+
+def run(st, q, k, v, dev, partition_tokens=0, max_group_size=None, max_prefix_len=None):
+    gs = torch.from_numpy(st.group_start).to(dev)
+    gp = torch.from_numpy(st.group_prefix_len).to(dev)
+    sizes = np.diff(st.group_start)
+    out = pda_decode_shared_prefix(
+        q, k, v, torch.from_numpy(st.block_table).to(dev), torch.from_numpy(st.context_lens).to(dev), st.scale,
+        gs, gp, max_context_len=st.max_context_len,
+        max_group_size=int(sizes.max(initial=1)) if max_group_size is None else max_group_size,
+        max_prefix_len=int(st.group_prefix_len.max(initial=0)) if max_prefix_len is None else max_prefix_len,
+        partition_tokens=partition_tokens)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def reference(st, q, k, v):
+    return oracle.decode(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table, st.context_lens,
+                         st.scale, threads=THREADS)
+
+
+def check(got, ref, what):
+    got = got.astype(np.float64)
+    assert np.isfinite(got).all(), f"{what}: non-finite output"
+    err = np.abs(got - ref)
+    print(f"{what}: max-abs {err.max():.3e} mean-abs {err.mean():.3e} over {err.size} elements", flush=True)
+    assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS, what
+
+
+GROUPS = [
+    (1024, [1024, 1025, 1100, 3000, 1040, 2047, 1500, 4096]),  # 8 samples; one with an empty suffix
+    (32, [33, 40, 100]),
+    (0, [5, 300]),                                              # a group without a prefix
+    (4096, [4100, 5000]),                                       # a prefix of several partitions
+    (16, [16]),                                                 # one member, prefix = whole context
+]
+
+
+@pytest.mark.parametrize("Hq,Hkv,D", [(32, 8, 128), (8, 1, 128), (16, 8, 64), (4, 4, 128)], ids=str)
+@pytest.mark.parametrize("partition_tokens", [0, 64, 1024])
+def test_groups_and_loners(dev, Hq, Hkv, D, partition_tokens):
+    st = W.custom_shared_structure(Hq, Hkv, D, GROUPS, loner_lens=[1, 700, 0, 2049], seed=Hq + D)
+    q, k, v = W.fill_values(st, dev, fill="nan")
+    got = run(st, q, k, v, dev, partition_tokens)
+    assert np.all(got[st.B - 2] == 0)  # the empty loner
+    check(got, reference(st, q, k, v), f"groups Hq={Hq} Hkv={Hkv} D={D} Tp={partition_tokens}")
+
+
+@pytest.mark.parametrize("G,members", [(4, 16), (8, 8), (1, 64), (16, 4), (3, 5)])
+def test_largest_groups(dev, G, members):
+    """Groups of the largest supported size: members x G = 64 (or just below)
+    query rows, i.e. 4 tiles of 16 rows in one work item."""
+    r = np.random.default_rng(members)
+    lens = [int(x) for x in 256 + r.integers(0, 600, members)]
+    st = W.custom_shared_structure(2 * G, 2, 128, [(256, lens)], loner_lens=[300], seed=G)
+    q, k, v = W.fill_values(st, dev, fill="nan")
+    check(run(st, q, k, v, dev), reference(st, q, k, v), f"G={G} members={members}")
+
+
+def test_bitwise_run_to_run_and_shuffle(dev):
+    st = W.custom_shared_structure(32, 8, 128, GROUPS, loner_lens=[900], seed=5)
+    q, k, v = W.fill_values(st, dev, fill="nan")
+    base = run(st, q, k, v, dev)
+    assert np.array_equal(base, run(st, q, k, v, dev)), "run-to-run"
+    st2, k2, v2 = W.permute_pool(st, k, v, seed=2)
+    assert np.array_equal(base, run(st2, q, k2, v2, dev)), "block shuffle"
+    _, kz, vz = W.fill_values(st, dev, fill="zero")
+    assert np.array_equal(base, run(st, q, kz, vz, dev)), "NaN poison vs zero fill"
+
+
+def test_host_bounds_above_contents(dev):
+    """Bounds larger than the contents (more room per group, a longer prefix
+    bound) give the same result."""
+    st = W.custom_shared_structure(32, 8, 128, GROUPS[:3], loner_lens=[50], seed=6)
+    q, k, v = W.fill_values(st, dev, fill="nan")
+    a = run(st, q, k, v, dev)
+    b = run(st, q, k, v, dev, max_group_size=16, max_prefix_len=2048)
+    check(b, reference(st, q, k, v), "larger host bounds")
+    np.testing.assert_allclose(a, b, rtol=0, atol=1e-5)
+
+
+def test_shared_prefix_config_full_size(dev):
+    """The 32 prompts x 8 samples workload at full size, in the launch
+    configuration the benchmark times; sampled rows against the oracle."""
+    st = W.make_structure("shared_prefix")
+    prob = make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq, st.max_context_len)
+    plan = pda_plan_shared_prefix(prob, make_prefix_groups(len(st.group_prefix_len), 8, 1024))
+    print(f"shared_prefix plan: {plan}", flush=True)
+    q, k, v = W.fill_values(st, dev, fill="nan")
+    got = run(st, q, k, v, dev)
+    assert np.isfinite(got).all()
+    rows = W.sample_rows(st, 64)
+    ref = oracle.decode_rows(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table, st.context_lens,
+                             st.scale, rows, threads=THREADS)
+    check(got[rows[:, 0], rows[:, 1]], ref, "shared_prefix sampled rows")

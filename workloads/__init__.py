@@ -99,6 +99,11 @@ class Structure:
     block_table: np.ndarray    # int32 [B][max_blocks_per_seq]; -1 where unused
     k_offset_std: float = 0.0
     block_size: int = BLOCK_SIZE
+    # Shared-prefix groups (parallel samples of one prompt), or None: members of
+    # group i are sequences [group_start[i], group_start[i+1]), whose first
+    # group_prefix_len[i] tokens sit in the same blocks.
+    group_start: Optional[np.ndarray] = None       # int32 [num_groups + 1]
+    group_prefix_len: Optional[np.ndarray] = None  # int32 [num_groups]
 
     @property
     def G(self) -> int:
@@ -196,7 +201,10 @@ def make_structure(name: str, seed: Optional[int] = None) -> Structure:
             table[b, pre_blocks:pre_blocks + n] = perm[cur:cur + n]
             cur += n
         assert cur == unique
+        group_start = (np.arange(P + 1) * S).astype(np.int32)
+        group_prefix_len = np.full(P, prefix, dtype=np.int32)
     else:
+        group_start = group_prefix_len = None
         lens = _draw_lens(rl, kind, lo, hi, B)
         mbs = (hi + BS - 1) // BS
         nblk = (lens.astype(np.int64) + BS - 1) // BS
@@ -212,7 +220,51 @@ def make_structure(name: str, seed: Optional[int] = None) -> Structure:
             cur += n
     return Structure(name=name, seed=seed, B=B, Hq=cfg["Hq"], Hkv=cfg["Hkv"], D=cfg["D"],
                      num_blocks=num_blocks, max_blocks_per_seq=int(mbs), context_lens=lens,
-                     block_table=table, k_offset_std=float(cfg.get("k_offset_std", 0.0)))
+                     block_table=table, k_offset_std=float(cfg.get("k_offset_std", 0.0)),
+                     group_start=group_start, group_prefix_len=group_prefix_len)
+
+
+def custom_shared_structure(Hq: int, Hkv: int, D: int, groups: Sequence, loner_lens: Sequence[int] = (),
+                            seed: int = 0, pool_slack: float = 1.25, name: str = "custom_shared") -> Structure:
+    """Sequences in shared-prefix groups, then sequences in none.  `groups` is
+    a list of (prefix_len, [context lengths of the members]): each group's
+    prefix_len tokens (a multiple of 16, at most every member's length) sit in
+    blocks that all its members' tables share; the rest of every context is
+    private.  Blocks are placed by a random permutation of the pool."""
+    BS = BLOCK_SIZE
+    lens, pre_blocks, group_start, group_prefix = [], [], [0], []
+    for prefix_len, members in groups:
+        assert prefix_len % BS == 0 and all(L >= prefix_len for L in members) and len(members) > 0
+        lens += list(members)
+        pre_blocks += [prefix_len // BS] * len(members)
+        group_start.append(group_start[-1] + len(members))
+        group_prefix.append(prefix_len)
+    lens += list(loner_lens)
+    pre_blocks += [0] * len(loner_lens)
+    B = len(lens)
+    lens = np.asarray(lens, dtype=np.int32)
+    nblk = (np.maximum(lens.astype(np.int64), 0) + BS - 1) // BS
+    unique = sum(prefix_len // BS for prefix_len, _ in groups) + int(sum(nblk - np.asarray(pre_blocks, np.int64)))
+    mbs = max(1, int(nblk.max(initial=1)))
+    num_blocks = max(1, int(math.ceil(pool_slack * max(unique, 1))))
+    perm = _rng(seed, _STREAM_POOL).permutation(num_blocks).astype(np.int32)
+    table = np.full((B, mbs), -1, dtype=np.int32)
+    cur, b = 0, 0
+    for prefix_len, members in groups:
+        ids = perm[cur:cur + prefix_len // BS]
+        cur += prefix_len // BS
+        for _ in members:
+            table[b, :len(ids)] = ids
+            b += 1
+    for b in range(B):
+        n0, n = pre_blocks[b], int(nblk[b])
+        table[b, n0:n] = perm[cur:cur + n - n0]
+        cur += n - n0
+    assert cur == unique
+    return Structure(name=name, seed=seed, B=B, Hq=Hq, Hkv=Hkv, D=D, num_blocks=num_blocks,
+                     max_blocks_per_seq=mbs, context_lens=lens, block_table=table,
+                     group_start=np.asarray(group_start, dtype=np.int32),
+                     group_prefix_len=np.asarray(group_prefix, dtype=np.int32))
 
 
 def custom_structure(B: int, Hq: int, Hkv: int, D: int, lens: Sequence[int], seed: int = 0,
