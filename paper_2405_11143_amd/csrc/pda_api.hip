@@ -19,7 +19,7 @@ namespace {
 // each of the kConcurrentItems workgroups the GPU runs at once has to do;
 // longer items amortise each workgroup's start-up (order, length, block ids,
 // q) over more streamed tiles.  With only max_context_len on the host, the
-// work is estimated as B * Hkv * chunks * max_context_len / 2 tokens (the
+// work is estimated as B * Hkv * chunk groups * max_context_len / 2 tokens (the
 // mean of contexts spread up to the maximum), and the partition is that
 // share rounded up to kPartitionQuantum tokens, within [kMinPartitionTokens,
 // kMaxPartitionTokens] and never longer than the longest context (then there
@@ -52,8 +52,9 @@ struct Plan {
   pda_plan_info info;
   int query_chunk;        // new tokens per work item: min(n, 16 / G)
   int num_query_chunks;   // ceil(n / query_chunk)
+  int num_chunk_groups;   // ceil(chunks / 4): chunks per work item share its tiles
   int prefix_partitions;  // Pp: partitions of the longest shared prefix (0 without groups)
-  size_t regular_items;   // P * B * Hkv * chunks (pass-1 workgroups of the sequences' own tokens)
+  size_t regular_items;   // P * B * Hkv * chunk groups (pass-1 workgroups of the sequences' own tokens)
   size_t items;           // regular items + num_groups * Pp * Hkv prefix items
   size_t slots;           // partial states: (Pp + P) per output row; 0 when nothing is split
 };
@@ -78,7 +79,8 @@ int make_plan(const pda_problem* p, const pda_prefix_groups* groups, Plan* plan)
   const int G = p->num_q_heads / p->num_kv_heads;
   const int qc = std::min(n, pda::kMaxGroup / G);
   const int nqc = (n + qc - 1) / qc;
-  const int64_t units = (int64_t)p->num_seqs * p->num_kv_heads * nqc;
+  const int ncg = (nqc + pda::kWaves - 1) / pda::kWaves;  // a work item takes up to 4 chunks
+  const int64_t units = (int64_t)p->num_seqs * p->num_kv_heads * ncg;
   int tp = p->partition_tokens;
   if (tp == 0) {
     const int64_t len = p->max_context_len > 0 ? p->max_context_len : 1;
@@ -99,6 +101,7 @@ int make_plan(const pda_problem* p, const pda_prefix_groups* groups, Plan* plan)
   plan->info.num_partitions = (int32_t)parts;
   plan->query_chunk = qc;
   plan->num_query_chunks = nqc;
+  plan->num_chunk_groups = ncg;
   plan->prefix_partitions = (int)pparts;
   if (p->num_seqs > 0) {
     plan->regular_items = (size_t)(parts * units);
@@ -141,6 +144,7 @@ void fill_args(const pda_problem* p, const Plan* plan, void* ws, pda::StepArgs* 
   args->num_query_tokens = query_tokens(p);
   args->query_chunk = plan->query_chunk;
   args->num_query_chunks = plan->num_query_chunks;
+  args->num_chunk_groups = plan->num_chunk_groups;
   args->partition_tokens = plan->info.partition_tokens;
   args->num_partitions = plan->info.num_partitions;
 }

@@ -39,6 +39,7 @@ struct StepArgs {
   int32_t num_query_tokens;  // n
   int32_t query_chunk;       // new tokens per work item: min(n, 16 / G)
   int32_t num_query_chunks;  // NQC = ceil(n / query_chunk)
+  int32_t num_chunk_groups;  // NCG = ceil(NQC / 4): chunks of one work item share its K/V tiles
   int32_t partition_tokens;  // T_p, multiple of 16
   int32_t num_partitions;    // P = max(1, ceil(max_context_len / T_p))
   // Shared-prefix groups (num_groups == 0: none).  The members of group i are

@@ -11,7 +11,7 @@
 // (partitions past what a context needs) come last and exit at once.
 //
 // The items come in pairs of equal size: a regular pair (sequence, partition)
-// stands for its items of every KV head and query chunk, a prefix pair
+// stands for its items of every KV head and group of query chunks, a prefix pair
 // (shared-prefix group, prefix partition) for its items of every KV head.
 // One workgroup counting-sorts the pairs by size in blocks (classes capped
 // at kOrderBuckets - 1 blocks) with LDS atomics, then writes the items of
@@ -99,7 +99,7 @@ __global__ void __launch_bounds__(kOrderThreads) order_kernel(const StepArgs a) 
   __syncthreads();
   // Position pos of the sorted pairs holds items pos * HC .. pos * HC + HC - 1;
   // prefix pairs (which come with groups only, where HC = Hkv) use the same stride.
-  const int HC = a.num_kv_heads * a.num_query_chunks;
+  const int HC = a.num_kv_heads * a.num_chunk_groups;
   for (int idx = tid; idx < pairs; idx += kOrderThreads) {
     const int pos = atomicAdd(&s_count[bucket(idx)], 1);
     if (idx < regular_pairs) {

@@ -1,14 +1,17 @@
 // Pass 1: one workgroup per work item, taken in the order pda_order.hip
 // computed (largest first).  Two kinds of items share the launch:
 //
-// Regular items: (partition of a context, sequence, KV head, chunk of new
-// query tokens).  A chunk holds up to 16 / G consecutive new tokens of the
-// sequence, so its query rows (token-major, then the G heads of the KV head)
-// fill at most one 16-row MFMA tile; a decode step has one token, i.e. one
-// chunk of G rows.  New token i of a sequence with n new tokens and context
-// length L sits at position L - n + i and sees tokens t < L - n + 1 + i.
-// With shared-prefix groups, a sequence's regular items cover only the
-// tokens after its group's prefix.
+// Regular items: (partition of a context, sequence, KV head, group of up to
+// 4 chunks of new query tokens).  A chunk holds up to 16 / G consecutive new
+// tokens of the sequence, so its query rows (token-major, then the G heads of
+// the KV head) fill one 16-row MFMA tile; a decode step has one token, i.e.
+// one chunk of G rows.  New token i of a sequence with n new tokens and
+// context length L sits at position L - n + i and sees tokens
+// t < L - n + 1 + i.  The 4 wavefronts take the item's chunks first and runs
+// of its blocks second (1 chunk: 4 runs; 2: 2 runs each; 3-4: 1 run), so the
+// chunks of one item read each tile on one compute unit.  Each chunk keeps
+// its own causal range and partition count.  With shared-prefix groups, a
+// sequence's regular items cover only the tokens after its group's prefix.
 //
 // Prefix items: (shared-prefix group, prefix partition, KV head).  All
 // members of a group read the same prefix blocks (parallel sampling, Section
@@ -91,43 +94,67 @@ __device__ void regular_item(const StepArgs& a, PassShared<D>& sh, int item) {
   using WA = WaveAttention<D>;
   const int Hq = a.num_q_heads;
   const int G = a.group;
-  const int HC = a.num_kv_heads * a.num_query_chunks;
-  const int gc = item % HC;  // item = (p * B + b) * HC + g * NQC + chunk
+  const int HC = a.num_kv_heads * a.num_chunk_groups;
+  const int gc = item % HC;  // item = (p * B + b) * HC + g * NCG + chunk group
   const int b = (item / HC) % a.num_seqs;
   const int p = item / (HC * a.num_seqs);
-  const int g = gc / a.num_query_chunks;
-  const int chunk = gc % a.num_query_chunks;
+  const int g = gc / a.num_chunk_groups;
+  const int cg = gc % a.num_chunk_groups;
   const int nq = a.num_query_tokens;
-  const int i0 = chunk * a.query_chunk;        // first new token of the chunk
-  const int nv = min(a.query_chunk, nq - i0);  // its tokens
-  const int rows = nv * G;                     // its query rows, token-major
+  const int ntile = min(kWaves, a.num_query_chunks - cg * kWaves);  // query chunks (16-row tiles) of the item
+  const int slices = kWaves / ntile;                               // runs of blocks per tile
   const int tid = threadIdx.x;
   const int lane = tid & (kWaveSize - 1);
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  auto out_row = [&](int r) {  // output row of chunk row r
-    return ((size_t)b * nq + i0 + r / G) * Hq + (size_t)g * G + r % G;
-  };
+  const int tile = w % ntile;
+  const int slice = w / ntile;
 
   int L = a.lens[b];
   L = L < 0 ? 0 : (L > a.max_context_len ? a.max_context_len : L);
-  const int l_vis = chunk_visible(a, L, chunk);  // the chunk's last row sees tokens below this
-  const int l_first = l_vis - nv + 1;            // its first row sees tokens below this
-  if (l_vis <= 0) {
-    if (p == 0)
-      for (int i = tid; i < rows * D; i += kWaves * kWaveSize) a.out[out_row(i / D) * D + i % D] = 0.f;
-    return;
-  }
-  const int t0 = min(seq_prefix_len(a, b), l_vis);  // tokens before t0 belong to the group's prefix items
   const int Tp = a.partition_tokens;
-  const int nparts = (l_vis - t0 + Tp - 1) / Tp;
-  if (p >= nparts) return;
-  const int t_end = min(l_vis, t0 + (p + 1) * Tp);
-  const int j_begin = (t0 + p * Tp) / kBlockTokens;
-  const int j_end = (t_end + kBlockTokens - 1) / kBlockTokens;
-  const int per_wave = (j_end - j_begin + kWaves - 1) / kWaves;
-  const int wj0 = min(j_end, j_begin + w * per_wave);
-  const int wj1 = min(j_end, wj0 + per_wave);
+  const int t0_all = seq_prefix_len(a, b);  // tokens before it belong to the group's prefix items
+  // Per chunk c: its tokens [i0, i0 + nv), the token limit of its last row
+  // (l_vis) and the partitions of its own tokens after the prefix.
+  auto chunk_of = [&](int t) { return cg * kWaves + t; };
+  auto parts_of = [&](int c) {
+    const int lv = chunk_visible(a, L, c);
+    const int t0 = min(t0_all, max(lv, 0));
+    return lv > 0 ? (lv - t0 + Tp - 1) / Tp : 0;
+  };
+  int nparts_max = 0;
+  for (int t = 0; t < ntile; ++t) nparts_max = max(nparts_max, parts_of(chunk_of(t)));
+  if (p == 0) {  // chunks that see nothing (L == 0, or new tokens before the context): zero rows
+    for (int t = 0; t < ntile; ++t) {
+      const int c = chunk_of(t);
+      if (chunk_visible(a, L, c) > 0) continue;
+      const int i0 = c * a.query_chunk;
+      const int rows = min(a.query_chunk, nq - i0) * G;
+      for (int i = tid; i < rows * D; i += kWaves * kWaveSize) {
+        const int r = i / D;
+        a.out[(((size_t)b * nq + i0 + r / G) * Hq + (size_t)g * G + r % G) * D + i % D] = 0.f;
+      }
+    }
+  }
+  if (p >= nparts_max) return;
 
+  // this wave's tile (chunk) and its run of the partition's blocks
+  const int c = chunk_of(tile);
+  const int i0 = c * a.query_chunk;
+  const int nv = min(a.query_chunk, nq - i0);
+  const int rows = nv * G;
+  const int l_vis = chunk_visible(a, L, c);
+  const int l_first = l_vis - nv + 1;
+  const int t0 = min(t0_all, max(l_vis, 0));
+  const int nparts = parts_of(c);
+  int wj0 = 0, wj1 = 0;
+  if (slice < slices && p < nparts) {
+    const int t_end = min(l_vis, t0 + (p + 1) * Tp);
+    const int j_begin = (t0 + p * Tp) / kBlockTokens;
+    const int j_end = (t_end + kBlockTokens - 1) / kBlockTokens;
+    const int per_slice = (j_end - j_begin + slices - 1) / slices;
+    wj0 = min(j_end, j_begin + slice * per_slice);
+    wj1 = min(j_end, wj0 + per_slice);
+  }
   // lane row n repeats real rows past the chunk's last one
   const int r = (lane & 15) % rows;
   const int qi = i0 + r / G;
@@ -135,28 +162,35 @@ __device__ void regular_item(const StepArgs& a, PassShared<D>& sh, int item) {
   wave.start(a.q + (((size_t)b * nq + qi) * Hq + (size_t)g * G + r % G) * D, nq - 1 - qi);
   const char* kpool = reinterpret_cast<const char*>(a.k) + (size_t)g * WA::kTileBytes;
   const char* vpool = reinterpret_cast<const char*>(a.v) + (size_t)g * WA::kTileBytes;
-  wave.run(a.table + (size_t)b * a.max_blocks_per_seq, wj0, wj1, L, l_first, l_vis, kpool, vpool,
+  wave.run(a.table + (size_t)b * a.max_blocks_per_seq, wj0, wj1, L, l_first, max(l_vis, 0), kpool, vpool,
            (size_t)a.num_kv_heads * WA::kTileBytes, a.num_blocks);
   wave.finish();
   publish(sh, wave, w, lane, rows);
   __syncthreads();
 
-  // ---- merge the 4 wavefront states in a fixed order ----
+  // ---- per chunk: merge its slices in a fixed order; final rows or partial states ----
   int any_bad = 0;
 #pragma unroll
   for (int x = 0; x < kWaves; ++x) any_bad |= sh.bad[x];
-  const bool single = nparts == 1 && t0 == 0;
-  for (int idx = tid; idx < rows * D; idx += kWaves * kWaveSize) {
-    const int h = idx / D;
-    const int d = idx % D;
-    float acc, M, lsum;
-    combine(sh, 0, 1, kWaves, h, d, acc, M, lsum);
-    if (any_bad) acc = __builtin_nanf("");
-    const size_t row = out_row(h);
-    if (single)
-      a.out[row * D + d] = lsum > 0.f ? acc / lsum : acc;  // acc is 0 (or NaN) for a row that sees nothing
-    else
-      store_partial(a, row * a.slots_per_row + a.prefix_partitions + p, d, D, acc, M, lsum);
+  for (int t = 0; t < ntile; ++t) {
+    const int ct = chunk_of(t);
+    const int ct_parts = parts_of(ct);
+    if (p >= ct_parts) continue;  // the chunk sees nothing in this partition
+    const int ci0 = ct * a.query_chunk;
+    const int crows = min(a.query_chunk, nq - ci0) * G;
+    const bool single = ct_parts == 1 && min(t0_all, chunk_visible(a, L, ct)) == 0;
+    for (int idx = tid; idx < crows * D; idx += kWaves * kWaveSize) {
+      const int h = idx / D;
+      const int d = idx % D;
+      float acc, M, lsum;
+      combine(sh, t, ntile, slices, h, d, acc, M, lsum);
+      if (any_bad) acc = __builtin_nanf("");
+      const size_t row = ((size_t)b * nq + ci0 + h / G) * Hq + (size_t)g * G + h % G;
+      if (single)
+        a.out[row * D + d] = lsum > 0.f ? acc / lsum : acc;  // acc is 0 (or NaN) for a row that sees nothing
+      else
+        store_partial(a, row * a.slots_per_row + a.prefix_partitions + p, d, D, acc, M, lsum);
+    }
   }
 }
 

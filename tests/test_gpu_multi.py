@@ -47,7 +47,7 @@ def check(got, ref, what):
     assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS, what
 
 
-LENS = [1, 2, 3, 4, 5, 15, 16, 17, 33, 64, 65, 300, 1000, 2049]
+LENS = [1, 2, 3, 4, 5, 15, 16, 17, 21, 33, 64, 65, 300, 1000, 2049]
 CASES = [  # (Hq, Hkv, D, n): rows per work item = min(n, 16 // G) * G
     (32, 8, 128, 4),   # G=4: one 16-row chunk
     (32, 8, 128, 7),   # two chunks (4 + 3 tokens)
@@ -56,6 +56,10 @@ CASES = [  # (Hq, Hkv, D, n): rows per work item = min(n, 16 // G) * G
     (16, 1, 64, 3),    # G=16: one token per chunk
     (12, 4, 64, 5),    # G=3: chunks of 5 tokens, 15 rows
     (8, 2, 64, 1),     # a decode step given as [B][1][Hq][D]
+    (8, 1, 128, 8),    # G=8: 4 chunks in one work item, one 16-row tile per wavefront
+    (32, 8, 128, 13),  # G=4: 4 chunks (3 full, 1 partial) in one item
+    (32, 8, 64, 21),   # G=4: 6 chunks, i.e. two items (4 + 2 chunks)
+    (4, 4, 128, 40),   # G=1: 3 chunks (16 + 16 + 8 tokens)
 ]
 
 
