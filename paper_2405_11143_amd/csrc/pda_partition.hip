@@ -19,9 +19,12 @@
 // query rows): the 4 wavefronts take 16-row tiles first and runs of blocks
 // second, and every block's tiles reach the compute unit once.
 //
-// Each wavefront streams its run of 16-token blocks with WaveAttention
-// (pda_wave.h); the states of the wavefronts that share a row are merged
-// through LDS in a fixed order.  A regular item with no prefix that sees a
+// With one tile, each wavefront streams its run of 16-token blocks with
+// WaveAttention (pda_wave.h), tiles straight into registers.  With several
+// tiles, the workgroup stages every block's K and V tiles through LDS once
+// (2 blocks per step, double-buffered) and each wavefront folds them from
+// there for its own rows.  The states of the wavefronts that share a row are
+// merged through LDS in a fixed order.  A regular item with no prefix that sees a
 // single partition writes its final output rows; every other item leaves a
 // partial softmax state (max, denominator, unnormalised output) for the
 // merge pass.  Nothing depends on physical block ids or on timing, so results
@@ -41,6 +44,37 @@ struct PassShared {
   int bad[kWaves];
 };
 
+// Tile staging for items with several 16-row tiles: every step brings SB
+// consecutive blocks' K and V tiles into LDS (double-buffered), loaded once
+// by the whole workgroup, and every wavefront reads its MFMA fragments from
+// there.  Block ids come through an LDS window.
+constexpr int kIdWindow = 256;
+
+template <int D, int SB>
+struct Staging {
+  static constexpr int kStepBlocks = SB;
+  static constexpr int TC = WaveAttention<D>::kTileBytes / 16;       // 16-byte pieces per tile
+  static constexpr int kLoads = SB * 2 * TC / (kWaves * kWaveSize);  // per thread and step
+  uint4 buf[2][SB][2][TC];
+  int ids[kIdWindow];
+};
+
+// Which paths a launch compiles.  A launch whose items all have one tile
+// (every decode step without shared-prefix groups) compiles the register
+// path only and keeps its register count (134 VGPRs at D = 128); otherwise
+// both paths are compiled (155).  Staging takes 2 blocks per step, so the
+// staging area (33 KiB at D = 128) fits in the epilogue's LDS and the kernel
+// keeps 3 workgroups per compute unit; 4 blocks per step at 2 workgroups per
+// compute unit measured slower on MI355X.
+constexpr int kModeRegister = 1, kModeMixed = 3;
+constexpr int kStepBlocks = 2;
+
+template <int D, int MODE>
+union PassLds {
+  PassShared<D> sh;                // the epilogue
+  Staging<D, kStepBlocks> st;      // the staged main loop (never live at the same time)
+};
+
 // Publish a finished wavefront's state: rows n < rows of the tile.
 template <int D>
 __device__ __forceinline__ void publish(PassShared<D>& sh, const WaveAttention<D>& wave, int w, int lane, int rows) {
@@ -51,7 +85,7 @@ __device__ __forceinline__ void publish(PassShared<D>& sh, const WaveAttention<D
       const int d0 = wave.d_of(i, 0);  // D = 128: 8 consecutive columns; D = 64: 4
       *reinterpret_cast<float4*>(&sh.o[w][n][d0]) =
           make_float4(wave.o[0][i], wave.o[1][i], wave.o[2][i], wave.o[3][i]);
-      if (D == 128)
+      if constexpr (D == 128)
         *reinterpret_cast<float4*>(&sh.o[w][n][d0 + 4]) =
             make_float4(wave.o[4][i], wave.o[5][i], wave.o[6][i], wave.o[7][i]);
     }
@@ -89,8 +123,82 @@ __device__ __forceinline__ void store_partial(const StepArgs& a, size_t slot, in
   }
 }
 
-template <int D>
-__device__ void regular_item(const StepArgs& a, PassShared<D>& sh, int item) {
+// Stream blocks [J0, J1) of one sequence through LDS.  All threads of the
+// workgroup call this.  Wavefront (tile, slice) folds the blocks of each step
+// whose position is slice, slice + slices, ... into its state, and only
+// blocks below its own end `j_stop` (its query chunk's causal range); an
+// inactive wavefront only helps to load.
+template <int D, int SB>
+__device__ void run_staged(WaveAttention<D>& wave, Staging<D, SB>& st, const int32_t* table_row, int J0, int J1,
+                           int j_stop, bool active, int slice, int slices, int L, int l_first, int l_vis,
+                           const char* kpool, const char* vpool, size_t block_bytes, int num_blocks) {
+  using WA = WaveAttention<D>;
+  constexpr int TC = Staging<D, SB>::TC;
+  constexpr int NL = Staging<D, SB>::kLoads;
+  const int tid = threadIdx.x;
+  bool bad = false;
+  uint4 r[NL];
+  // issue the loads of step `step` of the window starting at block jw
+  auto issue = [&](int jw, int jwe, int step) {
+#pragma unroll
+    for (int k = 0; k < NL; ++k) {
+      const int ci = k * kWaves * kWaveSize + tid;  // [block][K or V][piece]
+      const int blk = ci / (2 * TC);
+      const int j = jw + step * SB + blk;
+      const bool valid = j < jwe;
+      int phys = valid ? st.ids[j - jw] : 0;
+      if ((unsigned)phys >= (unsigned)num_blocks) {  // contract violation: never read outside the pool
+        bad |= valid;
+        phys = 0;
+      }
+      const char* pool = ((ci / TC) & 1) ? vpool : kpool;
+      r[k] = load_stream(tile_rsrc(pool + (size_t)phys * block_bytes, valid ? WA::kTileBytes : 0), (ci % TC) * 16);
+    }
+  };
+  auto commit = [&](int buf) {
+#pragma unroll
+    for (int k = 0; k < NL; ++k) {
+      const int ci = k * kWaves * kWaveSize + tid;
+      (&st.buf[buf][0][0][0])[ci] = r[k];
+    }
+  };
+  for (int jw = J0; jw < J1; jw += kIdWindow) {
+    const int jwe = min(J1, jw + kIdWindow);
+    for (int j = jw + tid; j < jwe; j += kWaves * kWaveSize) st.ids[j - jw] = table_row[j];
+    __syncthreads();
+    const int nsteps = (jwe - jw + SB - 1) / SB;
+    issue(jw, jwe, 0);
+    commit(0);
+    __syncthreads();
+    if (nsteps > 1) issue(jw, jwe, 1);
+    for (int step = 0; step < nsteps; ++step) {
+      const int buf = step & 1;
+      if (active) {
+        for (int k = slice; k < SB; k += slices) {
+          const int j = jw + step * SB + k;
+          if (j >= jwe || j >= j_stop) break;
+          uint4 kr[WA::NC], vr[4];
+          const uint4* kb = st.buf[buf][k][0];
+          const uint4* vb = st.buf[buf][k][1];
+#pragma unroll
+          for (int c = 0; c < WA::NC; ++c) kr[c] = kb[(c * 1024) / 16 + wave.lane];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) vr[e] = vb[(wave.v_off + e * WA::kRowBytes) / 16];
+          wave.process(kr, vr, j * kBlockTokens, L, l_first, l_vis);
+        }
+      }
+      if (step + 1 < nsteps) commit(buf ^ 1);  // the buffer read in step - 1
+      __syncthreads();
+      if (step + 2 < nsteps) issue(jw, jwe, step + 2);
+    }
+  }
+  wave.bad |= __builtin_amdgcn_ballot_w64(bad) != 0;
+  __syncthreads();  // the staging area is reused by the epilogue
+}
+
+template <int D, int MODE>
+__device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item) {
+  PassShared<D>& sh = lds.sh;
   using WA = WaveAttention<D>;
   const int Hq = a.num_q_heads;
   const int G = a.group;
@@ -146,15 +254,6 @@ __device__ void regular_item(const StepArgs& a, PassShared<D>& sh, int item) {
   const int l_first = l_vis - nv + 1;
   const int t0 = min(t0_all, max(l_vis, 0));
   const int nparts = parts_of(c);
-  int wj0 = 0, wj1 = 0;
-  if (slice < slices && p < nparts) {
-    const int t_end = min(l_vis, t0 + (p + 1) * Tp);
-    const int j_begin = (t0 + p * Tp) / kBlockTokens;
-    const int j_end = (t_end + kBlockTokens - 1) / kBlockTokens;
-    const int per_slice = (j_end - j_begin + slices - 1) / slices;
-    wj0 = min(j_end, j_begin + slice * per_slice);
-    wj1 = min(j_end, wj0 + per_slice);
-  }
   // lane row n repeats real rows past the chunk's last one
   const int r = (lane & 15) % rows;
   const int qi = i0 + r / G;
@@ -162,8 +261,28 @@ __device__ void regular_item(const StepArgs& a, PassShared<D>& sh, int item) {
   wave.start(a.q + (((size_t)b * nq + qi) * Hq + (size_t)g * G + r % G) * D, nq - 1 - qi);
   const char* kpool = reinterpret_cast<const char*>(a.k) + (size_t)g * WA::kTileBytes;
   const char* vpool = reinterpret_cast<const char*>(a.v) + (size_t)g * WA::kTileBytes;
-  wave.run(a.table + (size_t)b * a.max_blocks_per_seq, wj0, wj1, L, l_first, max(l_vis, 0), kpool, vpool,
-           (size_t)a.num_kv_heads * WA::kTileBytes, a.num_blocks);
+  const int32_t* table_row = a.table + (size_t)b * a.max_blocks_per_seq;
+  const size_t block_bytes = (size_t)a.num_kv_heads * WA::kTileBytes;
+  auto block_end = [&](int lv, int parts) {  // end block of this partition for a chunk limit lv
+    return p < parts ? (min(lv, t0 + (p + 1) * Tp) + kBlockTokens - 1) / kBlockTokens : 0;
+  };
+  const int j_begin = (t0 + p * Tp) / kBlockTokens;
+  if (MODE == kModeRegister && ntile != 1) return;  // not this launch's kind (never: the host picks the mode)
+  if (ntile == 1) {  // one tile: the 4 wavefronts split the blocks, tiles into registers
+    const int j_end = block_end(l_vis, nparts);
+    const int per_slice = (j_end - j_begin + kWaves - 1) / kWaves;
+    const int wj0 = min(j_end, j_begin + w * per_slice);
+    const int wj1 = min(j_end, wj0 + per_slice);
+    wave.run(table_row, wj0, wj1, L, l_first, max(l_vis, 0), kpool, vpool, block_bytes, a.num_blocks);
+  } else if constexpr (MODE != kModeRegister) {  // several tiles: every block staged once through LDS for all of them
+    int J1 = j_begin;
+    for (int t = 0; t < ntile; ++t) {
+      const int ct = chunk_of(t);
+      J1 = max(J1, block_end(chunk_visible(a, L, ct), parts_of(ct)));
+    }
+    run_staged(wave, lds.st, table_row, j_begin, J1, block_end(l_vis, nparts), slice < slices, slice, slices, L,
+               l_first, max(l_vis, 0), kpool, vpool, block_bytes, a.num_blocks);
+  }
   wave.finish();
   publish(sh, wave, w, lane, rows);
   __syncthreads();
@@ -194,8 +313,9 @@ __device__ void regular_item(const StepArgs& a, PassShared<D>& sh, int item) {
   }
 }
 
-template <int D>
-__device__ void prefix_item(const StepArgs& a, PassShared<D>& sh, int pitem) {
+template <int D, int MODE>
+__device__ void prefix_item(const StepArgs& a, PassLds<D, MODE>& lds, int pitem) {
+  PassShared<D>& sh = lds.sh;
   using WA = WaveAttention<D>;
   const int Hq = a.num_q_heads;
   const int G = a.group;
@@ -221,9 +341,6 @@ __device__ void prefix_item(const StepArgs& a, PassShared<D>& sh, int pitem) {
   const int t_end = min(plen, (pp + 1) * Tp);
   const int j_begin = (pp * Tp) / kBlockTokens;
   const int j_end = t_end / kBlockTokens;
-  const int per_slice = (j_end - j_begin + slices - 1) / slices;
-  const int wj0 = slice < slices ? min(j_end, j_begin + slice * per_slice) : j_end;
-  const int wj1 = min(j_end, wj0 + per_slice);
   const int tile_rows = min(kRows, rows - tile * kRows);
 
   // lane row n of this tile repeats real rows past the tile's last one
@@ -234,8 +351,18 @@ __device__ void prefix_item(const StepArgs& a, PassShared<D>& sh, int pitem) {
   const char* kpool = reinterpret_cast<const char*>(a.k) + (size_t)g * WA::kTileBytes;
   const char* vpool = reinterpret_cast<const char*>(a.v) + (size_t)g * WA::kTileBytes;
   // the prefix blocks are those of the group's first member (shared by contract)
-  wave.run(a.table + (size_t)first * a.max_blocks_per_seq, wj0, wj1, plen, plen, plen, kpool, vpool,
-           (size_t)a.num_kv_heads * WA::kTileBytes, a.num_blocks);
+  const int32_t* table_row = a.table + (size_t)first * a.max_blocks_per_seq;
+  const size_t block_bytes = (size_t)a.num_kv_heads * WA::kTileBytes;
+  if (MODE == kModeRegister && ntile != 1) return;  // not this launch's kind (never: the host picks the mode)
+  if (ntile == 1) {  // one tile: the 4 wavefronts split the blocks, tiles into registers
+    const int per_slice = (j_end - j_begin + kWaves - 1) / kWaves;
+    const int wj0 = min(j_end, j_begin + w * per_slice);
+    const int wj1 = min(j_end, wj0 + per_slice);
+    wave.run(table_row, wj0, wj1, plen, plen, plen, kpool, vpool, block_bytes, a.num_blocks);
+  } else if constexpr (MODE != kModeRegister) {  // several tiles: every block staged once through LDS for all of them
+    run_staged(wave, lds.st, table_row, j_begin, j_end, j_end, slice < slices, slice, slices, plen, plen, plen,
+               kpool, vpool, block_bytes, a.num_blocks);
+  }
   wave.finish();
   publish(sh, wave, w, lane, tile_rows);
   __syncthreads();
@@ -256,22 +383,33 @@ __device__ void prefix_item(const StepArgs& a, PassShared<D>& sh, int pitem) {
 }
 
 // Occupancy: 3 wavefronts per SIMD (12 per compute unit) at most 168 VGPRs.
-template <int D>
+template <int D, int MODE>
 __global__ void __launch_bounds__(kWaves * kWaveSize) __attribute__((amdgpu_waves_per_eu(3)))
 partition_kernel(const StepArgs a) {
-  __shared__ __align__(16) PassShared<D> sh;
+  __shared__ __align__(16) PassLds<D, MODE> lds;
   const int item = a.order[blockIdx.x];
   if (item < a.num_regular_items)
-    regular_item<D>(a, sh, item);
+    regular_item<D, MODE>(a, lds, item);
   else
-    prefix_item<D>(a, sh, item - a.num_regular_items);
+    prefix_item<D, MODE>(a, lds, item - a.num_regular_items);
 }
 
 template <int D>
 hipError_t launch_d(const StepArgs& a, hipStream_t stream) {
   const unsigned grid = (unsigned)a.num_regular_items +
                         (unsigned)a.num_groups * (unsigned)a.prefix_partitions * (unsigned)a.num_kv_heads;
-  hipLaunchKernelGGL((partition_kernel<D>), dim3(grid), dim3(kWaves * kWaveSize), 0, stream, a);
+  // which kinds of items the step has: a regular item has one tile when its
+  // chunk group holds one query chunk; a prefix item may have one tile
+  // whenever groups exist (a group can be small) and several when the bound
+  // on a group's rows exceeds one tile
+  const bool groups = a.num_groups > 0;
+  const bool one = a.num_query_chunks % kWaves == 1 || groups;
+  const bool several = a.num_query_chunks >= 2 || (groups && a.max_group_size * a.group > kRows);
+  const dim3 block(kWaves * kWaveSize);
+  if (one && !several)
+    hipLaunchKernelGGL((partition_kernel<D, kModeRegister>), dim3(grid), block, 0, stream, a);
+  else
+    hipLaunchKernelGGL((partition_kernel<D, kModeMixed>), dim3(grid), block, 0, stream, a);
   return hipGetLastError();
 }
 
