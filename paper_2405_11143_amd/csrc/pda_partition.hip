@@ -209,7 +209,8 @@ __device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item)
   const int g = gc / a.num_chunk_groups;
   const int cg = gc % a.num_chunk_groups;
   const int nq = a.num_query_tokens;
-  const int ntile = min(kWaves, a.num_query_chunks - cg * kWaves);  // query chunks (16-row tiles) of the item
+  // query chunks (16-row tiles) of the item: always one in the register-only variant
+  const int ntile = MODE == kModeRegister ? 1 : min(kWaves, a.num_query_chunks - cg * kWaves);
   const int slices = kWaves / ntile;                               // runs of blocks per tile
   const int tid = threadIdx.x;
   const int lane = tid & (kWaveSize - 1);
