@@ -167,6 +167,10 @@ int prepare_step(const pda_problem* p, const pda_prefix_groups* groups, const vo
   if (groups && groups->num_groups > 0 && p->num_seqs > 0 && (!groups->group_start || !groups->group_prefix_len))
     return PDA_ERR_NULL;
   fill_args(p, plan, ws, args);
+  // When the GPU runs every item at once the order is irrelevant: the step
+  // skips the work-order kernel (one dependent launch less) and item i is
+  // workgroup i.  Shared-prefix groups still need it for the prefix table.
+  if (plan->items <= (size_t)kConcurrentItems && !(groups && groups->num_groups > 0)) args->order = nullptr;
   if (groups && groups->num_groups > 0 && p->num_seqs > 0) {
     args->group_start = groups->group_start;
     args->group_prefix_len = groups->group_prefix_len;
@@ -205,7 +209,7 @@ int prepare_append(const pda_problem* p, const void* k_new, const void* v_new, c
 // The launches of one attention step (work order, pass 1, merge).
 int launch_attention(const pda_problem* p, const Plan& plan, const pda::StepArgs& args, hipStream_t stream) {
   if (p->num_seqs == 0) return PDA_OK;
-  if (pda::launch_order(args, stream) != hipSuccess) return PDA_ERR_HIP;
+  if (args.order && pda::launch_order(args, stream) != hipSuccess) return PDA_ERR_HIP;
   if (pda::launch_partition(args, p->head_dim, stream) != hipSuccess) return PDA_ERR_HIP;
   if (plan.slots > 0 && pda::launch_merge(args, p->head_dim, stream) != hipSuccess) return PDA_ERR_HIP;
   return PDA_OK;
@@ -254,7 +258,7 @@ int pda_partition_attention(const pda_problem* prob, const void* q, const void* 
                         workspace_bytes, &plan, &args);
   if (rc != PDA_OK) return rc;
   if (prob->num_seqs == 0) return PDA_OK;
-  if (pda::launch_order(args, stream) != hipSuccess) return PDA_ERR_HIP;
+  if (args.order && pda::launch_order(args, stream) != hipSuccess) return PDA_ERR_HIP;
   if (pda::launch_partition(args, prob->head_dim, stream) != hipSuccess) return PDA_ERR_HIP;
   return PDA_OK;
 }
@@ -325,7 +329,8 @@ int pda_step_graph_create(const pda_problem* prob, const void* q, const void* k_
   } else {
     // the same launches as pda_append_kv + pda_decode
     if (launch_append_of(prob, append_args, k_new, v_new, k_cache, v_cache, s) != hipSuccess ||
-        pda::launch_order(args, s) != hipSuccess || pda::launch_partition(args, prob->head_dim, s) != hipSuccess ||
+        (args.order && pda::launch_order(args, s) != hipSuccess) ||
+        pda::launch_partition(args, prob->head_dim, s) != hipSuccess ||
         (plan.slots > 0 && pda::launch_merge(args, prob->head_dim, s) != hipSuccess))
       rc = PDA_ERR_HIP;
     hipGraph_t captured = nullptr;

@@ -24,7 +24,7 @@ struct StepArgs {
   const int32_t* table;    // int32 [B][max_blocks_per_seq]
   const int32_t* lens;     // int32 [B]
   float* out;              // fp32 [B][n][Hq][D]
-  int32_t* order;          // int32 [items]: work items, largest partition first
+  int32_t* order;          // int32 [items]: work items, largest partition first (null: natural order)
   float* part_o;           // fp32 [B*n*Hq*slots_per_row][D]  unnormalised partition outputs
   float* part_m;           // fp32 [B*n*Hq*slots_per_row]     partition reference max, log2 domain
   float* part_l;           // fp32 [B*n*Hq*slots_per_row]     partition softmax denominators

@@ -388,7 +388,7 @@ template <int D, int MODE>
 __global__ void __launch_bounds__(kWaves * kWaveSize) __attribute__((amdgpu_waves_per_eu(3)))
 partition_kernel(const StepArgs a) {
   __shared__ __align__(16) PassLds<D, MODE> lds;
-  const int item = a.order[blockIdx.x];
+  const int item = a.order ? a.order[blockIdx.x] : (int)blockIdx.x;  // no order: every item runs at once
   if (item < a.num_regular_items)
     regular_item<D, MODE>(a, lds, item);
   else
