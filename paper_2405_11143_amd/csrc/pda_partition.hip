@@ -127,12 +127,14 @@ __device__ __forceinline__ void store_partial(const StepArgs& a, size_t slot, in
 // workgroup call this.  Wavefront (tile, slice) folds the blocks of each step
 // whose position is slice, slice + slices, ... into its state, and only
 // blocks below its own end `j_stop` (its query chunk's causal range); an
-// inactive wavefront only helps to load.
+// inactive wavefront only helps to load.  A wavefront that takes both blocks
+// of a step (slices = 1) folds them as one pair.
 template <int D, int SB>
 __device__ void run_staged(WaveAttention<D>& wave, Staging<D, SB>& st, const int32_t* table_row, int J0, int J1,
                            int j_stop, bool active, int slice, int slices, int L, int l_first, int l_vis,
                            const char* kpool, const char* vpool, size_t block_bytes, int num_blocks) {
   using WA = WaveAttention<D>;
+  static_assert(SB == 2, "a step is one pair of blocks");
   constexpr int TC = Staging<D, SB>::TC;
   constexpr int NL = Staging<D, SB>::kLoads;
   const int tid = threadIdx.x;
@@ -174,17 +176,35 @@ __device__ void run_staged(WaveAttention<D>& wave, Staging<D, SB>& st, const int
     for (int step = 0; step < nsteps; ++step) {
       const int buf = step & 1;
       if (active) {
-        for (int k = slice; k < SB; k += slices) {
-          const int j = jw + step * SB + k;
-          if (j >= jwe || j >= j_stop) break;
-          uint4 kr[WA::NC], vr[4];
-          const uint4* kb = st.buf[buf][k][0];
-          const uint4* vb = st.buf[buf][k][1];
+        const int j0 = jw + step * SB;
+        if (slices == 1 && j0 + 1 < min(jwe, j_stop)) {  // both blocks of the step: one pair
+          const int tok0 = j0 * kBlockTokens;
+          const bool tail = tok0 + 2 * kBlockTokens > l_first;  // wave-uniform
+          uint4 kr[2][WA::NC], vr[2][4];
 #pragma unroll
-          for (int c = 0; c < WA::NC; ++c) kr[c] = kb[(c * 1024) / 16 + wave.lane];
+          for (int k = 0; k < 2; ++k)
 #pragma unroll
-          for (int e = 0; e < 4; ++e) vr[e] = vb[(wave.v_off + e * WA::kRowBytes) / 16];
-          wave.process(kr, vr, j * kBlockTokens, L, l_first, l_vis);
+            for (int c = 0; c < WA::NC; ++c) kr[k][c] = st.buf[buf][k][0][(c * 1024) / 16 + wave.lane];
+          const auto f = wave.template softmax<2>(kr, tok0, L, tail);
+#pragma unroll
+          for (int k = 0; k < 2; ++k)  // V read only now: fewer registers live across the softmax
+#pragma unroll
+            for (int e = 0; e < 4; ++e) vr[k][e] = st.buf[buf][k][1][(wave.v_off + e * WA::kRowBytes) / 16];
+          wave.template mask_v<2>(vr, tok0, l_vis, tail);
+          wave.template pv<2>(vr, f);
+        } else {
+          for (int k = slice; k < SB; k += slices) {
+            const int j = j0 + k;
+            if (j >= jwe || j >= j_stop) break;
+            uint4 kr[WA::NC], vr[4];
+            const uint4* kb = st.buf[buf][k][0];
+            const uint4* vb = st.buf[buf][k][1];
+#pragma unroll
+            for (int c = 0; c < WA::NC; ++c) kr[c] = kb[(c * 1024) / 16 + wave.lane];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) vr[e] = vb[(wave.v_off + e * WA::kRowBytes) / 16];
+            wave.process(kr, vr, j * kBlockTokens, L, l_first, l_vis);
+          }
         }
       }
       if (step + 1 < nsteps) commit(buf ^ 1);  // the buffer read in step - 1

@@ -32,12 +32,14 @@
 //    max is reduced over its four lanes and the state is rescaled.
 //    Otherwise probabilities are taken against the stale maximum (they stay
 //    below 2^8, far inside fp32), so most blocks need neither the reduction
-//    nor the rescale; the result is the same softmax.
+//    nor the rescale; the result is the same softmax.  Blocks that every row
+//    sees whole take a path without any masking.
 //  * P V, transposed, on MFMA.  O^T = V^T P^T is D/16 MFMA f32_16x16x16_bf16
-//    per block and half: the probabilities of lane (kg, n) are already the B
-//    fragment (column n, k-group kg), and the A fragment of lane (kg, n) is
-//    4 tokens x 1 column of the V tile, picked out of the 16-byte row pieces
-//    the lane loaded.  Each probability p is split into bf16 hi = p with the
+//    per block and half (or D/16 f32_16x16x32_bf16 per pair of blocks): the
+//    probabilities of lane (kg, n) are already the B fragment (column n,
+//    k-group kg), and the A fragment of lane (kg, n) is 4 tokens x 1 column
+//    of the V tile (of each block), picked out of the 16-byte row pieces the
+//    lane loaded.  Each probability p is split into bf16 hi = p with the
 //    low 16 bits cleared and lo = bf16(p - hi), and both halves go through
 //    the MFMA, so P keeps about 16 significant bits (relative error below
 //    2^-15) instead of bf16's 8.  The output of row n stays in the lanes of
@@ -57,6 +59,12 @@ typedef short shortx4_t __attribute__((ext_vector_type(4)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// x * y rounded on its own: never fused with a following add.
+__device__ __forceinline__ float mul_rounded(float x, float y) {
+#pragma clang fp contract(off)
+  return x * y;
+}
 
 __device__ __forceinline__ float readlane_f(float x, int lane) {
   return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), lane));
@@ -149,96 +157,161 @@ struct WaveAttention {
     for (int e = 0; e < 4; ++e) vr[e] = load_stream(rv, v_off + e * kRowBytes);
   }
 
+  // The dword of token row e of a V tile piece `v` that holds this lane's
+  // column of output tile t (the column d_of gives for accumulator row 4kg+e).
+  __device__ __forceinline__ unsigned col_dword(const uint4 (&v)[4], int e, int t) const {
+    const int dw = t >> 1;
+    if (D == 128) return dw == 0 ? v[e].x : dw == 1 ? v[e].y : dw == 2 ? v[e].z : v[e].w;
+    const bool upper = n >= 8;  // D = 64: lanes n and n + 8 hold the same 8 columns
+    return dw == 0 ? (upper ? v[e].z : v[e].x) : (upper ? v[e].w : v[e].y);
+  }
+
+  // Move the running max to cover `mx` (this lane's largest scaled score),
+  // reduced over the row's four lanes, and rescale the state.
+  __device__ __forceinline__ void rescale(float mx) {
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mn = fmaxf(m_run, mx);  // the same in the four lanes of the row
+    const float al = exp2_fast(m_run - mn);
+    m_run = mn;
+    l_run *= al;
+#pragma unroll
+    for (int t = 0; t < VT; ++t) o[t] *= al;
+  }
+
+  // P^T of NB blocks as two bf16 B fragments per block: hi = p truncated,
+  // lo = bf16(p - hi); word 2b + h holds tokens 4kg + 2h, 4kg + 2h + 1 of block b.
+  template <int NB>
+  struct PFrag {
+    unsigned hw[2 * NB], lw[2 * NB];
+  };
+
+  // Fold the scores of NB consecutive blocks (NB = 1 or 2; logical tokens
+  // tok0 .. tok0 + 16 NB - 1) into the softmax state and return their
+  // probabilities.  `tail` (wave-uniform): some row may not see some of these
+  // tokens (the context ends in them, or a multi-token row's own position
+  // comes before them); only then is anything masked.
+  //
+  // Lane (kg, n) gets row n, tokens 4kg + i of each block.  Each probability
+  // is exp2(fl(s * scale) - max): the largest score of a row gets exactly 1,
+  // so a one-token context returns its V row exactly.  A masked score is
+  // -inf after scaling (so a zero scale masks too).
+  template <int NB>
+  __device__ __forceinline__ PFrag<NB> softmax(const uint4 (&kr)[NB][NC], int tok0, int L, bool tail) {
+    floatx4_t acc[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      acc[b] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+        acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kr[b][c]), qa[c], acc[b], 0, 0, 0);
+    }
+    // The scaled scores are formed here, in the MFMAs' own basic block: the
+    // compiler did not insert the wait states a VALU read of an MFMA result
+    // needs when the first such read came after the tail branch below.
+    float sc[NB][4];
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sc[b][i] = mul_rounded(acc[b][i], scale_log2);
+    if (tail) {
+      // An empty volatile asm keeps this a branch: as selects, the masking
+      // would run on every block.
+      asm volatile("");
+      const int lim = L - lim_off;
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (tok0 + kBlockTokens * b + 4 * kg + i >= lim) sc[b][i] = kNegInf;
+    }
+    float top = fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3]));
+    if constexpr (NB == 2) top = fmaxf(top, fmaxf(fmaxf(sc[1][0], sc[1][1]), fmaxf(sc[1][2], sc[1][3])));
+    if (__builtin_amdgcn_ballot_w64(top > m_run + kRescaleSlack) != 0) rescale(top);  // wave-uniform
+    float pr[NB][4];
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pr[b][i] = exp2_fast(sc[b][i] - m_run);
+    float ls = (pr[0][0] + pr[0][1]) + (pr[0][2] + pr[0][3]);
+    if constexpr (NB == 2) ls += (pr[1][0] + pr[1][1]) + (pr[1][2] + pr[1][3]);
+    l_run += ls;
+    PFrag<NB> f;
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const unsigned h0 = __float_as_uint(pr[b][2 * h]) & 0xffff0000u;
+        const unsigned h1 = __float_as_uint(pr[b][2 * h + 1]) & 0xffff0000u;
+        f.hw[2 * b + h] = pack_halves(h0, h1, true);
+        typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+        const bf16x2_t l2 = {(__bf16)(pr[b][2 * h] - __uint_as_float(h0)),
+                             (__bf16)(pr[b][2 * h + 1] - __uint_as_float(h1))};
+        f.lw[2 * b + h] = __builtin_bit_cast(unsigned, l2);
+      }
+    return f;
+  }
+
+  // Zero the V rows at or past `l_vis` (no row of the chunk sees them), so
+  // whatever those slots hold never meets a zero probability.
+  template <int NB>
+  __device__ __forceinline__ void mask_v(uint4 (&vr)[NB][4], int tok0, int l_vis, bool tail) const {
+    if (tail) {
+      asm volatile("");  // a branch, as in softmax
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (tok0 + kBlockTokens * b + 4 * kg + e >= l_vis) vr[b][e] = make_uint4(0u, 0u, 0u, 0u);
+    }
+  }
+
+  // O^T += V^T P^T.  One block takes D/16 MFMA f32_16x16x16_bf16 per half of
+  // P; two blocks take D/16 MFMA f32_16x16x32_bf16 per half, where k-group kg
+  // of the contraction holds tokens 4kg .. 4kg+3 of the first block, then the
+  // same slots of the second, in both operands.
+  template <int NB>
+  __device__ __forceinline__ void pv(const uint4 (&vr)[NB][4], const PFrag<NB>& f) {
+#pragma unroll
+    for (int t = 0; t < VT; ++t) {
+      const bool hi_half = t & 1;
+      unsigned aw[2 * NB];  // this lane's column of tile t, token rows 0..3 of each block
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        aw[2 * b] = pack_halves(col_dword(vr[b], 0, t), col_dword(vr[b], 1, t), hi_half);
+        aw[2 * b + 1] = pack_halves(col_dword(vr[b], 2, t), col_dword(vr[b], 3, t), hi_half);
+      }
+      if constexpr (NB == 1) {
+        const shortx4_t a = __builtin_bit_cast(shortx4_t, make_uint2(aw[0], aw[1]));
+        o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
+            a, __builtin_bit_cast(shortx4_t, make_uint2(f.hw[0], f.hw[1])), o[t], 0, 0, 0);
+        o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
+            a, __builtin_bit_cast(shortx4_t, make_uint2(f.lw[0], f.lw[1])), o[t], 0, 0, 0);
+      } else {
+        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, make_uint4(aw[0], aw[1], aw[2], aw[3]));
+        o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            a, __builtin_bit_cast(bf16x8_t, make_uint4(f.hw[0], f.hw[1], f.hw[2], f.hw[3])), o[t], 0, 0, 0);
+        o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            a, __builtin_bit_cast(bf16x8_t, make_uint4(f.lw[0], f.lw[1], f.lw[2], f.lw[3])), o[t], 0, 0, 0);
+      }
+    }
+  }
+
   // Fold one block (logical tokens tok0 .. tok0+15) into the state.  `L` is
   // the context length, `l_first` the limit of the chunk's first row (every
   // row sees tokens below it) and `l_vis` the limit of its last row (no row
   // sees a token at or above it).
   __device__ __forceinline__ void process(const uint4 (&kr)[NC], uint4 (&vr)[4], int tok0, int L, int l_first,
                                           int l_vis) {
-    // ---- scores S^T = K Q^T: lane (kg, n) gets row n, tokens 4kg + i ----
-    floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
+    uint4 k1[1][NC], v1[1][4];
 #pragma unroll
-    for (int c = 0; c < NC; ++c)
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kr[c]), qa[c], acc, 0, 0, 0);
+    for (int c = 0; c < NC; ++c) k1[0][c] = kr[c];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v1[0][e] = vr[e];
     const bool tail = tok0 + kBlockTokens > l_first;  // wave-uniform
-    const int lim = L - lim_off;
-    float sc[4];
-    bool grow = false;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      sc[i] = acc[i] * scale_log2;
-      if (tail && tok0 + 4 * kg + i >= lim) sc[i] = kNegInf;
-      grow |= sc[i] > m_run + kRescaleSlack;
-    }
-    // ---- move the running max only when a score outgrows it by 2^8 ----
-    if (__builtin_amdgcn_ballot_w64(grow) != 0) {  // wave-uniform
-      float mx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mn = fmaxf(m_run, mx);  // the same in the four lanes of the row
-      const float al = exp2_fast(m_run - mn);
-      m_run = mn;
-      l_run *= al;
-#pragma unroll
-      for (int t = 0; t < VT; ++t) o[t] *= al;
-    }
-    float pr[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) pr[i] = exp2_fast(sc[i] - m_run);
-    l_run += (pr[0] + pr[1]) + (pr[2] + pr[3]);
-    // ---- P^T as two bf16 B fragments: hi = p truncated, lo = bf16(p - hi) ----
-    unsigned hb[4];
-    float lo[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      hb[i] = __float_as_uint(pr[i]) & 0xffff0000u;
-      lo[i] = pr[i] - __uint_as_float(hb[i]);
-    }
-    const shortx4_t b_hi = __builtin_bit_cast(
-        shortx4_t, make_uint2(pack_halves(hb[0], hb[1], true), pack_halves(hb[2], hb[3], true)));
-    typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
-    const bf16x4_t lo4 = {(__bf16)lo[0], (__bf16)lo[1], (__bf16)lo[2], (__bf16)lo[3]};
-    const shortx4_t b_lo = __builtin_bit_cast(shortx4_t, lo4);
-    // ---- V^T A fragments; rows past what the chunk sees are zeroed ----
-    if (tail) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        if (tok0 + 4 * kg + e >= l_vis) vr[e] = make_uint4(0u, 0u, 0u, 0u);
-    }
-    unsigned w[4][2];  // the 4 bf16 columns of this lane's tiles, per token row e
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      if (D == 128) {
-        w[e][0] = 0;  // unused: tiles read vr directly below
-        w[e][1] = 0;
-      } else {
-        const bool upper = n >= 8;
-        w[e][0] = upper ? vr[e].z : vr[e].x;
-        w[e][1] = upper ? vr[e].w : vr[e].y;
-      }
-    }
-#pragma unroll
-    for (int t = 0; t < VT; ++t) {
-      unsigned r0, r1, r2, r3;  // dword holding column t of token rows 0..3
-      if (D == 128) {
-        const int dw = t >> 1;
-        r0 = dw == 0 ? vr[0].x : dw == 1 ? vr[0].y : dw == 2 ? vr[0].z : vr[0].w;
-        r1 = dw == 0 ? vr[1].x : dw == 1 ? vr[1].y : dw == 2 ? vr[1].z : vr[1].w;
-        r2 = dw == 0 ? vr[2].x : dw == 1 ? vr[2].y : dw == 2 ? vr[2].z : vr[2].w;
-        r3 = dw == 0 ? vr[3].x : dw == 1 ? vr[3].y : dw == 2 ? vr[3].z : vr[3].w;
-      } else {
-        const int dw = t >> 1;
-        r0 = w[0][dw];
-        r1 = w[1][dw];
-        r2 = w[2][dw];
-        r3 = w[3][dw];
-      }
-      const bool hi_half = t & 1;
-      const shortx4_t a = __builtin_bit_cast(
-          shortx4_t, make_uint2(pack_halves(r0, r1, hi_half), pack_halves(r2, r3, hi_half)));
-      o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b_hi, o[t], 0, 0, 0);
-      o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b_lo, o[t], 0, 0, 0);
-    }
+    const PFrag<1> f = softmax<1>(k1, tok0, L, tail);
+    mask_v<1>(v1, tok0, l_vis, tail);
+    pv<1>(v1, f);
   }
 
   // Stream blocks [j0, j1) of one sequence: block ids in `table_row`, tiles of

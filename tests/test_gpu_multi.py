@@ -122,3 +122,24 @@ def test_multi_token_full_size_sampled(dev):
     ref = oracle.decode_multi_rows(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
                                    st.context_lens, st.scale, rows.astype(np.int32), threads=THREADS)
     check(got[rows[:, 0], rows[:, 1], rows[:, 2]], ref, "llama3_8b 4 draft tokens, sampled rows")
+
+
+@pytest.mark.parametrize("factor", [-1.0, 0.0, 3.0, 25.0])
+def test_scale_sign_zero_and_peaked(dev, factor):
+    """Negative, zero and large scales, on the register path (one tile per
+    work item) and on the staged path (several tiles, folded in pairs of
+    blocks).  The kernels fold the sign of the scale into q and a zero scale
+    into zero scores; a large scale makes the softmax peaked, so the running
+    max moves often."""
+    lens = [1, 17, 300, 2049, 40, 64]
+    for (Hq, Hkv, D, n) in [(32, 8, 128, 1), (8, 2, 64, 1), (32, 8, 128, 16), (8, 1, 128, 8), (16, 4, 64, 13)]:
+        st = W.custom_structure(len(lens), Hq, Hkv, D, lens, seed=40 + n)
+        _, k, v = W.fill_values(st, dev, fill="nan")
+        q = W.fill_multi_q(st, n, dev)
+        scale = float(np.float32(st.scale * factor))
+        bt = torch.from_numpy(st.block_table).to(dev)
+        ln = torch.from_numpy(st.context_lens).to(dev)
+        got = pda_decode(q, k, v, bt, ln, scale, max_context_len=st.max_context_len).cpu().numpy()
+        ref = oracle.decode_multi(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
+                                  st.context_lens, scale, threads=THREADS)
+        check(got, ref, f"scale x{factor} Hq={Hq} Hkv={Hkv} D={D} n={n}")
