@@ -7,17 +7,18 @@
 // the KV head) fill one 16-row MFMA tile; a decode step has one token, i.e.
 // one chunk of G rows.  New token i of a sequence with n new tokens and
 // context length L sits at position L - n + i and sees tokens
-// t < L - n + 1 + i.  The 4 wavefronts take the item's chunks first and runs
-// of its blocks second (1 chunk: 4 runs; 2: 2 runs each; 3-4: 1 run), so the
-// chunks of one item read each tile on one compute unit.  Each chunk keeps
+// t < L - n + 1 + i.  The 4 wavefronts take the item's chunks first and
+// slices of its blocks second (1 chunk: 4 contiguous runs; 2: every other
+// step of 2 blocks each; 3-4: every block), so the chunks of one item read
+// each tile on one compute unit.  Each chunk keeps
 // its own causal range and partition count.  With shared-prefix groups, a
 // sequence's regular items cover only the tokens after its group's prefix.
 //
 // Prefix items: (shared-prefix group, prefix partition, KV head).  All
 // members of a group read the same prefix blocks (parallel sampling, Section
 // 3.2), so the prefix is attended once for all members x G heads (up to 64
-// query rows): the 4 wavefronts take 16-row tiles first and runs of blocks
-// second, and every block's tiles reach the compute unit once.
+// query rows): the 4 wavefronts take 16-row tiles first and slices of blocks
+// second, as above, and every block's tiles reach the compute unit once.
 //
 // With one tile, each wavefront streams its run of 16-token blocks with
 // WaveAttention (pda_wave.h), tiles straight into registers.  With several
@@ -123,12 +124,12 @@ __device__ __forceinline__ void store_partial(const StepArgs& a, size_t slot, in
   }
 }
 
-// Stream blocks [J0, J1) of one sequence through LDS.  All threads of the
-// workgroup call this.  Wavefront (tile, slice) folds the blocks of each step
-// whose position is slice, slice + slices, ... into its state, and only
-// blocks below its own end `j_stop` (its query chunk's causal range); an
-// inactive wavefront only helps to load.  A wavefront that takes both blocks
-// of a step (slices = 1) folds them as one pair.
+// Stream blocks [J0, J1) of one sequence through LDS, a step of 2 blocks at a
+// time.  All threads of the workgroup call this.  Wavefront (tile, slice)
+// folds the steps slice, slice + slices, ... of each window into its state,
+// both blocks of a step as one pair (every fold is a pair, so the output
+// accumulators stay put), and only blocks below its own end `j_stop` (its
+// query chunk's causal range); an inactive wavefront only helps to load.
 template <int D, int SB>
 __device__ void run_staged(WaveAttention<D>& wave, Staging<D, SB>& st, const int32_t* table_row, int J0, int J1,
                            int j_stop, bool active, int slice, int slices, int L, int l_first, int l_vis,
@@ -175,36 +176,29 @@ __device__ void run_staged(WaveAttention<D>& wave, Staging<D, SB>& st, const int
     if (nsteps > 1) issue(jw, jwe, 1);
     for (int step = 0; step < nsteps; ++step) {
       const int buf = step & 1;
-      if (active) {
+      if (active && step % slices == slice) {  // wave-uniform
+        // Both blocks of the step as one pair.  When only the first is this
+        // wavefront's (the run or its causal range ends there), the second
+        // is masked whole through t_stop (its slot in LDS holds zeros or
+        // another range's tiles).
         const int j0 = jw + step * SB;
-        if (slices == 1 && j0 + 1 < min(jwe, j_stop)) {  // both blocks of the step: one pair
+        const int j_lim = min(jwe, j_stop);
+        if (j0 < j_lim) {
           const int tok0 = j0 * kBlockTokens;
-          const bool tail = tok0 + 2 * kBlockTokens > l_first;  // wave-uniform
+          const int t_stop = j_lim * kBlockTokens;
+          const bool tail = tok0 + 2 * kBlockTokens > min(l_first, t_stop);  // wave-uniform
           uint4 kr[2][WA::NC], vr[2][4];
 #pragma unroll
           for (int k = 0; k < 2; ++k)
 #pragma unroll
             for (int c = 0; c < WA::NC; ++c) kr[k][c] = st.buf[buf][k][0][(c * 1024) / 16 + wave.lane];
-          const auto f = wave.template softmax<2>(kr, tok0, L, tail);
+          const auto f = wave.template softmax<2>(kr, tok0, L, tail, t_stop);
 #pragma unroll
           for (int k = 0; k < 2; ++k)  // V read only now: fewer registers live across the softmax
 #pragma unroll
             for (int e = 0; e < 4; ++e) vr[k][e] = st.buf[buf][k][1][(wave.v_off + e * WA::kRowBytes) / 16];
-          wave.template mask_v<2>(vr, tok0, l_vis, tail);
+          wave.template mask_v<2>(vr, tok0, min(l_vis, t_stop), tail);
           wave.template pv<2>(vr, f);
-        } else {
-          for (int k = slice; k < SB; k += slices) {
-            const int j = j0 + k;
-            if (j >= jwe || j >= j_stop) break;
-            uint4 kr[WA::NC], vr[4];
-            const uint4* kb = st.buf[buf][k][0];
-            const uint4* vb = st.buf[buf][k][1];
-#pragma unroll
-            for (int c = 0; c < WA::NC; ++c) kr[c] = kb[(c * 1024) / 16 + wave.lane];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) vr[e] = vb[(wave.v_off + e * WA::kRowBytes) / 16];
-            wave.process(kr, vr, j * kBlockTokens, L, l_first, l_vis);
-          }
         }
       }
       if (step + 1 < nsteps) commit(buf ^ 1);  // the buffer read in step - 1
@@ -231,7 +225,7 @@ __device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item)
   const int nq = a.num_query_tokens;
   // query chunks (16-row tiles) of the item: always one in the register-only variant
   const int ntile = MODE == kModeRegister ? 1 : min(kWaves, a.num_query_chunks - cg * kWaves);
-  const int slices = kWaves / ntile;                               // runs of blocks per tile
+  const int slices = kWaves / ntile;                               // slices of blocks per tile
   const int tid = threadIdx.x;
   const int lane = tid & (kWaveSize - 1);
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -356,7 +350,7 @@ __device__ void prefix_item(const StepArgs& a, PassLds<D, MODE>& lds, int pitem)
   if (members <= 0 || pp * Tp >= plen) return;
   const int rows = members * G;                    // member-major, then the G heads
   const int ntile = (rows + kRows - 1) / kRows;    // 16-row tiles: 1 .. 4
-  const int slices = kWaves / ntile;               // runs of blocks per tile
+  const int slices = kWaves / ntile;               // slices of blocks per tile
   const int tile = w % ntile;
   const int slice = w / ntile;
   const int t_end = min(plen, (pp + 1) * Tp);

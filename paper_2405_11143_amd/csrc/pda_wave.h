@@ -190,14 +190,16 @@ struct WaveAttention {
   // tok0 .. tok0 + 16 NB - 1) into the softmax state and return their
   // probabilities.  `tail` (wave-uniform): some row may not see some of these
   // tokens (the context ends in them, or a multi-token row's own position
-  // comes before them); only then is anything masked.
+  // comes before them, or they lie at or past `t_stop`); only then is
+  // anything masked.
   //
   // Lane (kg, n) gets row n, tokens 4kg + i of each block.  Each probability
   // is exp2(fl(s * scale) - max): the largest score of a row gets exactly 1,
   // so a one-token context returns its V row exactly.  A masked score is
   // -inf after scaling (so a zero scale masks too).
   template <int NB>
-  __device__ __forceinline__ PFrag<NB> softmax(const uint4 (&kr)[NB][NC], int tok0, int L, bool tail) {
+  __device__ __forceinline__ PFrag<NB> softmax(const uint4 (&kr)[NB][NC], int tok0, int L, bool tail,
+                                               int t_stop = 0x7fffffff) {
     floatx4_t acc[NB];
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
@@ -218,7 +220,7 @@ struct WaveAttention {
       // An empty volatile asm keeps this a branch: as selects, the masking
       // would run on every block.
       asm volatile("");
-      const int lim = L - lim_off;
+      const int lim = min(L - lim_off, t_stop);
 #pragma unroll
       for (int b = 0; b < NB; ++b)
 #pragma unroll
