@@ -23,8 +23,8 @@
 // With one tile, each wavefront streams its run of 16-token blocks with
 // WaveAttention (pda_wave.h), tiles straight into registers.  With several
 // tiles, the workgroup stages every block's K and V tiles through LDS once
-// (2 blocks per step, double-buffered) and each wavefront folds them from
-// there for its own rows.  The states of the wavefronts that share a row are
+// (2 blocks per step, two steps in flight) and each wavefront folds them
+// from there for its own rows, a pair of blocks at a time.  The states of the wavefronts that share a row are
 // merged through LDS in a fixed order.  A regular item with no prefix that sees a
 // single partition writes its final output rows; every other item leaves a
 // partial softmax state (max, denominator, unnormalised output) for the
@@ -46,9 +46,10 @@ struct PassShared {
 };
 
 // Tile staging for items with several 16-row tiles: every step brings SB
-// consecutive blocks' K and V tiles into LDS (double-buffered), loaded once
-// by the whole workgroup, and every wavefront reads its MFMA fragments from
-// there.  Block ids come through an LDS window.
+// consecutive blocks' K and V tiles into LDS, loaded once by the whole
+// workgroup, and every wavefront reads its MFMA fragments from there.  Three
+// buffers: one step is folded while the loads of the next two are in flight
+// (in registers, then written to LDS).  Block ids come through an LDS window.
 constexpr int kIdWindow = 256;
 
 template <int D, int SB>
@@ -56,17 +57,17 @@ struct Staging {
   static constexpr int kStepBlocks = SB;
   static constexpr int TC = WaveAttention<D>::kTileBytes / 16;       // 16-byte pieces per tile
   static constexpr int kLoads = SB * 2 * TC / (kWaves * kWaveSize);  // per thread and step
-  uint4 buf[2][SB][2][TC];
+  uint4 buf[3][SB][2][TC];
   int ids[kIdWindow];
 };
 
 // Which paths a launch compiles.  A launch whose items all have one tile
 // (every decode step without shared-prefix groups) compiles the register
-// path only and keeps its register count (134 VGPRs at D = 128); otherwise
-// both paths are compiled (155).  Staging takes 2 blocks per step, so the
-// staging area (33 KiB at D = 128) fits in the epilogue's LDS and the kernel
-// keeps 3 workgroups per compute unit; 4 blocks per step at 2 workgroups per
-// compute unit measured slower on MI355X.
+// path only (135 VGPRs at D = 128, 33 KiB of LDS); otherwise both paths are
+// compiled (165 VGPRs, 49 KiB).  Staging takes 2 blocks per step, so three
+// staging buffers (48 KiB at D = 128) still leave room for 3 workgroups per
+// compute unit; 4 blocks per step at 2 workgroups per compute unit measured
+// slower on MI355X.
 constexpr int kModeRegister = 1, kModeMixed = 3;
 constexpr int kStepBlocks = 2;
 
@@ -74,6 +75,11 @@ template <int D, int MODE>
 union PassLds {
   PassShared<D> sh;                // the epilogue
   Staging<D, kStepBlocks> st;      // the staged main loop (never live at the same time)
+};
+
+template <int D>
+union PassLds<D, kModeRegister> {  // no staging in the register-only variant
+  PassShared<D> sh;
 };
 
 // Publish a finished wavefront's state: rows n < rows of the tile.
@@ -140,9 +146,11 @@ __device__ void run_staged(WaveAttention<D>& wave, Staging<D, SB>& st, const int
   constexpr int NL = Staging<D, SB>::kLoads;
   const int tid = threadIdx.x;
   bool bad = false;
-  uint4 r[NL];
+  // Two steps' loads are in flight in two register sets while a third
+  // step is folded from LDS (three buffers).
+  uint4 ra[NL], rb[NL];
   // issue the loads of step `step` of the window starting at block jw
-  auto issue = [&](int jw, int jwe, int step) {
+  auto issue = [&](uint4(&r)[NL], int jw, int jwe, int step) {
 #pragma unroll
     for (int k = 0; k < NL; ++k) {
       const int ci = k * kWaves * kWaveSize + tid;  // [block][K or V][piece]
@@ -158,52 +166,65 @@ __device__ void run_staged(WaveAttention<D>& wave, Staging<D, SB>& st, const int
       r[k] = load_stream(tile_rsrc(pool + (size_t)phys * block_bytes, valid ? WA::kTileBytes : 0), (ci % TC) * 16);
     }
   };
-  auto commit = [&](int buf) {
+  auto commit = [&](const uint4(&r)[NL], int buf) {
 #pragma unroll
     for (int k = 0; k < NL; ++k) {
       const int ci = k * kWaves * kWaveSize + tid;
       (&st.buf[buf][0][0][0])[ci] = r[k];
     }
   };
+  // fold step `step` (in buffer buf) if it is this wavefront's
+  auto fold_step = [&](int jw, int jwe, int step, int buf) {
+    if (!active || step % slices != slice) return;  // wave-uniform
+    // Both blocks of the step as one pair.  When only the first is this
+    // wavefront's (the run or its causal range ends there), the second is
+    // masked whole through t_stop (its slot in LDS holds zeros or another
+    // range's tiles).
+    const int j0 = jw + step * SB;
+    const int j_lim = min(jwe, j_stop);
+    if (j0 >= j_lim) return;
+    const int tok0 = j0 * kBlockTokens;
+    const int t_stop = j_lim * kBlockTokens;
+    const bool tail = tok0 + 2 * kBlockTokens > min(l_first, t_stop);  // wave-uniform
+    uint4 kr[2][WA::NC], vr[2][4];
+#pragma unroll
+    for (int k = 0; k < 2; ++k)
+#pragma unroll
+      for (int c = 0; c < WA::NC; ++c) kr[k][c] = st.buf[buf][k][0][(c * 1024) / 16 + wave.lane];
+    const auto f = wave.template softmax<2>(kr, tok0, L, tail, t_stop);
+#pragma unroll
+    for (int k = 0; k < 2; ++k)  // V read only now: fewer registers live across the softmax
+#pragma unroll
+      for (int e = 0; e < 4; ++e) vr[k][e] = st.buf[buf][k][1][(wave.v_off + e * WA::kRowBytes) / 16];
+    wave.template mask_v<2>(vr, tok0, min(l_vis, t_stop), tail);
+    wave.template pv<2>(vr, f);
+  };
   for (int jw = J0; jw < J1; jw += kIdWindow) {
     const int jwe = min(J1, jw + kIdWindow);
     for (int j = jw + tid; j < jwe; j += kWaves * kWaveSize) st.ids[j - jw] = table_row[j];
     __syncthreads();
     const int nsteps = (jwe - jw + SB - 1) / SB;
-    issue(jw, jwe, 0);
-    commit(0);
+    issue(ra, jw, jwe, 0);
+    if (nsteps > 1) issue(rb, jw, jwe, 1);
+    commit(ra, 0);
     __syncthreads();
-    if (nsteps > 1) issue(jw, jwe, 1);
-    for (int step = 0; step < nsteps; ++step) {
-      const int buf = step & 1;
-      if (active && step % slices == slice) {  // wave-uniform
-        // Both blocks of the step as one pair.  When only the first is this
-        // wavefront's (the run or its causal range ends there), the second
-        // is masked whole through t_stop (its slot in LDS holds zeros or
-        // another range's tiles).
-        const int j0 = jw + step * SB;
-        const int j_lim = min(jwe, j_stop);
-        if (j0 < j_lim) {
-          const int tok0 = j0 * kBlockTokens;
-          const int t_stop = j_lim * kBlockTokens;
-          const bool tail = tok0 + 2 * kBlockTokens > min(l_first, t_stop);  // wave-uniform
-          uint4 kr[2][WA::NC], vr[2][4];
-#pragma unroll
-          for (int k = 0; k < 2; ++k)
-#pragma unroll
-            for (int c = 0; c < WA::NC; ++c) kr[k][c] = st.buf[buf][k][0][(c * 1024) / 16 + wave.lane];
-          const auto f = wave.template softmax<2>(kr, tok0, L, tail, t_stop);
-#pragma unroll
-          for (int k = 0; k < 2; ++k)  // V read only now: fewer registers live across the softmax
-#pragma unroll
-            for (int e = 0; e < 4; ++e) vr[k][e] = st.buf[buf][k][1][(wave.v_off + e * WA::kRowBytes) / 16];
-          wave.template mask_v<2>(vr, tok0, min(l_vis, t_stop), tail);
-          wave.template pv<2>(vr, f);
-        }
-      }
-      if (step + 1 < nsteps) commit(buf ^ 1);  // the buffer read in step - 1
+    if (nsteps > 2) issue(ra, jw, jwe, 2);
+    // Step s sits in buffer s % 3; before the barrier that ends step s, step
+    // s + 1 moves from its registers into buffer (s + 1) % 3 (last read in
+    // step s - 2), and after it the freed registers take step s + 3.
+    // Unrolled by two so that the register sets stay static.
+    for (int step = 0, buf = 0; step < nsteps; step += 2) {
+      fold_step(jw, jwe, step, buf);
+      buf = buf == 2 ? 0 : buf + 1;
+      if (step + 1 < nsteps) commit(rb, buf);
       __syncthreads();
-      if (step + 2 < nsteps) issue(jw, jwe, step + 2);
+      if (step + 3 < nsteps) issue(rb, jw, jwe, step + 3);
+      if (step + 1 >= nsteps) break;
+      fold_step(jw, jwe, step + 1, buf);
+      buf = buf == 2 ? 0 : buf + 1;
+      if (step + 2 < nsteps) commit(ra, buf);
+      __syncthreads();
+      if (step + 4 < nsteps) issue(ra, jw, jwe, step + 4);
     }
   }
   wave.bad |= __builtin_amdgcn_ballot_w64(bad) != 0;
