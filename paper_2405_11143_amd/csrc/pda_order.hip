@@ -97,19 +97,22 @@ __global__ void __launch_bounds__(kOrderThreads) order_kernel(const StepArgs a) 
     }
   }
   __syncthreads();
-  // Position pos of the sorted pairs holds items pos * HC .. pos * HC + HC - 1;
-  // prefix pairs (which come with groups only, where HC = Hkv) use the same stride.
+  // The sorted pairs are taken in octets: the octet holding pair pos starts
+  // at pair pos - r (r = pos % 8) and has c <= 8 pairs, and item x < HC of
+  // pair pos goes to slot (pos - r) HC + x c + r (prefix pairs, which come
+  // with groups only, where HC = Hkv, alike).  Workgroups go to the 8 XCDs
+  // round-robin by slot, so with c = 8 every item of a pair -- among them the
+  // chunk groups that read the same K/V tiles -- runs on one XCD and shares
+  // its L2, and all of them start within 8 HC slots of each other.
   const int HC = a.num_kv_heads * a.num_chunk_groups;
   for (int idx = tid; idx < pairs; idx += kOrderThreads) {
     const int pos = atomicAdd(&s_count[bucket(idx)], 1);
-    if (idx < regular_pairs) {
-      const int b = idx % B;
-      const int p = idx / B;
-      for (int g = 0; g < HC; ++g) a.order[(size_t)pos * HC + g] = (p * B + b) * HC + g;
-    } else {
-      const int q = idx - regular_pairs;  // = grp * Pp + pp
-      for (int g = 0; g < HC; ++g) a.order[(size_t)pos * HC + g] = a.num_regular_items + q * HC + g;
-    }
+    const int r = pos % 8;
+    const int c = min(8, pairs - (pos - r));
+    const size_t base = (size_t)(pos - r) * HC + r;
+    // pair idx holds items idx * HC .. idx * HC + HC - 1: a regular pair (p, b)
+    // has idx = p * B + b, and the prefix items follow the regular ones
+    for (int x = 0; x < HC; ++x) a.order[base + (size_t)x * c] = idx * HC + x;
   }
 }
 
