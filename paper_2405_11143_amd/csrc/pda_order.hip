@@ -97,22 +97,34 @@ __global__ void __launch_bounds__(kOrderThreads) order_kernel(const StepArgs a) 
     }
   }
   __syncthreads();
-  // The sorted pairs are taken in octets: the octet holding pair pos starts
-  // at pair pos - r (r = pos % 8) and has c <= 8 pairs, and item x < HC of
-  // pair pos goes to slot (pos - r) HC + x c + r (prefix pairs, which come
-  // with groups only, where HC = Hkv, alike).  Workgroups go to the 8 XCDs
-  // round-robin by slot, so with c = 8 every item of a pair -- among them the
-  // chunk groups that read the same K/V tiles -- runs on one XCD and shares
-  // its L2, and all of them start within 8 HC slots of each other.
-  const int HC = a.num_kv_heads * a.num_chunk_groups;
+  // Workgroups go to the 8 XCDs round-robin by slot, and each XCD has its own
+  // L2.  Two placements of the HC items of sorted pair pos:
+  //  * Hkv a multiple of 8: item (KV head g, chunk group cg) goes to slot
+  //    pos HC + cg Hkv + g, i.e. to XCD g % 8.  Every KV head stays on one
+  //    XCD, so sequences whose block tables share blocks (parallel samples of
+  //    a prompt) meet in its L2, and so do the chunk groups of one (sequence,
+  //    partition, KV head), which start within HC slots of each other.
+  //  * otherwise the pairs are taken in octets: the octet holding pair pos
+  //    starts at pair pos - r (r = pos % 8) and has c <= 8 pairs, and item x
+  //    < HC of pair pos goes to slot (pos - r) HC + x c + r, so (with c = 8)
+  //    every item of a pair, among them its chunk groups, runs on one XCD.
+  // Prefix pairs (which come with groups only, where HC = Hkv) are placed
+  // alike.  Pair idx holds items idx HC .. idx HC + HC - 1 (a regular pair
+  // (p, b) has idx = p B + b, and the prefix items follow the regular ones),
+  // item idx HC + g NCG + cg being KV head g, chunk group cg.
+  const int Hkv = a.num_kv_heads;
+  const int NCG = a.num_chunk_groups;
+  const int HC = Hkv * NCG;
   for (int idx = tid; idx < pairs; idx += kOrderThreads) {
     const int pos = atomicAdd(&s_count[bucket(idx)], 1);
-    const int r = pos % 8;
-    const int c = min(8, pairs - (pos - r));
-    const size_t base = (size_t)(pos - r) * HC + r;
-    // pair idx holds items idx * HC .. idx * HC + HC - 1: a regular pair (p, b)
-    // has idx = p * B + b, and the prefix items follow the regular ones
-    for (int x = 0; x < HC; ++x) a.order[base + (size_t)x * c] = idx * HC + x;
+    if (Hkv % 8 == 0) {
+      for (int x = 0; x < HC; ++x) a.order[(size_t)pos * HC + x] = idx * HC + (x % Hkv) * NCG + x / Hkv;
+    } else {
+      const int r = pos % 8;
+      const int c = min(8, pairs - (pos - r));
+      const size_t base = (size_t)(pos - r) * HC + r;
+      for (int x = 0; x < HC; ++x) a.order[base + (size_t)x * c] = idx * HC + x;
+    }
   }
 }
 
