@@ -11,7 +11,8 @@
 // per thread.  With k = log2(e) / T, each thread keeps an online state:
 //   m    running max of the raw logits, and mk = fp32(m * k),
 //   s = sum 2^d,  t = sum 2^d d,  d = fma(logit, k, -mk)   (<= ~0),
-// rescaled when m grows.  The fused multiply-add rounds d once, so a large
+// rescaled when m outgrows mk by more than 2^32 in probability (so d <= 32).
+// The fused multiply-add rounds d once, so a large
 // common offset of the logits (+-30000, say) costs no precision, and the
 // rounding of mk shifts every d of the state by the same amount, which
 // cancels in both results below.  t is relative to mk, so t / s stays small
@@ -34,6 +35,7 @@ constexpr int kLpUnroll = 4;  // 16-byte loads in flight per thread
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kFloorMax = -1e30f;  // running max (raw logit units) before any finite logit
+constexpr float kLpSlack = 32.f;     // log2 of the largest probability against a stale max
 
 struct LpState {
   float m, mk, s, t;  // max of the raw logits, fp32(m * k), sum 2^d, sum 2^d d
@@ -99,7 +101,11 @@ __global__ void __launch_bounds__(kLpThreads) logprob_kernel(const LogprobArgs a
 #pragma unroll
     for (int e = 0; e < E; ++e)
       if (e < valid) mx = fmaxf(mx, x[e]);
-    if (mx > st.m) {  // the max grows: rescale the state to the new mk
+    // The max moves only when some lane's logits outgrow it by more than
+    // 2^kLpSlack in probability (a wavefront vote), so the rescale is a rare,
+    // uniform branch; below that, probabilities against the stale max stay
+    // under 2^kLpSlack, far inside fp32.
+    if (__builtin_amdgcn_ballot_w64(mx * k > st.mk + kLpSlack) != 0 && mx > st.m) {
       const float mk = mx * k;
       const float dm = st.mk - mk;
       const float sc = __builtin_amdgcn_exp2f(dm);
