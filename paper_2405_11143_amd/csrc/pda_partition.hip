@@ -57,7 +57,13 @@ struct Staging {
   static constexpr int kStepBlocks = SB;
   static constexpr int TC = WaveAttention<D>::kTileBytes / 16;       // 16-byte pieces per tile
   static constexpr int kLoads = SB * 2 * TC / (kWaves * kWaveSize);  // per thread and step
-  uint4 buf[3][SB][2][TC];
+  static constexpr int kRowPieces = D / 8;                            // 16-byte pieces per V row
+  // A block is its K tile as loaded, then its V tile with 16 bytes of padding
+  // after every row, so that the transposed V reads (16 rows x 32 bytes per
+  // instruction) spread over the LDS banks: 2 passes, the minimum for 512
+  // bytes, instead of 16 rows on the same 8 banks.
+  static constexpr int kBlockPieces = TC + kBlockTokens * (kRowPieces + 1);
+  uint4 buf[3][SB][kBlockPieces];
   int ids[kIdWindow];
 };
 
@@ -87,14 +93,21 @@ template <int D>
 __device__ __forceinline__ void publish(PassShared<D>& sh, const WaveAttention<D>& wave, int w, int lane, int rows) {
   const int n = lane & 15;
   if (n < rows) {
+    if (wave.tr_cols) {  // o[t][i] = column 16t + 4kg + i
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int d0 = wave.d_of(i, 0);  // D = 128: 8 consecutive columns; D = 64: 4
-      *reinterpret_cast<float4*>(&sh.o[w][n][d0]) =
-          make_float4(wave.o[0][i], wave.o[1][i], wave.o[2][i], wave.o[3][i]);
-      if constexpr (D == 128)
-        *reinterpret_cast<float4*>(&sh.o[w][n][d0 + 4]) =
-            make_float4(wave.o[4][i], wave.o[5][i], wave.o[6][i], wave.o[7][i]);
+      for (int t = 0; t < WaveAttention<D>::VT; ++t)
+        *reinterpret_cast<float4*>(&sh.o[w][n][16 * t + 4 * wave.kg]) =
+            make_float4(wave.o[t][0], wave.o[t][1], wave.o[t][2], wave.o[t][3]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int d0 = wave.d_of(i, 0);  // D = 128: 8 consecutive columns; D = 64: 4
+        *reinterpret_cast<float4*>(&sh.o[w][n][d0]) =
+            make_float4(wave.o[0][i], wave.o[1][i], wave.o[2][i], wave.o[3][i]);
+        if constexpr (D == 128)
+          *reinterpret_cast<float4*>(&sh.o[w][n][d0 + 4]) =
+              make_float4(wave.o[4][i], wave.o[5][i], wave.o[6][i], wave.o[7][i]);
+      }
     }
     if (lane < 16) {
       sh.m[w][n] = wave.m_run;
@@ -142,6 +155,7 @@ __device__ void run_staged(WaveAttention<D>& wave, Staging<D, SB>& st, const int
                            const char* kpool, const char* vpool, size_t block_bytes, int num_blocks) {
   using WA = WaveAttention<D>;
   static_assert(SB == 2, "a step is one pair of blocks");
+  wave.tr_cols = true;  // every fold here goes through pv_staged
   constexpr int TC = Staging<D, SB>::TC;
   constexpr int NL = Staging<D, SB>::kLoads;
   const int tid = threadIdx.x;
@@ -166,12 +180,19 @@ __device__ void run_staged(WaveAttention<D>& wave, Staging<D, SB>& st, const int
       r[k] = load_stream(tile_rsrc(pool + (size_t)phys * block_bytes, valid ? WA::kTileBytes : 0), (ci % TC) * 16);
     }
   };
+  // where each of this thread's loads goes in a step's buffer
+  int dst[NL];
+#pragma unroll
+  for (int k = 0; k < NL; ++k) {
+    const int ci = k * kWaves * kWaveSize + tid;  // [block][K or V][piece]
+    const int pc = ci % TC;
+    constexpr int RP = Staging<D, SB>::kRowPieces;
+    dst[k] = ci / (2 * TC) * Staging<D, SB>::kBlockPieces +
+             (((ci / TC) & 1) ? TC + pc / RP * (RP + 1) + pc % RP : pc);
+  }
   auto commit = [&](const uint4(&r)[NL], int buf) {
 #pragma unroll
-    for (int k = 0; k < NL; ++k) {
-      const int ci = k * kWaves * kWaveSize + tid;
-      (&st.buf[buf][0][0][0])[ci] = r[k];
-    }
+    for (int k = 0; k < NL; ++k) (&st.buf[buf][0][0])[dst[k]] = r[k];
   };
   // fold step `step` (in buffer buf) if it is this wavefront's
   auto fold_step = [&](int jw, int jwe, int step, int buf) {
@@ -186,18 +207,14 @@ __device__ void run_staged(WaveAttention<D>& wave, Staging<D, SB>& st, const int
     const int tok0 = j0 * kBlockTokens;
     const int t_stop = j_lim * kBlockTokens;
     const bool tail = tok0 + 2 * kBlockTokens > min(l_first, t_stop);  // wave-uniform
-    uint4 kr[2][WA::NC], vr[2][4];
+    uint4 kr[2][WA::NC];
 #pragma unroll
     for (int k = 0; k < 2; ++k)
 #pragma unroll
-      for (int c = 0; c < WA::NC; ++c) kr[k][c] = st.buf[buf][k][0][(c * 1024) / 16 + wave.lane];
+      for (int c = 0; c < WA::NC; ++c) kr[k][c] = st.buf[buf][k][(c * 1024) / 16 + wave.lane];
     const auto f = wave.template softmax<2>(kr, tok0, L, tail, t_stop);
-#pragma unroll
-    for (int k = 0; k < 2; ++k)  // V read only now: fewer registers live across the softmax
-#pragma unroll
-      for (int e = 0; e < 4; ++e) vr[k][e] = st.buf[buf][k][1][(wave.v_off + e * WA::kRowBytes) / 16];
-    wave.template mask_v<2>(vr, tok0, min(l_vis, t_stop), tail);
-    wave.template pv<2>(vr, f);
+    wave.pv_staged(reinterpret_cast<const uint16_t*>(st.buf[buf][0] + TC),
+                   reinterpret_cast<const uint16_t*>(st.buf[buf][1] + TC), f, tail, tok0, min(l_vis, t_stop));
   };
   for (int jw = J0; jw < J1; jw += kIdWindow) {
     const int jwe = min(J1, jw + kIdWindow);

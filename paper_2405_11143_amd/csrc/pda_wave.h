@@ -95,12 +95,15 @@ struct WaveAttention {
   static constexpr int VT = D / 16;               // P.V MFMA output tiles (16 d each)
   static constexpr int kRowBytes = D * 2;         // one token row of a V tile
   static constexpr int kTileBytes = kBlockTokens * kRowBytes;
+  static constexpr int kStagedRow = D + 8;        // elements per V row staged in LDS (16 bytes of padding)
   static constexpr float kNegInf = -__builtin_huge_valf();
   static constexpr float kFloor = -1e30f;         // running max of a row that has seen no token
   static constexpr float kRescaleSlack = 8.f;     // log2 of the largest unnormalised probability
 
   int lane, n, kg;
   int k_off, v_off;  // this lane's byte offsets in a K / V tile
+  int tr_off;        // this lane's element offset in a V tile for transposed reads (pv_staged)
+  bool tr_cols;      // o[t][i] holds output column 16t + 4kg + i (pv_staged) instead of d_of(i, t)
   int lim_off;       // this lane's query row sees tokens t < L - lim_off
   float scale_log2;
   bool bad;          // a block id outside the pool was met (never dereferenced)
@@ -114,6 +117,8 @@ struct WaveAttention {
     kg = lane >> 4;
     k_off = 16 * lane;
     v_off = 4 * kg * kRowBytes + 16 * (n % (D / 8));
+    tr_off = (4 * kg + n / 4) * kStagedRow + 4 * (n % 4);
+    tr_cols = false;
   }
 
   // The output element d of this lane's row held in accumulator t, register i.
@@ -296,6 +301,54 @@ struct WaveAttention {
         o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
             a, __builtin_bit_cast(bf16x8_t, make_uint4(f.lw[0], f.lw[1], f.lw[2], f.lw[3])), o[t], 0, 0, 0);
       }
+    }
+  }
+
+  // O^T += V^T P^T for a pair of blocks whose V tiles (16 rows of D bf16,
+  // kStagedRow elements apart) are in LDS at va and vb, with D/16 MFMA
+  // f32_16x16x32_bf16 per half of P.
+  // The A fragments come straight from LDS through transposed reads
+  // (ds_read_b64_tr_b16): within each group of 16 lanes, source lane s reads
+  // 4 consecutive elements at its own address, and lane m receives element
+  // m % 4 of source lanes m / 4, m / 4 + 4, m / 4 + 8, m / 4 + 12.  With
+  // source lane (kg, s) pointing at row 4kg + s / 4, columns 16t + 4 (s % 4),
+  // lane (kg, m) receives V[4kg + j][16t + m], j = 0..3: tokens 4kg .. 4kg+3,
+  // as its probabilities, and column 16t + m, so the accumulators take the
+  // tr_cols assignment.  No v_perm is needed.  In a tail pair, fragment
+  // elements of tokens at or past l_vis are zeroed.
+  __device__ __forceinline__ void pv_staged(const uint16_t* va, const uint16_t* vb, const PFrag<2>& f, bool tail,
+                                            int tok0, int l_vis) {
+    typedef short v4s_t __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) v4s_t lds_v4s_t;
+    uint4 aw[VT];
+#pragma unroll
+    for (int t = 0; t < VT; ++t) {
+      const uint2 x = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                                    (lds_v4s_t*)(va + tr_off + 16 * t)));
+      const uint2 y = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                                    (lds_v4s_t*)(vb + tr_off + 16 * t)));
+      aw[t] = make_uint4(x.x, x.y, y.x, y.y);
+    }
+    if (tail) {
+      asm volatile("");  // a branch, as in softmax
+      unsigned mw[4];
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int t0 = tok0 + kBlockTokens * b + 4 * kg + 2 * h;
+          mw[2 * b + h] = (t0 < l_vis ? 0x0000ffffu : 0u) | (t0 + 1 < l_vis ? 0xffff0000u : 0u);
+        }
+#pragma unroll
+      for (int t = 0; t < VT; ++t) aw[t] = make_uint4(aw[t].x & mw[0], aw[t].y & mw[1], aw[t].z & mw[2], aw[t].w & mw[3]);
+    }
+    const bf16x8_t bh = __builtin_bit_cast(bf16x8_t, make_uint4(f.hw[0], f.hw[1], f.hw[2], f.hw[3]));
+    const bf16x8_t bl = __builtin_bit_cast(bf16x8_t, make_uint4(f.lw[0], f.lw[1], f.lw[2], f.lw[3]));
+#pragma unroll
+    for (int t = 0; t < VT; ++t) {
+      const bf16x8_t a = __builtin_bit_cast(bf16x8_t, aw[t]);
+      o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bh, o[t], 0, 0, 0);
+      o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bl, o[t], 0, 0, 0);
     }
   }
 
