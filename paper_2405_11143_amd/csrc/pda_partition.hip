@@ -1,5 +1,6 @@
 // Pass 1: one workgroup per work item, taken in the order pda_order.hip
-// computed (largest first).  Two kinds of items share the launch:
+// computed (largest first, placed for the XCDs), or in natural order when
+// every item runs at once.  Two kinds of items share the launch:
 //
 // Regular items: (partition of a context, sequence, KV head, group of up to
 // 4 chunks of new query tokens).  A chunk holds up to 16 / G consecutive new
@@ -10,9 +11,9 @@
 // t < L - n + 1 + i.  The 4 wavefronts take the item's chunks first and
 // slices of its blocks second (1 chunk: 4 contiguous runs; 2: every other
 // step of 2 blocks each; 3-4: every block), so the chunks of one item read
-// each tile on one compute unit.  Each chunk keeps
-// its own causal range and partition count.  With shared-prefix groups, a
-// sequence's regular items cover only the tokens after its group's prefix.
+// each tile on one compute unit.  Each chunk keeps its own causal range and
+// partition count.  With shared-prefix groups, a sequence's regular items
+// cover only the tokens after its group's prefix.
 //
 // Prefix items: (shared-prefix group, prefix partition, KV head).  All
 // members of a group read the same prefix blocks (parallel sampling, Section
@@ -24,11 +25,11 @@
 // WaveAttention (pda_wave.h), tiles straight into registers.  With several
 // tiles, the workgroup stages every block's K and V tiles through LDS once
 // (2 blocks per step, two steps in flight) and each wavefront folds them
-// from there for its own rows, a pair of blocks at a time.  The states of the wavefronts that share a row are
-// merged through LDS in a fixed order.  A regular item with no prefix that sees a
-// single partition writes its final output rows; every other item leaves a
-// partial softmax state (max, denominator, unnormalised output) for the
-// merge pass.  Nothing depends on physical block ids or on timing, so results
+// from there for its own rows, a pair of blocks at a time.  The states of
+// the wavefronts that share a row are merged through LDS in a fixed order.
+// A regular item with no prefix that sees a single partition writes its
+// final output rows; every other item leaves a partial softmax state (max,
+// denominator, unnormalised output) for the merge pass.  Nothing depends on physical block ids or on timing, so results
 // are bit-for-bit reproducible and independent of block placement.
 #include "pda_wave.h"
 
@@ -59,9 +60,10 @@ struct Staging {
   static constexpr int kLoads = SB * 2 * TC / (kWaves * kWaveSize);  // per thread and step
   static constexpr int kRowPieces = D / 8;                            // 16-byte pieces per V row
   // A block is its K tile as loaded, then its V tile with 16 bytes of padding
-  // after every row, so that the transposed V reads (16 rows x 32 bytes per
-  // instruction) spread over the LDS banks: 2 passes, the minimum for 512
-  // bytes, instead of 16 rows on the same 8 banks.
+  // after every row: the transposed V reads take 32 bytes from each of 16
+  // rows per instruction, and with the padding those rows start 4 banks
+  // apart instead of all on the same 8 banks (unpadded the staged step ran
+  // 10% slower).
   static constexpr int kBlockPieces = TC + kBlockTokens * (kRowPieces + 1);
   uint4 buf[3][SB][kBlockPieces];
   int ids[kIdWindow];
@@ -70,10 +72,10 @@ struct Staging {
 // Which paths a launch compiles.  A launch whose items all have one tile
 // (every decode step without shared-prefix groups) compiles the register
 // path only (135 VGPRs at D = 128, 33 KiB of LDS); otherwise both paths are
-// compiled (165 VGPRs, 49 KiB).  Staging takes 2 blocks per step, so three
-// staging buffers (48 KiB at D = 128) still leave room for 3 workgroups per
-// compute unit; 4 blocks per step at 2 workgroups per compute unit measured
-// slower on MI355X.
+// compiled (168 VGPRs, 50.5 KiB).  Staging takes 2 blocks per step, so three
+// staging buffers (49.5 KiB at D = 128) still leave room for 3 workgroups
+// per compute unit; 4 blocks per step at 2 workgroups per compute unit
+// measured slower on MI355X.
 constexpr int kModeRegister = 1, kModeMixed = 3;
 constexpr int kStepBlocks = 2;
 

@@ -35,11 +35,11 @@
 //    nor the rescale; the result is the same softmax.  Blocks that every row
 //    sees whole take a path without any masking.
 //  * P V, transposed, on MFMA.  O^T = V^T P^T is D/16 MFMA f32_16x16x16_bf16
-//    per block and half (or D/16 f32_16x16x32_bf16 per pair of blocks): the
-//    probabilities of lane (kg, n) are already the B fragment (column n,
-//    k-group kg), and the A fragment of lane (kg, n) is 4 tokens x 1 column
-//    of the V tile (of each block), picked out of the 16-byte row pieces the
-//    lane loaded.  Each probability p is split into bf16 hi = p with the
+//    per block and half (or D/16 f32_16x16x32_bf16 per pair of blocks staged
+//    in LDS): the probabilities of lane (kg, n) are already the B fragment
+//    (column n, k-group kg), and the A fragment of lane (kg, n) is 4 tokens
+//    x 1 column of the V tile (of each block), picked out of the 16-byte row
+//    pieces the lane loaded, or read transposed from LDS (pv_staged).  Each probability p is split into bf16 hi = p with the
 //    low 16 bits cleared and lo = bf16(p - hi), and both halves go through
 //    the MFMA, so P keeps about 16 significant bits (relative error below
 //    2^-15) instead of bf16's 8.  The output of row n stays in the lanes of
@@ -261,46 +261,29 @@ struct WaveAttention {
 
   // Zero the V rows at or past `l_vis` (no row of the chunk sees them), so
   // whatever those slots hold never meets a zero probability.
-  template <int NB>
-  __device__ __forceinline__ void mask_v(uint4 (&vr)[NB][4], int tok0, int l_vis, bool tail) const {
+  __device__ __forceinline__ void mask_v(uint4 (&vr)[4], int tok0, int l_vis, bool tail) const {
     if (tail) {
       asm volatile("");  // a branch, as in softmax
 #pragma unroll
-      for (int b = 0; b < NB; ++b)
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (tok0 + kBlockTokens * b + 4 * kg + e >= l_vis) vr[b][e] = make_uint4(0u, 0u, 0u, 0u);
+      for (int e = 0; e < 4; ++e)
+        if (tok0 + 4 * kg + e >= l_vis) vr[e] = make_uint4(0u, 0u, 0u, 0u);
     }
   }
 
-  // O^T += V^T P^T.  One block takes D/16 MFMA f32_16x16x16_bf16 per half of
-  // P; two blocks take D/16 MFMA f32_16x16x32_bf16 per half, where k-group kg
-  // of the contraction holds tokens 4kg .. 4kg+3 of the first block, then the
-  // same slots of the second, in both operands.
-  template <int NB>
-  __device__ __forceinline__ void pv(const uint4 (&vr)[NB][4], const PFrag<NB>& f) {
+  // O^T += V^T P^T for one block whose V rows 4kg .. 4kg+3 this lane holds
+  // (16 bytes of each): D/16 MFMA f32_16x16x16_bf16 per half of P, the A
+  // fragment of tile t picked out of those row pieces.
+  __device__ __forceinline__ void pv(const uint4 (&vr)[4], const PFrag<1>& f) {
+    const shortx4_t bh = __builtin_bit_cast(shortx4_t, make_uint2(f.hw[0], f.hw[1]));
+    const shortx4_t bl = __builtin_bit_cast(shortx4_t, make_uint2(f.lw[0], f.lw[1]));
 #pragma unroll
     for (int t = 0; t < VT; ++t) {
       const bool hi_half = t & 1;
-      unsigned aw[2 * NB];  // this lane's column of tile t, token rows 0..3 of each block
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        aw[2 * b] = pack_halves(col_dword(vr[b], 0, t), col_dword(vr[b], 1, t), hi_half);
-        aw[2 * b + 1] = pack_halves(col_dword(vr[b], 2, t), col_dword(vr[b], 3, t), hi_half);
-      }
-      if constexpr (NB == 1) {
-        const shortx4_t a = __builtin_bit_cast(shortx4_t, make_uint2(aw[0], aw[1]));
-        o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
-            a, __builtin_bit_cast(shortx4_t, make_uint2(f.hw[0], f.hw[1])), o[t], 0, 0, 0);
-        o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
-            a, __builtin_bit_cast(shortx4_t, make_uint2(f.lw[0], f.lw[1])), o[t], 0, 0, 0);
-      } else {
-        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, make_uint4(aw[0], aw[1], aw[2], aw[3]));
-        o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-            a, __builtin_bit_cast(bf16x8_t, make_uint4(f.hw[0], f.hw[1], f.hw[2], f.hw[3])), o[t], 0, 0, 0);
-        o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-            a, __builtin_bit_cast(bf16x8_t, make_uint4(f.lw[0], f.lw[1], f.lw[2], f.lw[3])), o[t], 0, 0, 0);
-      }
+      const shortx4_t a = __builtin_bit_cast(
+          shortx4_t, make_uint2(pack_halves(col_dword(vr, 0, t), col_dword(vr, 1, t), hi_half),
+                                pack_halves(col_dword(vr, 2, t), col_dword(vr, 3, t), hi_half)));
+      o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, bh, o[t], 0, 0, 0);
+      o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, bl, o[t], 0, 0, 0);
     }
   }
 
@@ -358,15 +341,13 @@ struct WaveAttention {
   // sees a token at or above it).
   __device__ __forceinline__ void process(const uint4 (&kr)[NC], uint4 (&vr)[4], int tok0, int L, int l_first,
                                           int l_vis) {
-    uint4 k1[1][NC], v1[1][4];
+    uint4 k1[1][NC];
 #pragma unroll
     for (int c = 0; c < NC; ++c) k1[0][c] = kr[c];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) v1[0][e] = vr[e];
     const bool tail = tok0 + kBlockTokens > l_first;  // wave-uniform
     const PFrag<1> f = softmax<1>(k1, tok0, L, tail);
-    mask_v<1>(v1, tok0, l_vis, tail);
-    pv<1>(v1, f);
+    mask_v(vr, tok0, l_vis, tail);
+    pv(vr, f);
   }
 
   // Stream blocks [j0, j1) of one sequence: block ids in `table_row`, tiles of
