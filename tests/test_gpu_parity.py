@@ -207,3 +207,30 @@ def test_full_config_sampled(dev, name):
     ref = oracle.decode_rows(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
                              st.context_lens, st.scale, rows, threads=THREADS)
     check(got[rows[:, 0], rows[:, 1]], ref, f"{name} sampled rows")
+
+
+@pytest.mark.parametrize("Hq,Hkv,n", [(8, 1, 1), (16, 2, 1), (8, 1, 12), (32, 8, 24)], ids=str)
+def test_work_order_placements(dev, Hq, Hkv, n):
+    """Steps with more work items than the GPU runs at once, so the work-order
+    kernel runs: with fewer than 8 KV heads (pairs placed in octets, the last
+    one partial: 301 sequences x 10 partitions) and with 8 (KV heads kept on
+    their XCD), with one and with two groups of query chunks per item."""
+    r = np.random.default_rng(Hq * 7 + n)
+    lens = [int(x) for x in r.integers(n, 600, 301)]
+    st = W.custom_structure(len(lens), Hq, Hkv, 128, lens, seed=60 + n)
+    _, k, v = W.fill_values(st, dev, fill="nan")
+    q = W.fill_multi_q(st, n, dev)
+    tp = 64
+    plan = pda_plan(make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq,
+                                 st.max_context_len, tp, num_query_tokens=n))
+    G = Hq // Hkv
+    chunks = -(-n // max(1, 16 // G))
+    pairs = plan["num_partitions"] * st.B
+    items = pairs * Hkv * -(-chunks // 4)
+    assert items > 768 and (Hkv % 8 == 0 or pairs % 8 != 0), (items, pairs)
+    bt, ln = gpu_tensors(st, dev)
+    got = pda_decode(q, k, v, bt, ln, st.scale, max_context_len=st.max_context_len,
+                     partition_tokens=tp).cpu().numpy()
+    ref = oracle.decode_multi(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
+                              st.context_lens, st.scale, threads=THREADS)
+    check(got, ref, f"order placement Hq={Hq} Hkv={Hkv} n={n} plan={plan}")
