@@ -43,6 +43,9 @@ struct PassShared {
   float o[kWaves][kRows][D];
   float m[kWaves][kRows];
   float l[kWaves][kRows];
+  float sc[kWaves][kRows];    // per wavefront and row: 2^(m - M), M the row's max over its slices
+  float mx[kWaves][kRows];    // per tile and row: M
+  float lsum[kWaves][kRows];  // per tile and row: sum of sc * l over the slices
   int bad[kWaves];
 };
 
@@ -119,21 +122,42 @@ __device__ __forceinline__ void publish(PassShared<D>& sh, const WaveAttention<D
   if (lane == 0) sh.bad[w] = wave.bad ? 1 : 0;
 }
 
-// Combine, for one output element, the states of wavefronts w0, w0 + step,
-// ... (count of them) at tile row n: returns (acc, M, lsum).
+// The weights that merge the slices of each tile, once per row: for tile t
+// (wavefronts t, t + ntile, ... : `slices` of them) and row h, the max M of
+// their running maxima, each one's scale 2^(m - M) (0 for a wavefront that
+// saw no token of the row) and the scaled sum of their denominators, all in
+// a fixed order.  Rows past a tile's last one hold values nobody reads.
+// Ends with a barrier.
 template <int D>
-__device__ __forceinline__ void combine(const PassShared<D>& sh, int w0, int step, int count, int n, int d,
-                                        float& acc, float& M, float& lsum) {
-  M = WaveAttention<D>::kFloor;
-  for (int x = 0; x < count; ++x) M = fmaxf(M, sh.m[w0 + x * step][n]);
-  acc = 0.f;
-  lsum = 0.f;
-  for (int x = 0; x < count; ++x) {
-    const int w = w0 + x * step;
-    const float sc = exp2_fast(sh.m[w][n] - M);  // 0 for a wavefront without tokens of this row
-    acc = fmaf(sc, sh.o[w][n][d], acc);
-    lsum = fmaf(sc, sh.l[w][n], lsum);
+__device__ __forceinline__ void row_weights(PassShared<D>& sh, int ntile, int slices) {
+  const int tid = threadIdx.x;
+  if (tid < ntile * kRows) {
+    const int t = tid / kRows;
+    const int h = tid % kRows;
+    float M = WaveAttention<D>::kFloor;
+    for (int x = 0; x < slices; ++x) M = fmaxf(M, sh.m[t + x * ntile][h]);
+    float lsum = 0.f;
+    for (int x = 0; x < slices; ++x) {
+      const int w = t + x * ntile;
+      const float sc = exp2_fast(sh.m[w][h] - M);
+      sh.sc[w][h] = sc;
+      lsum = fmaf(sc, sh.l[w][h], lsum);
+    }
+    sh.mx[t][h] = M;
+    sh.lsum[t][h] = lsum;
   }
+  __syncthreads();
+}
+
+// One merged output element of tile t, row h, column d (row_weights first).
+template <int D>
+__device__ __forceinline__ float combine(const PassShared<D>& sh, int t, int ntile, int slices, int h, int d) {
+  float acc = 0.f;
+  for (int x = 0; x < slices; ++x) {
+    const int w = t + x * ntile;
+    acc = fmaf(sh.sc[w][h], sh.o[w][h][d], acc);
+  }
+  return acc;
 }
 
 __device__ __forceinline__ void store_partial(const StepArgs& a, size_t slot, int d, int D, float acc, float M,
@@ -341,6 +365,7 @@ __device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item)
   wave.finish();
   publish(sh, wave, w, lane, rows);
   __syncthreads();
+  row_weights(sh, ntile, slices);
 
   // ---- per chunk: merge its slices in a fixed order; final rows or partial states ----
   int any_bad = 0;
@@ -356,8 +381,8 @@ __device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item)
     for (int idx = tid; idx < crows * D; idx += kWaves * kWaveSize) {
       const int h = idx / D;
       const int d = idx % D;
-      float acc, M, lsum;
-      combine(sh, t, ntile, slices, h, d, acc, M, lsum);
+      float acc = combine(sh, t, ntile, slices, h, d);
+      const float M = sh.mx[t][h], lsum = sh.lsum[t][h];
       if (any_bad) acc = __builtin_nanf("");
       const size_t row = ((size_t)b * nq + ci0 + h / G) * Hq + (size_t)g * G + h % G;
       if (single)
@@ -421,6 +446,7 @@ __device__ void prefix_item(const StepArgs& a, PassLds<D, MODE>& lds, int pitem)
   wave.finish();
   publish(sh, wave, w, lane, tile_rows);
   __syncthreads();
+  row_weights(sh, ntile, slices);
 
   // ---- merge the slices of each tile in a fixed order; every member row gets a partial state ----
   int any_bad = 0;
@@ -429,8 +455,9 @@ __device__ void prefix_item(const StepArgs& a, PassLds<D, MODE>& lds, int pitem)
   for (int idx = tid; idx < rows * D; idx += kWaves * kWaveSize) {
     const int rr = idx / D;
     const int d = idx % D;
-    float acc, M, lsum;
-    combine(sh, rr / kRows, ntile, slices, rr % kRows, d, acc, M, lsum);
+    const int t = rr / kRows, h = rr % kRows;
+    float acc = combine(sh, t, ntile, slices, h, d);
+    const float M = sh.mx[t][h], lsum = sh.lsum[t][h];
     if (any_bad) acc = __builtin_nanf("");
     const size_t row = (size_t)(first + rr / G) * Hq + (size_t)g * G + rr % G;
     store_partial(a, row * a.slots_per_row + pp, d, D, acc, M, lsum);
