@@ -45,8 +45,9 @@
  * Long contexts are split into partitions of `partition_tokens` tokens that
  * are processed independently; a second pass merges the partial softmax
  * states.  Pass 1 runs one workgroup per (partition, sequence, KV head,
- * chunk of at most 16 / G new tokens), largest partition first (a small
- * kernel sorts the items by size on the GPU).  The partition size depends
+ * group of up to 4 chunks of at most 16 / G new tokens each), largest
+ * partition first (a small kernel sorts the items by size on the GPU; it is
+ * skipped when every item runs at once).  The partition size depends
  * only on the problem descriptor and the arithmetic of an item only on its
  * data, never on physical block ids, timing or the order the items run in,
  * so for a given descriptor the output is bit-for-bit reproducible and
@@ -128,7 +129,8 @@ int pda_decode(const pda_problem *prob, const void *q, const void *k_cache, cons
                const int32_t *block_table, const int32_t *context_lens, float scale, float *out,
                void *workspace, size_t workspace_bytes, hipStream_t stream);
 
-/* Pass 1 alone (the work-order kernel, then one workgroup per partition):
+/* Pass 1 alone (the work-order kernel when needed, then one workgroup per
+ * work item):
  * rows that see a single partition, and rows that see no token, are final
  * in `out` after this pass; the others are left as partial softmax states in
  * `workspace`. */

@@ -24,7 +24,8 @@ struct StepArgs {
   const int32_t* table;    // int32 [B][max_blocks_per_seq]
   const int32_t* lens;     // int32 [B]
   float* out;              // fp32 [B][n][Hq][D]
-  int32_t* order;          // int32 [items]: work items, largest partition first (null: natural order)
+  int32_t* order;          // int32 [items]: work item of each workgroup, largest partition first,
+                           // placed for the XCDs (null: workgroup i runs item i)
   float* part_o;           // fp32 [B*n*Hq*slots_per_row][D]  unnormalised partition outputs
   float* part_m;           // fp32 [B*n*Hq*slots_per_row]     partition reference max, log2 domain
   float* part_l;           // fp32 [B*n*Hq*slots_per_row]     partition softmax denominators
@@ -37,7 +38,7 @@ struct StepArgs {
   int32_t max_blocks_per_seq;
   int32_t max_context_len;
   int32_t num_query_tokens;  // n
-  int32_t query_chunk;       // new tokens per work item: min(n, 16 / G)
+  int32_t query_chunk;       // new tokens per query chunk (one 16-row tile): min(n, 16 / G)
   int32_t num_query_chunks;  // NQC = ceil(n / query_chunk)
   int32_t num_chunk_groups;  // NCG = ceil(NQC / 4): chunks of one work item share its K/V tiles
   int32_t partition_tokens;  // T_p, multiple of 16
@@ -53,7 +54,7 @@ struct StepArgs {
   int32_t max_prefix_len;           // bound on group_prefix_len, multiple of 16
   int32_t prefix_partitions;        // Pp = ceil(max_prefix_len / T_p)
   int32_t slots_per_row;            // Pp + P partial states per output row (P when no groups)
-  int32_t num_regular_items;        // items below this index are (partition, sequence, KV head, chunk)
+  int32_t num_regular_items;        // items below this index are (partition, sequence, KV head, chunk group)
 };
 
 // Prefix tokens of sequence b's group (0 without groups); pass 1 and the

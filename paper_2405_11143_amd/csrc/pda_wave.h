@@ -66,10 +66,6 @@ __device__ __forceinline__ float mul_rounded(float x, float y) {
   return x * y;
 }
 
-__device__ __forceinline__ float readlane_f(float x, int lane) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), lane));
-}
-
 // Raw buffer resource over `bytes` bytes at `base` (gfx9 dword-3 default:
 // 32-bit raw accesses, bounds-checked against num_records).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const void* base, int bytes) {
