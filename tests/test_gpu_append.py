@@ -64,15 +64,24 @@ def check(got, ref, what):
     assert np.isfinite(got).all() and err.max() <= MAX_ABS and err.mean() <= MEAN_ABS, what
 
 
+GRAPH_CASES = {  # (Hq, Hkv, D, final context lengths, partition_tokens)
+    # every work item runs at once: append + partition kernel only
+    "small": (8, 2, 64, [50, 100, 17, 230], 0),
+    # 64 sequences in 16-token partitions: append, work order, partition and merge kernels
+    "split": (32, 8, 128, [int(x) for x in np.random.default_rng(3).integers(40, 700, 64)], 16),
+}
+
+
+@pytest.mark.parametrize("case", sorted(GRAPH_CASES))
 @pytest.mark.parametrize("n", [1, 4])
-def test_step_graph_replays(dev, n):
+def test_step_graph_replays(dev, n, case):
     """Replays of one captured step, each after new queries, new K/V rows and
     longer contexts were written by eager torch work, against the eager step
     (bitwise) and the oracle."""
-    growth = np.array([[s % 2, 1, 2, 3] for s in range(4)], dtype=np.int32)  # per replay and sequence
-    final = [50, 100, 17, 230]
-    st = W.custom_structure(4, 8, 2, 64, final, seed=77)
+    Hq, Hkv, D, final, tp = GRAPH_CASES[case]
+    st = W.custom_structure(len(final), Hq, Hkv, D, final, seed=77)
     B = st.B
+    growth = np.array([[(s + b) % 4 for b in range(B)] for s in range(4)], dtype=np.int32)  # per replay and sequence
     lens0 = (np.asarray(final) - growth.sum(axis=0)).astype(np.int32)  # every context stays in its blocks
     bt = torch.from_numpy(st.block_table).to(dev)
     lens = torch.from_numpy(lens0).to(dev)
@@ -81,7 +90,8 @@ def test_step_graph_replays(dev, n):
     q = torch.empty((B, n, st.Hq, st.D), dtype=torch.bfloat16, device=dev)
     kn = torch.empty((B, n, st.Hkv, st.D), dtype=torch.bfloat16, device=dev)
     vn = torch.empty_like(kn)
-    graph = StepGraph(q, kn, vn, k_g, v_g, bt, lens, st.scale, max_context_len=st.max_context_len)
+    graph = StepGraph(q, kn, vn, k_g, v_g, bt, lens, st.scale, max_context_len=st.max_context_len,
+                      partition_tokens=tp)
     try:
         for step in range(4):
             # eager work between replays: new inputs, one more token per sequence
@@ -95,13 +105,15 @@ def test_step_graph_replays(dev, n):
             torch.cuda.synchronize()
             # the same step eagerly
             pda_append_kv(kn, vn, bt, lens, k_e, v_e, max_context_len=st.max_context_len, num_q_heads=st.Hq)
-            out_e = pda_decode(q, k_e, v_e, bt, lens, st.scale, max_context_len=st.max_context_len)
+            out_e = pda_decode(q, k_e, v_e, bt, lens, st.scale, max_context_len=st.max_context_len,
+                               partition_tokens=tp)
             torch.cuda.synchronize()
             assert torch.equal(k_g.view(torch.int16), k_e.view(torch.int16)), f"replay {step}: K cache"
             assert torch.equal(v_g.view(torch.int16), v_e.view(torch.int16)), f"replay {step}: V cache"
             assert torch.equal(out_g, out_e), f"replay {step}: output differs from the eager step"
             lens_h = lens.cpu().numpy()
-            ref = oracle.decode_multi(bits16(q), bits16(k_g), bits16(v_g), st.block_table, lens_h, st.scale)
-            check(out_g.cpu().numpy(), ref, f"graph replay {step} n={n}")
+            ref = oracle.decode_multi(bits16(q), bits16(k_g), bits16(v_g), st.block_table, lens_h, st.scale,
+                                      threads=16)
+            check(out_g.cpu().numpy(), ref, f"graph replay {step} n={n} {case}")
     finally:
         graph.close()
