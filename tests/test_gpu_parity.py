@@ -234,3 +234,28 @@ def test_work_order_placements(dev, Hq, Hkv, n):
     ref = oracle.decode_multi(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
                               st.context_lens, st.scale, threads=THREADS)
     check(got, ref, f"order placement Hq={Hq} Hkv={Hkv} n={n} plan={plan}")
+
+
+@pytest.mark.parametrize("n,partition_tokens", [(1, 0), (1, 64), (8, 0), (16, 64)], ids=str)
+def test_out_of_range_block_ids_give_nan_rows(dev, n, partition_tokens):
+    """A block-table entry outside the pool (within a context) is never
+    dereferenced: every output row of that sequence comes out NaN, and the
+    other sequences are unaffected.  Covers the register path (one tile per
+    work item) and the staged path (8 and 16 new tokens at G = 4), with and
+    without split contexts."""
+    lens = [100, 300, 50, 1000, 777]
+    st = W.custom_structure(len(lens), 32, 8, 128, lens, seed=90 + n)
+    _, k, v = W.fill_values(st, dev, fill="nan")
+    q = W.fill_multi_q(st, n, dev)
+    table = st.block_table.copy()
+    table[1, 3] = st.num_blocks + 7
+    table[3, 40] = -1
+    bt = torch.from_numpy(table).to(dev)
+    ln = torch.from_numpy(st.context_lens).to(dev)
+    got = pda_decode(q, k, v, bt, ln, st.scale, max_context_len=st.max_context_len,
+                     partition_tokens=partition_tokens).cpu().numpy()
+    assert np.isnan(got[1]).all() and np.isnan(got[3]).all()
+    ok = [0, 2, 4]
+    ref = oracle.decode_multi(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
+                              st.context_lens, st.scale, threads=THREADS)
+    check(got[ok], ref[ok], f"sequences with valid tables n={n} Tp={partition_tokens}")
