@@ -238,9 +238,11 @@ __device__ void run_staged(WaveAttention<D>& wave, Staging<D, SB>& st, const int
     for (int k = 0; k < 2; ++k)
 #pragma unroll
       for (int c = 0; c < WA::NC; ++c) kr[k][c] = st.buf[buf][k][(c * 1024) / 16 + wave.lane];
+    uint4 aw[WA::VT];
+    wave.v_frags(reinterpret_cast<const uint16_t*>(st.buf[buf][0] + TC),
+                 reinterpret_cast<const uint16_t*>(st.buf[buf][1] + TC), aw);
     const auto f = wave.template softmax<2>(kr, tok0, L, tail, t_stop);
-    wave.pv_staged(reinterpret_cast<const uint16_t*>(st.buf[buf][0] + TC),
-                   reinterpret_cast<const uint16_t*>(st.buf[buf][1] + TC), f, tail, tok0, min(l_vis, t_stop));
+    wave.pv_staged(aw, f, tail, tok0, min(l_vis, t_stop));
   };
   for (int jw = J0; jw < J1; jw += kIdWindow) {
     const int jwe = min(J1, jw + kIdWindow);

@@ -283,23 +283,20 @@ struct WaveAttention {
     }
   }
 
-  // O^T += V^T P^T for a pair of blocks whose V tiles (16 rows of D bf16,
-  // kStagedRow elements apart) are in LDS at va and vb, with D/16 MFMA
-  // f32_16x16x32_bf16 per half of P.
-  // The A fragments come straight from LDS through transposed reads
-  // (ds_read_b64_tr_b16): within each group of 16 lanes, source lane s reads
-  // 4 consecutive elements at its own address, and lane m receives element
-  // m % 4 of source lanes m / 4, m / 4 + 4, m / 4 + 8, m / 4 + 12.  With
-  // source lane (kg, s) pointing at row 4kg + s / 4, columns 16t + 4 (s % 4),
-  // lane (kg, m) receives V[4kg + j][16t + m], j = 0..3: tokens 4kg .. 4kg+3,
-  // as its probabilities, and column 16t + m, so the accumulators take the
-  // tr_cols assignment.  No v_perm is needed.  In a tail pair, fragment
-  // elements of tokens at or past l_vis are zeroed.
-  __device__ __forceinline__ void pv_staged(const uint16_t* va, const uint16_t* vb, const PFrag<2>& f, bool tail,
-                                            int tok0, int l_vis) {
+  // The V^T A fragments of a pair of blocks whose V tiles (16 rows of D
+  // bf16, kStagedRow elements apart) are in LDS at va and vb, read straight
+  // from LDS through transposed reads (ds_read_b64_tr_b16): within each group
+  // of 16 lanes, source lane s reads 4 consecutive elements at its own
+  // address, and lane m receives element m % 4 of source lanes m / 4,
+  // m / 4 + 4, m / 4 + 8, m / 4 + 12.  With source lane (kg, s) pointing at
+  // row 4kg + s / 4, columns 16t + 4 (s % 4), lane (kg, m) receives
+  // V[4kg + j][16t + m], j = 0..3: tokens 4kg .. 4kg+3, as its
+  // probabilities, and column 16t + m, so the accumulators take the tr_cols
+  // assignment.  No v_perm is needed.  The caller reads them before the
+  // pair's softmax, so that the LDS latency overlaps it.
+  __device__ __forceinline__ void v_frags(const uint16_t* va, const uint16_t* vb, uint4 (&aw)[VT]) const {
     typedef short v4s_t __attribute__((ext_vector_type(4)));
     typedef __attribute__((address_space(3))) v4s_t lds_v4s_t;
-    uint4 aw[VT];
 #pragma unroll
     for (int t = 0; t < VT; ++t) {
       const uint2 x = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
@@ -308,6 +305,12 @@ struct WaveAttention {
                                                     (lds_v4s_t*)(vb + tr_off + 16 * t)));
       aw[t] = make_uint4(x.x, x.y, y.x, y.y);
     }
+  }
+
+  // O^T += V^T P^T for a staged pair (fragments from v_frags), with D/16
+  // MFMA f32_16x16x32_bf16 per half of P.  In a tail pair, fragment elements
+  // of tokens at or past l_vis are zeroed first.
+  __device__ __forceinline__ void pv_staged(uint4 (&aw)[VT], const PFrag<2>& f, bool tail, int tok0, int l_vis) {
     if (tail) {
       asm volatile("");  // a branch, as in softmax
       unsigned mw[4];
