@@ -419,7 +419,7 @@ def main(argv=None):
                     help="> 0: split-K partition size in tokens (0: the library's choice)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-min-seconds", type=float, default=10.0)
-    ap.add_argument("--cpu-max-reps", type=int, default=20)
+    ap.add_argument("--cpu-max-reps", type=int, default=60)
     ap.add_argument("--pass1-only", action="store_true",
                     help="time and launch only the pass-1 kernels (for counter runs)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
