@@ -192,7 +192,8 @@ def test_empty_and_nonpositive_lengths(dev):
 
 # ------------------------------------------------- full-size configurations --
 
-@pytest.mark.parametrize("name", ["llama3_8b", "long_cot", "llama3_70b_tp8", "shared_prefix"])
+@pytest.mark.parametrize("name", ["llama3_8b", "long_cot", "llama3_70b_tp8", "shared_prefix", "r1_qwen7b",
+                                  "r1_qwen14b"])
 def test_full_config_sampled(dev, name):
     st = W.make_structure(name)
     plan = pda_plan(make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq,

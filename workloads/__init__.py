@@ -68,6 +68,14 @@ CONFIGS: Dict[str, dict] = {
                           lens=("uniform", 256, 8192), pool_slack=1.1,
                           desc="shared-prefix rollouts: 32 prompts x 8 samples, 1024-token shared prefix "
                                "+ response ~U[256,8192], 32/8 heads, D=128"),
+    # The attention shapes of the distilled Qwen models the paper trains on
+    # (Table 1): a prompt of up to 1024 tokens plus up to 8K generated ones.
+    "r1_qwen7b": dict(index=5, B=256, Hq=28, Hkv=4, D=128, lens=("uniform", 1024, 9216), pool_slack=1.1,
+                      desc="long-CoT rollout, DeepSeek-R1-Distill-Qwen-7B attention shape: B=256, "
+                           "28 q / 4 kv heads (G=7), D=128, L~U[1024,9216]"),
+    "r1_qwen14b": dict(index=6, B=256, Hq=40, Hkv=8, D=128, lens=("uniform", 1024, 9216), pool_slack=1.1,
+                       desc="long-CoT rollout, DeepSeek-R1-Distill-Qwen-14B attention shape: B=256, "
+                            "40 q / 8 kv heads (G=5), D=128, L~U[1024,9216]"),
 }
 CONFIG_NAMES = sorted(CONFIGS, key=lambda n: CONFIGS[n]["index"])
 
