@@ -72,11 +72,37 @@ __device__ __forceinline__ int clamped_len(const StepArgs& a, int b) {
 // at slots row * S .. row * S + S - 1 (S = slots_per_row): first the prefix
 // partitions of its group, then, from slot row * S + Pp, its own partitions
 // (as many as the query chunk of new token i sees after the prefix).
+//
+// Without groups and with at most kSpec slots per row (every split decode
+// step up to 8 partitions), the row's states are loaded before its length
+// is known -- they lie in the row's own slots, whatever it sees -- so that
+// the length, the states and the outputs take one memory round trip instead
+// of a chain of them; the arithmetic is that of merge_partitions, in the
+// same order.
+constexpr int kSpec = 8;
+
 template <int D>
 __global__ void __launch_bounds__(kWaveSize) merge_kernel(const StepArgs a) {
+  constexpr int PER = D / kWaveSize;
   const int row = blockIdx.x;
+  const int lane = threadIdx.x;
   const int i = (row / a.num_q_heads) % a.num_query_tokens;
   const int b = row / (a.num_q_heads * a.num_query_tokens);
+  const int S = a.slots_per_row;
+  const size_t first = (size_t)row * S;
+  const bool spec = a.num_groups == 0 && S <= kSpec;  // uniform
+  float m_s = -__builtin_huge_valf(), l_s = 0.f;
+  float o_s[kSpec][PER];
+  if (spec) {
+    if (lane < S) {
+      m_s = a.part_m[first + lane];
+      l_s = a.part_l[first + lane];
+    }
+#pragma unroll
+    for (int x = 0; x < kSpec; ++x)
+#pragma unroll
+      for (int e = 0; e < PER; ++e) o_s[x][e] = x < S ? a.part_o[(first + x) * D + lane * PER + e] : 0.f;
+  }
   const int L = clamped_len(a, b);
   const int vis = chunk_visible(a, L, i / a.query_chunk);
   if (vis <= 0) return;  // pass 1 wrote zeros
@@ -85,8 +111,29 @@ __global__ void __launch_bounds__(kWaveSize) merge_kernel(const StepArgs a) {
   const int n_pre = (t0 + Tp - 1) / Tp;
   const int n_own = (vis - t0 + Tp - 1) / Tp;
   if (n_pre == 0 && n_own <= 1) return;  // pass 1 wrote the final row
-  merge_partitions<D>(a, (size_t)row * a.slots_per_row, n_pre, a.prefix_partitions - n_pre, n_pre + n_own,
-                      a.out + (size_t)row * D);
+  float* orow = a.out + (size_t)row * D;
+  if (!spec) {
+    merge_partitions<D>(a, first, n_pre, a.prefix_partitions - n_pre, n_pre + n_own, orow);
+    return;
+  }
+  const int n = n_own;  // no groups: the row's partitions are slots 0 .. n - 1 (n <= S)
+  const float M = wave_max(lane < n ? fmaxf(-__builtin_huge_valf(), m_s) : -__builtin_huge_valf());
+  const float wgt = lane < n ? __builtin_amdgcn_exp2f(m_s - M) : 0.f;  // 2^(m_p - M)
+  const float lpart = lane < n ? fmaf(wgt, l_s, 0.f) : 0.f;
+  float acc[PER];
+#pragma unroll
+  for (int e = 0; e < PER; ++e) acc[e] = 0.f;
+#pragma unroll
+  for (int x = 0; x < kSpec; ++x) {
+    if (x < n) {
+      const float sc = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, wgt), x));
+#pragma unroll
+      for (int e = 0; e < PER; ++e) acc[e] = fmaf(sc, o_s[x][e], acc[e]);
+    }
+  }
+  const float lsum = wave_sum(lpart);
+#pragma unroll
+  for (int e = 0; e < PER; ++e) orow[lane * PER + e] = lsum > 0.f ? acc[e] / lsum : acc[e];  // 0: sees nothing
 }
 
 }  // namespace
