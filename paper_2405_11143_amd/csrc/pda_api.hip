@@ -157,7 +157,7 @@ int prepare_step(const pda_problem* p, const pda_prefix_groups* groups, const vo
   if (rc != PDA_OK) return rc;
   if (p->num_seqs > 0 && (!q || !k || !v || !bt || !lens || !out)) return PDA_ERR_NULL;
   if (!isfinite(scale)) return PDA_ERR_VALUE;
-  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 4)) return PDA_ERR_ALIGNMENT;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16)) return PDA_ERR_ALIGNMENT;
   rc = make_plan(p, groups, plan);
   if (rc != PDA_OK) return rc;
   if (plan->info.workspace_bytes > 0) {
@@ -269,7 +269,7 @@ int pda_merge_partitions(const pda_problem* prob, const int32_t* context_lens, f
   if (rc != PDA_OK) return rc;
   if (prob->num_seqs == 0) return PDA_OK;
   if (!context_lens || !out) return PDA_ERR_NULL;
-  if (!aligned(workspace, 16) || !aligned(out, 4)) return PDA_ERR_ALIGNMENT;
+  if (!aligned(workspace, 16) || !aligned(out, 16)) return PDA_ERR_ALIGNMENT;
   Plan plan;
   rc = make_plan(prob, nullptr, &plan);
   if (rc != PDA_OK) return rc;

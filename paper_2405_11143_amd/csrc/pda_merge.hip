@@ -59,8 +59,11 @@ __device__ __forceinline__ void merge_partitions(const StepArgs& a, size_t first
     }
   }
   const float lsum = wave_sum(lpart);
-#pragma unroll
-  for (int e = 0; e < PER; ++e) orow[lane * PER + e] = lsum > 0.f ? acc[e] / lsum : acc[e];  // 0: sees nothing
+  const bool pos = lsum > 0.f;  // 0: the row sees nothing
+  if constexpr (PER == 2)
+    store_nt2(orow + lane * PER, pos ? acc[0] / lsum : acc[0], pos ? acc[1] / lsum : acc[1]);
+  else
+    __builtin_nontemporal_store(pos ? acc[0] / lsum : acc[0], orow + lane);
 }
 
 __device__ __forceinline__ int clamped_len(const StepArgs& a, int b) {
@@ -132,8 +135,11 @@ __global__ void __launch_bounds__(kWaveSize) merge_kernel(const StepArgs a) {
     }
   }
   const float lsum = wave_sum(lpart);
-#pragma unroll
-  for (int e = 0; e < PER; ++e) orow[lane * PER + e] = lsum > 0.f ? acc[e] / lsum : acc[e];  // 0: sees nothing
+  const bool pos = lsum > 0.f;  // 0: the row sees nothing
+  if constexpr (PER == 2)
+    store_nt2(orow + lane * PER, pos ? acc[0] / lsum : acc[0], pos ? acc[1] / lsum : acc[1]);
+  else
+    __builtin_nontemporal_store(pos ? acc[0] / lsum : acc[0], orow + lane);
 }
 
 }  // namespace

@@ -160,13 +160,24 @@ __device__ __forceinline__ float combine(const PassShared<D>& sh, int t, int nti
   return acc;
 }
 
-__device__ __forceinline__ void store_partial(const StepArgs& a, size_t slot, int d, int D, float acc, float M,
-                                              float lsum) {
-  a.part_o[slot * D + d] = acc;
-  if (d == 0) {
+// The partial state of one row and partition: 4 output columns d0 .. d0+3,
+// and with the first of them the max and the denominator.  Plain (cached)
+// stores: the merge pass reads them right after.
+__device__ __forceinline__ void store_partial4(const StepArgs& a, size_t slot, int d0, int D, const float (&acc)[4],
+                                               float M, float lsum) {
+  *reinterpret_cast<f32x4_t*>(a.part_o + slot * D + d0) = f32x4_t{acc[0], acc[1], acc[2], acc[3]};
+  if (d0 == 0) {
     a.part_m[slot] = M;
     a.part_l[slot] = lsum;
   }
+}
+
+// One final output row's columns d0 .. d0+3: acc / lsum, or acc itself (0,
+// or NaN) for a row that sees nothing.
+__device__ __forceinline__ void store_final4(float* p, const float (&acc)[4], float lsum) {
+  const bool pos = lsum > 0.f;
+  store_nt4(p, pos ? acc[0] / lsum : acc[0], pos ? acc[1] / lsum : acc[1], pos ? acc[2] / lsum : acc[2],
+            pos ? acc[3] / lsum : acc[3]);
 }
 
 // Stream blocks [J0, J1) of one sequence through LDS, a step of 2 blocks at a
@@ -380,17 +391,17 @@ __device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item)
     const int ci0 = ct * a.query_chunk;
     const int crows = min(a.query_chunk, nq - ci0) * G;
     const bool single = ct_parts == 1 && min(t0_all, chunk_visible(a, L, ct)) == 0;
-    for (int idx = tid; idx < crows * D; idx += kWaves * kWaveSize) {
-      const int h = idx / D;
-      const int d = idx % D;
-      float acc = combine(sh, t, ntile, slices, h, d);
-      const float M = sh.mx[t][h], lsum = sh.lsum[t][h];
-      if (any_bad) acc = __builtin_nanf("");
+    for (int idx = tid; idx < crows * (D / 4); idx += kWaves * kWaveSize) {  // 4 columns per thread
+      const int h = idx / (D / 4);
+      const int d0 = 4 * (idx % (D / 4));
+      float acc[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[e] = any_bad ? __builtin_nanf("") : combine(sh, t, ntile, slices, h, d0 + e);
       const size_t row = ((size_t)b * nq + ci0 + h / G) * Hq + (size_t)g * G + h % G;
       if (single)
-        a.out[row * D + d] = lsum > 0.f ? acc / lsum : acc;  // acc is 0 (or NaN) for a row that sees nothing
+        store_final4(a.out + row * D + d0, acc, sh.lsum[t][h]);
       else
-        store_partial(a, row * a.slots_per_row + a.prefix_partitions + p, d, D, acc, M, lsum);
+        store_partial4(a, row * a.slots_per_row + a.prefix_partitions + p, d0, D, acc, sh.mx[t][h], sh.lsum[t][h]);
     }
   }
 }
@@ -454,15 +465,15 @@ __device__ void prefix_item(const StepArgs& a, PassLds<D, MODE>& lds, int pitem)
   int any_bad = 0;
 #pragma unroll
   for (int x = 0; x < kWaves; ++x) any_bad |= sh.bad[x];
-  for (int idx = tid; idx < rows * D; idx += kWaves * kWaveSize) {
-    const int rr = idx / D;
-    const int d = idx % D;
+  for (int idx = tid; idx < rows * (D / 4); idx += kWaves * kWaveSize) {  // 4 columns per thread
+    const int rr = idx / (D / 4);
+    const int d0 = 4 * (idx % (D / 4));
     const int t = rr / kRows, h = rr % kRows;
-    float acc = combine(sh, t, ntile, slices, h, d);
-    const float M = sh.mx[t][h], lsum = sh.lsum[t][h];
-    if (any_bad) acc = __builtin_nanf("");
+    float acc[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc[e] = any_bad ? __builtin_nanf("") : combine(sh, t, ntile, slices, h, d0 + e);
     const size_t row = (size_t)(first + rr / G) * Hq + (size_t)g * G + rr % G;
-    store_partial(a, row * a.slots_per_row + pp, d, D, acc, M, lsum);
+    store_partial4(a, row * a.slots_per_row + pp, d0, D, acc, sh.mx[t][h], sh.lsum[t][h]);
   }
 }
 

@@ -123,6 +123,7 @@ def test_step_validation(fn):
     assert call(fn, prob(), q=0x1008) == pda.pda.PDA_ERR_ALIGNMENT
     assert call(fn, prob(), k=0x1004) == pda.pda.PDA_ERR_ALIGNMENT
     assert call(fn, prob(), out=0x1002) == pda.pda.PDA_ERR_ALIGNMENT
+    assert call(fn, prob(), out=0x1004) == pda.pda.PDA_ERR_ALIGNMENT  # rows are written 16 bytes at a time
     assert call(fn, prob()) == pda.pda.PDA_ERR_WORKSPACE  # the work order always needs one
     split = prob(partition_tokens=64)
     assert call(fn, split) == pda.pda.PDA_ERR_WORKSPACE
@@ -144,6 +145,7 @@ def test_merge_validation():
     assert f(ctypes.byref(split), None, 0x1000, 0x1000, need, None) == pda.pda.PDA_ERR_NULL
     assert f(ctypes.byref(split), 0x1000, 0x1000, 0x1000, need - 1, None) == pda.pda.PDA_ERR_WORKSPACE
     assert f(ctypes.byref(split), 0x1000, 0x1000, 0x1004, need, None) == pda.pda.PDA_ERR_ALIGNMENT
+    assert f(ctypes.byref(split), 0x1000, 0x1004, 0x1000, need, None) == pda.pda.PDA_ERR_ALIGNMENT  # out
     # nothing split: nothing to merge, no launch
     single = prob(max_context_len=200, partition_tokens=208)
     assert f(ctypes.byref(single), 0x1000, 0x1000, None, 0, None) == pda.pda.PDA_OK
