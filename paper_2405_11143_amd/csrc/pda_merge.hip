@@ -8,7 +8,8 @@
 //   out = sum_k 2^(m_k - M) O_k / sum_k 2^(m_k - M) l_k.
 // The output sum runs in ascending k and the denominator in a fixed
 // butterfly, so the result is reproducible.  One wavefront per output row
-// (sequence, new token, query head); each lane owns D/64 output columns.
+// (sequence, new token, query head), 4 rows per workgroup; each lane owns
+// D/64 output columns.
 #include "pda_internal.h"
 
 namespace pda {
@@ -34,7 +35,7 @@ template <int D>
 __device__ __forceinline__ void merge_partitions(const StepArgs& a, size_t first, int n_pre, int gap, int n,
                                                  float* orow) {
   constexpr int PER = D / kWaveSize;
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & (kWaveSize - 1);
   auto slot = [&](int k) { return first + (size_t)k + (k >= n_pre ? gap : 0); };
   // States are read lane-parallel (lane x holds partition p0 + x), so the
   // dependent chain is states -> outputs, whatever n is.
@@ -84,11 +85,14 @@ __device__ __forceinline__ int clamped_len(const StepArgs& a, int b) {
 // same order.
 constexpr int kSpec = 8;
 
+constexpr int kMergeRows = 4;  // rows (wavefronts) per workgroup
+
 template <int D>
-__global__ void __launch_bounds__(kWaveSize) merge_kernel(const StepArgs a) {
+__global__ void __launch_bounds__(kMergeRows * kWaveSize) merge_kernel(const StepArgs a) {
   constexpr int PER = D / kWaveSize;
-  const int row = blockIdx.x;
-  const int lane = threadIdx.x;
+  const int row = blockIdx.x * kMergeRows + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & (kWaveSize - 1);
+  if ((size_t)row >= (size_t)a.num_seqs * a.num_query_tokens * a.num_q_heads) return;  // spare wavefronts
   const int i = (row / a.num_q_heads) % a.num_query_tokens;
   const int b = row / (a.num_q_heads * a.num_query_tokens);
   const int S = a.slots_per_row;
@@ -145,11 +149,12 @@ __global__ void __launch_bounds__(kWaveSize) merge_kernel(const StepArgs a) {
 }  // namespace
 
 hipError_t launch_merge(const StepArgs& a, int head_dim, hipStream_t stream) {
-  const unsigned grid = (unsigned)a.num_seqs * (unsigned)a.num_query_tokens * (unsigned)a.num_q_heads;
+  const unsigned rows = (unsigned)a.num_seqs * (unsigned)a.num_query_tokens * (unsigned)a.num_q_heads;
+  const unsigned grid = (rows + kMergeRows - 1) / kMergeRows;
   if (head_dim == 64)
-    hipLaunchKernelGGL(merge_kernel<64>, dim3(grid), dim3(kWaveSize), 0, stream, a);
+    hipLaunchKernelGGL(merge_kernel<64>, dim3(grid), dim3(kMergeRows * kWaveSize), 0, stream, a);
   else if (head_dim == 128)
-    hipLaunchKernelGGL(merge_kernel<128>, dim3(grid), dim3(kWaveSize), 0, stream, a);
+    hipLaunchKernelGGL(merge_kernel<128>, dim3(grid), dim3(kMergeRows * kWaveSize), 0, stream, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
