@@ -18,15 +18,21 @@ namespace {
 // duration after the ideal one, so an item should be short next to the work
 // each of the kConcurrentItems workgroups the GPU runs at once has to do;
 // longer items amortise each workgroup's start-up (order, length, block ids,
-// q) over more streamed tiles.  With only max_context_len on the host, the
-// work is estimated as B * Hkv * chunk groups * max_context_len / 2 tokens (the
-// mean of contexts spread up to the maximum), and the partition is that
-// share rounded up to kPartitionQuantum tokens, within [kMinPartitionTokens,
-// kMaxPartitionTokens] and never longer than the longest context (then there
-// is one partition and no merge pass).  On MI355X this picks the fastest or
-// within 1% of the fastest of the sizes measured on the four Llama-3-shaped
-// decode steps; above 4096 tokens the step slowed down on all of them.
-constexpr int kMaxPartitionTokens = 4096;
+// q) and its partial state over more streamed tiles.  With only
+// max_context_len on the host, the work is estimated as B * Hkv * chunk
+// groups * max_context_len / 2 tokens (the mean of contexts spread up to the
+// maximum), and the share is that over kConcurrentItems.  Items of 16 or more
+// query rows (several new tokens per sequence) take kRowsShareNum /
+// kRowsShareDen of it: on MI355X the 70B TP=8 shard with 2, 4 and 8 new
+// tokens ran 1%, 8% and 6% faster at 3584 tokens than at the plain share
+// (2816), while the one-token step is flat between 2816 and 4096.  A share
+// above kMaxPartitionTokens splits the longest context into the fewest equal
+// partitions of at most that size (9216 -> 2 x 4608, 16384 -> 4 x 4096).
+// The result is rounded up to kPartitionQuantum tokens, at least
+// kMinPartitionTokens and never longer than the longest context (then there
+// is one partition and no merge pass).
+constexpr int kMaxPartitionTokens = 4608;
+constexpr int64_t kRowsShareNum = 13, kRowsShareDen = 10;
 constexpr int kMinPartitionTokens = 256;
 constexpr int kPartitionQuantum = 256;
 constexpr int64_t kConcurrentItems = 768;  // 256 compute units x 3 workgroups of 4 wavefronts
@@ -84,7 +90,12 @@ int make_plan(const pda_problem* p, const pda_prefix_groups* groups, Plan* plan)
   int tp = p->partition_tokens;
   if (tp == 0) {
     const int64_t len = p->max_context_len > 0 ? p->max_context_len : 1;
-    const int64_t share = (units * len / 2 + kConcurrentItems - 1) / kConcurrentItems;
+    int64_t share = (units * len / 2 + kConcurrentItems - 1) / kConcurrentItems;
+    if (std::min(nqc, pda::kWaves) * qc * G >= pda::kMaxGroup) share = share * kRowsShareNum / kRowsShareDen;
+    if (share > kMaxPartitionTokens) {
+      const int64_t pieces = (len + kMaxPartitionTokens - 1) / kMaxPartitionTokens;
+      share = (len + pieces - 1) / pieces;
+    }
     const int64_t quanta = (share + kPartitionQuantum - 1) / kPartitionQuantum;
     tp = (int)std::min<int64_t>(kMaxPartitionTokens, std::max<int64_t>(kMinPartitionTokens, quanta * kPartitionQuantum));
     const int rounded = (int)((len + pda::kBlockTokens - 1) / pda::kBlockTokens * pda::kBlockTokens);

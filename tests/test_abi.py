@@ -90,15 +90,21 @@ def test_plan_workspace():
 
 
 def test_plan_partition_choice():
-    # B * Hkv * max_len / 2 tokens over 768 concurrent workgroups, rounded up
-    # to 256 tokens, within [256, 4096]
-    assert plan()[:2] == (4096, 1)                        # share 5462 -> 4096
+    # B * Hkv * chunk groups * max_len / 2 tokens over 768 concurrent
+    # workgroups (x 1.3 for items of 16 or more query rows); above 4608 the
+    # fewest equal pieces of at most 4608; rounded up to 256 tokens, at least 256
+    assert plan()[:2] == (4096, 1)                        # share 5462 -> one piece of 4096
     assert plan(num_seqs=9000)[:2] == (4096, 1)
     assert plan(num_seqs=64)[:2] == (1536, 3)             # share 1366
     assert plan(num_seqs=32)[:2] == (768, 6)              # share 683
     assert plan(num_seqs=1)[:2] == (256, 16)              # share 22
-    assert plan(num_seqs=512, num_kv_heads=1, num_q_heads=8, max_context_len=8183)[:2] == (2816, 3)
-    assert plan(num_seqs=64, max_context_len=15288)[:2] == (4096, 4)
+    shard = dict(num_seqs=512, num_kv_heads=1, num_q_heads=8, max_context_len=8183)
+    assert plan(**shard)[:2] == (2816, 3)                 # share 2728
+    assert plan(**shard, num_query_tokens=2)[:2] == (3584, 3)  # 16 rows per item: 2728 * 1.3
+    assert plan(**shard, num_query_tokens=8)[:2] == (3584, 3)  # 64 rows per item
+    assert plan(num_seqs=64, max_context_len=15288)[:2] == (3840, 4)   # share 5096: 4 x 3822
+    assert plan(num_seqs=64, max_context_len=16384)[:2] == (4096, 4)   # share 5462: 4 x 4096
+    assert plan(num_q_heads=28, num_kv_heads=4, max_context_len=9216)[:2] == (4608, 2)  # share 6144
     # never longer than the longest context, rounded up to a whole block
     assert plan(num_seqs=9000, max_context_len=2001)[:2] == (2016, 1)
     assert plan(max_context_len=0)[:2] == (16, 1)
