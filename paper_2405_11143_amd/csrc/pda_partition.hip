@@ -192,6 +192,7 @@ __device__ void run_staged(WaveAttention<D>& wave, Staging<D, SB>& st, const int
                            const char* kpool, const char* vpool, size_t block_bytes, int num_blocks) {
   using WA = WaveAttention<D>;
   static_assert(SB == 2, "a step is one pair of blocks");
+  static_assert(Staging<D, SB>::TC % kWaveSize == 0, "a wavefront's loads stay within one tile");
   wave.tr_cols = true;  // every fold here goes through pv_staged
   constexpr int TC = Staging<D, SB>::TC;
   constexpr int NL = Staging<D, SB>::kLoads;
@@ -200,21 +201,37 @@ __device__ void run_staged(WaveAttention<D>& wave, Staging<D, SB>& st, const int
   // Two steps' loads are in flight in two register sets while a third
   // step is folded from LDS (three buffers).
   uint4 ra[NL], rb[NL];
+  // Load k of a thread takes piece ci = k * 256 + tid of the step, in
+  // [block][K or V][piece] order.  A tile is a multiple of 64 pieces, so the
+  // 64 lanes of a wavefront share the block and the K or V side of each load:
+  // both are taken from the wavefront's first piece, and the block ids go
+  // through scalar registers, so every load has one buffer descriptor per
+  // wavefront (a per-lane one costs a loop over the distinct values).
+  const int wbase = __builtin_amdgcn_readfirstlane(tid & ~(kWaveSize - 1));
+  const int lane_piece = tid & (kWaveSize - 1);
   // issue the loads of step `step` of the window starting at block jw
   auto issue = [&](uint4(&r)[NL], int jw, int jwe, int step) {
+    int phys[SB], bytes[SB];  // (readfirstlane keeps them in scalar registers)
+#pragma unroll
+    for (int s = 0; s < SB; ++s) {
+      const int j = jw + step * SB + s;
+      const bool valid = j < jwe;
+      int id = __builtin_amdgcn_readfirstlane(valid ? st.ids[j - jw] : 0);
+      if ((unsigned)id >= (unsigned)num_blocks) {  // contract violation: never read outside the pool
+        bad |= valid;
+        id = 0;
+      }
+      phys[s] = id;
+      bytes[s] = __builtin_amdgcn_readfirstlane(valid ? WA::kTileBytes : 0);
+    }
 #pragma unroll
     for (int k = 0; k < NL; ++k) {
-      const int ci = k * kWaves * kWaveSize + tid;  // [block][K or V][piece]
-      const int blk = ci / (2 * TC);
-      const int j = jw + step * SB + blk;
-      const bool valid = j < jwe;
-      int phys = valid ? st.ids[j - jw] : 0;
-      if ((unsigned)phys >= (unsigned)num_blocks) {  // contract violation: never read outside the pool
-        bad |= valid;
-        phys = 0;
-      }
-      const char* pool = ((ci / TC) & 1) ? vpool : kpool;
-      r[k] = load_stream(tile_rsrc(pool + (size_t)phys * block_bytes, valid ? WA::kTileBytes : 0), (ci % TC) * 16);
+      const int cb = k * kWaves * kWaveSize + wbase;  // the wavefront's first piece
+      const int blk = cb / (2 * TC);
+      const char* pool = ((cb / TC) & 1) ? vpool : kpool;
+      r[k] = load_stream(tile_rsrc(pool + (size_t)(blk == 0 ? phys[0] : phys[1]) * block_bytes,
+                                   __builtin_amdgcn_readfirstlane(blk == 0 ? bytes[0] : bytes[1])),
+                         (cb % TC + lane_piece) * 16);
     }
   };
   // where each of this thread's loads goes in a step's buffer
