@@ -60,6 +60,11 @@ typedef float floatx4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// IEEE 754-2019 maximum of three values (NaN propagates; one instruction).
+__device__ __forceinline__ float max3(float a, float b, float c) {
+  return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
+}
+
 // x * y rounded on its own: never fused with a following add.
 __device__ __forceinline__ float mul_rounded(float x, float y) {
 #pragma clang fp contract(off)
@@ -221,15 +226,17 @@ struct WaveAttention {
       // An empty volatile asm keeps this a branch: as selects, the masking
       // would run on every block.
       asm volatile("");
-      const int lim = min(L - lim_off, t_stop);
+      const int rel = min(L - lim_off, t_stop) - (tok0 + 4 * kg);  // this lane's first token at or past it is masked
 #pragma unroll
       for (int b = 0; b < NB; ++b)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          if (tok0 + kBlockTokens * b + 4 * kg + i >= lim) sc[b][i] = kNegInf;
+          if (kBlockTokens * b + i >= rel) sc[b][i] = kNegInf;
     }
-    float top = fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3]));
-    if constexpr (NB == 2) top = fmaxf(top, fmaxf(fmaxf(sc[1][0], sc[1][1]), fmaxf(sc[1][2], sc[1][3])));
+    // IEEE maximum (v_maximum3_f32): unlike fmaxf it needs no quieting of
+    // its inputs, which come from another basic block after the masking.
+    float top = max3(sc[0][0], sc[0][1], max3(sc[0][2], sc[0][3], NB == 2 ? sc[1][0] : kNegInf));
+    if constexpr (NB == 2) top = max3(top, max3(sc[1][1], sc[1][2], sc[1][3]), kNegInf);
     if (__builtin_amdgcn_ballot_w64(top > m_run + kRescaleSlack) != 0) rescale(top);  // wave-uniform
     float pr[NB][4];
 #pragma unroll
@@ -260,9 +267,10 @@ struct WaveAttention {
   __device__ __forceinline__ void mask_v(uint4 (&vr)[4], int tok0, int l_vis, bool tail) const {
     if (tail) {
       asm volatile("");  // a branch, as in softmax
+      const int rel = l_vis - (tok0 + 4 * kg);  // this lane's rows from it on are zeroed
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        if (tok0 + 4 * kg + e >= l_vis) vr[e] = make_uint4(0u, 0u, 0u, 0u);
+        if (e >= rel) vr[e] = make_uint4(0u, 0u, 0u, 0u);
     }
   }
 
@@ -313,13 +321,14 @@ struct WaveAttention {
   __device__ __forceinline__ void pv_staged(uint4 (&aw)[VT], const PFrag<2>& f, bool tail, int tok0, int l_vis) {
     if (tail) {
       asm volatile("");  // a branch, as in softmax
+      const int rel = l_vis - (tok0 + 4 * kg);  // this lane's tokens below it are kept
       unsigned mw[4];
 #pragma unroll
       for (int b = 0; b < 2; ++b)
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          const int t0 = tok0 + kBlockTokens * b + 4 * kg + 2 * h;
-          mw[2 * b + h] = (t0 < l_vis ? 0x0000ffffu : 0u) | (t0 + 1 < l_vis ? 0xffff0000u : 0u);
+          const int t0 = kBlockTokens * b + 2 * h;
+          mw[2 * b + h] = (t0 < rel ? 0x0000ffffu : 0u) | (t0 + 1 < rel ? 0xffff0000u : 0u);
         }
 #pragma unroll
       for (int t = 0; t < VT; ++t) aw[t] = make_uint4(aw[t].x & mw[0], aw[t].y & mw[1], aw[t].z & mw[2], aw[t].w & mw[3]);
