@@ -47,6 +47,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_GBS = 8000.0  # MI355X HBM3E, datasheet
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, datasheet (no sparsity)
 METRIC = "decode-attention HBM GB/s (% of peak) + seq-steps/s, Llama-3-8B shape"
 PROFILES = os.path.join(ROOT, "profiles")
 CSRC = "paper_2405_11143_amd/csrc/"
@@ -154,6 +155,15 @@ def roofline(achieved_gbs, ms, kernel, workload):
             "ms_per_launch": round(ms, 5)}
 
 
+def roofline_mfma(flops, ms, kernel):
+    """Dense bf16 MFMA roofline of a launch whose work is bound by its
+    contractions rather than by its bytes."""
+    achieved = flops / (ms * 1e-3) / 1e12
+    return {"bound": "mfma", "kernel": kernel, "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+            "ms_per_launch": round(ms, 5), "algorithmic_flops_per_launch": int(flops)}
+
+
 def config_of(st, cfg_desc, name, plan=None, **extra):
     c = {"workload": cfg_desc, "name": name, "batch": st.B, "q_heads": st.Hq, "kv_heads": st.Hkv,
          "head_dim": st.D, "block_size": st.block_size, "pool_blocks": st.num_blocks,
@@ -226,6 +236,10 @@ def op_decode(args, n_tokens=1):
                    "cpu_baseline": None})
     if n_tokens > 1:
         result["query_tokens_per_s"] = round(st.B * n_tokens / (ms_step * 1e-3), 1)
+        # many new tokens make the step a contraction: then the MFMA roofline binds
+        flops = st.algorithmic_flops(n_tokens)
+        if flops / (PEAK_BF16_TFLOPS * 1e12) > alg / (PEAK_GBS * 1e9):
+            result["roofline"] = roofline_mfma(flops, ms_pass1, KERNEL)
     if n_tokens == 1 and not args.no_cpu_baseline and not args.pass1_only:
         result["cpu_baseline"] = cpu_baseline(st, q, k, v, args.cpu_min_seconds, args.cpu_max_reps)
     return result

@@ -58,7 +58,8 @@ struct Plan {
   pda_plan_info info;
   int query_chunk;        // new tokens per work item: min(n, 16 / G)
   int num_query_chunks;   // ceil(n / query_chunk)
-  int num_chunk_groups;   // ceil(chunks / 4): chunks per work item share its tiles
+  int chunks_per_group;   // 4, or 8 with more than 4 chunks (two 16-row tiles per wavefront)
+  int num_chunk_groups;   // ceil(chunks / chunks_per_group): chunks per work item share its tiles
   int prefix_partitions;  // Pp: partitions of the longest shared prefix (0 without groups)
   size_t regular_items;   // P * B * Hkv * chunk groups (pass-1 workgroups of the sequences' own tokens)
   size_t items;           // regular items + num_groups * Pp * Hkv prefix items
@@ -85,13 +86,14 @@ int make_plan(const pda_problem* p, const pda_prefix_groups* groups, Plan* plan)
   const int G = p->num_q_heads / p->num_kv_heads;
   const int qc = std::min(n, pda::kMaxGroup / G);
   const int nqc = (n + qc - 1) / qc;
-  const int ncg = (nqc + pda::kWaves - 1) / pda::kWaves;  // a work item takes up to 4 chunks
+  const int cpg = nqc > pda::kWaves ? pda::kWideChunks : pda::kWaves;  // chunks per work item
+  const int ncg = (nqc + cpg - 1) / cpg;
   const int64_t units = (int64_t)p->num_seqs * p->num_kv_heads * ncg;
   int tp = p->partition_tokens;
   if (tp == 0) {
     const int64_t len = p->max_context_len > 0 ? p->max_context_len : 1;
     int64_t share = (units * len / 2 + kConcurrentItems - 1) / kConcurrentItems;
-    if (std::min(nqc, pda::kWaves) * qc * G >= pda::kMaxGroup) share = share * kRowsShareNum / kRowsShareDen;
+    if (std::min(nqc, cpg) * qc * G >= pda::kMaxGroup) share = share * kRowsShareNum / kRowsShareDen;
     if (share > kMaxPartitionTokens) {
       const int64_t pieces = (len + kMaxPartitionTokens - 1) / kMaxPartitionTokens;
       share = (len + pieces - 1) / pieces;
@@ -112,6 +114,7 @@ int make_plan(const pda_problem* p, const pda_prefix_groups* groups, Plan* plan)
   plan->info.num_partitions = (int32_t)parts;
   plan->query_chunk = qc;
   plan->num_query_chunks = nqc;
+  plan->chunks_per_group = cpg;
   plan->num_chunk_groups = ncg;
   plan->prefix_partitions = (int)pparts;
   if (p->num_seqs > 0) {
@@ -155,6 +158,7 @@ void fill_args(const pda_problem* p, const Plan* plan, void* ws, pda::StepArgs* 
   args->num_query_tokens = query_tokens(p);
   args->query_chunk = plan->query_chunk;
   args->num_query_chunks = plan->num_query_chunks;
+  args->chunks_per_group = plan->chunks_per_group;
   args->num_chunk_groups = plan->num_chunk_groups;
   args->partition_tokens = plan->info.partition_tokens;
   args->num_partitions = plan->info.num_partitions;

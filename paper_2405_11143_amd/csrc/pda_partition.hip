@@ -74,12 +74,14 @@ struct Staging {
 
 // Which paths a launch compiles.  A launch whose items all have one tile
 // (every decode step without shared-prefix groups) compiles the register
-// path only (135 VGPRs at D = 128, 33 KiB of LDS); otherwise both paths are
-// compiled (168 VGPRs, 50.5 KiB).  Staging takes 2 blocks per step, so three
+// path only (135 VGPRs at D = 128, 33 KiB of LDS); with up to 4 query chunks
+// per item both paths are compiled (168 VGPRs, 50.5 KiB); with more, the
+// wide variant also folds two tiles per wavefront (at most 256 VGPRs, 2
+// workgroups per compute unit).  Staging takes 2 blocks per step, so three
 // staging buffers (49.5 KiB at D = 128) still leave room for 3 workgroups
 // per compute unit; 4 blocks per step at 2 workgroups per compute unit
 // measured slower on MI355X.
-constexpr int kModeRegister = 1, kModeMixed = 3;
+constexpr int kModeRegister = 1, kModeMixed = 3, kModeWide = 7;
 constexpr int kStepBlocks = 2;
 
 template <int D, int MODE>
@@ -186,14 +188,19 @@ __device__ __forceinline__ void store_final4(float* p, const float (&acc)[4], fl
 // both blocks of a step as one pair (every fold is a pair, so the output
 // accumulators stay put), and only blocks below its own end `j_stop` (its
 // query chunk's causal range); an inactive wavefront only helps to load.
-template <int D, int SB>
-__device__ void run_staged(WaveAttention<D>& wave, Staging<D, SB>& st, const int32_t* table_row, int J0, int J1,
-                           int j_stop, bool active, int slice, int slices, int L, int l_first, int l_vis,
-                           const char* kpool, const char* vpool, size_t block_bytes, int num_blocks) {
+// With NT = 2 the wavefront also folds a second, later chunk into `wave_b`
+// (blocks below j_stop_b, which is 0 when it has none) from the same K and V
+// fragments.
+template <int D, int SB, int NT>
+__device__ void run_staged(WaveAttention<D>& wave, WaveAttention<D>& wave_b, Staging<D, SB>& st,
+                           const int32_t* table_row, int J0, int J1, int j_stop, int j_stop_b, bool active, int slice,
+                           int slices, int L, int l_first, int l_vis, int l_first_b, int l_vis_b, const char* kpool,
+                           const char* vpool, size_t block_bytes, int num_blocks) {
   using WA = WaveAttention<D>;
   static_assert(SB == 2, "a step is one pair of blocks");
   static_assert(Staging<D, SB>::TC % kWaveSize == 0, "a wavefront's loads stay within one tile");
   wave.tr_cols = true;  // every fold here goes through pv_staged
+  wave_b.tr_cols = true;
   constexpr int TC = Staging<D, SB>::TC;
   constexpr int NL = Staging<D, SB>::kLoads;
   const int tid = threadIdx.x;
@@ -251,16 +258,16 @@ __device__ void run_staged(WaveAttention<D>& wave, Staging<D, SB>& st, const int
   // fold step `step` (in buffer buf) if it is this wavefront's
   auto fold_step = [&](int jw, int jwe, int step, int buf) {
     if (!active || step % slices != slice) return;  // wave-uniform
-    // Both blocks of the step as one pair.  When only the first is this
-    // wavefront's (the run or its causal range ends there), the second is
-    // masked whole through t_stop (its slot in LDS holds zeros or another
-    // range's tiles).
+    // Both blocks of the step as one pair.  When only the first is a chunk's
+    // (the run or its causal range ends there), the second is masked whole
+    // through t_stop (its slot in LDS holds zeros or another range's tiles).
     const int j0 = jw + step * SB;
     const int j_lim = min(jwe, j_stop);
-    if (j0 >= j_lim) return;
+    const int j_lim_b = NT == 2 ? min(jwe, j_stop_b) : 0;
+    const bool fold_a = j0 < j_lim;
+    const bool fold_b = NT == 2 && j0 < j_lim_b;
+    if (!fold_a && !fold_b) return;
     const int tok0 = j0 * kBlockTokens;
-    const int t_stop = j_lim * kBlockTokens;
-    const bool tail = tok0 + 2 * kBlockTokens > min(l_first, t_stop);  // wave-uniform
     uint4 kr[2][WA::NC];
 #pragma unroll
     for (int k = 0; k < 2; ++k)
@@ -269,8 +276,23 @@ __device__ void run_staged(WaveAttention<D>& wave, Staging<D, SB>& st, const int
     uint4 aw[WA::VT];
     wave.v_frags(reinterpret_cast<const uint16_t*>(st.buf[buf][0] + TC),
                  reinterpret_cast<const uint16_t*>(st.buf[buf][1] + TC), aw);
-    const auto f = wave.template softmax<2>(kr, tok0, L, tail, t_stop);
-    wave.pv_staged(aw, f, tail, tok0, min(l_vis, t_stop));
+    if constexpr (NT == 2) {
+      // The later chunk first: pv_staged zeroes (in aw) the V rows its last
+      // row does not see, which no row of the earlier chunk sees either; the
+      // earlier chunk's rows give the rows between them probability 0.
+      if (fold_b) {
+        const int t_stop = j_lim_b * kBlockTokens;
+        const bool tail = tok0 + 2 * kBlockTokens > min(l_first_b, t_stop);  // wave-uniform
+        const auto f = wave_b.template softmax<2>(kr, tok0, L, tail, t_stop);
+        wave_b.pv_staged(aw, f, tail, tok0, min(l_vis_b, t_stop));
+      }
+    }
+    if (fold_a) {
+      const int t_stop = j_lim * kBlockTokens;
+      const bool tail = tok0 + 2 * kBlockTokens > min(l_first, t_stop);  // wave-uniform
+      const auto f = wave.template softmax<2>(kr, tok0, L, tail, t_stop);
+      wave.pv_staged(aw, f, tail, tok0, min(l_vis, t_stop));
+    }
   };
   for (int jw = J0; jw < J1; jw += kIdWindow) {
     const int jwe = min(J1, jw + kIdWindow);
@@ -301,6 +323,7 @@ __device__ void run_staged(WaveAttention<D>& wave, Staging<D, SB>& st, const int
     }
   }
   wave.bad |= __builtin_amdgcn_ballot_w64(bad) != 0;
+  wave_b.bad |= wave.bad;
   __syncthreads();  // the staging area is reused by the epilogue
 }
 
@@ -317,9 +340,14 @@ __device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item)
   const int g = gc / a.num_chunk_groups;
   const int cg = gc % a.num_chunk_groups;
   const int nq = a.num_query_tokens;
+  const int CPG = a.chunks_per_group;
   // query chunks (16-row tiles) of the item: always one in the register-only variant
-  const int ntile = MODE == kModeRegister ? 1 : min(kWaves, a.num_query_chunks - cg * kWaves);
-  const int slices = kWaves / ntile;                               // slices of blocks per tile
+  const int nchunk = MODE == kModeRegister ? 1 : min(CPG, a.num_query_chunks - cg * CPG);
+  // more than 4 (wide variant only): wavefront w folds chunks w and, when it
+  // exists, w + 4, and the epilogue takes the two sets of tiles in turn
+  const bool two = MODE == kModeWide && nchunk > kWaves;
+  const int ntile = two ? kWaves : nchunk;  // tiles of the first (or only) set
+  const int slices = kWaves / ntile;        // slices of blocks per tile
   const int tid = threadIdx.x;
   const int lane = tid & (kWaveSize - 1);
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -332,16 +360,16 @@ __device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item)
   const int t0_all = seq_prefix_len(a, b);  // tokens before it belong to the group's prefix items
   // Per chunk c: its tokens [i0, i0 + nv), the token limit of its last row
   // (l_vis) and the partitions of its own tokens after the prefix.
-  auto chunk_of = [&](int t) { return cg * kWaves + t; };
+  auto chunk_of = [&](int t) { return cg * CPG + t; };
   auto parts_of = [&](int c) {
     const int lv = chunk_visible(a, L, c);
     const int t0 = min(t0_all, max(lv, 0));
     return lv > 0 ? (lv - t0 + Tp - 1) / Tp : 0;
   };
   int nparts_max = 0;
-  for (int t = 0; t < ntile; ++t) nparts_max = max(nparts_max, parts_of(chunk_of(t)));
+  for (int t = 0; t < nchunk; ++t) nparts_max = max(nparts_max, parts_of(chunk_of(t)));
   if (p == 0) {  // chunks that see nothing (L == 0, or new tokens before the context): zero rows
-    for (int t = 0; t < ntile; ++t) {
+    for (int t = 0; t < nchunk; ++t) {
       const int c = chunk_of(t);
       if (chunk_visible(a, L, c) > 0) continue;
       const int i0 = c * a.query_chunk;
@@ -354,73 +382,107 @@ __device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item)
   }
   if (p >= nparts_max) return;
 
-  // this wave's tile (chunk) and its run of the partition's blocks
-  const int c = chunk_of(tile);
-  const int i0 = c * a.query_chunk;
-  const int nv = min(a.query_chunk, nq - i0);
-  const int rows = nv * G;
-  const int l_vis = chunk_visible(a, L, c);
-  const int l_first = l_vis - nv + 1;
-  const int t0 = min(t0_all, max(l_vis, 0));
-  const int nparts = parts_of(c);
-  // lane row n repeats real rows past the chunk's last one
-  const int r = (lane & 15) % rows;
-  const int qi = i0 + r / G;
-  WA wave(a.scale_log2);
-  wave.start(a.q + (((size_t)b * nq + qi) * Hq + (size_t)g * G + r % G) * D, nq - 1 - qi);
   const char* kpool = reinterpret_cast<const char*>(a.k) + (size_t)g * WA::kTileBytes;
   const char* vpool = reinterpret_cast<const char*>(a.v) + (size_t)g * WA::kTileBytes;
   const int32_t* table_row = a.table + (size_t)b * a.max_blocks_per_seq;
   const size_t block_bytes = (size_t)a.num_kv_heads * WA::kTileBytes;
+  // the partition's first block: chunk 0's (several chunks come only without a shared prefix)
+  const int j_begin = (min(t0_all, max(chunk_visible(a, L, chunk_of(0)), 0)) + p * Tp) / kBlockTokens;
   auto block_end = [&](int lv, int parts) {  // end block of this partition for a chunk limit lv
+    const int t0 = min(t0_all, max(lv, 0));
     return p < parts ? (min(lv, t0 + (p + 1) * Tp) + kBlockTokens - 1) / kBlockTokens : 0;
   };
-  const int j_begin = (t0 + p * Tp) / kBlockTokens;
+
+  // One chunk's rows in a wavefront: lane row n repeats real rows past the
+  // chunk's last one.
+  struct ChunkRows {
+    int c, rows, l_vis, l_first, nparts;
+  };
+  auto setup = [&](WA& wv, int c) {
+    const int i0 = c * a.query_chunk;
+    const int nv = min(a.query_chunk, nq - i0);
+    ChunkRows cr{c, nv * G, chunk_visible(a, L, c), 0, parts_of(c)};
+    cr.l_first = cr.l_vis - nv + 1;
+    const int r = (lane & 15) % cr.rows;
+    const int qi = i0 + r / G;
+    wv.start(a.q + (((size_t)b * nq + qi) * Hq + (size_t)g * G + r % G) * D, nq - 1 - qi);
+    return cr;
+  };
+
+  // Publish the wavefronts' states of the tiles [t_first, t_first + nt)
+  // (wavefront w holds tile t_first + w % nt; `publishes` false: it holds
+  // none of them), merge the slices of each in a fixed order and store
+  // final rows or partial states.
+  auto epilogue = [&](const WA& wv, int rows, bool publishes, int t_first, int nt, int sl, int& any_bad, bool first) {
+    if (publishes) publish(sh, wv, w, lane, rows);
+    __syncthreads();
+    row_weights(sh, nt, sl);
+    if (first) {
+      any_bad = 0;
+#pragma unroll
+      for (int x = 0; x < kWaves; ++x) any_bad |= sh.bad[x];
+    }
+    for (int t = 0; t < nt; ++t) {
+      const int ct = chunk_of(t_first + t);
+      const int ct_parts = parts_of(ct);
+      if (p >= ct_parts) continue;  // the chunk sees nothing in this partition
+      const int ci0 = ct * a.query_chunk;
+      const int crows = min(a.query_chunk, nq - ci0) * G;
+      const bool single = ct_parts == 1 && min(t0_all, chunk_visible(a, L, ct)) == 0;
+      for (int idx = tid; idx < crows * (D / 4); idx += kWaves * kWaveSize) {  // 4 columns per thread
+        const int h = idx / (D / 4);
+        const int d0 = 4 * (idx % (D / 4));
+        float acc[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[e] = any_bad ? __builtin_nanf("") : combine(sh, t, nt, sl, h, d0 + e);
+        const size_t row = ((size_t)b * nq + ci0 + h / G) * Hq + (size_t)g * G + h % G;
+        if (single)
+          store_final4(a.out + row * D + d0, acc, sh.lsum[t][h]);
+        else
+          store_partial4(a, row * a.slots_per_row + a.prefix_partitions + p, d0, D, acc, sh.mx[t][h], sh.lsum[t][h]);
+      }
+    }
+  };
+
+  WA wave(a.scale_log2);
+  const ChunkRows ca = setup(wave, chunk_of(tile));
   if (MODE == kModeRegister && ntile != 1) return;  // not this launch's kind (never: the host picks the mode)
+  int any_bad = 0;
   if (ntile == 1) {  // one tile: the 4 wavefronts split the blocks, tiles into registers
-    const int j_end = block_end(l_vis, nparts);
+    const int j_end = block_end(ca.l_vis, ca.nparts);
     const int per_slice = (j_end - j_begin + kWaves - 1) / kWaves;
     const int wj0 = min(j_end, j_begin + w * per_slice);
     const int wj1 = min(j_end, wj0 + per_slice);
-    wave.run(table_row, wj0, wj1, L, l_first, max(l_vis, 0), kpool, vpool, block_bytes, a.num_blocks);
+    wave.run(table_row, wj0, wj1, L, ca.l_first, max(ca.l_vis, 0), kpool, vpool, block_bytes, a.num_blocks);
   } else if constexpr (MODE != kModeRegister) {  // several tiles: every block staged once through LDS for all of them
     int J1 = j_begin;
-    for (int t = 0; t < ntile; ++t) {
+    for (int t = 0; t < nchunk; ++t) {
       const int ct = chunk_of(t);
       J1 = max(J1, block_end(chunk_visible(a, L, ct), parts_of(ct)));
     }
-    run_staged(wave, lds.st, table_row, j_begin, J1, block_end(l_vis, nparts), slice < slices, slice, slices, L,
-               l_first, max(l_vis, 0), kpool, vpool, block_bytes, a.num_blocks);
+    if constexpr (MODE == kModeWide) {
+      if (two) {
+        const bool has_b = tile + kWaves < nchunk;
+        WA wave_b(a.scale_log2);
+        const ChunkRows cb = setup(wave_b, chunk_of(has_b ? tile + kWaves : tile));
+        run_staged<D, kStepBlocks, 2>(wave, wave_b, lds.st, table_row, j_begin, J1, block_end(ca.l_vis, ca.nparts),
+                                      has_b ? block_end(cb.l_vis, cb.nparts) : 0, true, 0, 1, L, ca.l_first,
+                                      max(ca.l_vis, 0), cb.l_first, max(cb.l_vis, 0), kpool, vpool, block_bytes,
+                                      a.num_blocks);
+        wave.finish();
+        wave_b.finish();
+        epilogue(wave, ca.rows, true, 0, kWaves, 1, any_bad, true);
+        __syncthreads();  // the second set reuses the epilogue's LDS
+        epilogue(wave_b, cb.rows, has_b, kWaves, nchunk - kWaves, 1, any_bad, false);
+        return;
+      }
+    }
+    run_staged<D, kStepBlocks, 1>(wave, wave, lds.st, table_row, j_begin, J1, block_end(ca.l_vis, ca.nparts), 0,
+                                  slice < slices, slice, slices, L, ca.l_first, max(ca.l_vis, 0), 0, 0, kpool, vpool,
+                                  block_bytes, a.num_blocks);
   }
   wave.finish();
-  publish(sh, wave, w, lane, rows);
-  __syncthreads();
-  row_weights(sh, ntile, slices);
-
-  // ---- per chunk: merge its slices in a fixed order; final rows or partial states ----
-  int any_bad = 0;
-#pragma unroll
-  for (int x = 0; x < kWaves; ++x) any_bad |= sh.bad[x];
-  for (int t = 0; t < ntile; ++t) {
-    const int ct = chunk_of(t);
-    const int ct_parts = parts_of(ct);
-    if (p >= ct_parts) continue;  // the chunk sees nothing in this partition
-    const int ci0 = ct * a.query_chunk;
-    const int crows = min(a.query_chunk, nq - ci0) * G;
-    const bool single = ct_parts == 1 && min(t0_all, chunk_visible(a, L, ct)) == 0;
-    for (int idx = tid; idx < crows * (D / 4); idx += kWaves * kWaveSize) {  // 4 columns per thread
-      const int h = idx / (D / 4);
-      const int d0 = 4 * (idx % (D / 4));
-      float acc[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) acc[e] = any_bad ? __builtin_nanf("") : combine(sh, t, ntile, slices, h, d0 + e);
-      const size_t row = ((size_t)b * nq + ci0 + h / G) * Hq + (size_t)g * G + h % G;
-      if (single)
-        store_final4(a.out + row * D + d0, acc, sh.lsum[t][h]);
-      else
-        store_partial4(a, row * a.slots_per_row + a.prefix_partitions + p, d0, D, acc, sh.mx[t][h], sh.lsum[t][h]);
-    }
-  }
+  epilogue(wave, ca.rows, true, 0, ntile, slices, any_bad, true);
 }
 
 template <int D, int MODE>
@@ -470,8 +532,8 @@ __device__ void prefix_item(const StepArgs& a, PassLds<D, MODE>& lds, int pitem)
     const int wj1 = min(j_end, wj0 + per_slice);
     wave.run(table_row, wj0, wj1, plen, plen, plen, kpool, vpool, block_bytes, a.num_blocks);
   } else if constexpr (MODE != kModeRegister) {  // several tiles: every block staged once through LDS for all of them
-    run_staged(wave, lds.st, table_row, j_begin, j_end, j_end, slice < slices, slice, slices, plen, plen, plen,
-               kpool, vpool, block_bytes, a.num_blocks);
+    run_staged<D, kStepBlocks, 1>(wave, wave, lds.st, table_row, j_begin, j_end, j_end, 0, slice < slices, slice,
+                                  slices, plen, plen, plen, 0, 0, kpool, vpool, block_bytes, a.num_blocks);
   }
   wave.finish();
   publish(sh, wave, w, lane, tile_rows);
@@ -494,9 +556,10 @@ __device__ void prefix_item(const StepArgs& a, PassLds<D, MODE>& lds, int pitem)
   }
 }
 
-// Occupancy: 3 wavefronts per SIMD (12 per compute unit) at most 168 VGPRs.
+// Occupancy: 3 wavefronts per SIMD (12 per compute unit) at most 168 VGPRs;
+// the wide variant 2 (256 VGPRs).
 template <int D, int MODE>
-__global__ void __launch_bounds__(kWaves * kWaveSize) __attribute__((amdgpu_waves_per_eu(3)))
+__global__ void __launch_bounds__(kWaves * kWaveSize) __attribute__((amdgpu_waves_per_eu(MODE == kModeWide ? 2 : 3)))
 partition_kernel(const StepArgs a) {
   __shared__ __align__(16) PassLds<D, MODE> lds;
   const int item = a.order ? a.order[blockIdx.x] : (int)blockIdx.x;  // no order: every item runs at once
@@ -518,7 +581,9 @@ hipError_t launch_d(const StepArgs& a, hipStream_t stream) {
   const bool one = a.num_query_chunks % kWaves == 1 || groups;
   const bool several = a.num_query_chunks >= 2 || (groups && a.max_group_size * a.group > kRows);
   const dim3 block(kWaves * kWaveSize);
-  if (one && !several)
+  if (a.chunks_per_group > kWaves)
+    hipLaunchKernelGGL((partition_kernel<D, kModeWide>), dim3(grid), block, 0, stream, a);
+  else if (one && !several)
     hipLaunchKernelGGL((partition_kernel<D, kModeRegister>), dim3(grid), block, 0, stream, a);
   else
     hipLaunchKernelGGL((partition_kernel<D, kModeMixed>), dim3(grid), block, 0, stream, a);

@@ -207,12 +207,15 @@ def test_append_and_graph_validation():
 
 def test_multi_token_plan():
     # n new tokens per sequence: query chunks of min(n, 16 // G) tokens; one
-    # work item per (partition, sequence, KV head, group of up to 4 chunks)
+    # work item per (partition, sequence, KV head, group of chunks): up to 4,
+    # or up to 8 when there are more than 4
     d = pda.pda_plan(llama(num_query_tokens=4, partition_tokens=4096))     # G = 4: one chunk
     assert d["workspace_bytes"] == 256 * 8 * 4
     d = pda.pda_plan(llama(num_query_tokens=7, partition_tokens=4096))     # two chunks, one item
     assert d["workspace_bytes"] == 256 * 8 * 4
-    d = pda.pda_plan(llama(num_query_tokens=17, partition_tokens=4096))    # five chunks, two items
+    d = pda.pda_plan(llama(num_query_tokens=17, partition_tokens=4096))    # five chunks: one item of up to 8
+    assert d["workspace_bytes"] == 256 * 8 * 4
+    d = pda.pda_plan(llama(num_query_tokens=33, partition_tokens=4096))    # nine chunks, two items
     assert d["workspace_bytes"] == 256 * 8 * 2 * 4
     d = pda.pda_plan(llama(num_query_tokens=4, partition_tokens=2048))     # 2 partitions: partials per row
     assert d["workspace_bytes"] == 256 * 4 * 32 * 2 * (128 + 2) * 4 + 2 * 256 * 8 * 4

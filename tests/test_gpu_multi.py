@@ -58,8 +58,13 @@ CASES = [  # (Hq, Hkv, D, n): rows per work item = min(n, 16 // G) * G
     (8, 2, 64, 1),     # a decode step given as [B][1][Hq][D]
     (8, 1, 128, 8),    # G=8: 4 chunks in one work item, one 16-row tile per wavefront
     (32, 8, 128, 13),  # G=4: 4 chunks (3 full, 1 partial) in one item
-    (32, 8, 64, 21),   # G=4: 6 chunks, i.e. two items (4 + 2 chunks)
+    (32, 8, 64, 21),   # G=4: 6 chunks in one item, two tiles on wavefronts 0-1
     (4, 4, 128, 40),   # G=1: 3 chunks (16 + 16 + 8 tokens)
+    (32, 8, 128, 32),  # G=4: 8 chunks in one item, two tiles per wavefront
+    (8, 1, 128, 12),   # G=8: 6 chunks, two tiles on wavefronts 0-1
+    (12, 4, 128, 26),  # G=3: 6 chunks of 5 tokens (the last one 1), 15 rows each
+    (32, 8, 128, 37),  # G=4: 10 chunks, two items (8 + 2 chunks)
+    (32, 8, 128, 64),  # G=4: 16 chunks, two items of 8
 ]
 
 
@@ -90,10 +95,11 @@ def test_one_token_equals_decode_step(dev):
     assert np.array_equal(a, b[:, 0])
 
 
-def test_multi_token_poison_and_shuffle_bit_identical(dev):
+@pytest.mark.parametrize("n", [4, 32])
+def test_multi_token_poison_and_shuffle_bit_identical(dev, n):
     lens = [40, 7, 900, 2047]
     st = W.custom_structure(len(lens), 32, 8, 128, lens, seed=9)
-    q = W.fill_multi_q(st, 4, dev)
+    q = W.fill_multi_q(st, n, dev)
     _, k, v = W.fill_values(st, dev, fill="nan")
     base = run_multi(st, q, k, v, dev)
     assert np.array_equal(base, run_multi(st, q, k, v, dev)), "run-to-run"

@@ -163,6 +163,16 @@ class Structure:
         bt = int(self.blocks_used().sum()) * 4
         return int(kv + q + out + bt + self.B * 4)
 
+    def algorithmic_flops(self, query_tokens: int = 1) -> int:
+        """Multiply-add work of an attention step, 2 flops each: q.k and p.v
+        (D multiply-adds each) per query head and visible context token.  New
+        token i of n sees the first L - n + 1 + i tokens of a context of L."""
+        n = int(query_tokens)
+        lens = np.maximum(self.context_lens.astype(np.int64), 0)
+        i = np.arange(n, dtype=np.int64)
+        vis = np.clip(lens[:, None] - n + 1 + i[None, :], 0, None).sum()
+        return int(vis * self.Hq * 2 * self.D * 2)
+
     def append_bytes(self, new_tokens: int = 1) -> int:
         """Bytes a KV-cache append must move: the new K and V rows read and
         written once, the block-table entry of each new token, the lengths."""
