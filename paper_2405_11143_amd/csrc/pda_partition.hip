@@ -277,17 +277,28 @@ __device__ void run_staged(WaveAttention<D>& wave, WaveAttention<D>& wave_b, Sta
     wave.v_frags(reinterpret_cast<const uint16_t*>(st.buf[buf][0] + TC),
                  reinterpret_cast<const uint16_t*>(st.buf[buf][1] + TC), aw);
     if constexpr (NT == 2) {
-      // The later chunk first: pv_staged zeroes (in aw) the V rows its last
-      // row does not see, which no row of the earlier chunk sees either; the
-      // earlier chunk's rows give the rows between them probability 0.
+      // Both chunks' score MFMAs first, back to back (a chunk that does not
+      // fold this step discards its scores), so that those of the earlier
+      // chunk run under the later chunk's softmax.  The later chunk folds
+      // first: pv_staged zeroes (in aw) the V rows its last row does not
+      // see, which no row of the earlier chunk sees either; the earlier
+      // chunk's rows give the rows between them probability 0.
+      float sc_b[2][4], sc_a[2][4];
+      wave_b.template scores<2>(kr, sc_b);
+      wave.template scores<2>(kr, sc_a);
       if (fold_b) {
         const int t_stop = j_lim_b * kBlockTokens;
         const bool tail = tok0 + 2 * kBlockTokens > min(l_first_b, t_stop);  // wave-uniform
-        const auto f = wave_b.template softmax<2>(kr, tok0, L, tail, t_stop);
+        const auto f = wave_b.template probs<2>(sc_b, tok0, L, tail, t_stop);
         wave_b.pv_staged(aw, f, tail, tok0, min(l_vis_b, t_stop));
       }
-    }
-    if (fold_a) {
+      if (fold_a) {
+        const int t_stop = j_lim * kBlockTokens;
+        const bool tail = tok0 + 2 * kBlockTokens > min(l_first, t_stop);  // wave-uniform
+        const auto f = wave.template probs<2>(sc_a, tok0, L, tail, t_stop);
+        wave.pv_staged(aw, f, tail, tok0, min(l_vis, t_stop));
+      }
+    } else {
       const int t_stop = j_lim * kBlockTokens;
       const bool tail = tok0 + 2 * kBlockTokens > min(l_first, t_stop);  // wave-uniform
       const auto f = wave.template softmax<2>(kr, tok0, L, tail, t_stop);

@@ -206,6 +206,17 @@ struct WaveAttention {
   template <int NB>
   __device__ __forceinline__ PFrag<NB> softmax(const uint4 (&kr)[NB][NC], int tok0, int L, bool tail,
                                                int t_stop = 0x7fffffff) {
+    float sc[NB][4];
+    scores<NB>(kr, sc);
+    return probs<NB>(sc, tok0, L, tail, t_stop);
+  }
+
+  // The scaled scores of NB blocks: D/32 MFMAs per block, then the scaling.
+  // The scaled scores are formed here, in the MFMAs' own basic block: the
+  // compiler did not insert the wait states a VALU read of an MFMA result
+  // needs when the first such read came after the tail branch of probs.
+  template <int NB>
+  __device__ __forceinline__ void scores(const uint4 (&kr)[NB][NC], float (&sc)[NB][4]) const {
     floatx4_t acc[NB];
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
@@ -214,14 +225,15 @@ struct WaveAttention {
       for (int c = 0; c < NC; ++c)
         acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kr[b][c]), qa[c], acc[b], 0, 0, 0);
     }
-    // The scaled scores are formed here, in the MFMAs' own basic block: the
-    // compiler did not insert the wait states a VALU read of an MFMA result
-    // needs when the first such read came after the tail branch below.
-    float sc[NB][4];
 #pragma unroll
     for (int b = 0; b < NB; ++b)
 #pragma unroll
       for (int i = 0; i < 4; ++i) sc[b][i] = mul_rounded(acc[b][i], scale_log2);
+  }
+
+  // The masking, the running max and the probabilities of scaled scores.
+  template <int NB>
+  __device__ __forceinline__ PFrag<NB> probs(float (&sc)[NB][4], int tok0, int L, bool tail, int t_stop) {
     if (tail) {
       // An empty volatile asm keeps this a branch: as selects, the masking
       // would run on every block.
