@@ -8,17 +8,23 @@
 // One 1024-thread workgroup streams one row once; the row (250-300 KB for
 // Llama-3 / Qwen vocabularies in bf16) is read with 16-byte non-temporal
 // buffer loads (descriptor = the row, so no read leaves it), four in flight
-// per thread.  With k = log2(e) / T, each thread keeps an online state:
-//   m    running max of the raw logits, and mk = fp32(m * k),
-//   s = sum 2^d,  t = sum 2^d d,  d = fma(logit, k, -mk)   (<= ~0),
-// rescaled when m outgrows mk by more than 2^32 in probability (so d <= 32).
-// The fused multiply-add rounds d once, so a large
-// common offset of the logits (+-30000, say) costs no precision, and the
-// rounding of mk shifts every d of the state by the same amount, which
-// cancels in both results below.  t is relative to mk, so t / s stays small
-// and the entropy keeps its precision in fp32.  The states are combined over
-// the workgroup in a fixed order (a wavefront butterfly, then the 16
-// wavefronts in index order), so results are reproducible.  Finally
+// per thread.  With k = log2(e) / T, each thread keeps an online state
+// relative to a reference mk (an fp32 multiple of k, never above k times the
+// largest logit it has seen):
+//   s = sum 2^d,  t = sum 2^d d,  d = fma(logit, k, -mk).
+// The hot loop computes no max: it folds a pass of 4 chunks against the
+// current reference, and only when that makes s exceed 2^64 (some logit
+// outgrew the reference by that much, or the reference is the floor of a
+// fresh state) does the thread take the pass again from its saved state,
+// with the reference moved to k times the pass's largest logit.  The first
+// pass starts from k times its first logit.  The fused multiply-add rounds d
+// once, so a large common offset of the logits (+-30000, say) costs no
+// precision, and the rounding of mk shifts every d of the state by the same
+// amount, which cancels in both results below.  t is relative to mk, so
+// t / s stays small and the entropy keeps its precision in fp32.  The states
+// are combined over the workgroup in a fixed order (a wavefront butterfly,
+// then the 16 wavefronts in index order), so results are reproducible.
+// Finally
 //   logprob = ln2 (fma(logit_tok, k, -mk) - log2 s),  entropy = ln2 (log2 s - t / s).
 // The hot loop covers whole 16-byte chunks of the vocabulary; the one partial
 // chunk at its end is handled after it, with elements past the vocabulary at
@@ -35,22 +41,20 @@ constexpr int kLpUnroll = 4;  // 16-byte loads in flight per thread
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kFloorMax = -1e30f;  // running max (raw logit units) before any finite logit
-constexpr float kLpSlack = 32.f;     // log2 of the largest probability against a stale max
+constexpr float kLpOverflow = 18446744073709551616.f;  // 2^64: s above it retakes the pass
 
 struct LpState {
-  float m, mk, s, t;  // max of the raw logits, fp32(m * k), sum 2^d, sum 2^d d
+  float mk, s, t;  // reference (fp32, k times a logit), sum 2^d, sum 2^d d
 };
 
 // Merge two states (both relative to their own mk).
 __device__ __forceinline__ LpState lp_merge(LpState a, LpState b) {
-  const bool a_big = a.m >= b.m;
-  const float MK = a_big ? a.mk : b.mk;
+  const float MK = fmaxf(a.mk, b.mk);
   const float da = a.mk - MK, db = b.mk - MK;  // <= 0
   const float fa = __builtin_amdgcn_exp2f(da);
   const float fb = __builtin_amdgcn_exp2f(db);
   // sum p (d relative to MK) = sum p (d relative to mk) + (mk - MK) sum p, rescaled
   LpState r;
-  r.m = a_big ? a.m : b.m;
   r.mk = MK;
   r.s = a.s * fa + b.s * fb;
   r.t = (a.s > 0.f ? (a.t + da * a.s) * fa : 0.f) + (b.s > 0.f ? (b.t + db * b.s) * fb : 0.f);
@@ -93,27 +97,18 @@ __global__ void __launch_bounds__(kLpThreads) logprob_kernel(const LogprobArgs a
   const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base), 0, row_bytes, 0x00020000);
   const float k = a.inv_temperature * kLog2e;
 
-  LpState st = {kFloorMax, kFloorMax * k, 0.f, 0.f};
-  // Fold one chunk of E logits into the state; `valid` elements past the
-  // vocabulary (only in the last, partial chunk) get probability 0.
-  auto fold = [&](float (&x)[E], int valid) {
-    float mx = kFloorMax;
-#pragma unroll
-    for (int e = 0; e < E; ++e)
-      if (e < valid) mx = fmaxf(mx, x[e]);
-    // The max moves only when some lane's logits outgrow it by more than
-    // 2^kLpSlack in probability (a wavefront vote), so the rescale is a rare,
-    // uniform branch; below that, probabilities against the stale max stay
-    // under 2^kLpSlack, far inside fp32.
-    if (__builtin_amdgcn_ballot_w64(mx * k > st.mk + kLpSlack) != 0 && mx > st.m) {
-      const float mk = mx * k;
-      const float dm = st.mk - mk;
-      const float sc = __builtin_amdgcn_exp2f(dm);
-      st.t = st.s > 0.f ? (st.t + dm * st.s) * sc : 0.f;
-      st.s *= sc;
-      st.m = mx;
-      st.mk = mk;
-    }
+  LpState st = {kFloorMax * k, 0.f, 0.f};
+  // Move the reference up to mk (>= st.mk) and rescale the state.
+  auto rescale_to = [&](float mk) {
+    const float dm = st.mk - mk;
+    const float sc = __builtin_amdgcn_exp2f(dm);
+    st.t = st.s > 0.f ? (st.t + dm * st.s) * sc : 0.f;
+    st.s *= sc;
+    st.mk = mk;
+  };
+  // Fold `valid` logits of a chunk against the current reference (elements
+  // past the vocabulary, only in the last, partial chunk, get probability 0).
+  auto fold = [&](const float (&x)[E], int valid) {
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       if (e < valid) {
@@ -124,6 +119,14 @@ __global__ void __launch_bounds__(kLpThreads) logprob_kernel(const LogprobArgs a
       }
     }
   };
+  // k times the largest of `valid` logits, floored
+  auto top = [&](const float (&x)[E], int valid) {
+    float mx = kFloorMax;
+#pragma unroll
+    for (int e = 0; e < E; ++e)
+      if (e < valid) mx = fmaxf(mx, x[e]);
+    return mx * k;
+  };
   auto load = [&](int c) {
     const u32x4_t t = __builtin_amdgcn_raw_buffer_load_b128(rsrc, c * 16, 0, 2);
     return make_uint4(t[0], t[1], t[2], t[3]);
@@ -132,10 +135,18 @@ __global__ void __launch_bounds__(kLpThreads) logprob_kernel(const LogprobArgs a
   // Every pass issues all its loads first (those past the row return zeros
   // and are skipped), so the last, partly filled pass costs one round trip
   // like the others.
+  bool first = true;  // the same in every thread that runs the loop
   for (int c = tid; c < nfull; c += kLpUnroll * kLpThreads) {
     uint4 u[kLpUnroll];
 #pragma unroll
     for (int j = 0; j < kLpUnroll; ++j) u[j] = load(c + j * kLpThreads);
+    if (first) {  // a reference from the pass's first logit (always a whole chunk's)
+      first = false;
+      float x[E];
+      unpack<ESIZE>(u[0], x);
+      st.mk = fmaxf(st.mk, x[0] * k);
+    }
+    const LpState saved = st;
 #pragma unroll
     for (int j = 0; j < kLpUnroll; ++j) {
       if (c + j * kLpThreads < nfull) {
@@ -144,15 +155,39 @@ __global__ void __launch_bounds__(kLpThreads) logprob_kernel(const LogprobArgs a
         fold(x, E);
       }
     }
+    if (st.s > kLpOverflow) {  // rare: again from the saved state, against the pass's max
+      st = saved;
+      float mk = st.mk;
+#pragma unroll
+      for (int j = 0; j < kLpUnroll; ++j) {
+        if (c + j * kLpThreads < nfull) {
+          float x[E];
+          unpack<ESIZE>(u[j], x);
+          mk = fmaxf(mk, top(x, E));
+        }
+      }
+      if (mk > st.mk) rescale_to(mk);
+#pragma unroll
+      for (int j = 0; j < kLpUnroll; ++j) {
+        if (c + j * kLpThreads < nfull) {
+          float x[E];
+          unpack<ESIZE>(u[j], x);
+          fold(x, E);
+        }
+      }
+    }
   }
   if (tid == nfull % kLpThreads && nfull * E < a.vocab) {  // the partial chunk (the descriptor covers it)
     float x[E];
     unpack<ESIZE>(load(nfull), x);
-    fold(x, a.vocab - nfull * E);
+    const int valid = a.vocab - nfull * E;
+    const float mk = top(x, valid);
+    if (mk > st.mk) rescale_to(mk);
+    fold(x, valid);
   }
   // ---- combine: wavefront butterfly, then the wavefronts in index order ----
   for (int o = 1; o < kWaveSize; o <<= 1) {
-    LpState other = {__shfl_xor(st.m, o), __shfl_xor(st.mk, o), __shfl_xor(st.s, o), __shfl_xor(st.t, o)};
+    LpState other = {__shfl_xor(st.mk, o), __shfl_xor(st.s, o), __shfl_xor(st.t, o)};
     st = (tid & o) ? lp_merge(other, st) : lp_merge(st, other);  // the same order in both lanes
   }
   const int w = tid / kWaveSize;

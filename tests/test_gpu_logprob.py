@@ -2,15 +2,16 @@
 oracle, through the C ABI.
 
 Bar: max-abs error <= 1e-4 on both log-probabilities and entropies (natural
-log units).  The kernel works in fp32 on d = (logit - m) / T * log2(e), m the running
-max of the raw logits:
+log units).  The kernel works in fp32 on d = logit / T * log2(e) - mk, mk a
+per-thread reference at most 2^64 (in probability) below the running max:
 - the difference is taken on the raw values, so a large common offset costs
   nothing; rounding d costs at most |d| * 2^-24 (< 3e-6 here);
 - each thread sums about 130 terms in order and 16 + 64 partial states are
   merged, so the relative error of the sums stays below ~1e-5, i.e. ~1e-5
   after the logarithm;
-- the entropy is formed from sum p (y - m) relative to the running max, so
-  its error scales with the entropy (< 12 nats here), not with |y|.
+- the entropy is formed from sum p d relative to the reference, so its error
+  scales with the entropy and the reference's distance from the max (at most
+  64 in log2 units), not with |y|.
 1e-4 leaves several times that margin.
 """
 import numpy as np
@@ -110,3 +111,34 @@ def test_no_entropy_output(dev):
     assert ent is None
     ref_lp, _ = oracle.logprob(W.bf16_bits(x), tok, 1.0, entropy=False)
     assert np.abs(lp.cpu().numpy() - ref_lp).max() <= TOL
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32], ids=["bf16", "f32"])
+def test_rising_logits_retake_passes(dev, dtype):
+    """Rows whose logits outgrow each thread's reference within a pass (a
+    ramp, a jump from -1e4 to +1e4, -inf before the only finite logit, a
+    sharp temperature), so that passes are taken again against their max,
+    and a row whose first logit is its max (never)."""
+    V = 40000
+    x, tok = W.make_logits(6, V, seed=21, device=dev, dtype=torch.float32)
+    x[0] = torch.arange(V, device=dev, dtype=torch.float32) * 0.01
+    x[1, : V // 2], x[1, V // 2:] = -1e4, 1e4
+    x[2] = float("-inf")
+    x[2, V - 3] = 5.0
+    tok[2] = V - 3
+    x[3, 0] = 60.0
+    x[4] = x[4] * 8
+    x = x.to(dtype)
+    for inv_t in (1.0, 25.0):
+        lp, ent = pda_token_logprobs(x, torch.from_numpy(tok).to(dev), inv_t)
+        torch.cuda.synchronize()
+        ref_lp, ref_ent = oracle.logprob(host_values(x), tok, np.float32(inv_t))
+        # log-probabilities down to -2e5 here: an fp32 result of that size
+        # carries a rounding of 2^-24 of itself (d is rounded once, then the
+        # log is subtracted), so their bar grows with |log p|
+        lp, ent = lp.cpu().numpy().astype(np.float64), ent.cpu().numpy().astype(np.float64)
+        e_lp = np.abs(lp - ref_lp) / (TOL + 4 * 2.0 ** -24 * np.abs(ref_lp))
+        e_ent = np.abs(ent - ref_ent)
+        print(f"rising logits {dtype} 1/T={inv_t}: logprob error / bar {e_lp.max():.2f}, "
+              f"entropy max-abs {e_ent.max():.2e}", flush=True)
+        assert e_lp.max() <= 1.0 and e_ent.max() <= TOL, (dtype, inv_t)
