@@ -109,14 +109,16 @@ def test_multi_token_poison_and_shuffle_bit_identical(dev, n):
     assert np.array_equal(base, run_multi(st, q, kz, vz, dev)), "NaN poison vs zero fill"
 
 
-def test_multi_token_full_size_sampled(dev):
-    """The Llama-3-8B decode step with 4 draft tokens per sequence to verify
-    (speculative decoding), in the launch configuration the benchmark times."""
-    st = W.make_structure("llama3_8b")
-    n = 4
+@pytest.mark.parametrize("name,n", [("llama3_8b", 4), ("llama3_8b", 32), ("llama3_70b_tp8", 16),
+                                    ("long_cot", 64)], ids=lambda x: str(x))
+def test_multi_token_full_size_sampled(dev, name, n):
+    """Full-size steps with n new tokens per sequence (4 draft tokens to
+    verify in speculative decoding; 16-64 for wide items, split contexts and
+    two chunk groups), in the launch configuration the benchmark times."""
+    st = W.make_structure(name)
     plan = pda_plan(make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq,
                                  st.max_context_len, num_query_tokens=n))
-    print(f"llama3_8b x {n} tokens: plan={plan}", flush=True)
+    print(f"{name} x {n} tokens: plan={plan}", flush=True)
     _, k, v = W.fill_values(st, dev, fill="nan")
     q = W.fill_multi_q(st, n, dev)
     got = run_multi(st, q, k, v, dev)
@@ -127,7 +129,7 @@ def test_multi_token_full_size_sampled(dev):
     rows[1] = [int(np.argmin(st.context_lens)), 0, 0]
     ref = oracle.decode_multi_rows(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
                                    st.context_lens, st.scale, rows.astype(np.int32), threads=THREADS)
-    check(got[rows[:, 0], rows[:, 1], rows[:, 2]], ref, "llama3_8b 4 draft tokens, sampled rows")
+    check(got[rows[:, 0], rows[:, 1], rows[:, 2]], ref, f"{name} {n} new tokens, sampled rows")
 
 
 @pytest.mark.parametrize("factor", [-1.0, 0.0, 3.0, 25.0])
