@@ -74,9 +74,9 @@ struct Staging {
 
 // Which paths a launch compiles.  A launch whose items all have one tile
 // (every decode step without shared-prefix groups) compiles the register
-// path only (135 VGPRs at D = 128, 33 KiB of LDS); with up to 4 query chunks
-// per item both paths are compiled (168 VGPRs, 50.5 KiB); with more, the
-// wide variant also folds two tiles per wavefront (at most 256 VGPRs, 2
+// path only (136 VGPRs at D = 128, 33 KiB of LDS); with up to 4 query chunks
+// per item both paths are compiled (164 VGPRs, 50.5 KiB); with more, the
+// wide variant also folds two tiles per wavefront (229 VGPRs, 2
 // workgroups per compute unit).  Staging takes 2 blocks per step, so three
 // staging buffers (49.5 KiB at D = 128) still leave room for 3 workgroups
 // per compute unit; 4 blocks per step at 2 workgroups per compute unit
