@@ -45,7 +45,8 @@
  * Long contexts are split into partitions of `partition_tokens` tokens that
  * are processed independently; a second pass merges the partial softmax
  * states.  Pass 1 runs one workgroup per (partition, sequence, KV head,
- * group of up to 4 chunks of at most 16 / G new tokens each), largest
+ * group of up to 4 chunks of at most 16 / G new tokens each; up to 8 when
+ * there are more than 4 chunks), largest
  * partition first (a small kernel sorts the items by size on the GPU; it is
  * skipped when every item runs at once).  The partition size depends
  * only on the problem descriptor and the arithmetic of an item only on its

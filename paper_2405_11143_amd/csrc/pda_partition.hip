@@ -3,14 +3,16 @@
 // every item runs at once.  Two kinds of items share the launch:
 //
 // Regular items: (partition of a context, sequence, KV head, group of up to
-// 4 chunks of new query tokens).  A chunk holds up to 16 / G consecutive new
+// 4 chunks of new query tokens, or up to 8 when there are more than 4).  A
+// chunk holds up to 16 / G consecutive new
 // tokens of the sequence, so its query rows (token-major, then the G heads of
 // the KV head) fill one 16-row MFMA tile; a decode step has one token, i.e.
 // one chunk of G rows.  New token i of a sequence with n new tokens and
 // context length L sits at position L - n + i and sees tokens
 // t < L - n + 1 + i.  The 4 wavefronts take the item's chunks first and
 // slices of its blocks second (1 chunk: 4 contiguous runs; 2: every other
-// step of 2 blocks each; 3-4: every block), so the chunks of one item read
+// step of 2 blocks each; 3-4: every block; 5-8, the wide variant: chunks w
+// and w + 4 on wavefront w, every block), so the chunks of one item read
 // each tile on one compute unit.  Each chunk keeps its own causal range and
 // partition count.  With shared-prefix groups, a sequence's regular items
 // cover only the tokens after its group's prefix.
