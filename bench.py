@@ -2,7 +2,11 @@
 
 Default (--op decode): a step is one pda_decode call (work order + pass 1 +
 merge pass) over a whole batch: every sequence's new query token attends over
-its paged KV cache.  The default workload is the Llama-3-8B-shaped rollout
+its paged KV cache.  The timed calls are bound once (bind_decode), as a
+serving loop issues them: each step is one call into the library, which
+validates the descriptor, plans the step and launches its kernels;
+`ms_per_step_per_call_binding` gives the same step through the per-call
+Python function (its tensor checks every step).  The default workload is the Llama-3-8B-shaped rollout
 step (B=256, 32 query / 8 KV heads, head_dim 128, contexts uniform in
 [512, 4096], random block placement in a pool of the used blocks + 10%);
 inputs are synthetic and already resident in HBM when the timed region
@@ -24,8 +28,8 @@ Other steps around attention (--op):
            speculative-decoding drafts), same KV bytes, n times the rows
   append   the KV-cache append of the step's new tokens alone
   graph    append + attention as one captured HIP graph against the same
-           calls issued eagerly (default workload: the tiny batch, where
-           launch overhead dominates)
+           calls issued eagerly from bound calls (default workload: the tiny
+           batch, where launch overhead dominates)
   prefix   the shared-prefix workload (32 prompts x 8 samples) with each
            prompt's prefix attended once for its samples, against the plain
            decode step
@@ -199,18 +203,19 @@ def op_decode(args, n_tokens=1):
     import torch
 
     import workloads as W
-    from paper_2405_11143_amd import pda_decode, pda_partition_attention
+    from paper_2405_11143_amd import bind_decode, pda_decode
 
     dev, st, q, k, v, bt, lens, plan, out, ws = setup(args, n_tokens)
     stream = torch.cuda.current_stream(dev)
     kw = dict(max_context_len=st.max_context_len, partition_tokens=args.partition_tokens, workspace=ws,
               stream=stream)
+    # A serving loop binds its buffers once: each step is then one call into
+    # the library, which validates, plans and launches the whole step.
+    step = bind_decode(q, k, v, bt, lens, st.scale, out, **kw)
+    pass1 = bind_decode(q, k, v, bt, lens, st.scale, out, pass1_only=True, **kw)
 
-    def step():
+    def per_call():  # the per-call binding: Python checks and descriptor every step
         pda_decode(q, k, v, bt, lens, st.scale, out, **kw)
-
-    def pass1():
-        pda_partition_attention(q, k, v, bt, lens, st.scale, out, **kw)
 
     fn = pass1 if args.pass1_only else step
     for _ in range(args.warmup):
@@ -218,6 +223,7 @@ def op_decode(args, n_tokens=1):
     torch.cuda.synchronize()
     ms_step = timed(fn, args.steps, stream)
     ms_pass1 = ms_step if args.pass1_only else timed(pass1, args.steps, stream)
+    ms_per_call = timed(per_call, args.steps, stream)
     alg = st.algorithmic_bytes(query_tokens=n_tokens)
     value = alg / (ms_step * 1e-3) / 1e9
     cfg = W.CONFIGS[args.config]
@@ -230,6 +236,7 @@ def op_decode(args, n_tokens=1):
                          config_of(st, desc, args.config, plan, query_tokens=n_tokens,
                                    timed="pass1 only" if args.pass1_only else "full step"))
     result.update({"seq_steps_per_s": round(st.B / (ms_step * 1e-3), 1),
+                   "ms_per_step_per_call_binding": round(ms_per_call, 5),
                    "pct_of_peak": round(100.0 * value / PEAK_GBS, 2), "algorithmic_bytes_per_step": alg,
                    "roofline": roofline(alg / (ms_pass1 * 1e-3) / 1e9, ms_pass1, KERNEL,
                                         args.config if n_tokens == 1 else f"{args.config}_x{n_tokens}"),
@@ -285,7 +292,7 @@ def op_graph(args):
     import torch
 
     import workloads as W
-    from paper_2405_11143_amd import StepGraph, pda_append_kv, pda_decode
+    from paper_2405_11143_amd import StepGraph, bind_append_kv, bind_decode, pda_append_kv, pda_decode
 
     n = args.tokens
     dev, st, q, k, v, bt, lens, plan, out, ws = setup(args, n)
@@ -293,11 +300,14 @@ def op_graph(args):
     stream = torch.cuda.current_stream(dev)
     graph = StepGraph(q, kn, vn, k, v, bt, lens, st.scale, out, max_context_len=st.max_context_len,
                       partition_tokens=args.partition_tokens, workspace=ws)
+    append = bind_append_kv(kn, vn, bt, lens, k, v, max_context_len=st.max_context_len, num_q_heads=st.Hq,
+                            stream=stream)
+    attend = bind_decode(q, k, v, bt, lens, st.scale, out, max_context_len=st.max_context_len,
+                         partition_tokens=args.partition_tokens, workspace=ws, stream=stream)
 
-    def eager():
-        pda_append_kv(kn, vn, bt, lens, k, v, max_context_len=st.max_context_len, num_q_heads=st.Hq, stream=stream)
-        pda_decode(q, k, v, bt, lens, st.scale, out, max_context_len=st.max_context_len,
-                   partition_tokens=args.partition_tokens, workspace=ws, stream=stream)
+    def eager():  # the same launches issued from bound calls
+        append()
+        attend()
 
     def replay():
         graph.launch(stream)

@@ -226,20 +226,9 @@ def _workspace(prob, workspace, device):
 
 def _step(fn_name, q, k_cache, v_cache, block_table, context_lens, scale, out, max_context_len,
           partition_tokens, workspace, stream):
-    import torch
-
-    if out is None:
-        out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
-    _check_tensors(q, k_cache, v_cache, block_table, context_lens, out)
-    prob = _problem_from(q, k_cache, block_table, max_context_len, partition_tokens)
-    workspace, ws_ptr, ws_bytes = _workspace(prob, workspace, q.device)
-    rc = getattr(load_library(), fn_name)(
-        ctypes.byref(prob), q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(),
-        context_lens.data_ptr(), ctypes.c_float(scale), out.data_ptr(), ws_ptr, ws_bytes,
-        _stream_handle(stream, q.device))
-    if rc != PDA_OK:
-        raise PdaError(rc, fn_name)
-    return out
+    return bind_decode(q, k_cache, v_cache, block_table, context_lens, scale, out, max_context_len=max_context_len,
+                       partition_tokens=partition_tokens, workspace=workspace, stream=stream,
+                       pass1_only=fn_name == "pda_partition_attention")()
 
 
 def pda_decode(q, k_cache, v_cache, block_table, context_lens, scale: float, out=None, *,
@@ -278,6 +267,56 @@ def pda_append_kv(k_new, v_new, block_table, context_lens, k_cache, v_cache, *, 
                   num_q_heads: int = None, stream=None):
     """Store the K/V rows of each sequence's n new tokens (bf16 [B][n][Hkv][D])
     at positions L - n .. L - 1 of its paged cache, in place."""
+    bind_append_kv(k_new, v_new, block_table, context_lens, k_cache, v_cache, max_context_len=max_context_len,
+                   num_q_heads=num_q_heads, stream=stream)()
+
+
+class BoundCall:
+    """One entry point with its arguments bound once, for a serving loop that
+    runs the same step on the same buffers again and again: the Python checks,
+    the problem descriptor, the workspace and the stream are prepared when the
+    call is built, and each call is then a single foreign-function call (the
+    library still validates the descriptor, plans the step and launches its
+    kernels every time).  The bound tensors are kept alive and must keep their
+    storage; their contents may change between calls."""
+
+    def __init__(self, fn_name, args, keep, result=None):
+        self._fn = getattr(load_library(), fn_name)
+        self._name = fn_name
+        self._args = args
+        self._keep = keep
+        self.result = result
+
+    def __call__(self):
+        rc = self._fn(*self._args)
+        if rc != PDA_OK:
+            raise PdaError(rc, self._name)
+        return self.result
+
+
+def bind_decode(q, k_cache, v_cache, block_table, context_lens, scale: float, out=None, *, max_context_len: int,
+                partition_tokens: int = 0, workspace=None, stream=None, pass1_only: bool = False) -> BoundCall:
+    """pda_decode (or, with pass1_only, pda_partition_attention) bound to these
+    tensors and the given (else the current) stream; call it to run a step.
+    The arguments are those of pda_decode."""
+    import torch
+
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    _check_tensors(q, k_cache, v_cache, block_table, context_lens, out)
+    prob = _problem_from(q, k_cache, block_table, max_context_len, partition_tokens)
+    workspace, ws_ptr, ws_bytes = _workspace(prob, workspace, q.device)
+    args = (ctypes.byref(prob), q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(),
+            context_lens.data_ptr(), ctypes.c_float(scale), out.data_ptr(), ws_ptr, ws_bytes,
+            _stream_handle(stream, q.device))
+    keep = (prob, q, k_cache, v_cache, block_table, context_lens, out, workspace)
+    return BoundCall("pda_partition_attention" if pass1_only else "pda_decode", args, keep, out)
+
+
+def bind_append_kv(k_new, v_new, block_table, context_lens, k_cache, v_cache, *, max_context_len: int,
+                   num_q_heads: int = None, stream=None) -> BoundCall:
+    """pda_append_kv bound to these tensors and the given (else the current)
+    stream; the arguments are those of pda_append_kv."""
     import torch
 
     if k_new.dim() != 4:
@@ -294,11 +333,10 @@ def pda_append_kv(k_new, v_new, block_table, context_lens, k_cache, v_cache, *, 
     if block_table.dim() != 2 or block_table.shape[0] != B or context_lens.shape != (B,):
         raise ValueError("block_table [B][max_blocks], context_lens [B]")
     prob = make_problem(B, q_shape[2], Hkv, D, NB, block_table.shape[1], max_context_len, 0, BS, n)
-    rc = load_library().pda_append_kv(ctypes.byref(prob), k_new.data_ptr(), v_new.data_ptr(),
-                                      block_table.data_ptr(), context_lens.data_ptr(), k_cache.data_ptr(),
-                                      v_cache.data_ptr(), _stream_handle(stream, k_cache.device))
-    if rc != PDA_OK:
-        raise PdaError(rc, "pda_append_kv")
+    args = (ctypes.byref(prob), k_new.data_ptr(), v_new.data_ptr(), block_table.data_ptr(), context_lens.data_ptr(),
+            k_cache.data_ptr(), v_cache.data_ptr(), _stream_handle(stream, k_cache.device))
+    keep = (prob, k_new, v_new, block_table, context_lens, k_cache, v_cache)
+    return BoundCall("pda_append_kv", args, keep)
 
 
 class StepGraph:
