@@ -50,7 +50,9 @@ def check(got, ref, what):
 LENS = [1, 2, 3, 4, 5, 15, 16, 17, 21, 33, 64, 65, 300, 1000, 2049]
 CASES = [  # (Hq, Hkv, D, n): rows per work item = min(n, 16 // G) * G
     (32, 8, 128, 4),   # G=4: one 16-row chunk
-    (32, 8, 128, 7),   # two chunks (4 + 3 tokens)
+    (32, 8, 128, 7),   # two chunks (4 + 3 tokens): both folded by every wavefront, in registers
+    (8, 1, 128, 4),    # G=8: two chunks of 2 tokens
+    (32, 8, 64, 8),    # G=4, D=64: two full chunks
     (8, 1, 128, 2),    # G=8
     (8, 8, 128, 16),   # G=1: 16 tokens in one chunk
     (16, 1, 64, 3),    # G=16: one token per chunk
