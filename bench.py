@@ -35,7 +35,7 @@ Other steps around attention (--op):
            decode step
   logprob  log-probability of each sampled token and the entropy over the
            LM-head logits of one decode step (256 rows x 128256 Llama-3
-           vocabulary, bf16; --logits-f32, --config qwen_vocab)
+           vocabulary, bf16; --logits-f32, --config qwen_vocab, --no-entropy)
 """
 from __future__ import annotations
 
@@ -404,21 +404,22 @@ def op_logprob(args):
     tokens = torch.from_numpy(tok).to(dev)
     B, V = x.shape
     lp = torch.empty(B, dtype=torch.float32, device=dev)
-    ent = torch.empty(B, dtype=torch.float32, device=dev)
+    ent = None if args.no_entropy else torch.empty(B, dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream(dev)
 
     def step():  # on the current stream
-        pda_token_logprobs(x, tokens, 1.0, logprobs=lp, entropies=ent)
+        pda_token_logprobs(x, tokens, 1.0, entropy=not args.no_entropy, logprobs=lp, entropies=ent)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
     ms_eager = timed(step, args.steps, stream)
     ms = timed_graph(step, args.steps)
-    alg = B * V * x.element_size() + B * 4 + B * 8
+    alg = B * V * x.element_size() + B * 4 + B * (4 if args.no_entropy else 8)
     value = alg / (ms * 1e-3) / 1e9
     cfg = W.LOGIT_CONFIGS[name]
-    result = base_result(args, value, "GB/s", ms, "token log-prob + entropy HBM GB/s over the LM-head logits",
+    what = "token log-prob" if args.no_entropy else "token log-prob + entropy"
+    result = base_result(args, value, "GB/s", ms, f"{what} HBM GB/s over the LM-head logits",
                          {"workload": cfg["desc"] + f", {str(dtype).split('.')[-1]} logits", "name": name,
                           "rows": B, "vocab": V}, dtype="bf16" if dtype == torch.bfloat16 else "f32")
     result["config"]["timed"] = "HIP graph of the timed calls (GPU time); ms_per_call_eager: issued from Python"
@@ -436,6 +437,8 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--op", default="decode", choices=["decode", "multi", "append", "graph", "logprob", "prefix"])
     ap.add_argument("--logits-f32", action="store_true", help="--op logprob: float32 logits (default bf16)")
+    ap.add_argument("--no-entropy", action="store_true",
+                    help="--op logprob: log-probabilities only (what a rollout records), no entropies")
     ap.add_argument("--config", default=None, help="workload (default: llama3_8b; tiny for --op graph)")
     ap.add_argument("--tokens", type=int, default=None,
                     help="new tokens per sequence (--op multi: 4; append, graph: 1)")

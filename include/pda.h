@@ -217,7 +217,8 @@ int pda_step_graph_destroy(pda_step_graph *graph);
  * loss uses the entropy of the same distribution (Appendix C).  With
  * x_j = logits[r][j] * inv_temperature over j in [0, vocab):
  *   logprobs[r]  = x_{tokens[r]} - log sum_j exp(x_j)
- *   entropies[r] = -sum_j p_j log p_j,  p = softmax(x)      (skipped if NULL)
+ *   entropies[r] = -sum_j p_j log p_j,  p = softmax(x)      (skipped if NULL:
+ *   a leaner kernel then runs, with bitwise the same log-probabilities)
  * in natural-log units.  logits: device rows of `vocab` values (bf16 for
  * PDA_DTYPE_BF16, fp32 for PDA_DTYPE_F32), row r starting at element
  * r * row_stride (row_stride >= vocab); the buffer holds num_rows * row_stride

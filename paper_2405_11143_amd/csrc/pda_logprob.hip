@@ -80,8 +80,10 @@ __device__ __forceinline__ void unpack(const uint4 u, float (&f)[16 / ESIZE]) {
   }
 }
 
-// ESIZE: bytes per logit (2 = bf16, 4 = fp32).
-template <int ESIZE>
+// ESIZE: bytes per logit (2 = bf16, 4 = fp32).  ENTROPY: whether t (and the
+// entropy) is accumulated; without it a logit costs two VALU instructions
+// less, for callers that record log-probabilities only.
+template <int ESIZE, bool ENTROPY>
 __global__ void __launch_bounds__(kLpThreads) logprob_kernel(const LogprobArgs a) {
   constexpr int E = 16 / ESIZE;  // logits per 16-byte load
   __shared__ LpState s_state[kLpThreads / kWaveSize];
@@ -115,7 +117,7 @@ __global__ void __launch_bounds__(kLpThreads) logprob_kernel(const LogprobArgs a
         const float d = fmaf(x[e], k, -st.mk);
         const float p = __builtin_amdgcn_exp2f(d);
         st.s += p;
-        st.t = fmaf(p, fmaxf(d, kFloorMax), st.t);  // p = 0 exactly where d = -inf: adds 0
+        if constexpr (ENTROPY) st.t = fmaf(p, fmaxf(d, kFloorMax), st.t);  // p = 0 exactly where d = -inf: adds 0
       }
     }
   };
@@ -208,17 +210,23 @@ __global__ void __launch_bounds__(kLpThreads) logprob_kernel(const LogprobArgs a
       lp = __builtin_nanf("");
     }
     a.logprobs[row] = lp;
-    if (a.entropies) a.entropies[row] = kLn2 * (log2s - r.t / r.s);
+    if (ENTROPY) a.entropies[row] = kLn2 * (log2s - r.t / r.s);
   }
 }
 
 }  // namespace
 
 hipError_t launch_logprob(const LogprobArgs& a, hipStream_t stream) {
-  if (a.elem_bytes == 2)
-    hipLaunchKernelGGL(logprob_kernel<2>, dim3(a.num_rows), dim3(kLpThreads), 0, stream, a);
+  const dim3 grid(a.num_rows), block(kLpThreads);
+  const bool ent = a.entropies != nullptr;
+  if (a.elem_bytes == 2 && ent)
+    hipLaunchKernelGGL((logprob_kernel<2, true>), grid, block, 0, stream, a);
+  else if (a.elem_bytes == 2)
+    hipLaunchKernelGGL((logprob_kernel<2, false>), grid, block, 0, stream, a);
+  else if (a.elem_bytes == 4 && ent)
+    hipLaunchKernelGGL((logprob_kernel<4, true>), grid, block, 0, stream, a);
   else if (a.elem_bytes == 4)
-    hipLaunchKernelGGL(logprob_kernel<4>, dim3(a.num_rows), dim3(kLpThreads), 0, stream, a);
+    hipLaunchKernelGGL((logprob_kernel<4, false>), grid, block, 0, stream, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

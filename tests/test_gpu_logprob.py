@@ -66,6 +66,10 @@ def test_full_size(dev, name, dtype):
     compare(lp, ent, ref_lp, ref_ent, f"{name} {dtype}")
     lp2, ent2 = pda_token_logprobs(x, torch.from_numpy(tok).to(dev), 1.0)
     assert torch.equal(lp, lp2) and torch.equal(ent, ent2), "run-to-run"
+    # the log-probabilities-only kernel sums the same terms in the same order
+    lp3, none = pda_token_logprobs(x, torch.from_numpy(tok).to(dev), 1.0, entropy=False)
+    torch.cuda.synchronize()
+    assert none is None and torch.equal(lp, lp3), "without entropies"
 
 
 @pytest.mark.parametrize("V,stride", [(1001, 1008), (7, 8), (1, 8), (33000, 33024)])
