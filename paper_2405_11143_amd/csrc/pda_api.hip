@@ -5,6 +5,8 @@
 // state between calls.
 #include <math.h>
 
+#include <stdint.h>
+
 #include <algorithm>
 #include <new>
 
@@ -92,7 +94,9 @@ int make_plan(const pda_problem* p, const pda_prefix_groups* groups, Plan* plan)
   int tp = p->partition_tokens;
   if (tp == 0) {
     const int64_t len = p->max_context_len > 0 ? p->max_context_len : 1;
-    int64_t share = (units * len / 2 + kConcurrentItems - 1) / kConcurrentItems;
+    // (a product that would overflow only means: as long as allowed)
+    int64_t share = units > (INT64_MAX / 4) / len ? INT64_MAX / 4
+                                                  : (units * len / 2 + kConcurrentItems - 1) / kConcurrentItems;
     if (std::min(nqc, cpg) * qc * G >= pda::kMaxGroup) share = share * kRowsShareNum / kRowsShareDen;
     if (share > kMaxPartitionTokens) {
       const int64_t pieces = (len + kMaxPartitionTokens - 1) / kMaxPartitionTokens;

@@ -110,6 +110,11 @@ def test_plan_partition_choice():
     assert plan(max_context_len=0)[:2] == (16, 1)
     # a forced size is kept
     assert plan(partition_tokens=16)[:2] == (16, 256)
+    # sizes whose work estimate overflows 64 bits: the grid bound rejects them
+    with pytest.raises(pda.PdaError) as e:
+        plan(num_seqs=2 ** 20, num_q_heads=16, num_kv_heads=16, max_blocks_per_seq=2 ** 27,
+             max_context_len=2 ** 31 - 16, num_blocks=10 ** 9)
+    assert e.value.status == pda.pda.PDA_ERR_SHAPE
 
 
 def call(fn, p, q=0x1000, k=0x1000, v=0x1000, bt=0x1000, lens=0x1000, scale=0.125, out=0x1000,
