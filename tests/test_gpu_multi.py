@@ -70,6 +70,20 @@ CASES = [  # (Hq, Hkv, D, n): rows per work item = min(n, 16 // G) * G
 ]
 
 
+def test_many_chunk_groups(dev):
+    """128 new tokens at G = 4: 32 query chunks in 4 wide work items per
+    (partition, sequence, KV head), every element against the oracle."""
+    lens = [1, 200, 700, 3000, 128, 1500]
+    n = 128
+    st = W.custom_structure(len(lens), 32, 8, 128, lens, seed=73)
+    _, k, v = W.fill_values(st, dev, fill="nan")
+    q = W.fill_multi_q(st, n, dev)
+    ref = oracle.decode_multi(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
+                              st.context_lens, st.scale, threads=THREADS)
+    got = run_multi(st, q, k, v, dev)
+    check(got, ref, "128 new tokens, 4 chunk groups")
+
+
 @pytest.mark.parametrize("Hq,Hkv,D,n", CASES, ids=lambda x: str(x))
 @pytest.mark.parametrize("partition_tokens", [0, 16, 64])
 def test_multi_token_parity(dev, Hq, Hkv, D, n, partition_tokens):

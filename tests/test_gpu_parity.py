@@ -210,12 +210,34 @@ def test_full_config_sampled(dev, name):
     check(got[rows[:, 0], rows[:, 1]], ref, f"{name} sampled rows")
 
 
-@pytest.mark.parametrize("Hq,Hkv,n", [(8, 1, 1), (16, 2, 1), (8, 1, 12), (32, 8, 24)], ids=str)
+def test_long_contexts_sampled(dev):
+    """Contexts up to 64K tokens with the automatic partition size (16
+    partitions, so the merge takes its general path), sampled rows against
+    the oracle, including every row of the longest context's first KV head."""
+    lens = [65536, 40000, 1, 17, 8191, 65535, 30000, 4096, 100, 65520, 12345, 2]
+    st = W.custom_structure(len(lens), 32, 8, 128, lens, seed=71)
+    plan = pda_plan(make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq,
+                                 st.max_context_len))
+    print(f"long contexts: plan={plan}", flush=True)
+    assert plan["num_partitions"] > 8
+    q, k, v = W.fill_values(st, dev, fill="nan")
+    got = run(st, q, k, v, dev)
+    assert np.isfinite(got).all()
+    r = np.random.default_rng(72)
+    rows = np.stack([r.integers(0, st.B, 48), r.integers(0, st.Hq, 48)], axis=1)
+    rows = np.concatenate([rows, np.stack([np.zeros(4, int), np.arange(4)], axis=1)]).astype(np.int32)
+    ref = oracle.decode_rows(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
+                             st.context_lens, st.scale, rows, threads=THREADS)
+    check(got[rows[:, 0], rows[:, 1]], ref, "long contexts, sampled rows")
+
+
+@pytest.mark.parametrize("Hq,Hkv,n", [(8, 1, 1), (16, 2, 1), (8, 1, 12), (32, 8, 24), (32, 8, 40)], ids=str)
 def test_work_order_placements(dev, Hq, Hkv, n):
     """Steps with more work items than the GPU runs at once, so the work-order
     kernel runs: with fewer than 8 KV heads (pairs placed in octets, the last
     one partial: 301 sequences x 10 partitions) and with 8 (KV heads kept on
-    their XCD), with one and with two groups of query chunks per item."""
+    their XCD), with one group of query chunks per (sequence, KV head) and
+    with two (40 new tokens: 10 chunks in groups of 8 and 2)."""
     r = np.random.default_rng(Hq * 7 + n)
     lens = [int(x) for x in r.integers(n, 600, 301)]
     st = W.custom_structure(len(lens), Hq, Hkv, 128, lens, seed=60 + n)
@@ -227,7 +249,8 @@ def test_work_order_placements(dev, Hq, Hkv, n):
     G = Hq // Hkv
     chunks = -(-n // max(1, 16 // G))
     pairs = plan["num_partitions"] * st.B
-    items = pairs * Hkv * -(-chunks // 4)
+    per_item = 8 if chunks > 4 else 4  # chunks per work item
+    items = pairs * Hkv * -(-chunks // per_item)
     assert items > 768 and (Hkv % 8 == 0 or pairs % 8 != 0), (items, pairs)
     bt, ln = gpu_tensors(st, dev)
     got = pda_decode(q, k, v, bt, ln, st.scale, max_context_len=st.max_context_len,
