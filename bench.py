@@ -21,7 +21,9 @@ Prints one JSON line:
              (HIP events on its stream), against the 8 TB/s HBM peak;
              `traffic` is the measured HBM bytes per launch from rocprofv3
              counters when they were taken on this kernel source
-  cpu_baseline  the fp64 oracle on the host cores, same workload
+  cpu_baseline  the fp64 oracle on the host cores, same workload (and, as
+             one_thread, on one core over the batch's first 16 sequences)
+  ms_per_step_median / _min  single steps timed one by one (a separate pass)
 
 Other steps around attention (--op):
   multi    n new query tokens per sequence (--tokens, default 4: verifying
@@ -87,6 +89,8 @@ def measured_traffic(kernel: str, workload: str):
 
 
 def cpu_baseline(st, q, k, v, min_seconds: float, max_reps: int):
+    import numpy as np
+
     import oracle
     import workloads as W
 
@@ -99,11 +103,28 @@ def cpu_baseline(st, q, k, v, min_seconds: float, max_reps: int):
         t_total += time.perf_counter() - t0
         reps += 1
     per_step = t_total / reps
+    # the same oracle on one thread, over the first sequences of the batch
+    nb = min(st.B, 16)
+    lens = st.context_lens[:nb]
+    blocks = int(((lens.astype(np.int64).clip(0) + st.block_size - 1) // st.block_size).sum())
+    sub_bytes = (int(lens.astype(np.int64).clip(0).sum()) * st.Hkv * st.D * 2 * 2
+                 + nb * st.Hq * st.D * (2 + 4) + blocks * 4 + nb * 4)
+    reps1, t1 = 0, 0.0
+    while reps1 < max_reps and (reps1 == 0 or t1 < min_seconds / 2):
+        t0 = time.perf_counter()
+        oracle.decode(qb[:nb], kb, vb, st.block_table[:nb], lens, st.scale, threads=1)
+        t1 += time.perf_counter() - t0
+        reps1 += 1
+    one = t1 / reps1
     return {"value": round(st.algorithmic_bytes() / per_step / 1e9, 4), "unit": "GB/s",
             "seq_steps_per_s": round(st.B / per_step, 3), "s_per_step": round(per_step, 4),
             "cores": threads, "kind": "oracle",
             "sample": f"the full {st.name} step (all {st.B} sequences x {st.Hq} heads), "
-                      f"{reps} repetition(s), {t_total:.1f} s total, fp64, {threads} threads"}
+                      f"{reps} repetition(s), {t_total:.1f} s total, fp64, {threads} threads",
+            "one_thread": {"value": round(sub_bytes / one / 1e9, 4), "unit": "GB/s",
+                           "seq_steps_per_s": round(nb / one, 3), "cores": 1,
+                           "sample": f"the first {nb} sequences of the step, {reps1} repetition(s), "
+                                     f"{t1:.1f} s total, fp64, 1 thread"}}
 
 
 def timed(fn, n, stream):
@@ -118,6 +139,21 @@ def timed(fn, n, stream):
     e1.record(stream)
     torch.cuda.synchronize()
     return e0.elapsed_time(e1) / n
+
+
+def timed_each(fn, n, stream):
+    """Median and minimum ms of single calls of fn (HIP events around each)."""
+    import torch
+
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    torch.cuda.synchronize()
+    for a, b in evs:
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    ms = sorted(a.elapsed_time(b) for a, b in evs)
+    return ms[len(ms) // 2], ms[0]
 
 
 def timed_graph(fn, n):
@@ -224,6 +260,7 @@ def op_decode(args, n_tokens=1):
     ms_step = timed(fn, args.steps, stream)
     ms_pass1 = ms_step if args.pass1_only else timed(pass1, args.steps, stream)
     ms_per_call = timed(per_call, args.steps, stream)
+    ms_median, ms_min = timed_each(fn, args.steps, stream)  # a separate pass: one event pair per step
     alg = st.algorithmic_bytes(query_tokens=n_tokens)
     value = alg / (ms_step * 1e-3) / 1e9
     cfg = W.CONFIGS[args.config]
@@ -237,6 +274,7 @@ def op_decode(args, n_tokens=1):
                                    timed="pass1 only" if args.pass1_only else "full step"))
     result.update({"seq_steps_per_s": round(st.B / (ms_step * 1e-3), 1),
                    "ms_per_step_per_call_binding": round(ms_per_call, 5),
+                   "ms_per_step_median": round(ms_median, 5), "ms_per_step_min": round(ms_min, 5),
                    "pct_of_peak": round(100.0 * value / PEAK_GBS, 2), "algorithmic_bytes_per_step": alg,
                    "roofline": roofline(alg / (ms_pass1 * 1e-3) / 1e9, ms_pass1, KERNEL,
                                         args.config if n_tokens == 1 else f"{args.config}_x{n_tokens}"),
