@@ -6,10 +6,13 @@ its paged KV cache.  The timed calls are bound once (bind_decode), as a
 serving loop issues them: each step is one call into the library, which
 validates the descriptor, plans the step and launches its kernels;
 `ms_per_step_per_call_binding` gives the same step through the per-call
-Python function (its tensor checks every step).  The default workload is the Llama-3-8B-shaped rollout
-step (B=256, 32 query / 8 KV heads, head_dim 128, contexts uniform in
-[512, 4096], random block placement in a pool of the used blocks + 10%);
-inputs are synthetic and already resident in HBM when the timed region
+Python function (its tensor checks every step), and
+`ms_per_step_order_reused` the step as a model's later layers run it
+(pda_decode_reusing_order: the work order of the step's first layer
+reused).  The default workload is the Llama-3-8B-shaped rollout step
+(B=256, 32 query / 8 KV heads, head_dim 128, contexts uniform in [512,
+4096], random block placement in a pool of the used blocks + 10%); inputs
+are synthetic and already resident in HBM when the timed region
 starts.
 
 Prints one JSON line:
@@ -249,6 +252,8 @@ def op_decode(args, n_tokens=1):
     # the library, which validates, plans and launches the whole step.
     step = bind_decode(q, k, v, bt, lens, st.scale, out, **kw)
     pass1 = bind_decode(q, k, v, bt, lens, st.scale, out, pass1_only=True, **kw)
+    # a model's later layers reuse the work order the step's first call left in `ws`
+    reused = bind_decode(q, k, v, bt, lens, st.scale, out, reuse_order=True, **kw)
 
     def per_call():  # the per-call binding: Python checks and descriptor every step
         pda_decode(q, k, v, bt, lens, st.scale, out, **kw)
@@ -260,6 +265,7 @@ def op_decode(args, n_tokens=1):
     ms_step = timed(fn, args.steps, stream)
     ms_pass1 = ms_step if args.pass1_only else timed(pass1, args.steps, stream)
     ms_per_call = timed(per_call, args.steps, stream)
+    ms_reused = timed(reused, args.steps, stream)
     ms_median, ms_min = timed_each(fn, args.steps, stream)  # a separate pass: one event pair per step
     alg = st.algorithmic_bytes(query_tokens=n_tokens)
     value = alg / (ms_step * 1e-3) / 1e9
@@ -274,6 +280,7 @@ def op_decode(args, n_tokens=1):
                                    timed="pass1 only" if args.pass1_only else "full step"))
     result.update({"seq_steps_per_s": round(st.B / (ms_step * 1e-3), 1),
                    "ms_per_step_per_call_binding": round(ms_per_call, 5),
+                   "ms_per_step_order_reused": round(ms_reused, 5),
                    "ms_per_step_median": round(ms_median, 5), "ms_per_step_min": round(ms_min, 5),
                    "pct_of_peak": round(100.0 * value / PEAK_GBS, 2), "algorithmic_bytes_per_step": alg,
                    "roofline": roofline(alg / (ms_pass1 * 1e-3) / 1e9, ms_pass1, KERNEL,

@@ -146,6 +146,33 @@ int pda_partition_attention(const pda_problem *prob, const void *q, const void *
 int pda_merge_partitions(const pda_problem *prob, const int32_t *context_lens, float *out,
                          const void *workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* The work order of one step's pass 1 (largest item first, placed for the
+ * XCDs), written into `workspace`: every layer of a model's decode step
+ * attends over the same lengths and block tables, so the order can be
+ * computed once per step and reused by each layer's
+ * pda_decode_reusing_order.  pda_decode leaves the same order in its
+ * workspace.  Nothing is launched when the step needs no order (all its
+ * items run at once).  Only the lengths are read; the order is a
+ * permutation of the step's work items whatever they were, so a stale one
+ * (lengths changed since) costs schedule quality, never correctness.
+ * `context_lens` is device int32 [num_seqs]; `workspace` (16 B aligned, at
+ * least pda_workspace_bytes) is caller-owned.  Errors as pda_decode's:
+ * PDA_ERR_NULL for a NULL length array, _WORKSPACE, _ALIGNMENT, and the
+ * descriptor checks; an empty batch returns PDA_OK and reads nothing. */
+int pda_work_order(const pda_problem *prob, const int32_t *context_lens, void *workspace,
+                   size_t workspace_bytes, hipStream_t stream);
+
+/* pda_decode without the work-order kernel: pass 1 takes its items in the
+ * order already in `workspace`, which a pda_work_order or pda_decode call for
+ * the same descriptor (and workspace) must have written; the partial states
+ * of the workspace are rewritten as in pda_decode.  With any other contents
+ * the kernels stay memory-safe (item indices are bounds-checked) but the
+ * output is undefined. */
+int pda_decode_reusing_order(const pda_problem *prob, const void *q, const void *k_cache,
+                             const void *v_cache, const int32_t *block_table,
+                             const int32_t *context_lens, float scale, float *out,
+                             void *workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Shared-prefix groups for parallel sampling (Section 3.2: PagedAttention
  * lets the samples of one prompt share the prompt's KV blocks).  The members
  * of group i are the sequences [group_start[i], group_start[i+1]) -- a

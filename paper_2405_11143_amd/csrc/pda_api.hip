@@ -282,6 +282,38 @@ int pda_partition_attention(const pda_problem* prob, const void* q, const void* 
   return PDA_OK;
 }
 
+int pda_work_order(const pda_problem* prob, const int32_t* context_lens, void* workspace, size_t workspace_bytes,
+                   hipStream_t stream) {
+  int rc = check_problem(prob);
+  if (rc != PDA_OK) return rc;
+  if (prob->num_seqs == 0) return PDA_OK;
+  if (!context_lens) return PDA_ERR_NULL;
+  Plan plan;
+  rc = make_plan(prob, nullptr, &plan);
+  if (rc != PDA_OK) return rc;
+  if (!workspace || workspace_bytes < plan.info.workspace_bytes) return PDA_ERR_WORKSPACE;
+  if (!aligned(workspace, 16)) return PDA_ERR_ALIGNMENT;
+  if (plan.items <= (size_t)kConcurrentItems) return PDA_OK;  // the step runs without an order
+  pda::StepArgs args;
+  fill_args(prob, &plan, workspace, &args);
+  args.lens = context_lens;
+  return pda::launch_order(args, stream) == hipSuccess ? PDA_OK : PDA_ERR_HIP;
+}
+
+int pda_decode_reusing_order(const pda_problem* prob, const void* q, const void* k_cache, const void* v_cache,
+                             const int32_t* block_table, const int32_t* context_lens, float scale, float* out,
+                             void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  Plan plan;
+  pda::StepArgs args;
+  int rc = prepare_step(prob, nullptr, q, k_cache, v_cache, block_table, context_lens, scale, out, workspace,
+                        workspace_bytes, &plan, &args);
+  if (rc != PDA_OK) return rc;
+  if (prob->num_seqs == 0) return PDA_OK;
+  if (pda::launch_partition(args, prob->head_dim, stream) != hipSuccess) return PDA_ERR_HIP;
+  if (plan.slots > 0 && pda::launch_merge(args, prob->head_dim, stream) != hipSuccess) return PDA_ERR_HIP;
+  return PDA_OK;
+}
+
 int pda_merge_partitions(const pda_problem* prob, const int32_t* context_lens, float* out, const void* workspace,
                          size_t workspace_bytes, hipStream_t stream) {
   int rc = check_problem(prob);

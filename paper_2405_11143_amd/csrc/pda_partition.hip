@@ -576,6 +576,8 @@ __global__ void __launch_bounds__(kWaves * kWaveSize) __attribute__((amdgpu_wave
 partition_kernel(const StepArgs a) {
   __shared__ __align__(16) PassLds<D, MODE> lds;
   const int item = a.order ? a.order[blockIdx.x] : (int)blockIdx.x;  // no order: every item runs at once
+  // an order reused from an earlier call is the caller's contract; never step outside the items
+  if ((unsigned)item >= (unsigned)(a.num_regular_items + a.num_groups * a.prefix_partitions * a.num_kv_heads)) return;
   if (item < a.num_regular_items)
     regular_item<D, MODE>(a, lds, item);
   else

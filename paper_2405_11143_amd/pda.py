@@ -24,7 +24,7 @@ PDA_ERR_WORKSPACE, PDA_ERR_ALIGNMENT, PDA_ERR_VALUE, PDA_ERR_HIP = 4, 5, 6, 7
 EXPORTED = ("pda_plan", "pda_workspace_bytes", "pda_decode", "pda_partition_attention",
             "pda_merge_partitions", "pda_plan_shared_prefix", "pda_decode_shared_prefix", "pda_append_kv",
             "pda_step_graph_create", "pda_step_graph_launch", "pda_step_graph_destroy", "pda_token_logprobs",
-            "pda_validate_host", "pda_status_string")
+            "pda_validate_host", "pda_work_order", "pda_decode_reusing_order", "pda_status_string")
 PDA_DTYPE_BF16, PDA_DTYPE_F32 = 0, 1
 
 
@@ -73,6 +73,8 @@ def load_library(path: str = LIB_PATH):
     step = [P, vp, vp, vp, vp, vp, ctypes.c_float, vp, vp, sz, vp]
     lib.pda_decode.argtypes = step
     lib.pda_partition_attention.argtypes = step
+    lib.pda_decode_reusing_order.argtypes = step
+    lib.pda_work_order.argtypes = [P, vp, vp, sz, vp]
     lib.pda_merge_partitions.argtypes = [P, vp, vp, vp, sz, vp]
     G = ctypes.POINTER(pda_prefix_groups)
     lib.pda_plan_shared_prefix.argtypes = [P, G, ctypes.POINTER(pda_plan_info)]
@@ -295,10 +297,12 @@ class BoundCall:
 
 
 def bind_decode(q, k_cache, v_cache, block_table, context_lens, scale: float, out=None, *, max_context_len: int,
-                partition_tokens: int = 0, workspace=None, stream=None, pass1_only: bool = False) -> BoundCall:
-    """pda_decode (or, with pass1_only, pda_partition_attention) bound to these
-    tensors and the given (else the current) stream; call it to run a step.
-    The arguments are those of pda_decode."""
+                partition_tokens: int = 0, workspace=None, stream=None, pass1_only: bool = False,
+                reuse_order: bool = False) -> BoundCall:
+    """pda_decode (or, with pass1_only, pda_partition_attention; with
+    reuse_order, pda_decode_reusing_order) bound to these tensors and the
+    given (else the current) stream; call it to run a step.  The arguments
+    are those of pda_decode."""
     import torch
 
     if out is None:
@@ -310,7 +314,27 @@ def bind_decode(q, k_cache, v_cache, block_table, context_lens, scale: float, ou
             context_lens.data_ptr(), ctypes.c_float(scale), out.data_ptr(), ws_ptr, ws_bytes,
             _stream_handle(stream, q.device))
     keep = (prob, q, k_cache, v_cache, block_table, context_lens, out, workspace)
-    return BoundCall("pda_partition_attention" if pass1_only else "pda_decode", args, keep, out)
+    name = "pda_partition_attention" if pass1_only else "pda_decode_reusing_order" if reuse_order else "pda_decode"
+    return BoundCall(name, args, keep, out)
+
+
+def pda_work_order(prob: pda_problem, context_lens, workspace, stream=None):
+    """The step's work order into `workspace` (see include/pda.h): computed
+    once per decode step, reused by every layer's pda_decode_reusing_order."""
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    rc = load_library().pda_work_order(ctypes.byref(prob), context_lens.data_ptr(),
+                                       workspace.data_ptr() if workspace is not None else None, ws_bytes,
+                                       _stream_handle(stream, context_lens.device))
+    if rc != PDA_OK:
+        raise PdaError(rc, "pda_work_order")
+
+
+def pda_decode_reusing_order(q, k_cache, v_cache, block_table, context_lens, scale: float, out=None, *,
+                             max_context_len: int, partition_tokens: int = 0, workspace, stream=None):
+    """pda_decode with the work order already in `workspace` (pda_work_order
+    or an earlier pda_decode on it, same descriptor)."""
+    return bind_decode(q, k_cache, v_cache, block_table, context_lens, scale, out, max_context_len=max_context_len,
+                       partition_tokens=partition_tokens, workspace=workspace, stream=stream, reuse_order=True)()
 
 
 def bind_append_kv(k_new, v_new, block_table, context_lens, k_cache, v_cache, *, max_context_len: int,

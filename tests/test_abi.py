@@ -123,7 +123,7 @@ def call(fn, p, q=0x1000, k=0x1000, v=0x1000, bt=0x1000, lens=0x1000, scale=0.12
     return getattr(lib, fn)(ctypes.byref(p), q, k, v, bt, lens, ctypes.c_float(scale), out, ws, ws_bytes, None)
 
 
-@pytest.mark.parametrize("fn", ["pda_decode", "pda_partition_attention"])
+@pytest.mark.parametrize("fn", ["pda_decode", "pda_partition_attention", "pda_decode_reusing_order"])
 def test_step_validation(fn):
     lib = pda.load_library()
     assert call(fn, prob(), q=None) == pda.pda.PDA_ERR_NULL
@@ -146,6 +146,22 @@ def test_step_validation(fn):
                             None) == pda.pda.PDA_ERR_NULL
     # an empty batch is valid and launches nothing, even with NULL pointers
     assert call(fn, prob(num_seqs=0), q=None, k=None, v=None, bt=None, lens=None, out=None) == pda.pda.PDA_OK
+
+
+def test_work_order_validation():
+    lib = pda.load_library()
+    p = prob(partition_tokens=64)
+    need = pda.pda_workspace_bytes(p)
+    wo = lib.pda_work_order
+    assert wo(None, 0x1000, 0x1000, need, None) == pda.pda.PDA_ERR_NULL
+    assert wo(ctypes.byref(p), None, 0x1000, need, None) == pda.pda.PDA_ERR_NULL
+    assert wo(ctypes.byref(p), 0x1000, None, 0, None) == pda.pda.PDA_ERR_WORKSPACE
+    assert wo(ctypes.byref(p), 0x1000, 0x1000, need - 4, None) == pda.pda.PDA_ERR_WORKSPACE
+    assert wo(ctypes.byref(p), 0x1000, 0x1008, need, None) == pda.pda.PDA_ERR_ALIGNMENT
+    assert wo(ctypes.byref(prob(head_dim=80)), 0x1000, 0x1000, need, None) == pda.pda.PDA_ERR_UNSUPPORTED
+    # nothing to order (an empty batch, or every item runs at once): no launch, no device access
+    assert wo(ctypes.byref(prob(num_seqs=0)), None, None, 0, None) == pda.pda.PDA_OK
+    assert pda.pda_plan(p)["num_partitions"] > 1
 
 
 def test_merge_validation():

@@ -8,7 +8,8 @@ import torch
 
 import workloads as W
 from paper_2405_11143_amd import (bind_append_kv, bind_decode, make_problem, pda_append_kv, pda_decode,
-                                  pda_partition_attention, pda_plan)
+                                  pda_decode_reusing_order, pda_partition_attention, pda_plan, pda_work_order,
+                                  pda_workspace_bytes)
 
 pytestmark = pytest.mark.gpu
 
@@ -50,6 +51,49 @@ def test_bound_decode_matches_and_follows_contents(dev, n):
     state_bytes = st.B * n * st.Hq * parts * (st.D + 2) * 4 if parts > 1 else 0
     assert state_bytes > 0
     assert torch.equal(outs[0], outs[1]) and torch.equal(wss[0][:state_bytes], wss[1][:state_bytes])
+
+
+@pytest.mark.parametrize("n", [1, 8])
+def test_reused_work_order_matches_decode(dev, n):
+    """One work order per step, reused by every layer: bitwise pda_decode's
+    result, also when the order is stale (lengths changed since it was taken)
+    and when an earlier pda_decode left it."""
+    rng = np.random.default_rng(70 + n)
+    B = 48
+    lens = rng.integers(1, 3000, size=B).tolist()
+    st = W.custom_structure(B, 32, 8, 128, lens, seed=71 + n)
+    _, k, v = W.fill_values(st, dev, fill="nan")
+    qs = [W.fill_multi_q(st, n, dev) if n > 1 else W.fill_values(st, dev, fill="nan")[0] for _ in range(2)]
+    qs[1].mul_(0.5)
+    bt = torch.from_numpy(st.block_table).to(dev)
+    ln = torch.from_numpy(st.context_lens).to(dev)
+    kw = dict(max_context_len=st.max_context_len, partition_tokens=64)
+    prob = make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq, st.max_context_len, 64,
+                        num_query_tokens=n)
+    plan = pda_plan(prob)
+    assert plan["num_partitions"] * st.B * st.Hkv > 768  # large enough that pass 1 takes an ordered list
+    ws = torch.zeros(pda_workspace_bytes(prob), dtype=torch.uint8, device=dev)
+    pda_work_order(prob, ln, ws)
+    for layer, q in enumerate(qs):
+        got = pda_decode_reusing_order(q, k, v, bt, ln, st.scale, workspace=ws, **kw)
+        want = pda_decode(q, k, v, bt, ln, st.scale, **kw)
+        torch.cuda.synchronize()
+        assert torch.equal(got, want), layer
+    # stale order: after it was taken, the lengths change rank (each stays
+    # within its own sequence's blocks, so no row reads an unwritten slot)
+    ln2 = torch.from_numpy(np.minimum(rng.permutation(st.context_lens), st.context_lens)).to(dev)
+    assert not torch.equal(ln2, ln)
+    got = pda_decode_reusing_order(qs[0], k, v, bt, ln2, st.scale, workspace=ws, **kw)
+    want = pda_decode(qs[0], k, v, bt, ln2, st.scale, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(got, want)
+    # the order pda_decode leaves in its workspace serves the next layer
+    ws2 = torch.zeros_like(ws)
+    pda_decode(qs[0], k, v, bt, ln, st.scale, workspace=ws2, **kw)
+    got = bind_decode(qs[1], k, v, bt, ln, st.scale, workspace=ws2, reuse_order=True, **kw)()
+    want = pda_decode(qs[1], k, v, bt, ln, st.scale, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(got, want)
 
 
 def test_bound_append_matches(dev):
