@@ -409,12 +409,11 @@ class StepGraph:
             pass
 
 
-def pda_token_logprobs(logits, tokens, inv_temperature: float = 1.0, entropy: bool = True, vocab: int = None,
-                       logprobs=None, entropies=None, stream=None):
-    """Log-probability of tokens[r] under softmax(logits[r][:vocab] * inv_temperature),
-    and the entropy of that distribution (natural-log units).  logits: a device
-    tensor [rows][row_stride] of bf16 or float32 (16-byte aligned rows); tokens
-    int32 [rows].  Returns (logprobs fp32 [rows], entropies fp32 [rows] or None)."""
+def bind_token_logprobs(logits, tokens, inv_temperature: float = 1.0, entropy: bool = True, vocab: int = None,
+                        logprobs=None, entropies=None, stream=None) -> BoundCall:
+    """pda_token_logprobs bound to these tensors and the given (else the
+    current) stream; calling it returns (logprobs, entropies or None).  The
+    arguments are those of pda_token_logprobs."""
     import torch
 
     if logits.dim() != 2 or logits.stride(1) != 1:
@@ -436,13 +435,20 @@ def pda_token_logprobs(logits, tokens, inv_temperature: float = 1.0, entropy: bo
         logprobs = torch.empty(rows, dtype=torch.float32, device=logits.device)
     if entropy and entropies is None:
         entropies = torch.empty(rows, dtype=torch.float32, device=logits.device)
-    rc = load_library().pda_token_logprobs(rows, vocab, logits.stride(0), dtype, logits.data_ptr(), tokens.data_ptr(),
-                                           ctypes.c_float(inv_temperature), logprobs.data_ptr(),
-                                           entropies.data_ptr() if entropy else None,
-                                           _stream_handle(stream, logits.device))
-    if rc != PDA_OK:
-        raise PdaError(rc, "pda_token_logprobs")
-    return logprobs, (entropies if entropy else None)
+    args = (rows, vocab, logits.stride(0), dtype, logits.data_ptr(), tokens.data_ptr(),
+            ctypes.c_float(inv_temperature), logprobs.data_ptr(), entropies.data_ptr() if entropy else None,
+            _stream_handle(stream, logits.device))
+    keep = (logits, tokens, logprobs, entropies)
+    return BoundCall("pda_token_logprobs", args, keep, (logprobs, entropies if entropy else None))
+
+
+def pda_token_logprobs(logits, tokens, inv_temperature: float = 1.0, entropy: bool = True, vocab: int = None,
+                       logprobs=None, entropies=None, stream=None):
+    """Log-probability of tokens[r] under softmax(logits[r][:vocab] * inv_temperature),
+    and the entropy of that distribution (natural-log units).  logits: a device
+    tensor [rows][row_stride] of bf16 or float32 (16-byte aligned rows); tokens
+    int32 [rows].  Returns (logprobs fp32 [rows], entropies fp32 [rows] or None)."""
+    return bind_token_logprobs(logits, tokens, inv_temperature, entropy, vocab, logprobs, entropies, stream)()
 
 
 def pda_decode_shared_prefix(q, k_cache, v_cache, block_table, context_lens, scale: float, group_start,
