@@ -40,7 +40,9 @@ Other steps around attention (--op):
            decode step
   logprob  log-probability of each sampled token and the entropy over the
            LM-head logits of one decode step (256 rows x 128256 Llama-3
-           vocabulary, bf16; --logits-f32, --config qwen_vocab, --no-entropy)
+           vocabulary, bf16; --logits-f32, --config qwen_vocab, --no-entropy);
+           bound calls rotate over copies of the logits (>= 512 MB in all,
+           past the 256 MB Infinity Cache), so each reads them from HBM
 """
 from __future__ import annotations
 
