@@ -28,8 +28,11 @@
 //   logprob = ln2 (fma(logit_tok, k, -mk) - log2 s),  entropy = ln2 (log2 s - t / s).
 // The hot loop covers whole 16-byte chunks of the vocabulary; the one partial
 // chunk at its end is handled after it, with elements past the vocabulary at
-// probability 0.  -inf logits get 2^-inf = 0 and add nothing to t.  A token
-// id outside [0, vocab) gives NaN.  The inverse temperature must be >= 0 (the
+// probability 0.  -inf logits get 2^-inf = 0 and add nothing to s.  The hot
+// loop leaves d unguarded in t (one instruction less per logit), so a row
+// with a -inf logit gets a NaN t there; it takes t again in a second,
+// guarded pass over the row against its final reference.  A token id
+// outside [0, vocab) gives NaN.  The inverse temperature must be >= 0 (the
 // host checks it), so the max of the logits is the max of the scaled values.
 #include "pda_internal.h"
 
@@ -117,7 +120,9 @@ __global__ void __launch_bounds__(kLpThreads) logprob_kernel(const LogprobArgs a
         const float d = fmaf(x[e], k, -st.mk);
         const float p = __builtin_amdgcn_exp2f(d);
         st.s += p;
-        if constexpr (ENTROPY) st.t = fmaf(p, fmaxf(d, kFloorMax), st.t);  // p = 0 exactly where d = -inf: adds 0
+        // A -inf logit (d = -inf, p = 0) makes t NaN here; such a row's t is
+        // taken again, guarded, after the combine.
+        if constexpr (ENTROPY) st.t = fmaf(p, d, st.t);
       }
     }
   };
@@ -195,9 +200,50 @@ __global__ void __launch_bounds__(kLpThreads) logprob_kernel(const LogprobArgs a
   const int w = tid / kWaveSize;
   if ((tid & (kWaveSize - 1)) == 0) s_state[w] = st;
   __syncthreads();
-  if (tid == 0) {
-    LpState r = s_state[0];
+  LpState r = {0.f, 0.f, 0.f};
+  __shared__ int s_redo;
+  __shared__ float s_ref;
+  if (w == 0) {  // the wavefronts' states in index order
+    r = s_state[0];
     for (int x = 1; x < kLpThreads / kWaveSize; ++x) r = lp_merge(r, s_state[x]);
+    if (ENTROPY && tid == 0) {
+      s_redo = __builtin_isnan(r.t) && __builtin_isfinite(r.s);
+      s_ref = r.mk;
+    }
+  }
+  if (ENTROPY) __syncthreads();
+  if (ENTROPY && s_redo) {
+    // Some logit is -inf (a NaN logit would have made s NaN as well): take
+    // t again against the final reference, with d floored so that those
+    // logits add 0 * floor = 0.  s is unchanged (they add 0 to it either way).
+    __shared__ float s_tsum[kLpThreads / kWaveSize];
+    const float ref = s_ref;
+    float t = 0.f;
+    auto fold_t = [&](const float (&x)[E], int valid) {
+#pragma unroll
+      for (int e = 0; e < E; ++e)
+        if (e < valid) {
+          const float d = fmaf(x[e], k, -ref);
+          t = fmaf(__builtin_amdgcn_exp2f(d), fmaxf(d, kFloorMax), t);
+        }
+    };
+    for (int c = tid; c < nfull; c += kLpThreads) {
+      float x[E];
+      unpack<ESIZE>(load(c), x);
+      fold_t(x, E);
+    }
+    if (tid == nfull % kLpThreads && nfull * E < a.vocab) {
+      float x[E];
+      unpack<ESIZE>(load(nfull), x);
+      fold_t(x, a.vocab - nfull * E);
+    }
+    for (int o = 1; o < kWaveSize; o <<= 1) t += __shfl_xor(t, o);
+    if ((tid & (kWaveSize - 1)) == 0) s_tsum[w] = t;
+    __syncthreads();
+    r.t = s_tsum[0];
+    for (int x = 1; x < kLpThreads / kWaveSize; ++x) r.t += s_tsum[x];
+  }
+  if (tid == 0) {
     const float log2s = __builtin_amdgcn_logf(r.s);  // log2
     const int tok = a.tokens[row];
     float lp;
