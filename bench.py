@@ -513,7 +513,7 @@ def main(argv=None):
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the decode step shards by "
-              "sequence or KV head with no exchange, and this build runs on a single MI355X.",
+              "sequence or KV head with no exchange, and the benchmark runs on a single MI355X.",
               file=sys.stderr)
         return 2
     if args.config is None:
