@@ -132,6 +132,41 @@ def cpu_baseline(st, q, k, v, min_seconds: float, max_reps: int):
                                      f"{t1:.1f} s total, fp64, 1 thread"}}
 
 
+def oracle_timed(run, min_seconds: float, max_reps: int):
+    """Seconds per call of `run` (the oracle on the host), repeated until
+    min_seconds have passed or max_reps calls were made: (seconds, reps, total)."""
+    reps, total = 0, 0.0
+    while reps < max_reps and (reps == 0 or total < min_seconds):
+        t0 = time.perf_counter()
+        run()
+        total += time.perf_counter() - t0
+        reps += 1
+    return total / reps, reps, total
+
+
+def cpu_baseline_multi(st, q, k, v, n, min_seconds: float, max_reps: int):
+    """The oracle's n-token attention on the host over the batch's first
+    sequences (at most 32), in GB/s of those sequences' algorithmic bytes."""
+    import numpy as np
+
+    import oracle
+    import workloads as W
+
+    threads = max(1, min(16, os.cpu_count() or 1))
+    nb = min(st.B, 32)
+    qb, kb, vb = W.bf16_bits(q)[:nb], W.bf16_bits(k), W.bf16_bits(v)
+    lens = st.context_lens[:nb]
+    L = lens.astype(np.int64).clip(0)
+    sub_bytes = (int(L.sum()) * st.Hkv * st.D * 2 * 2 + nb * n * st.Hq * st.D * (2 + 4)
+                 + int(((L + st.block_size - 1) // st.block_size).sum()) * 4 + nb * 4)
+    sec, reps, total = oracle_timed(
+        lambda: oracle.decode_multi(qb, kb, vb, st.block_table[:nb], lens, st.scale, threads=threads),
+        min_seconds, max_reps)
+    return {"value": round(sub_bytes / sec / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": f"the first {nb} sequences of the {st.name} step with {n} new tokens each, {reps} "
+                      f"repetition(s), {total:.1f} s total, fp64, {threads} threads"}
+
+
 def timed(fn, n, stream):
     """Average ms per call of fn over n calls, HIP events on `stream`."""
     import torch
@@ -296,6 +331,9 @@ def op_decode(args, n_tokens=1):
             result["roofline"] = roofline_mfma(flops, ms_pass1, KERNEL)
     if n_tokens == 1 and not args.no_cpu_baseline and not args.pass1_only:
         result["cpu_baseline"] = cpu_baseline(st, q, k, v, args.cpu_min_seconds, args.cpu_max_reps)
+    elif not args.no_cpu_baseline and not args.pass1_only:
+        result["cpu_baseline"] = cpu_baseline_multi(st, q, k, v, n_tokens, args.cpu_min_seconds / 2,
+                                                    args.cpu_max_reps)
     return result
 
 
@@ -435,6 +473,20 @@ def op_prefix(args):
                    "algorithmic_bytes_per_step": alg, "ms_per_step_plain_decode": round(ms_plain, 5),
                    "speedup_vs_plain_decode": round(ms_plain / ms, 3),
                    "roofline": roofline(value, ms, KERNEL, args.config + "_shared"), "cpu_baseline": None})
+    if not args.no_cpu_baseline:
+        # the oracle computes the same attention (it reads each member's prefix itself); the rate is
+        # per unique byte like the GPU's
+        import oracle
+
+        threads = max(1, min(16, os.cpu_count() or 1))
+        qb, kb, vb = W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v)
+        sec, reps, total = oracle_timed(
+            lambda: oracle.decode(qb, kb, vb, st.block_table, st.context_lens, st.scale, threads=threads),
+            args.cpu_min_seconds / 2, args.cpu_max_reps)
+        result["cpu_baseline"] = {"value": round(alg / sec / 1e9, 4), "unit": "GB/s", "cores": threads,
+                                  "kind": "oracle", "seq_steps_per_s": round(st.B / sec, 3),
+                                  "sample": f"the full {st.name} step, {reps} repetition(s), {total:.1f} s "
+                                            f"total, fp64, {threads} threads"}
     return result
 
 
@@ -483,6 +535,18 @@ def op_logprob(args):
     result.update({"rows_per_s": round(B / (ms * 1e-3), 1), "algorithmic_bytes_per_step": alg,
                    "pct_of_peak": round(100.0 * value / PEAK_GBS, 2),
                    "roofline": roofline(value, ms, "logprob_kernel", name), "cpu_baseline": None})
+    if not args.no_cpu_baseline:
+        import oracle
+
+        nr = min(B, 64)  # the oracle is single-threaded: the first rows
+        xh = x[:nr].float().cpu().numpy() if dtype == torch.float32 else W.bf16_bits(x[:nr])
+        sec, reps, total = oracle_timed(lambda: oracle.logprob(xh, tok[:nr], 1.0, entropy=not args.no_entropy),
+                                        args.cpu_min_seconds / 2, args.cpu_max_reps)
+        sub = nr * V * x.element_size() + nr * 4 + nr * (4 if args.no_entropy else 8)
+        result["cpu_baseline"] = {"value": round(sub / sec / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+                                  "rows_per_s": round(nr / sec, 3),
+                                  "sample": f"the first {nr} rows, {reps} repetition(s), {total:.1f} s total, "
+                                            f"fp64, 1 thread"}
     return result
 
 
