@@ -146,3 +146,30 @@ def test_rising_logits_retake_passes(dev, dtype):
         print(f"rising logits {dtype} 1/T={inv_t}: logprob error / bar {e_lp.max():.2f}, "
               f"entropy max-abs {e_ent.max():.2e}", flush=True)
         assert e_lp.max() <= 1.0 and e_ent.max() <= TOL, (dtype, inv_t)
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_neg_inf_rows_take_entropy_again_alone(dev, dtype):
+    """A row with -inf logits has its entropy sum taken again in a second,
+    guarded pass; rows without any keep their one-pass results bit for bit,
+    and the log-probabilities (which never depend on that pass) are the same
+    bits with or without it."""
+    x, tok = W.make_logits(8, 128256, seed=21, device=dev, dtype=dtype)
+    tt = torch.from_numpy(tok).to(dev)
+    lp0, ent0 = pda_token_logprobs(x, tt, 1.0)
+    y = x.clone()
+    y[3, 1000:90000] = float("-inf")   # a wide masked band
+    y[5, ::7] = float("-inf")          # scattered masked tokens
+    tok2 = tok.copy()
+    tok2[3], tok2[5] = 17, 1
+    tt2 = torch.from_numpy(tok2).to(dev)
+    lp1, ent1 = pda_token_logprobs(y, tt2, 1.0)
+    torch.cuda.synchronize()
+    keep = [0, 1, 2, 4, 6, 7]
+    assert torch.equal(ent1[keep], ent0[keep]) and torch.equal(lp1[keep], lp0[keep])
+    ref_lp, ref_ent = oracle.logprob(host_values(y), tok2, 1.0)
+    compare(lp1, ent1, ref_lp, ref_ent, f"-inf rows {dtype}")
+    assert np.isfinite(ent1.cpu().numpy()).all()
+    lp_only, none = pda_token_logprobs(y, tt2, 1.0, entropy=False)
+    torch.cuda.synchronize()
+    assert none is None and torch.equal(lp_only, lp1)
