@@ -300,3 +300,32 @@ def test_status_strings():
 def test_binding_has_no_fallback(tmp_path):
     with pytest.raises(RuntimeError, match="no fallback"):
         pda.load_library(str(tmp_path / "missing.so"))
+
+
+def test_plan_invariants_over_random_descriptors():
+    """For seeded random valid descriptors, the library's own partition choice
+    covers the longest context, is a multiple of 256 (or the whole context
+    rounded to 16) and at most 4608 tokens, and the workspace holds the
+    partial states (when split) and one order entry per work item."""
+    rng = np.random.default_rng(2405)
+    for _ in range(400):
+        G = int(rng.choice([1, 2, 4, 5, 7, 8, 16]))
+        hkv = int(rng.integers(1, 9))
+        n = int(rng.choice([1, 1, 2, 4, 8, 16, 33]))
+        max_len = int(rng.integers(0, 40000))
+        mb = max(1, -(-max_len // 16) + int(rng.integers(0, 4)))
+        p = pda.make_problem(int(rng.integers(1, 600)), G * hkv, hkv, int(rng.choice([64, 128])), 1 << 20, mb,
+                             max_len, 0, 16, n)
+        info = pda.pda_plan(p)
+        tp, parts = info["partition_tokens"], info["num_partitions"]
+        assert tp % 16 == 0 and 16 <= tp <= 4608
+        assert tp % 256 == 0 or tp == -(-max(max_len, 1) // 16) * 16
+        assert parts == (-(-max_len // tp) if max_len > 0 else 1)
+        assert parts * tp >= max_len
+        qc = min(n, 16 // G)
+        nqc = -(-n // qc)
+        cpg = 8 if nqc > 4 else 4
+        items = p.num_seqs * hkv * -(-nqc // cpg) * parts
+        split = p.num_seqs * n * p.num_q_heads * parts * (p.head_dim + 2) * 4 if parts > 1 else 0
+        assert info["workspace_bytes"] == split + items * 4
+        assert pda.pda_workspace_bytes(p) == info["workspace_bytes"]
