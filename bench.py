@@ -93,13 +93,36 @@ def measured_traffic(kernel: str, workload: str):
     return float(m_bytes.group(1))
 
 
+def host_threads() -> int:
+    """Threads for the oracle: every CPU this process may run on, capped by
+    OMP_NUM_THREADS when that is set (a machine's share of its host)."""
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:
+        avail = os.cpu_count() or 1
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    if env.isdigit() and int(env) > 0:
+        return max(1, min(avail, int(env)))
+    return max(1, avail)
+
+
+def host_cpu_fields(threads: int) -> dict:
+    """What the host offers beside the threads the oracle used."""
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:
+        avail = None
+    return {"cores": threads, "host_cpus": os.cpu_count(), "cpus_available_to_process": avail,
+            "omp_num_threads": os.environ.get("OMP_NUM_THREADS")}
+
+
 def cpu_baseline(st, q, k, v, min_seconds: float, max_reps: int):
     import numpy as np
 
     import oracle
     import workloads as W
 
-    threads = max(1, min(16, os.cpu_count() or 1))
+    threads = host_threads()
     qb, kb, vb = W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v)
     reps, t_total = 0, 0.0
     while reps < max_reps and (reps == 0 or t_total < min_seconds):
@@ -123,7 +146,7 @@ def cpu_baseline(st, q, k, v, min_seconds: float, max_reps: int):
     one = t1 / reps1
     return {"value": round(st.algorithmic_bytes() / per_step / 1e9, 4), "unit": "GB/s",
             "seq_steps_per_s": round(st.B / per_step, 3), "s_per_step": round(per_step, 4),
-            "cores": threads, "kind": "oracle",
+            **host_cpu_fields(threads), "kind": "oracle",
             "sample": f"the full {st.name} step (all {st.B} sequences x {st.Hq} heads), "
                       f"{reps} repetition(s), {t_total:.1f} s total, fp64, {threads} threads",
             "one_thread": {"value": round(sub_bytes / one / 1e9, 4), "unit": "GB/s",
@@ -152,7 +175,7 @@ def cpu_baseline_multi(st, q, k, v, n, min_seconds: float, max_reps: int):
     import oracle
     import workloads as W
 
-    threads = max(1, min(16, os.cpu_count() or 1))
+    threads = host_threads()
     nb = min(st.B, 32)
     qb, kb, vb = W.bf16_bits(q)[:nb], W.bf16_bits(k), W.bf16_bits(v)
     lens = st.context_lens[:nb]
@@ -162,7 +185,7 @@ def cpu_baseline_multi(st, q, k, v, n, min_seconds: float, max_reps: int):
     sec, reps, total = oracle_timed(
         lambda: oracle.decode_multi(qb, kb, vb, st.block_table[:nb], lens, st.scale, threads=threads),
         min_seconds, max_reps)
-    return {"value": round(sub_bytes / sec / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+    return {"value": round(sub_bytes / sec / 1e9, 4), "unit": "GB/s", **host_cpu_fields(threads), "kind": "oracle",
             "sample": f"the first {nb} sequences of the {st.name} step with {n} new tokens each, {reps} "
                       f"repetition(s), {total:.1f} s total, fp64, {threads} threads"}
 
@@ -478,12 +501,12 @@ def op_prefix(args):
         # per unique byte like the GPU's
         import oracle
 
-        threads = max(1, min(16, os.cpu_count() or 1))
+        threads = host_threads()
         qb, kb, vb = W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v)
         sec, reps, total = oracle_timed(
             lambda: oracle.decode(qb, kb, vb, st.block_table, st.context_lens, st.scale, threads=threads),
             args.cpu_min_seconds / 2, args.cpu_max_reps)
-        result["cpu_baseline"] = {"value": round(alg / sec / 1e9, 4), "unit": "GB/s", "cores": threads,
+        result["cpu_baseline"] = {"value": round(alg / sec / 1e9, 4), "unit": "GB/s", **host_cpu_fields(threads),
                                   "kind": "oracle", "seq_steps_per_s": round(st.B / sec, 3),
                                   "sample": f"the full {st.name} step, {reps} repetition(s), {total:.1f} s "
                                             f"total, fp64, {threads} threads"}

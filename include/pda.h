@@ -100,9 +100,11 @@ typedef struct pda_problem {
   int32_t block_size;         /* tokens per KV block: must be 16 */
   int32_t num_blocks;         /* rows of k_cache / v_cache, >= 1 */
   int32_t max_blocks_per_seq; /* row stride of block_table, >= 1 */
-  int32_t max_context_len;    /* host-known bound on context_lens[]; 0 <= it <= 16*max_blocks_per_seq */
+  int32_t max_context_len;    /* host-known bound on context_lens[]; 0 <= it <= 16*max_blocks_per_seq
+                                 and <= 2^28 */
   int32_t partition_tokens;   /* split-K partition size: 0 lets the library choose, otherwise a
-                                 positive multiple of 16 */
+                                 positive multiple of 16 (a size beyond max_context_len acts as
+                                 max_context_len rounded up to a multiple of 16: one partition) */
   int32_t num_query_tokens;   /* n, new tokens per sequence: 0 or 1 = a decode step */
 } pda_problem;
 

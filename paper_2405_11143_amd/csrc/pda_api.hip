@@ -38,6 +38,9 @@ constexpr int64_t kRowsShareNum = 13, kRowsShareDen = 10;
 constexpr int kMinPartitionTokens = 256;
 constexpr int kPartitionQuantum = 256;
 constexpr int64_t kConcurrentItems = 768;  // 256 compute units x 3 workgroups of 4 wavefronts
+// Longest context a descriptor may announce: keeps every token sum of the
+// kernels (a position plus a partition size) far inside int32.
+constexpr int32_t kMaxContextTokens = 1 << 28;
 
 int query_tokens(const pda_problem* p) { return p->num_query_tokens > 0 ? p->num_query_tokens : 1; }
 
@@ -49,7 +52,10 @@ int check_problem(const pda_problem* p) {
   if (p->num_q_heads % p->num_kv_heads != 0) return PDA_ERR_SHAPE;
   if (p->partition_tokens % pda::kBlockTokens != 0) return PDA_ERR_SHAPE;
   if ((int64_t)p->max_context_len > (int64_t)pda::kBlockTokens * p->max_blocks_per_seq) return PDA_ERR_SHAPE;
-  if ((int64_t)p->num_seqs * query_tokens(p) * p->num_q_heads > 0x7fffffff) return PDA_ERR_SHAPE;
+  if (p->max_context_len > kMaxContextTokens) return PDA_ERR_SHAPE;
+  // output rows B * n * Hq must fit an int (two factors at a time: three int32 factors can overflow int64)
+  const int64_t rows_per_seq = (int64_t)query_tokens(p) * p->num_q_heads;
+  if (rows_per_seq > 0x7fffffff || (int64_t)p->num_seqs * rows_per_seq > 0x7fffffff) return PDA_ERR_SHAPE;
   if (p->block_size != pda::kBlockTokens) return PDA_ERR_UNSUPPORTED;
   if (p->head_dim != 64 && p->head_dim != 128) return PDA_ERR_UNSUPPORTED;
   if (p->num_q_heads / p->num_kv_heads > pda::kMaxGroup) return PDA_ERR_UNSUPPORTED;
@@ -76,7 +82,8 @@ int check_groups(const pda_problem* p, const pda_prefix_groups* g) {
       g->max_prefix_len % pda::kBlockTokens != 0 || g->max_prefix_len > p->max_context_len)
     return PDA_ERR_SHAPE;
   if (p->num_query_tokens > 1) return PDA_ERR_UNSUPPORTED;  // one new token per sequence
-  if (g->max_group_size * (p->num_q_heads / p->num_kv_heads) > 64) return PDA_ERR_UNSUPPORTED;
+  // (in 64 bits: a huge bound must not wrap past the check)
+  if ((int64_t)g->max_group_size * (p->num_q_heads / p->num_kv_heads) > 64) return PDA_ERR_UNSUPPORTED;
   return PDA_OK;
 }
 
@@ -104,8 +111,14 @@ int make_plan(const pda_problem* p, const pda_prefix_groups* groups, Plan* plan)
     }
     const int64_t quanta = (share + kPartitionQuantum - 1) / kPartitionQuantum;
     tp = (int)std::min<int64_t>(kMaxPartitionTokens, std::max<int64_t>(kMinPartitionTokens, quanta * kPartitionQuantum));
-    const int rounded = (int)((len + pda::kBlockTokens - 1) / pda::kBlockTokens * pda::kBlockTokens);
-    if (rounded < tp) tp = rounded;  // the whole context fits one partition
+    const int64_t rounded = (len + pda::kBlockTokens - 1) / pda::kBlockTokens * pda::kBlockTokens;
+    if (rounded < tp) tp = (int)rounded;  // the whole context fits one partition
+  } else {
+    // a forced size beyond the longest context means one partition: the same
+    // step as with that context's length rounded up to a whole block
+    const int64_t whole = std::max<int64_t>(pda::kBlockTokens, ((int64_t)p->max_context_len + pda::kBlockTokens - 1) /
+                                                                   pda::kBlockTokens * pda::kBlockTokens);
+    if (tp > whole) tp = (int)whole;
   }
   const int64_t parts = p->max_context_len > 0 ? ((int64_t)p->max_context_len + tp - 1) / tp : 1;
   const int num_groups = groups ? groups->num_groups : 0;

@@ -594,7 +594,7 @@ hipError_t launch_d(const StepArgs& a, hipStream_t stream) {
   // on a group's rows exceeds one tile
   const bool groups = a.num_groups > 0;
   const bool one = a.num_query_chunks % kWaves == 1 || groups;
-  const bool several = a.num_query_chunks >= 2 || (groups && a.max_group_size * a.group > kRows);
+  const bool several = a.num_query_chunks >= 2 || (groups && (int64_t)a.max_group_size * a.group > kRows);
   const dim3 block(kWaves * kWaveSize);
   if (a.chunks_per_group > kWaves)
     hipLaunchKernelGGL((partition_kernel<D, kModeWide>), dim3(grid), block, 0, stream, a);

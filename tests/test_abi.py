@@ -83,7 +83,7 @@ def test_plan_workspace():
     # (partition, sequence, KV head)
     assert plan(partition_tokens=2048) == (2048, 2, 256 * 32 * 2 * (128 + 2) * 4 + 2 * 256 * 8 * 4)
     assert plan(partition_tokens=4096) == (4096, 1, 256 * 8 * 4)
-    assert plan(partition_tokens=8192) == (8192, 1, 256 * 8 * 4)
+    assert plan(partition_tokens=8192) == (4096, 1, 256 * 8 * 4)  # beyond the longest context: clamped
     assert pda.pda_plan(prob(partition_tokens=64))["workspace_bytes"] == 4 * 8 * 5 * 66 * 4 + 5 * 4 * 2 * 4
     assert plan(num_seqs=0)[2] == 0
     assert pda.pda_workspace_bytes(llama()) == plan()[2]
@@ -110,10 +110,23 @@ def test_plan_partition_choice():
     assert plan(max_context_len=0)[:2] == (16, 1)
     # a forced size is kept
     assert plan(partition_tokens=16)[:2] == (16, 256)
+    # a forced size beyond the longest context is one partition of that context
+    assert plan(partition_tokens=2 ** 31 - 16)[:2] == (4096, 1)
+    assert plan(max_context_len=0, partition_tokens=1024)[:2] == (16, 1)
     # sizes whose work estimate overflows 64 bits: the grid bound rejects them
     with pytest.raises(pda.PdaError) as e:
-        plan(num_seqs=2 ** 20, num_q_heads=16, num_kv_heads=16, max_blocks_per_seq=2 ** 27,
-             max_context_len=2 ** 31 - 16, num_blocks=10 ** 9)
+        plan(num_seqs=2 ** 20, num_q_heads=16, num_kv_heads=16, max_blocks_per_seq=2 ** 24,
+             max_context_len=2 ** 28, num_blocks=10 ** 9)
+    assert e.value.status == pda.pda.PDA_ERR_SHAPE
+    # contexts beyond 2^28 tokens are refused (token sums stay far inside int32)
+    for mcl in (2 ** 28 + 1, 2 ** 31 - 1):
+        with pytest.raises(pda.PdaError) as e:
+            plan(max_blocks_per_seq=2 ** 27, max_context_len=mcl)
+        assert e.value.status == pda.pda.PDA_ERR_SHAPE
+    # rows B * n * Hq beyond int32, with every factor alone in range (the product of
+    # the three overflows even int64)
+    with pytest.raises(pda.PdaError) as e:
+        plan(num_seqs=2 ** 30, num_query_tokens=2 ** 30, num_q_heads=2 ** 30, num_kv_heads=2 ** 26)
     assert e.value.status == pda.pda.PDA_ERR_SHAPE
 
 
@@ -256,6 +269,10 @@ def test_shared_prefix_validation():
     assert plan(max_prefix_len=100) == pda.pda.PDA_ERR_SHAPE        # not a multiple of 16
     assert plan(max_prefix_len=8192) == pda.pda.PDA_ERR_SHAPE       # beyond max_context_len
     assert plan(max_group_size=17) == pda.pda.PDA_ERR_UNSUPPORTED   # 17 x G=4 > 64 rows
+    # a bound whose product with G wraps in 32 bits (2^30 x 4 = 2^32 -> 0; (2^28 + 2) x 16 -> 32)
+    assert plan(max_group_size=1 << 30) == pda.pda.PDA_ERR_UNSUPPORTED
+    assert plan(llama(num_q_heads=16, num_kv_heads=1), max_group_size=(1 << 28) + 2) == \
+        pda.pda.PDA_ERR_UNSUPPORTED
     assert plan(llama(num_query_tokens=2)) == pda.pda.PDA_ERR_UNSUPPORTED
     assert plan(group_start=None) == pda.pda.PDA_OK  # planning reads the host bounds only
     assert plan(num_groups=0, group_start=None, group_prefix_len=None) == pda.pda.PDA_OK

@@ -4,24 +4,21 @@ chunked prefill: Section 3.2) through the C ABI, against the fp64 oracle.
 New token i of a sequence with n new tokens and context length L sits at
 position L - n + i and attends to tokens t < L - n + 1 + i.  Bar as for the
 decode step: max-abs <= 8e-3 and mean-abs <= 1e-3 over every compared
-element.  Small problems are compared on every element; a Llama-3-8B-shaped
-step with 4 draft tokens per sequence runs at full size and is compared on
-sampled rows.
+element.  Small problems and the full-size steps (Llama-3-8B, long
+chain-of-thought and 70B-shard shapes with 4 to 64 new tokens) are compared
+on every element.
 """
-import os
-
 import numpy as np
 import pytest
 import torch
 
 import oracle
 import workloads as W
+from parity_common import THREADS, check
 from paper_2405_11143_amd import make_problem, pda_decode, pda_plan
 
 pytestmark = pytest.mark.gpu
 
-MAX_ABS, MEAN_ABS = 8e-3, 1e-3
-THREADS = max(1, min(16, os.cpu_count() or 1))
 
 
 @pytest.fixture(scope="module")
@@ -39,12 +36,6 @@ def run_multi(st, q, k, v, dev, partition_tokens=0):
     return out.cpu().numpy()
 
 
-def check(got, ref, what):
-    got = got.astype(np.float64)
-    assert np.isfinite(got).all(), f"{what}: non-finite output"
-    err = np.abs(got - ref)
-    print(f"{what}: max-abs {err.max():.3e} mean-abs {err.mean():.3e} over {err.size} elements", flush=True)
-    assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS, what
 
 
 LENS = [1, 2, 3, 4, 5, 15, 16, 17, 21, 33, 64, 65, 300, 1000, 2049]
@@ -125,12 +116,36 @@ def test_multi_token_poison_and_shuffle_bit_identical(dev, n):
     assert np.array_equal(base, run_multi(st, q, kz, vz, dev)), "NaN poison vs zero fill"
 
 
+@pytest.mark.parametrize("D", [64, 128])
+@pytest.mark.parametrize("n", [1, 8, 32], ids=["register", "mixed", "wide"])
+@pytest.mark.parametrize("partition_tokens", [0, 64])
+def test_run_to_run_bitwise_every_variant(dev, D, n, partition_tokens):
+    """Three runs give identical bits in each compiled variant of the
+    partition kernel at both head dims: one 16-row tile per item in registers
+    (n = 1), up to 4 tiles staged through LDS (n = 8 at G = 4: 2 tiles), and
+    the wide variant with two tiles per wavefront (n = 32: 8 tiles); with
+    whole and split contexts.  These runs guard the ordering of the score
+    MFMAs and their first VALU reads, which the compiler once left without
+    the wait states a read of an MFMA result needs."""
+    lens = [1, 17, 300, 2049, 40, 64, 1000, 513]
+    st = W.custom_structure(len(lens), 32, 8, D, lens, seed=300 + n + D)
+    _, k, v = W.fill_values(st, dev, fill="nan")
+    q = W.fill_multi_q(st, n, dev)
+    base = run_multi(st, q, k, v, dev, partition_tokens)
+    for _ in range(2):
+        assert np.array_equal(base, run_multi(st, q, k, v, dev, partition_tokens)), "run-to-run"
+    ref = oracle.decode_multi(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
+                              st.context_lens, st.scale, threads=THREADS)
+    check(base, ref, f"variant n={n} D={D} Tp={partition_tokens}")
+
+
 @pytest.mark.parametrize("name,n", [("llama3_8b", 4), ("llama3_8b", 32), ("llama3_70b_tp8", 16),
                                     ("long_cot", 64)], ids=lambda x: str(x))
-def test_multi_token_full_size_sampled(dev, name, n):
+def test_multi_token_full_size(dev, name, n):
     """Full-size steps with n new tokens per sequence (4 draft tokens to
     verify in speculative decoding; 16-64 for wide items, split contexts and
-    two chunk groups), in the launch configuration the benchmark times."""
+    two chunk groups), in the launch configuration the benchmark times:
+    sampled rows first, then every one of the B*n*Hq*D output elements."""
     st = W.make_structure(name)
     plan = pda_plan(make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq,
                                  st.max_context_len, num_query_tokens=n))
@@ -139,13 +154,17 @@ def test_multi_token_full_size_sampled(dev, name, n):
     q = W.fill_multi_q(st, n, dev)
     got = run_multi(st, q, k, v, dev)
     assert np.isfinite(got).all()
+    qb, kb, vb = W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v)
+    del k, v
     r = np.random.default_rng(5)
     rows = np.stack([r.integers(0, st.B, 64), r.integers(0, n, 64), r.integers(0, st.Hq, 64)], axis=1)
     rows[0] = [int(np.argmax(st.context_lens)), n - 1, st.Hq - 1]
     rows[1] = [int(np.argmin(st.context_lens)), 0, 0]
-    ref = oracle.decode_multi_rows(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
-                                   st.context_lens, st.scale, rows.astype(np.int32), threads=THREADS)
+    ref = oracle.decode_multi_rows(qb, kb, vb, st.block_table, st.context_lens, st.scale, rows.astype(np.int32),
+                                   threads=THREADS)
     check(got[rows[:, 0], rows[:, 1], rows[:, 2]], ref, f"{name} {n} new tokens, sampled rows")
+    ref = oracle.decode_multi(qb, kb, vb, st.block_table, st.context_lens, st.scale, threads=THREADS)
+    check(got, ref, f"{name} {n} new tokens, every element", f"B*n*Hq*D = {st.B}*{n}*{st.Hq}*{st.D}")
 
 
 @pytest.mark.parametrize("factor", [-1.0, 0.0, 3.0, 25.0])

@@ -6,25 +6,22 @@ method fixes the bits: a one-token context returns its V row exactly, moving
 physical blocks around the pool or filling unread slots with NaN leaves the
 output bit-identical, and two runs give identical bits.
 
-Small problems are compared on every element; the five named decode
+Small problems are compared on every element.  The named decode
 configurations run at full size in the launch configuration the benchmark
-times, and are compared on sampled (sequence, head) rows that the oracle
-computes one by one.
+times and are compared on every element too (after a quick check of
+sampled rows); the 64K-token case is compared on sampled rows.
 """
-import os
-
 import numpy as np
 import pytest
 import torch
 
 import oracle
 import workloads as W
+from parity_common import THREADS, check
 from paper_2405_11143_amd import pda_decode, pda_plan, make_problem
 
 pytestmark = pytest.mark.gpu
 
-MAX_ABS, MEAN_ABS = 8e-3, 1e-3
-THREADS = max(1, min(16, os.cpu_count() or 1))
 
 
 @pytest.fixture(scope="module")
@@ -50,12 +47,6 @@ def reference(st, q, k, v):
                          st.context_lens, st.scale, threads=THREADS)
 
 
-def check(got, ref, what):
-    got = got.astype(np.float64)
-    assert np.isfinite(got).all(), f"{what}: non-finite output"
-    err = np.abs(got - ref)
-    print(f"{what}: max-abs {err.max():.3e} mean-abs {err.mean():.3e} over {err.size} elements", flush=True)
-    assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS, what
 
 
 # ------------------------------------------------------------ small, full --
@@ -194,7 +185,10 @@ def test_empty_and_nonpositive_lengths(dev):
 
 @pytest.mark.parametrize("name", ["llama3_8b", "long_cot", "llama3_70b_tp8", "shared_prefix", "r1_qwen7b",
                                   "r1_qwen14b"])
-def test_full_config_sampled(dev, name):
+def test_full_config(dev, name):
+    """A named decode configuration at full size, in the launch configuration
+    the benchmark times: sampled rows first (a quick check that names the
+    rows), then every one of the B*Hq*D output elements against the oracle."""
     st = W.make_structure(name)
     plan = pda_plan(make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq,
                                  st.max_context_len))
@@ -204,10 +198,13 @@ def test_full_config_sampled(dev, name):
     assert np.isfinite(got).all()
     vmax = float(torch.nan_to_num(v.float().abs(), nan=0.0).max())
     assert np.abs(got).max() <= vmax  # each output is a convex combination of V rows
+    qb, kb, vb = W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v)
+    del k, v
     rows = W.sample_rows(st, 64)
-    ref = oracle.decode_rows(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
-                             st.context_lens, st.scale, rows, threads=THREADS)
+    ref = oracle.decode_rows(qb, kb, vb, st.block_table, st.context_lens, st.scale, rows, threads=THREADS)
     check(got[rows[:, 0], rows[:, 1]], ref, f"{name} sampled rows")
+    ref = oracle.decode(qb, kb, vb, st.block_table, st.context_lens, st.scale, threads=THREADS)
+    check(got, ref, f"{name} every element", f"B*Hq*D = {st.B}*{st.Hq}*{st.D}")
 
 
 def test_long_contexts_sampled(dev):

@@ -6,20 +6,17 @@ that each group's prefix is attended once for all members; the fp64 oracle
 is the plain decode definition.  Bar: max-abs <= 8e-3, mean-abs <= 1e-3 over
 every compared element; bitwise run-to-run and under block shuffles.
 """
-import os
-
 import numpy as np
 import pytest
 import torch
 
 import oracle
 import workloads as W
+from parity_common import THREADS, check
 from paper_2405_11143_amd import make_prefix_groups, make_problem, pda_decode_shared_prefix, pda_plan_shared_prefix
 
 pytestmark = pytest.mark.gpu
 
-MAX_ABS, MEAN_ABS = 8e-3, 1e-3
-THREADS = max(1, min(16, os.cpu_count() or 1))
 
 
 @pytest.fixture(scope="module")
@@ -47,12 +44,6 @@ def reference(st, q, k, v):
                          st.scale, threads=THREADS)
 
 
-def check(got, ref, what):
-    got = got.astype(np.float64)
-    assert np.isfinite(got).all(), f"{what}: non-finite output"
-    err = np.abs(got - ref)
-    print(f"{what}: max-abs {err.max():.3e} mean-abs {err.mean():.3e} over {err.size} elements", flush=True)
-    assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS, what
 
 
 GROUPS = [
@@ -109,7 +100,8 @@ def test_host_bounds_above_contents(dev):
 
 def test_shared_prefix_config_full_size(dev):
     """The 32 prompts x 8 samples workload at full size, in the launch
-    configuration the benchmark times; sampled rows against the oracle."""
+    configuration the benchmark times: sampled rows first, then every one of
+    the B*Hq*D output elements against the oracle."""
     st = W.make_structure("shared_prefix")
     prob = make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq, st.max_context_len)
     plan = pda_plan_shared_prefix(prob, make_prefix_groups(len(st.group_prefix_len), 8, 1024))
@@ -117,7 +109,10 @@ def test_shared_prefix_config_full_size(dev):
     q, k, v = W.fill_values(st, dev, fill="nan")
     got = run(st, q, k, v, dev)
     assert np.isfinite(got).all()
+    qb, kb, vb = W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v)
+    del k, v
     rows = W.sample_rows(st, 64)
-    ref = oracle.decode_rows(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table, st.context_lens,
-                             st.scale, rows, threads=THREADS)
+    ref = oracle.decode_rows(qb, kb, vb, st.block_table, st.context_lens, st.scale, rows, threads=THREADS)
     check(got[rows[:, 0], rows[:, 1]], ref, "shared_prefix sampled rows")
+    ref = oracle.decode(qb, kb, vb, st.block_table, st.context_lens, st.scale, threads=THREADS)
+    check(got, ref, "shared_prefix every element", f"B*Hq*D = {st.B}*{st.Hq}*{st.D}")
