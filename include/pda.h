@@ -88,7 +88,8 @@ enum pda_status {
   PDA_ERR_WORKSPACE = 4,   /* workspace NULL or smaller than pda_workspace_bytes() */
   PDA_ERR_ALIGNMENT = 5,   /* q, k_cache, v_cache, k_new, v_new, out or workspace not 16-byte aligned */
   PDA_ERR_VALUE = 6,       /* non-finite scale, or a host-side content check failed */
-  PDA_ERR_HIP = 7          /* a HIP call failed (launch, graph capture or instantiation) */
+  PDA_ERR_HIP = 7,         /* a HIP call failed (launch, graph capture or instantiation) */
+  PDA_ERR_SCRATCH = 8      /* pda_decode_noalloc: the step needs more than PDA_NOALLOC_SCRATCH_BYTES */
 };
 
 /* Sizes of one step.  All fields are plain host integers. */
@@ -131,6 +132,27 @@ int pda_workspace_bytes(const pda_problem *prob, size_t *bytes);
 int pda_decode(const pda_problem *prob, const void *q, const void *k_cache, const void *v_cache,
                const int32_t *block_table, const int32_t *context_lens, float scale, float *out,
                void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* pda_decode for callers that cannot allocate: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation.  There is no
+ * workspace argument: the step's workspace (work order and partial softmax
+ * states) lives in a static device array of PDA_NOALLOC_SCRATCH_BYTES that
+ * the library holds on each GPU it runs on until the process ends; its
+ * address is looked up once per device, on the first call made with that
+ * device current.  The call allocates nothing.  Arguments, layouts, results
+ * (bitwise those of pda_decode) and errors are pda_decode's, plus
+ * PDA_ERR_SCRATCH, returned without touching the GPU, when
+ * pda_workspace_bytes() of the descriptor exceeds PDA_NOALLOC_SCRATCH_BYTES
+ * (decode steps of the named Llama-3 shapes need at most a few MB; many new
+ * tokens per sequence with split contexts can need more).  Nothing in the
+ * scratch needs clearing: each call writes every entry it reads.  All calls
+ * on one GPU share its scratch, so calls that overlap on the GPU (on
+ * different streams, or from several host threads) race: the caller orders
+ * them, e.g. on one stream. */
+#define PDA_NOALLOC_SCRATCH_BYTES (64u << 20)
+int pda_decode_noalloc(const pda_problem *prob, const void *q, const void *k_cache, const void *v_cache,
+                       const int32_t *block_table, const int32_t *context_lens, float scale, float *out,
+                       hipStream_t stream);
 
 /* Pass 1 alone (the work-order kernel when needed, then one workgroup per
  * work item):

@@ -8,6 +8,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <mutex>
 #include <new>
 
 #include "pda.h"
@@ -255,6 +256,36 @@ hipError_t launch_append_of(const pda_problem* p, const pda::StepArgs& args, con
 
 }  // namespace
 
+// The scratch of pda_decode_noalloc: the workspace of a step (work order and
+// partial softmax states) for callers that cannot allocate.  Each GPU the
+// library runs on holds its own copy of this array from the code object's
+// load until the process ends.  In host code `scratch` names a host-side
+// stand-in, not device memory: the device address comes from
+// hipGetSymbolAddress, once per device, and only that address is used.
+static __device__ __align__(256) unsigned char scratch[PDA_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mutex;
+void* scratch_ptr[kMaxDevices];  // device address of `scratch` on each device (null: not yet looked up)
+
+// The current device's scratch address (looked up on its first use), or null
+// when the device cannot be named or the lookup fails.
+void* device_scratch() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(scratch_mutex);
+  if (!scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    scratch_ptr[dev] = ptr;
+  }
+  return scratch_ptr[dev];
+}
+
+}  // namespace
+
 struct pda_step_graph {
   hipGraph_t graph;
   hipGraphExec_t exec;
@@ -353,6 +384,22 @@ int pda_decode(const pda_problem* prob, const void* q, const void* k_cache, cons
                                    workspace_bytes, stream);
   if (rc != PDA_OK) return rc;
   return pda_merge_partitions(prob, context_lens, out, workspace, workspace_bytes, stream);
+}
+
+int pda_decode_noalloc(const pda_problem* prob, const void* q, const void* k_cache, const void* v_cache,
+                       const int32_t* block_table, const int32_t* context_lens, float scale, float* out,
+                       hipStream_t stream) {
+  Plan plan;
+  int rc = make_plan(prob, nullptr, &plan);
+  if (rc != PDA_OK) return rc;
+  if (plan.info.workspace_bytes > (size_t)PDA_NOALLOC_SCRATCH_BYTES) return PDA_ERR_SCRATCH;
+  void* ws = nullptr;
+  if (prob->num_seqs > 0 && !(ws = device_scratch())) return PDA_ERR_HIP;
+  pda::StepArgs args;
+  rc = prepare_step(prob, nullptr, q, k_cache, v_cache, block_table, context_lens, scale, out, ws,
+                    PDA_NOALLOC_SCRATCH_BYTES, &plan, &args);
+  if (rc != PDA_OK) return rc;
+  return launch_attention(prob, plan, args, stream);
 }
 
 int pda_append_kv(const pda_problem* prob, const void* k_new, const void* v_new, const int32_t* block_table,
@@ -509,6 +556,8 @@ const char* pda_status_string(int status) {
       return "PDA_ERR_ALIGNMENT: q/k_cache/v_cache/k_new/v_new/workspace need 16-byte alignment, out 4-byte";
     case PDA_ERR_VALUE: return "PDA_ERR_VALUE: non-finite scale or invalid device contents";
     case PDA_ERR_HIP: return "PDA_ERR_HIP: a HIP launch, graph capture or instantiation failed";
+    case PDA_ERR_SCRATCH:
+      return "PDA_ERR_SCRATCH: the step needs more workspace than pda_decode_noalloc's static scratch holds";
     default: return "unknown pda status";
   }
 }

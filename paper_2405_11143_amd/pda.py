@@ -18,13 +18,15 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libpda.so")
 
 PDA_OK, PDA_ERR_NULL, PDA_ERR_SHAPE, PDA_ERR_UNSUPPORTED = 0, 1, 2, 3
-PDA_ERR_WORKSPACE, PDA_ERR_ALIGNMENT, PDA_ERR_VALUE, PDA_ERR_HIP = 4, 5, 6, 7
+PDA_ERR_WORKSPACE, PDA_ERR_ALIGNMENT, PDA_ERR_VALUE, PDA_ERR_HIP, PDA_ERR_SCRATCH = 4, 5, 6, 7, 8
+PDA_NOALLOC_SCRATCH_BYTES = 64 << 20  # the static scratch of pda_decode_noalloc
 
 # Every function include/pda.h declares.
 EXPORTED = ("pda_plan", "pda_workspace_bytes", "pda_decode", "pda_partition_attention",
             "pda_merge_partitions", "pda_plan_shared_prefix", "pda_decode_shared_prefix", "pda_append_kv",
             "pda_step_graph_create", "pda_step_graph_launch", "pda_step_graph_destroy", "pda_token_logprobs",
-            "pda_validate_host", "pda_work_order", "pda_decode_reusing_order", "pda_status_string")
+            "pda_validate_host", "pda_work_order", "pda_decode_reusing_order", "pda_decode_noalloc",
+            "pda_status_string")
 PDA_DTYPE_BF16, PDA_DTYPE_F32 = 0, 1
 
 
@@ -74,6 +76,7 @@ def load_library(path: str = LIB_PATH):
     lib.pda_decode.argtypes = step
     lib.pda_partition_attention.argtypes = step
     lib.pda_decode_reusing_order.argtypes = step
+    lib.pda_decode_noalloc.argtypes = [P, vp, vp, vp, vp, vp, ctypes.c_float, vp, vp]
     lib.pda_work_order.argtypes = [P, vp, vp, sz, vp]
     lib.pda_merge_partitions.argtypes = [P, vp, vp, vp, sz, vp]
     G = ctypes.POINTER(pda_prefix_groups)
@@ -335,6 +338,32 @@ def pda_decode_reusing_order(q, k_cache, v_cache, block_table, context_lens, sca
     or an earlier pda_decode on it, same descriptor)."""
     return bind_decode(q, k_cache, v_cache, block_table, context_lens, scale, out, max_context_len=max_context_len,
                        partition_tokens=partition_tokens, workspace=workspace, stream=stream, reuse_order=True)()
+
+
+def bind_decode_noalloc(q, k_cache, v_cache, block_table, context_lens, scale: float, out=None, *,
+                        max_context_len: int, partition_tokens: int = 0, stream=None) -> BoundCall:
+    """pda_decode_noalloc bound to these tensors and the given (else the
+    current) stream: the step of pda_decode with its workspace in the
+    library's static scratch, so no call allocates (`out` is allocated here,
+    once, when not given)."""
+    import torch
+
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    _check_tensors(q, k_cache, v_cache, block_table, context_lens, out)
+    prob = _problem_from(q, k_cache, block_table, max_context_len, partition_tokens)
+    args = (ctypes.byref(prob), q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), block_table.data_ptr(),
+            context_lens.data_ptr(), ctypes.c_float(scale), out.data_ptr(), _stream_handle(stream, q.device))
+    return BoundCall("pda_decode_noalloc", args, (prob, q, k_cache, v_cache, block_table, context_lens, out), out)
+
+
+def pda_decode_noalloc(q, k_cache, v_cache, block_table, context_lens, scale: float, out=None, *,
+                       max_context_len: int, partition_tokens: int = 0, stream=None):
+    """pda_decode without a workspace argument (see include/pda.h): raises
+    PdaError with PDA_ERR_SCRATCH when the step needs more than
+    PDA_NOALLOC_SCRATCH_BYTES of workspace."""
+    return bind_decode_noalloc(q, k_cache, v_cache, block_table, context_lens, scale, out,
+                               max_context_len=max_context_len, partition_tokens=partition_tokens, stream=stream)()
 
 
 def bind_append_kv(k_new, v_new, block_table, context_lens, k_cache, v_cache, *, max_context_len: int,

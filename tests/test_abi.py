@@ -346,3 +346,21 @@ def test_plan_invariants_over_random_descriptors():
         split = p.num_seqs * n * p.num_q_heads * parts * (p.head_dim + 2) * 4 if parts > 1 else 0
         assert info["workspace_bytes"] == split + items * 4
         assert pda.pda_workspace_bytes(p) == info["workspace_bytes"]
+
+
+def test_noalloc_host_checks():
+    """pda_decode_noalloc's host-side answers, which touch no GPU: descriptor
+    errors as pda_decode's, PDA_ERR_SCRATCH for a step whose workspace exceeds
+    the static scratch, and nothing to do for an empty batch."""
+    f = pda.load_library().pda_decode_noalloc
+
+    def call_na(p):
+        return f(ctypes.byref(p), 0x1000, 0x1000, 0x1000, 0x1000, 0x1000, ctypes.c_float(0.125), 0x1000, None)
+
+    assert call_na(llama(head_dim=96)) == pda.pda.PDA_ERR_UNSUPPORTED
+    assert call_na(llama(num_q_heads=30)) == pda.pda.PDA_ERR_SHAPE
+    big = llama(num_query_tokens=64, partition_tokens=16)
+    assert pda.pda_workspace_bytes(big) > pda.pda.PDA_NOALLOC_SCRATCH_BYTES
+    assert call_na(big) == pda.pda.PDA_ERR_SCRATCH
+    assert call_na(llama(num_seqs=0)) == pda.pda.PDA_OK
+    assert "scratch" in pda.pda_status_string(pda.pda.PDA_ERR_SCRATCH)
