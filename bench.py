@@ -23,7 +23,11 @@ Prints one JSON line:
              kernel before it): the same algorithmic bytes / pass-1 time
              (HIP events on its stream), against the 8 TB/s HBM peak;
              `traffic` is the measured HBM bytes per launch from rocprofv3
-             counters when they were taken on this kernel source
+             counters when they were taken on this kernel source;
+             `ceiling_gbs` / `ceiling_frac`: the same K/V tiles read by a bare
+             gather kernel with the same loads and no arithmetic (the practical
+             read ceiling of this access pattern) and pass-1 time over it;
+             `stream_read_gbs`: a contiguous read of the K and V pools
   cpu_baseline  the fp64 oracle on the host cores, same workload (and, as
              one_thread, on one core over the batch's first 16 sequences)
   ms_per_step_median / _min  single steps timed one by one (a separate pass)
@@ -245,6 +249,58 @@ def timed_graph(fn, n):
     return e0.elapsed_time(e1) / n
 
 
+def step_block_ids(st):
+    """Physical ids of the blocks a step reads, each once, in first-use order."""
+    import numpy as np
+
+    nb = st.blocks_used()
+    ids = np.concatenate([st.block_table[b, :int(nb[b])] for b in range(st.B)] or [np.zeros(0, np.int32)])
+    _, first = np.unique(ids, return_index=True)
+    return ids[np.sort(first)].astype(np.int32)
+
+
+def measure_ceilings(st, k, v, stream, reps: int):
+    """HBM read ceilings of a step's traffic: the K/V tiles of every block it
+    reads gathered with the attention kernel's loads and no arithmetic (best
+    of a few workgroup counts), and a contiguous stream over the K and V pools.
+    Returns (tile bytes, gather ms, gather workgroups, stream GB/s)."""
+    import torch
+
+    from paper_2405_11143_amd import bind_gather_ceiling, bind_stream_ceiling
+
+    ids = torch.from_numpy(step_block_ids(st)).to(k.device)
+    tile_bytes = int(ids.numel()) * st.Hkv * 2 * st.block_size * st.D * 2
+    best = None
+    for wg in (1024, 2048, 4096, 8192):
+        g = bind_gather_ceiling(ids, k, v, wg, stream=stream)
+        for _ in range(3):
+            g()
+        ms = timed(g, reps, stream)
+        if best is None or ms < best[0]:
+            best = (ms, wg)
+    stream_gbs = []
+    for buf in (k, v):
+        sfn = bind_stream_ceiling(buf, 8192, stream=stream)
+        for _ in range(3):
+            sfn()
+        ms = timed(sfn, reps, stream)
+        stream_gbs.append(buf.numel() * buf.element_size() / (ms * 1e-3) / 1e9)
+    return tile_bytes, best[0], best[1], sum(stream_gbs) / len(stream_gbs)
+
+
+def ceiling_fields(st, k, v, stream, reps: int, ms_pass1: float) -> dict:
+    """The pass-1 kernel against the ceilings of its own traffic: the same K/V
+    tiles gathered without arithmetic (ceiling_frac = gather time / pass-1
+    time, both reading whole 16-token tiles) and a contiguous stream."""
+    tile_bytes, ms_g, wg, stream_gbs = measure_ceilings(st, k, v, stream, reps)
+    return {"ceiling_gbs": round(tile_bytes / (ms_g * 1e-3) / 1e9, 2),
+            "ceiling_frac": round(ms_g / ms_pass1, 4),
+            "ceiling_kind": f"gather of the step's {tile_bytes} bytes of K/V tiles with the kernel's loads, "
+                            f"no arithmetic ({wg} workgroups, {ms_g:.5f} ms)",
+            "tile_gbs_pass1": round(tile_bytes / (ms_pass1 * 1e-3) / 1e9, 2),
+            "stream_read_gbs": round(stream_gbs, 2)}
+
+
 def base_result(args, value, unit, ms_step, metric, config, dtype="bf16"):
     return {"metric": metric, "value": round(value, 2), "unit": unit, "n_gpus": 1, "steps": args.steps,
             "warmup": args.warmup, "ms_per_step": round(ms_step, 5), "higher_is_better": True,
@@ -346,6 +402,8 @@ def op_decode(args, n_tokens=1):
                    "roofline": roofline(alg / (ms_pass1 * 1e-3) / 1e9, ms_pass1, KERNEL,
                                         args.config if n_tokens == 1 else f"{args.config}_x{n_tokens}"),
                    "cpu_baseline": None})
+    if not args.no_ceiling:
+        result["roofline"].update(ceiling_fields(st, k, v, stream, args.steps, ms_pass1))
     if n_tokens > 1:
         result["query_tokens_per_s"] = round(st.B * n_tokens / (ms_step * 1e-3), 1)
         # many new tokens make the step a contraction: then the MFMA roofline binds
@@ -590,6 +648,8 @@ def main(argv=None):
     ap.add_argument("--partition-tokens", type=int, default=0,
                     help="> 0: split-K partition size in tokens (0: the library's choice)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the read-ceiling kernels (gather of the step's tiles, contiguous stream)")
     ap.add_argument("--cpu-min-seconds", type=float, default=10.0)
     ap.add_argument("--cpu-max-reps", type=int, default=60)
     ap.add_argument("--pass1-only", action="store_true",

@@ -13,4 +13,5 @@ from .pda import (EXPORTED, LIB_PATH, BoundCall, PdaError, StepGraph, bind_appen
                   make_problem, pda_append_kv, pda_decode, pda_decode_shared_prefix, pda_merge_partitions,
                   pda_partition_attention, pda_plan, pda_plan_info, pda_plan_shared_prefix, pda_prefix_groups,
                   pda_problem, pda_status_string, pda_token_logprobs, pda_validate_host, pda_workspace_bytes,
-                  pda_work_order, pda_decode_reusing_order, pda_decode_noalloc, bind_decode_noalloc)
+                  pda_work_order, pda_decode_reusing_order, pda_decode_noalloc, bind_decode_noalloc,
+                  bind_gather_ceiling, bind_stream_ceiling)

@@ -26,7 +26,7 @@ EXPORTED = ("pda_plan", "pda_workspace_bytes", "pda_decode", "pda_partition_atte
             "pda_merge_partitions", "pda_plan_shared_prefix", "pda_decode_shared_prefix", "pda_append_kv",
             "pda_step_graph_create", "pda_step_graph_launch", "pda_step_graph_destroy", "pda_token_logprobs",
             "pda_validate_host", "pda_work_order", "pda_decode_reusing_order", "pda_decode_noalloc",
-            "pda_status_string")
+            "pda_gather_ceiling", "pda_stream_ceiling", "pda_status_string")
 PDA_DTYPE_BF16, PDA_DTYPE_F32 = 0, 1
 
 
@@ -77,6 +77,8 @@ def load_library(path: str = LIB_PATH):
     lib.pda_partition_attention.argtypes = step
     lib.pda_decode_reusing_order.argtypes = step
     lib.pda_decode_noalloc.argtypes = [P, vp, vp, vp, vp, vp, ctypes.c_float, vp, vp]
+    lib.pda_gather_ceiling.argtypes = [i32, i32, i32, vp, vp, vp, i32, i32, vp, vp]
+    lib.pda_stream_ceiling.argtypes = [vp, sz, i32, vp, vp]
     lib.pda_work_order.argtypes = [P, vp, vp, sz, vp]
     lib.pda_merge_partitions.argtypes = [P, vp, vp, vp, sz, vp]
     G = ctypes.POINTER(pda_prefix_groups)
@@ -511,3 +513,35 @@ def pda_decode_shared_prefix(q, k_cache, v_cache, block_table, context_lens, sca
     if rc != PDA_OK:
         raise PdaError(rc, "pda_decode_shared_prefix")
     return out
+
+
+def bind_gather_ceiling(block_ids, k_cache, v_cache, workgroups: int, sink=None, stream=None) -> BoundCall:
+    """pda_gather_ceiling (include/pda_ceiling.h) bound to these tensors: read
+    the K and V tiles of every KV head of the listed physical blocks (device
+    int32 [n]) with the attention kernel's loads and no arithmetic."""
+    import torch
+
+    _require("block_ids", block_ids, torch.int32)
+    _require("k_cache", k_cache, torch.bfloat16)
+    _require("v_cache", v_cache, torch.bfloat16)
+    if sink is None:
+        sink = torch.empty(4 * workgroups, dtype=torch.int32, device=k_cache.device)
+    NB, Hkv, C, BS, E = k_cache.shape
+    args = (int(Hkv), int(C * E), int(NB), k_cache.data_ptr(), v_cache.data_ptr(), block_ids.data_ptr(),
+            int(block_ids.numel()), int(workgroups), sink.data_ptr(), _stream_handle(stream, k_cache.device))
+    return BoundCall("pda_gather_ceiling", args, (block_ids, k_cache, v_cache, sink), sink)
+
+
+def bind_stream_ceiling(buf, workgroups: int, sink=None, stream=None) -> BoundCall:
+    """pda_stream_ceiling bound to a contiguous device tensor: read all its
+    bytes with 16-byte non-temporal loads."""
+    import torch
+
+    if not buf.is_cuda or not buf.is_contiguous():
+        raise ValueError("buf must be a contiguous device tensor")
+    if sink is None:
+        sink = torch.empty(4 * workgroups, dtype=torch.int32, device=buf.device)
+    nbytes = buf.numel() * buf.element_size() // 16 * 16
+    args = (buf.data_ptr(), ctypes.c_size_t(nbytes), int(workgroups), sink.data_ptr(),
+            _stream_handle(stream, buf.device))
+    return BoundCall("pda_stream_ceiling", args, (buf, sink), sink)

@@ -15,13 +15,17 @@ import paper_2405_11143_amd as pda
 import workloads as W
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "pda.h")
+INCLUDE = os.path.join(ROOT, "include")
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(pda_\w+)\s*\(", text)))
+    """Every pda_* function that a header under include/ declares."""
+    names = set()
+    for h in sorted(os.listdir(INCLUDE)):
+        if h.endswith(".h"):
+            text = re.sub(r"/\*.*?\*/", "", open(os.path.join(INCLUDE, h)).read(), flags=re.S)
+            names |= set(re.findall(r"\b(pda_\w+)\s*\(", text))
+    return sorted(names)
 
 
 def test_header_declarations_match_binding():
@@ -364,3 +368,17 @@ def test_noalloc_host_checks():
     assert call_na(big) == pda.pda.PDA_ERR_SCRATCH
     assert call_na(llama(num_seqs=0)) == pda.pda.PDA_OK
     assert "scratch" in pda.pda_status_string(pda.pda.PDA_ERR_SCRATCH)
+
+
+def test_ceiling_host_checks():
+    """The read-ceiling kernels' argument checks (no launch)."""
+    lib = pda.load_library()
+    g, st = lib.pda_gather_ceiling, lib.pda_stream_ceiling
+    assert g(8, 96, 10, 0x1000, 0x1000, 0x1000, 5, 4, 0x1000, None) == pda.pda.PDA_ERR_SHAPE
+    assert g(0, 128, 10, 0x1000, 0x1000, 0x1000, 5, 4, 0x1000, None) == pda.pda.PDA_ERR_SHAPE
+    assert g(8, 128, 10, 0x1000, 0x1000, None, 5, 4, 0x1000, None) == pda.pda.PDA_ERR_NULL
+    assert g(8, 128, 10, 0x1008, 0x1000, 0x1000, 5, 4, 0x1000, None) == pda.pda.PDA_ERR_ALIGNMENT
+    assert st(0x1000, 24, 4, 0x1000, None) == pda.pda.PDA_ERR_SHAPE
+    assert st(0x1000, 0, 4, 0x1000, None) == pda.pda.PDA_ERR_SHAPE
+    assert st(None, 32, 4, 0x1000, None) == pda.pda.PDA_ERR_NULL
+    assert st(0x1004, 32, 4, 0x1000, None) == pda.pda.PDA_ERR_ALIGNMENT
