@@ -316,11 +316,15 @@ def roofline(achieved_gbs, ms, kernel, workload):
 
 def roofline_mfma(flops, ms, kernel):
     """Dense bf16 MFMA roofline of a launch whose work is bound by its
-    contractions rather than by its bytes."""
+    contractions rather than by its bytes.  The kernel runs P.V twice (the
+    bf16 high and low halves of the probabilities), so the MFMA work it
+    issues is 1.5x the algorithmic flops (q.k once, p.v twice):
+    `issued_frac` is the MFMA units' busy share that implies."""
     achieved = flops / (ms * 1e-3) / 1e12
     return {"bound": "mfma", "kernel": kernel, "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
-            "ms_per_launch": round(ms, 5), "algorithmic_flops_per_launch": int(flops)}
+            "ms_per_launch": round(ms, 5), "algorithmic_flops_per_launch": int(flops),
+            "issued_flops_factor": 1.5, "issued_frac": round(1.5 * achieved / PEAK_BF16_TFLOPS, 4)}
 
 
 def config_of(st, cfg_desc, name, plan=None, **extra):
@@ -592,8 +596,12 @@ def op_logprob(args):
     # logits from HBM.
     nbuf = args.logits_buffers or max(1, -(-512 * 2 ** 20 // (x.numel() * x.element_size())))
     bufs = [x] + [x.clone() for _ in range(nbuf - 1)]
+    ws_arg = None if args.logprob_one_workgroup else "auto"
     calls = [bind_token_logprobs(xb, tokens, 1.0, entropy=not args.no_entropy, logprobs=lp, entropies=ent,
-                                 stream=stream) for xb in bufs]  # bound once, as a serving loop would
+                                 stream=stream, workspace=ws_arg) for xb in bufs]  # bound once, as a serving loop would
+    from paper_2405_11143_amd.pda import PDA_DTYPE_BF16, PDA_DTYPE_F32, pda_logprob_workspace_bytes
+    ws_bytes = pda_logprob_workspace_bytes(B, V, PDA_DTYPE_BF16 if dtype == torch.bfloat16 else PDA_DTYPE_F32)
+    slices = 1 if (args.logprob_one_workgroup or ws_bytes == 0) else ws_bytes // (16 * B)
     turn = [0]
 
     def step():  # on the current stream
@@ -610,7 +618,7 @@ def op_logprob(args):
     what = "token log-prob" if args.no_entropy else "token log-prob + entropy"
     result = base_result(args, value, "GB/s", ms, f"{what} HBM GB/s over the LM-head logits",
                          {"workload": cfg["desc"] + f", {str(dtype).split('.')[-1]} logits", "name": name,
-                          "rows": B, "vocab": V, "logits_buffers": nbuf},
+                          "rows": B, "vocab": V, "logits_buffers": nbuf, "workgroups_per_row": slices},
                          dtype="bf16" if dtype == torch.bfloat16 else "f32")
     result["config"]["timed"] = "bound calls back to back on one stream"
     result.update({"rows_per_s": round(B / (ms * 1e-3), 1), "algorithmic_bytes_per_step": alg,
@@ -640,6 +648,8 @@ def main(argv=None):
     ap.add_argument("--logits-f32", action="store_true", help="--op logprob: float32 logits (default bf16)")
     ap.add_argument("--logits-buffers", type=int, default=0,
                     help="--op logprob: copies of the logits the calls rotate over (default: >= 512 MB in all)")
+    ap.add_argument("--logprob-one-workgroup", action="store_true",
+                    help="--op logprob: no workspace, one workgroup per row (default: rows split over workgroups)")
     ap.add_argument("--no-entropy", action="store_true",
                     help="--op logprob: log-probabilities only (what a rollout records), no entropies")
     ap.add_argument("--config", default=None, help="workload (default: llama3_8b; tiny for --op graph)")

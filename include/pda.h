@@ -275,11 +275,23 @@ int pda_step_graph_destroy(pda_step_graph *graph);
  * r * row_stride (row_stride >= vocab); the buffer holds num_rows * row_stride
  * elements and every row must be 16-byte aligned.  -inf logits have probability 0; a token id outside
  * [0, vocab) gives a NaN log-probability.  inv_temperature must be finite
- * and >= 0 (0: the uniform distribution). */
+ * and >= 0 (0: the uniform distribution).
+ *
+ * `workspace` may be NULL: one workgroup then streams each row.  Given a
+ * workspace of at least pda_logprob_workspace_bytes() bytes (16-byte
+ * aligned, any contents; 0 bytes when the batch has at least as many rows as
+ * the GPU has compute units), a smaller batch has its rows split over
+ * several workgroups whose partial states a second, small kernel merges in a
+ * fixed order; results are reproducible for a given (num_rows, vocab, dtype)
+ * and agree with the one-workgroup results to fp32 rounding.  Calls that
+ * share a workspace must not overlap on the GPU.  PDA_ERR_WORKSPACE: smaller
+ * than pda_logprob_workspace_bytes(). */
 enum pda_dtype { PDA_DTYPE_BF16 = 0, PDA_DTYPE_F32 = 1 };
+int pda_logprob_workspace_bytes(int32_t num_rows, int32_t vocab, int32_t logits_dtype, size_t *bytes);
 int pda_token_logprobs(int32_t num_rows, int32_t vocab, int64_t row_stride, int32_t logits_dtype,
                        const void *logits, const int32_t *tokens, float inv_temperature,
-                       float *logprobs, float *entropies, hipStream_t stream);
+                       float *logprobs, float *entropies, void *workspace, size_t workspace_bytes,
+                       hipStream_t stream);
 
 /* Host-side check of device contents, on HOST copies: every context length
  * is at most max_context_len and every block id a sequence reads is in

@@ -31,17 +31,25 @@ namespace {
 // (2816), while the one-token step is flat between 2816 and 4096.  A share
 // above kMaxPartitionTokens splits the longest context into the fewest equal
 // partitions of at most that size (9216 -> 2 x 4608, 16384 -> 4 x 4096).
+// Items of kWideItemRows or more query rows (tens of new tokens per
+// sequence) skip that cap: each partition beyond the first costs a partial
+// state per row written and read back, which for them is as large as the
+// partition's K/V bytes (2 MB per 4096 tokens of one KV head against 2 MB of
+// states for 2048 rows); on MI355X the chunked-prefill step (32 sequences,
+// 512 or 256 new tokens, contexts up to 8192) ran 2% and 4.5% faster in one
+// partition than in two of 4096.
 // The result is rounded up to kPartitionQuantum tokens, at least
 // kMinPartitionTokens and never longer than the longest context (then there
 // is one partition and no merge pass).
+// Longest context a descriptor may announce: keeps every token sum of the
+// kernels (a position plus a partition size) far inside int32.
+constexpr int32_t kMaxContextTokens = 1 << 28;
 constexpr int kMaxPartitionTokens = 4608;
+constexpr int64_t kWideItemRows = 64;
 constexpr int64_t kRowsShareNum = 13, kRowsShareDen = 10;
 constexpr int kMinPartitionTokens = 256;
 constexpr int kPartitionQuantum = 256;
 constexpr int64_t kConcurrentItems = 768;  // 256 compute units x 3 workgroups of 4 wavefronts
-// Longest context a descriptor may announce: keeps every token sum of the
-// kernels (a position plus a partition size) far inside int32.
-constexpr int32_t kMaxContextTokens = 1 << 28;
 
 int query_tokens(const pda_problem* p) { return p->num_query_tokens > 0 ? p->num_query_tokens : 1; }
 
@@ -105,13 +113,15 @@ int make_plan(const pda_problem* p, const pda_prefix_groups* groups, Plan* plan)
     // (a product that would overflow only means: as long as allowed)
     int64_t share = units > (INT64_MAX / 4) / len ? INT64_MAX / 4
                                                   : (units * len / 2 + kConcurrentItems - 1) / kConcurrentItems;
-    if (std::min(nqc, cpg) * qc * G >= pda::kMaxGroup) share = share * kRowsShareNum / kRowsShareDen;
-    if (share > kMaxPartitionTokens) {
-      const int64_t pieces = (len + kMaxPartitionTokens - 1) / kMaxPartitionTokens;
+    const int64_t item_rows = (int64_t)std::min(nqc, cpg) * qc * G;
+    if (item_rows >= pda::kMaxGroup) share = share * kRowsShareNum / kRowsShareDen;
+    const int64_t cap = item_rows >= kWideItemRows ? kMaxContextTokens : kMaxPartitionTokens;
+    if (share > cap) {
+      const int64_t pieces = (len + cap - 1) / cap;
       share = (len + pieces - 1) / pieces;
     }
     const int64_t quanta = (share + kPartitionQuantum - 1) / kPartitionQuantum;
-    tp = (int)std::min<int64_t>(kMaxPartitionTokens, std::max<int64_t>(kMinPartitionTokens, quanta * kPartitionQuantum));
+    tp = (int)std::min<int64_t>(cap, std::max<int64_t>(kMinPartitionTokens, quanta * kPartitionQuantum));
     const int64_t rounded = (len + pda::kBlockTokens - 1) / pda::kBlockTokens * pda::kBlockTokens;
     if (rounded < tp) tp = (int)rounded;  // the whole context fits one partition
   } else {
@@ -496,13 +506,23 @@ int pda_decode_shared_prefix(const pda_problem* prob, const pda_prefix_groups* g
   return launch_attention(prob, plan, args, stream);
 }
 
+int pda_logprob_workspace_bytes(int32_t num_rows, int32_t vocab, int32_t logits_dtype, size_t* bytes) {
+  if (!bytes) return PDA_ERR_NULL;
+  if (num_rows < 0 || vocab < 1) return PDA_ERR_SHAPE;
+  if (logits_dtype != PDA_DTYPE_BF16 && logits_dtype != PDA_DTYPE_F32) return PDA_ERR_UNSUPPORTED;
+  const int S = pda::logprob_slices(num_rows, vocab, logits_dtype == PDA_DTYPE_BF16 ? 2 : 4);
+  *bytes = S > 1 ? (size_t)num_rows * S * 16 : 0;  // S partial states of 16 bytes per row
+  return PDA_OK;
+}
+
 int pda_token_logprobs(int32_t num_rows, int32_t vocab, int64_t row_stride, int32_t logits_dtype, const void* logits,
                        const int32_t* tokens, float inv_temperature, float* logprobs, float* entropies,
-                       hipStream_t stream) {
+                       void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (num_rows < 0 || vocab < 1 || row_stride < vocab) return PDA_ERR_SHAPE;
   if (logits_dtype != PDA_DTYPE_BF16 && logits_dtype != PDA_DTYPE_F32) return PDA_ERR_UNSUPPORTED;
   const int esize = logits_dtype == PDA_DTYPE_BF16 ? 2 : 4;
   if ((int64_t)vocab * esize + 64 > 0x7fffffff) return PDA_ERR_SHAPE;  // one row must fit a buffer descriptor
+  if ((int64_t)num_rows * pda::kLpMaxSlices > 0x7fffffff) return PDA_ERR_SHAPE;  // the grid
   if (num_rows == 0) return PDA_OK;
   if (!logits || !tokens || !logprobs) return PDA_ERR_NULL;
   if (!isfinite(inv_temperature) || inv_temperature < 0.f) return PDA_ERR_VALUE;
@@ -518,6 +538,18 @@ int pda_token_logprobs(int32_t num_rows, int32_t vocab, int64_t row_stride, int3
   a.vocab = vocab;
   a.row_stride = row_stride;
   a.elem_bytes = esize;
+  a.slices = 1;
+  a.part = nullptr;
+  if (workspace) {
+    size_t need = 0;
+    pda_logprob_workspace_bytes(num_rows, vocab, logits_dtype, &need);
+    if (workspace_bytes < need) return PDA_ERR_WORKSPACE;
+    if (!aligned(workspace, 16)) return PDA_ERR_ALIGNMENT;
+    if (need > 0) {
+      a.slices = pda::logprob_slices(num_rows, vocab, esize);
+      a.part = static_cast<float*>(workspace);
+    }
+  }
   return pda::launch_logprob(a, stream) == hipSuccess ? PDA_OK : PDA_ERR_HIP;
 }
 

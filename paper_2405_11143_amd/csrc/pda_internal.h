@@ -72,6 +72,24 @@ __device__ __forceinline__ int chunk_visible(const StepArgs& a, int L, int chunk
   return L - a.num_query_tokens + i0 + nv;
 }
 
+// The token log-probability kernel: 1024-thread workgroups, one per row; a
+// batch with fewer rows than compute units has its rows split into `slices`
+// workgroups when the caller gives a workspace, so that every compute unit
+// streams part of a row.
+constexpr int kLpThreads = 1024;
+constexpr int kLpTargetWorkgroups = 256;  // one per compute unit
+constexpr int kLpMaxSlices = 16;
+
+// Workgroups per row for a log-prob call with a workspace (1: none needed).
+inline int logprob_slices(int rows, int vocab, int elem_bytes) {
+  if (rows <= 0) return 1;
+  const long chunks = (long)vocab * elem_bytes / 16;  // whole 16-byte chunks of a row
+  long s = (kLpTargetWorkgroups + (long)rows - 1) / rows;
+  if (s > kLpMaxSlices) s = kLpMaxSlices;
+  if (s > chunks / kLpThreads) s = chunks / kLpThreads;  // at least a chunk per thread in each slice
+  return s < 1 ? 1 : (int)s;
+}
+
 // Arguments of the token log-probability kernel (passed by value).
 struct LogprobArgs {
   const void* logits;      // [num_rows][row_stride] bf16 or fp32, the first `vocab` of each row used
@@ -83,6 +101,8 @@ struct LogprobArgs {
   int32_t vocab;
   int64_t row_stride;      // elements
   int32_t elem_bytes;      // 2 (bf16) or 4 (fp32)
+  int32_t slices;          // workgroups per row (1: no workspace, or enough rows)
+  float* part;             // [num_rows][slices][4] partial states (mk, s, t, -) when slices > 1
 };
 
 typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));

@@ -64,12 +64,13 @@ struct Staging {
   static constexpr int TC = WaveAttention<D>::kTileBytes / 16;       // 16-byte pieces per tile
   static constexpr int kLoads = SB * 2 * TC / (kWaves * kWaveSize);  // per thread and step
   static constexpr int kRowPieces = D / 8;                            // 16-byte pieces per V row
-  // A block is its K tile as loaded, then its V tile with 16 bytes of padding
-  // after every row: the transposed V reads take 32 bytes from each of 16
-  // rows per instruction, and with the padding those rows start 4 banks
-  // apart instead of all on the same 8 banks (unpadded the staged step ran
-  // 10% slower).
-  static constexpr int kBlockPieces = TC + kBlockTokens * (kRowPieces + 1);
+  // A block is its K tile as loaded, then its V tile with 32 bytes of padding
+  // after every row: a transposed V read takes 32 bytes from each of 4 rows
+  // per group of 16 lanes, and with the padding those rows start 8 banks
+  // apart, so the 4 pieces fall on disjoint banks (unpadded the staged step
+  // ran 10% slower; 16 bytes of padding, which overlaps neighbouring rows'
+  // banks by half, ran 0.5-1.3% slower than 32 on MI355X).
+  static constexpr int kBlockPieces = TC + kBlockTokens * (kRowPieces + 2);
   uint4 buf[3][SB][kBlockPieces];
   int ids[kIdWindow];
 };
@@ -251,7 +252,7 @@ __device__ void run_staged(WaveAttention<D>& wave, WaveAttention<D>& wave_b, Sta
     const int pc = ci % TC;
     constexpr int RP = Staging<D, SB>::kRowPieces;
     dst[k] = ci / (2 * TC) * Staging<D, SB>::kBlockPieces +
-             (((ci / TC) & 1) ? TC + pc / RP * (RP + 1) + pc % RP : pc);
+             (((ci / TC) & 1) ? TC + pc / RP * (RP + 2) + pc % RP : pc);
   }
   auto commit = [&](const uint4(&r)[NL], int buf) {
 #pragma unroll

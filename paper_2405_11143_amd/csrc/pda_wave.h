@@ -96,7 +96,7 @@ struct WaveAttention {
   static constexpr int VT = D / 16;               // P.V MFMA output tiles (16 d each)
   static constexpr int kRowBytes = D * 2;         // one token row of a V tile
   static constexpr int kTileBytes = kBlockTokens * kRowBytes;
-  static constexpr int kStagedRow = D + 8;        // elements per V row staged in LDS (16 bytes of padding)
+  static constexpr int kStagedRow = D + 16;       // elements per V row staged in LDS (32 bytes of padding)
   static constexpr float kNegInf = -__builtin_huge_valf();
   static constexpr float kFloor = -1e30f;         // running max of a row that has seen no token
   static constexpr float kRescaleSlack = 8.f;     // log2 of the largest unnormalised probability

@@ -25,6 +25,7 @@ PDA_NOALLOC_SCRATCH_BYTES = 64 << 20  # the static scratch of pda_decode_noalloc
 EXPORTED = ("pda_plan", "pda_workspace_bytes", "pda_decode", "pda_partition_attention",
             "pda_merge_partitions", "pda_plan_shared_prefix", "pda_decode_shared_prefix", "pda_append_kv",
             "pda_step_graph_create", "pda_step_graph_launch", "pda_step_graph_destroy", "pda_token_logprobs",
+            "pda_logprob_workspace_bytes",
             "pda_validate_host", "pda_work_order", "pda_decode_reusing_order", "pda_decode_noalloc",
             "pda_gather_ceiling", "pda_stream_ceiling", "pda_status_string")
 PDA_DTYPE_BF16, PDA_DTYPE_F32 = 0, 1
@@ -90,7 +91,8 @@ def load_library(path: str = LIB_PATH):
     lib.pda_step_graph_launch.argtypes = [vp, vp]
     lib.pda_step_graph_destroy.argtypes = [vp]
     lib.pda_token_logprobs.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, vp, vp,
-                                       ctypes.c_float, vp, vp, vp]
+                                       ctypes.c_float, vp, vp, vp, sz, vp]
+    lib.pda_logprob_workspace_bytes.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(sz)]
     lib.pda_validate_host.argtypes = [P, vp, vp, ctypes.POINTER(ctypes.c_int64)]
     lib.pda_status_string.argtypes = [i32]
     lib.pda_status_string.restype = ctypes.c_char_p
@@ -440,11 +442,21 @@ class StepGraph:
             pass
 
 
+def pda_logprob_workspace_bytes(rows: int, vocab: int, dtype: int) -> int:
+    ws = ctypes.c_size_t()
+    rc = load_library().pda_logprob_workspace_bytes(int(rows), int(vocab), int(dtype), ctypes.byref(ws))
+    if rc != PDA_OK:
+        raise PdaError(rc, "pda_logprob_workspace_bytes")
+    return ws.value
+
+
 def bind_token_logprobs(logits, tokens, inv_temperature: float = 1.0, entropy: bool = True, vocab: int = None,
-                        logprobs=None, entropies=None, stream=None) -> BoundCall:
+                        logprobs=None, entropies=None, stream=None, workspace="auto") -> BoundCall:
     """pda_token_logprobs bound to these tensors and the given (else the
     current) stream; calling it returns (logprobs, entropies or None).  The
-    arguments are those of pda_token_logprobs."""
+    arguments are those of pda_token_logprobs; `workspace` is "auto" (a uint8
+    tensor of pda_logprob_workspace_bytes, allocated here once), None (one
+    workgroup per row) or a caller's uint8 device tensor."""
     import torch
 
     if logits.dim() != 2 or logits.stride(1) != 1:
@@ -466,20 +478,26 @@ def bind_token_logprobs(logits, tokens, inv_temperature: float = 1.0, entropy: b
         logprobs = torch.empty(rows, dtype=torch.float32, device=logits.device)
     if entropy and entropies is None:
         entropies = torch.empty(rows, dtype=torch.float32, device=logits.device)
+    if isinstance(workspace, str):
+        need = pda_logprob_workspace_bytes(rows, vocab, dtype) if vocab >= 1 else 0
+        workspace = torch.empty(need, dtype=torch.uint8, device=logits.device) if need > 0 else None
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     args = (rows, vocab, logits.stride(0), dtype, logits.data_ptr(), tokens.data_ptr(),
             ctypes.c_float(inv_temperature), logprobs.data_ptr(), entropies.data_ptr() if entropy else None,
-            _stream_handle(stream, logits.device))
-    keep = (logits, tokens, logprobs, entropies)
+            ws_ptr, ws_bytes, _stream_handle(stream, logits.device))
+    keep = (logits, tokens, logprobs, entropies, workspace)
     return BoundCall("pda_token_logprobs", args, keep, (logprobs, entropies if entropy else None))
 
 
 def pda_token_logprobs(logits, tokens, inv_temperature: float = 1.0, entropy: bool = True, vocab: int = None,
-                       logprobs=None, entropies=None, stream=None):
+                       logprobs=None, entropies=None, stream=None, workspace="auto"):
     """Log-probability of tokens[r] under softmax(logits[r][:vocab] * inv_temperature),
     and the entropy of that distribution (natural-log units).  logits: a device
     tensor [rows][row_stride] of bf16 or float32 (16-byte aligned rows); tokens
     int32 [rows].  Returns (logprobs fp32 [rows], entropies fp32 [rows] or None)."""
-    return bind_token_logprobs(logits, tokens, inv_temperature, entropy, vocab, logprobs, entropies, stream)()
+    return bind_token_logprobs(logits, tokens, inv_temperature, entropy, vocab, logprobs, entropies, stream,
+                               workspace)()
 
 
 def pda_decode_shared_prefix(q, k_cache, v_cache, block_table, context_lens, scale: float, group_start,

@@ -117,11 +117,18 @@ int main() {
   }
   // log-prob argument checks
   EXPECT(pda_token_logprobs(4, 0, 0, PDA_DTYPE_BF16, dummy, (const int32_t*)dummy, 1.f, (float*)dummy, nullptr,
-                            nullptr) == PDA_ERR_SHAPE);
+                            nullptr, 0, nullptr) == PDA_ERR_SHAPE);
   EXPECT(pda_token_logprobs(4, 0x7fffffff, 0x7fffffff, PDA_DTYPE_F32, dummy, (const int32_t*)dummy, 1.f,
-                            (float*)dummy, nullptr, nullptr) == PDA_ERR_SHAPE);
+                            (float*)dummy, nullptr, nullptr, 0, nullptr) == PDA_ERR_SHAPE);
   EXPECT(pda_token_logprobs(4, 1000, 1000, PDA_DTYPE_BF16, dummy, (const int32_t*)dummy, 1.f, (float*)dummy,
-                            nullptr, nullptr) == PDA_ERR_HIP);
+                            nullptr, nullptr, 0, nullptr) == PDA_ERR_HIP);
+  // log-prob workspace sizes over random shapes
+  for (int it = 0; it < 2000; ++it) {
+    const int32_t rows = pick(sizes), vocab = pick(sizes);
+    size_t bytes = 1;
+    const int rc = pda_logprob_workspace_bytes(rows, vocab, (int32_t)(next_u32() % 3), &bytes);
+    EXPECT(rc != PDA_OK || rows < 0 || vocab < 1 || bytes == 0 || bytes % 16 == 0);
+  }
   for (int s = -2; s < 12; ++s) EXPECT(strlen(pda_status_string(s)) > 0);
   if (fails) {
     fprintf(stderr, "%d check(s) failed\n", fails);

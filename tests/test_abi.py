@@ -201,10 +201,10 @@ def test_logprob_validation():
     ok = dict(rows=4, vocab=1000, stride=1000, dtype=pda.pda.PDA_DTYPE_BF16, logits=0x1000, tokens=0x1000,
               inv_t=1.0, lp=0x1000, ent=0x1000)
 
-    def call(**kw):
+    def call(ws=None, ws_bytes=0, **kw):
         a = dict(ok, **kw)
         return f(a["rows"], a["vocab"], a["stride"], a["dtype"], a["logits"], a["tokens"],
-                 ctypes.c_float(a["inv_t"]), a["lp"], a["ent"], None)
+                 ctypes.c_float(a["inv_t"]), a["lp"], a["ent"], ws, ws_bytes, None)
     assert call(rows=-1) == pda.pda.PDA_ERR_SHAPE
     assert call(vocab=0) == pda.pda.PDA_ERR_SHAPE
     assert call(stride=999) == pda.pda.PDA_ERR_SHAPE
@@ -219,6 +219,15 @@ def test_logprob_validation():
     assert call(stride=1004) == pda.pda.PDA_ERR_ALIGNMENT          # rows of 2008 bytes
     assert call(stride=1002, dtype=pda.pda.PDA_DTYPE_F32) == pda.pda.PDA_ERR_ALIGNMENT
     assert call(rows=0, logits=None, tokens=None, lp=None) == pda.pda.PDA_OK  # nothing to do
+    # the workspace: rows split over workgroups when it is given and the batch has fewer rows than compute
+    # units (at most 16 per row, at least one 16-byte chunk per thread of each)
+    need = pda.pda.pda_logprob_workspace_bytes(100, 128256, pda.pda.PDA_DTYPE_BF16)
+    assert need == 100 * 3 * 16
+    assert pda.pda.pda_logprob_workspace_bytes(8, 128256, pda.pda.PDA_DTYPE_BF16) == 8 * 15 * 16
+    assert pda.pda.pda_logprob_workspace_bytes(256, 128256, pda.pda.PDA_DTYPE_BF16) == 0  # enough rows
+    assert pda.pda.pda_logprob_workspace_bytes(4, 1000, pda.pda.PDA_DTYPE_BF16) == 0  # rows too short to split
+    assert call(rows=100, vocab=128256, stride=128256, ws=0x1000, ws_bytes=need - 1) == pda.pda.PDA_ERR_WORKSPACE
+    assert call(rows=100, vocab=128256, stride=128256, ws=0x1008, ws_bytes=need) == pda.pda.PDA_ERR_ALIGNMENT
 
 
 def test_append_and_graph_validation():
@@ -326,8 +335,9 @@ def test_binding_has_no_fallback(tmp_path):
 def test_plan_invariants_over_random_descriptors():
     """For seeded random valid descriptors, the library's own partition choice
     covers the longest context, is a multiple of 256 (or the whole context
-    rounded to 16) and at most 4608 tokens, and the workspace holds the
-    partial states (when split) and one order entry per work item."""
+    rounded to 16) and at most 4608 tokens unless its items hold 64 or more
+    query rows (then it is not capped), and the workspace holds the partial
+    states (when split) and one order entry per work item."""
     rng = np.random.default_rng(2405)
     for _ in range(400):
         G = int(rng.choice([1, 2, 4, 5, 7, 8, 16]))
@@ -339,13 +349,14 @@ def test_plan_invariants_over_random_descriptors():
                              max_len, 0, 16, n)
         info = pda.pda_plan(p)
         tp, parts = info["partition_tokens"], info["num_partitions"]
-        assert tp % 16 == 0 and 16 <= tp <= 4608
-        assert tp % 256 == 0 or tp == -(-max(max_len, 1) // 16) * 16
-        assert parts == (-(-max_len // tp) if max_len > 0 else 1)
-        assert parts * tp >= max_len
         qc = min(n, 16 // G)
         nqc = -(-n // qc)
         cpg = 8 if nqc > 4 else 4
+        wide = min(nqc, cpg) * qc * G >= 64
+        assert tp % 16 == 0 and 16 <= tp and (wide or tp <= 4608)
+        assert tp % 256 == 0 or tp == -(-max(max_len, 1) // 16) * 16
+        assert parts == (-(-max_len // tp) if max_len > 0 else 1)
+        assert parts * tp >= max_len
         items = p.num_seqs * hkv * -(-nqc // cpg) * parts
         split = p.num_seqs * n * p.num_q_heads * parts * (p.head_dim + 2) * 4 if parts > 1 else 0
         assert info["workspace_bytes"] == split + items * 4

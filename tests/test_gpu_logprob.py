@@ -173,3 +173,63 @@ def test_neg_inf_rows_take_entropy_again_alone(dev, dtype):
     lp_only, none = pda_token_logprobs(y, tt2, 1.0, entropy=False)
     torch.cuda.synchronize()
     assert none is None and torch.equal(lp_only, lp1)
+
+
+@pytest.mark.parametrize("rows,V,dtype", [(100, 128256, torch.bfloat16), (8, 128256, torch.bfloat16),
+                                          (3, 151936, torch.float32), (40, 33000, torch.bfloat16)],
+                         ids=str)
+def test_rows_split_over_workgroups(dev, rows, V, dtype):
+    """A batch with fewer rows than compute units, given a workspace, has each
+    row streamed by several workgroups whose states a second kernel merges in
+    slice order: results agree with one workgroup per row to fp32 rounding,
+    match the oracle and repeat bit for bit, whatever the workspace held
+    before (NaN bytes, or another call's states)."""
+    from paper_2405_11143_amd.pda import PDA_DTYPE_BF16, PDA_DTYPE_F32, pda_logprob_workspace_bytes
+
+    x, tok = W.make_logits(rows, V, seed=rows + V, device=dev, dtype=dtype)
+    tt = torch.from_numpy(tok).to(dev)
+    need = pda_logprob_workspace_bytes(rows, V, PDA_DTYPE_BF16 if dtype == torch.bfloat16 else PDA_DTYPE_F32)
+    assert need > 0
+    ws = torch.full((need + 4096,), 0xff, dtype=torch.uint8, device=dev)  # NaN patterns; larger than needed
+    lp, ent = pda_token_logprobs(x, tt, 1.0, workspace=ws)
+    lp1, ent1 = pda_token_logprobs(x, tt, 1.0, workspace=None)  # one workgroup per row
+    torch.cuda.synchronize()
+    ref_lp, ref_ent = oracle.logprob(host_values(x), tok, 1.0)
+    compare(lp, ent, ref_lp, ref_ent, f"split rows={rows} V={V} {dtype}")
+    compare(lp1, ent1, ref_lp, ref_ent, f"one workgroup per row rows={rows} V={V} {dtype}")
+    d_lp = (lp - lp1).abs().max().item()
+    d_ent = (ent - ent1).abs().max().item()
+    print(f"split vs one workgroup: logprob {d_lp:.2e}, entropy {d_ent:.2e}", flush=True)
+    assert d_lp <= 2e-5 and d_ent <= 2e-5
+    for _ in range(2):
+        lp2, ent2 = pda_token_logprobs(x, tt, 1.0, workspace=ws)
+        assert torch.equal(lp, lp2) and torch.equal(ent, ent2), "run-to-run"
+    lp3, none = pda_token_logprobs(x, tt, 1.0, entropy=False, workspace=ws)
+    torch.cuda.synchronize()
+    assert none is None and torch.equal(lp, lp3), "without entropies"
+    # the same workspace for a call of another shape, then this one again
+    xs, toks = W.make_logits(2, 50000, seed=5, device=dev, dtype=torch.bfloat16)
+    lps, ents = pda_token_logprobs(xs, torch.from_numpy(toks).to(dev), 1.0, workspace=ws)
+    ref_lps, ref_ents = oracle.logprob(W.bf16_bits(xs), toks, 1.0)
+    compare(lps, ents, ref_lps, ref_ents, "another shape on the same workspace")
+    lp4, ent4 = pda_token_logprobs(x, tt, 1.0, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(lp, lp4) and torch.equal(ent, ent4)
+
+
+def test_split_rows_with_neg_inf(dev):
+    """-inf logits in some slices of split rows: each slice takes its entropy
+    sum again, guarded, against its own reference before the merge."""
+    x, tok = W.make_logits(8, 128256, seed=33, device=dev, dtype=torch.bfloat16)
+    x[1, 5000:70000] = float("-inf")   # spans several slices
+    x[4, ::11] = float("-inf")
+    x[6, 127000:] = float("-inf")      # the partial chunk's slice only
+    tok[1], tok[4], tok[6] = 3, 1, 5
+    tt = torch.from_numpy(tok).to(dev)
+    lp, ent = pda_token_logprobs(x, tt, 1.0)
+    lp1, ent1 = pda_token_logprobs(x, tt, 1.0, workspace=None)
+    torch.cuda.synchronize()
+    ref_lp, ref_ent = oracle.logprob(W.bf16_bits(x), tok, 1.0)
+    compare(lp, ent, ref_lp, ref_ent, "split rows with -inf logits")
+    compare(lp1, ent1, ref_lp, ref_ent, "one workgroup per row with -inf logits")
+    assert np.isfinite(ent.cpu().numpy()).all()

@@ -75,6 +75,56 @@ def test_many_chunk_groups(dev):
     check(got, ref, "128 new tokens, 4 chunk groups")
 
 
+@pytest.mark.parametrize("Hq,Hkv", [(32, 8), (8, 1)], ids=["G4", "G8"])
+@pytest.mark.parametrize("n", [256, 512])
+@pytest.mark.parametrize("partition_tokens", [0, 256])
+def test_chunked_prefill_sizes(dev, Hq, Hkv, n, partition_tokens):
+    """Chunked-prefill-sized steps (256 and 512 new tokens per sequence: 32 to
+    128 query chunks in 4 to 16 wide items per (partition, sequence, KV
+    head)), with contexts shorter than the chunk (its first tokens see
+    nothing or a few tokens), equal to it and longer, whole and split in
+    256-token partitions; every element against the oracle."""
+    lens = [n - 100, n, n + 37, 1500, 2049]
+    st = W.custom_structure(len(lens), Hq, Hkv, 128, lens, seed=400 + n + Hq)
+    _, k, v = W.fill_values(st, dev, fill="nan")
+    q = W.fill_multi_q(st, n, dev)
+    plan = pda_plan(make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq,
+                                 st.max_context_len, partition_tokens, num_query_tokens=n))
+    print(f"chunked prefill n={n} G={Hq // Hkv} Tp={partition_tokens}: plan {plan}", flush=True)
+    got = run_multi(st, q, k, v, dev, partition_tokens)
+    for b, L in enumerate(lens):  # rows of tokens before the context's start see nothing
+        assert np.all(got[b, :max(0, n - L)] == 0), b
+    ref = oracle.decode_multi(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
+                              st.context_lens, st.scale, threads=THREADS)
+    check(got, ref, f"chunked prefill n={n} Hq={Hq} Hkv={Hkv} Tp={partition_tokens}",
+          f"B*n*Hq*D = {st.B}*{n}*{Hq}*128")
+
+
+def test_chunked_prefill_full_size_sampled(dev):
+    """The chunked-prefill workload at full size (32 sequences, contexts of
+    1024-8192 tokens whose last 512 are the chunk), in the launch
+    configuration the benchmark times; rows sampled over sequences, chunk
+    positions and heads (the oracle would need minutes for all of them), plus
+    properties of every row: finite, and each a convex combination of V rows."""
+    st = W.make_structure("chunked_prefill")
+    n = 512
+    plan = pda_plan(make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq,
+                                 st.max_context_len, num_query_tokens=n))
+    print(f"chunked_prefill x {n}: plan={plan}", flush=True)
+    _, k, v = W.fill_values(st, dev, fill="nan")
+    q = W.fill_multi_q(st, n, dev)
+    got = run_multi(st, q, k, v, dev)
+    assert np.isfinite(got).all()
+    vmax = float(torch.nan_to_num(v.float().abs(), nan=0.0).max())
+    assert np.abs(got).max() <= vmax
+    r = np.random.default_rng(17)
+    rows = np.stack([r.integers(0, st.B, 256), r.integers(0, n, 256), r.integers(0, st.Hq, 256)], axis=1)
+    rows[:8, 1] = [0, 1, 2, 255, 256, 509, 510, 511]
+    ref = oracle.decode_multi_rows(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
+                                   st.context_lens, st.scale, rows.astype(np.int32), threads=THREADS)
+    check(got[rows[:, 0], rows[:, 1], rows[:, 2]], ref, "chunked_prefill 512 new tokens, sampled rows")
+
+
 @pytest.mark.parametrize("Hq,Hkv,D,n", CASES, ids=lambda x: str(x))
 @pytest.mark.parametrize("partition_tokens", [0, 16, 64])
 def test_multi_token_parity(dev, Hq, Hkv, D, n, partition_tokens):

@@ -76,6 +76,12 @@ CONFIGS: Dict[str, dict] = {
     "r1_qwen14b": dict(index=6, B=256, Hq=40, Hkv=8, D=128, lens=("uniform", 1024, 9216), pool_slack=1.1,
                        desc="long-CoT rollout, DeepSeek-R1-Distill-Qwen-14B attention shape: B=256, "
                             "40 q / 8 kv heads (G=5), D=128, L~U[1024,9216]"),
+    # Chunked prefill (Section 3.2 names it among vLLM's features): a chunk of
+    # a prompt's tokens (bench.py --tokens, e.g. 512) attends over the
+    # cached context plus itself, causally.
+    "chunked_prefill": dict(index=7, B=32, Hq=32, Hkv=8, D=128, lens=("uniform", 1024, 8192), pool_slack=1.1,
+                            desc="chunked prefill: B=32, 32 q / 8 kv heads, D=128, contexts L~U[1024,8192] "
+                                 "whose last n tokens are the chunk"),
 }
 CONFIG_NAMES = sorted(CONFIGS, key=lambda n: CONFIGS[n]["index"])
 
@@ -456,6 +462,8 @@ LOGIT_CONFIGS: Dict[str, dict] = {
     "qwen_vocab": dict(index=11, B=256, V=151936,
                        desc="LM-head logits of a Qwen decode step: B=256 rows x 151936 vocabulary"),
     "tiny_vocab": dict(index=12, B=5, V=1000, desc="tiny: 5 rows x 1000 vocabulary"),
+    "llama3_vocab_b32": dict(index=13, B=32, V=128256,
+                             desc="LM-head logits of a small Llama-3 decode batch: B=32 rows x 128256 vocabulary"),
 }
 
 
