@@ -39,6 +39,12 @@ Other steps around attention (--op):
   graph    append + attention as one captured HIP graph against the same
            calls issued eagerly from bound calls (default workload: the tiny
            batch, where launch overhead dominates)
+  model_step  a model's decode step over --layers layers (default 32; each
+           layer's append into its own cache and its attention, the work
+           order once) as one HIP graph (with one new token, each layer's
+           append folded into its pass 1) against the same work as bound
+           calls issued one by one (append and attention, and the folded
+           pda_decode_append): per-layer microseconds (default: tiny)
   prefix   the shared-prefix workload (32 prompts x 8 samples) with each
            prompt's prefix attended once for its samples, against the plain
            decode step
@@ -512,6 +518,103 @@ def op_graph(args):
     return result
 
 
+def op_model_step(args):
+    """A model's decode step: for each of --layers layers, the KV append into
+    that layer's own cache and its attention step (work order once per step),
+    as bound calls issued one by one and as one captured HIP graph
+    (pda_model_step_graph_create)."""
+    import torch
+
+    import workloads as W
+    from paper_2405_11143_amd import BoundCall, ModelStepGraph, bind_append_kv, bind_decode
+    from paper_2405_11143_amd.pda import _stream_handle
+
+    n, nl = args.tokens, args.layers
+    dev = torch.device("cuda:0")
+    st = W.make_structure(args.config)
+    bt = torch.from_numpy(st.block_table).to(dev)
+    lens = torch.from_numpy(st.context_lens).to(dev)
+    stream = torch.cuda.current_stream(dev)
+    layers = []
+    shared = None
+    for l in range(nl):
+        if shared is None or not args.shared_cache:
+            _, k, v = W.fill_values(st, dev, fill="nan")
+            shared = (k, v)
+        k, v = shared
+        q = W.fill_multi_q(st, n, dev) if n > 1 else W.fill_values(st, dev, fill="nan")[0][:, None].contiguous()
+        kn, vn = W.fill_new_kv(st, n, dev)
+        layers.append(dict(q=q, k_new=kn, v_new=vn, k_cache=k, v_cache=v,
+                           out=torch.empty(q.shape, dtype=torch.float32, device=dev)))
+    from paper_2405_11143_amd import make_problem, pda_plan
+    prob = make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq, st.max_context_len,
+                        args.partition_tokens, num_query_tokens=n)
+    plan = pda_plan(prob)
+    ws = torch.empty(max(plan["workspace_bytes"], 16), dtype=torch.uint8, device=dev)
+    kw = dict(max_context_len=st.max_context_len, partition_tokens=args.partition_tokens, workspace=ws, stream=stream)
+    order = BoundCall("pda_work_order", (ctypes_ref(prob), lens.data_ptr(), ws.data_ptr(), ws.numel(),
+                                         _stream_handle(stream, dev)), (prob, lens, ws))
+    calls = []
+    for L in layers:
+        calls.append(bind_append_kv(L["k_new"], L["v_new"], bt, lens, L["k_cache"], L["v_cache"],
+                                    max_context_len=st.max_context_len, num_q_heads=st.Hq, stream=stream))
+        calls.append(bind_decode(L["q"], L["k_cache"], L["v_cache"], bt, lens, st.scale, L["out"],
+                                 reuse_order=True, **kw))
+
+    def eager():  # the same work, one bound call per launch
+        order()
+        for c in calls:
+            c()
+
+    fused = None
+    if n == 1:  # one new token: pda_decode_append folds each layer's append into its pass 1
+        from paper_2405_11143_amd import bind_decode_append
+        fused_calls = [bind_decode_append(L["q"], L["k_new"], L["v_new"], L["k_cache"], L["v_cache"], bt, lens,
+                                          st.scale, L["out"], **kw) for L in layers]
+
+        def fused():
+            for c in fused_calls:
+                c()
+
+    graph = ModelStepGraph(layers, bt, lens, st.scale, max_context_len=st.max_context_len,
+                           partition_tokens=args.partition_tokens, workspace=ws)
+    try:
+        for f in (eager, lambda: graph.launch(stream)):
+            for _ in range(args.warmup):
+                f()
+        torch.cuda.synchronize()
+        ms_eager = timed(eager, args.steps, stream)
+        ms_graph = timed(lambda: graph.launch(stream), args.steps, stream)
+        ms_fused = None
+        if fused is not None:
+            for _ in range(args.warmup):
+                fused()
+            ms_fused = timed(fused, args.steps, stream)
+    finally:
+        graph.close()
+    alg = nl * (st.algorithmic_bytes(query_tokens=n) + st.append_bytes(n))
+    cfg = W.CONFIGS[args.config]
+    result = base_result(args, st.B / (ms_graph * 1e-3), "seq-steps/s", ms_graph,
+                         f"{nl}-layer decode step (append + attention per layer) as one HIP graph, seq-steps/s",
+                         config_of(st, f"{cfg['desc']}; {nl} layers, {n} new token(s) per sequence"
+                                       + (", one cache shared by every layer" if args.shared_cache else
+                                          ", a cache per layer"), args.config, plan, layers=nl, query_tokens=n))
+    result.update({"us_per_layer_graph": round(1000 * ms_graph / nl, 3),
+                   "us_per_layer_eager": round(1000 * ms_eager / nl, 3),
+                   "ms_per_step_eager": round(ms_eager, 5), "graph_speedup": round(ms_eager / ms_graph, 3),
+                   "us_per_layer_eager_folded_append": None if ms_fused is None else round(1000 * ms_fused / nl, 3),
+                   "algorithmic_bytes_per_step": alg,
+                   "roofline": roofline(alg / (ms_graph * 1e-3) / 1e9, ms_graph, KERNEL, args.config),
+                   "cpu_baseline": None})
+    return result
+
+
+def ctypes_ref(x):
+    import ctypes
+
+    return ctypes.byref(x)
+
+
 def op_prefix(args):
     """The shared-prefix workload with each prompt's prefix attended once
     (pda_decode_shared_prefix), against the plain decode step on the same
@@ -644,7 +747,11 @@ def main(argv=None):
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--op", default="decode", choices=["decode", "multi", "append", "graph", "logprob", "prefix"])
+    ap.add_argument("--op", default="decode",
+                    choices=["decode", "multi", "append", "graph", "model_step", "logprob", "prefix"])
+    ap.add_argument("--layers", type=int, default=32, help="--op model_step: layers of the decode step")
+    ap.add_argument("--shared-cache", action="store_true",
+                    help="--op model_step: every layer reads (and appends to) one KV cache")
     ap.add_argument("--logits-f32", action="store_true", help="--op logprob: float32 logits (default bf16)")
     ap.add_argument("--logits-buffers", type=int, default=0,
                     help="--op logprob: copies of the logits the calls rotate over (default: >= 512 MB in all)")
@@ -674,7 +781,8 @@ def main(argv=None):
               file=sys.stderr)
         return 2
     if args.config is None:
-        args.config = {"graph": "tiny", "logprob": "llama3_vocab", "prefix": "shared_prefix"}.get(args.op, "llama3_8b")
+        args.config = {"graph": "tiny", "model_step": "tiny", "logprob": "llama3_vocab",
+                       "prefix": "shared_prefix"}.get(args.op, "llama3_8b")
     if args.tokens is None:
         args.tokens = 4 if args.op == "multi" else 1
 
@@ -704,6 +812,8 @@ def main(argv=None):
         result = op_logprob(args)
     elif args.op == "prefix":
         result = op_prefix(args)
+    elif args.op == "model_step":
+        result = op_model_step(args)
     else:
         result = op_graph(args)
     print(json.dumps(result), flush=True)

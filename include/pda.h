@@ -244,6 +244,20 @@ int pda_append_kv(const pda_problem *prob, const void *k_new, const void *v_new,
                   const int32_t *block_table, const int32_t *context_lens, void *k_cache,
                   void *v_cache, hipStream_t stream);
 
+/* pda_append_kv followed by pda_decode, for one new token per sequence
+ * (num_query_tokens 0 or 1; the KV-cache management and attention of one
+ * rollout step, Section 3.2 and Appendix C).  When every pass-1 work item of
+ * the step runs at once (a small batch, where each launch is a large part of
+ * the step), the append is folded into pass 1: the wavefront that reads
+ * position L - 1 of a (sequence, KV head) first stores the new token's K and
+ * V rows there, and the step needs no append launch.  Larger steps run the
+ * append kernel first.  Arguments are those of pda_append_kv and pda_decode;
+ * the caches and the output (bitwise those of the two calls) are written in
+ * place.  PDA_ERR_UNSUPPORTED for num_query_tokens > 1. */
+int pda_decode_append(const pda_problem *prob, const void *q, const void *k_new, const void *v_new,
+                      void *k_cache, void *v_cache, const int32_t *block_table, const int32_t *context_lens,
+                      float scale, float *out, void *workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* A whole step captured once as a HIP graph: pda_append_kv, then pda_decode,
  * with the pointers given here (vLLM runs its decode steps as captured
  * graphs, Section 3.2).  Each pda_step_graph_launch replays the step on
@@ -261,6 +275,33 @@ int pda_step_graph_create(const pda_problem *prob, const void *q, const void *k_
                           float *out, void *workspace, size_t workspace_bytes,
                           pda_step_graph **graph);
 int pda_step_graph_launch(pda_step_graph *graph, hipStream_t stream);
+
+/* A whole decode step of a model as one HIP graph: for each of num_layers
+ * layers, the append of its new tokens' K/V into its own cache and its
+ * attention step, with the work order (the lengths and block tables are the
+ * same in every layer) computed once, in the first layer.  This is the
+ * per-token loop a rollout engine replays (vLLM runs its decode steps as
+ * captured graphs, Section 3.2): one graph launch stands for num_layers x 1-4
+ * kernel launches (with one new token per sequence and a small batch, each
+ * layer's append is folded into its pass 1, as in pda_decode_append).  Every layer has its own q, k_new, v_new, caches and out
+ * (the layouts of pda_append_kv / pda_decode); the descriptor, block table,
+ * lengths, scale and workspace are shared.  Launch and destroy the result
+ * with pda_step_graph_launch / pda_step_graph_destroy; launches of one graph
+ * must not overlap on the GPU.  Every layer is validated as pda_append_kv and
+ * pda_decode validate their arguments before anything is captured;
+ * num_layers < 1 is PDA_ERR_SHAPE.  pda_step_graph_create is this with one
+ * layer. */
+typedef struct pda_layer_buffers {
+  const void *q;      /* bf16 [B][n][Hq][D] */
+  const void *k_new;  /* bf16 [B][n][Hkv][D] */
+  const void *v_new;  /* bf16 [B][n][Hkv][D] */
+  void *k_cache;      /* bf16 [num_blocks][Hkv][D/8][16][8] */
+  void *v_cache;      /* bf16 [num_blocks][Hkv][16][D] */
+  float *out;         /* fp32 [B][n][Hq][D] */
+} pda_layer_buffers;
+int pda_model_step_graph_create(const pda_problem *prob, int32_t num_layers, const pda_layer_buffers *layers,
+                                const int32_t *block_table, const int32_t *context_lens, float scale,
+                                void *workspace, size_t workspace_bytes, pda_step_graph **graph);
 int pda_step_graph_destroy(pda_step_graph *graph);
 
 /* Token log-probabilities and entropies of one step's LM-head logits: the

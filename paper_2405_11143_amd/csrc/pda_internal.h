@@ -57,6 +57,13 @@ struct StepArgs {
   int32_t prefix_partitions;        // Pp = ceil(max_prefix_len / T_p)
   int32_t slots_per_row;            // Pp + P partial states per output row (P when no groups)
   int32_t num_regular_items;        // items below this index are (partition, sequence, KV head, chunk group)
+  // The step's KV append folded into pass 1 (one new token per sequence, no
+  // shared-prefix groups), or null: the item that reads position L - 1 of
+  // (sequence, KV head) first stores that token's K and V rows there.
+  const uint16_t* k_new;            // bf16 [B][Hkv][D]
+  const uint16_t* v_new;            // bf16 [B][Hkv][D]
+  uint16_t* k_store;                // the K cache (a.k, writable)
+  uint16_t* v_store;                // the V cache (a.v, writable)
 };
 
 // Prefix tokens of sequence b's group (0 without groups); pass 1 and the

@@ -341,6 +341,34 @@ __device__ void run_staged(WaveAttention<D>& wave, WaveAttention<D>& wave_b, Sta
   __syncthreads();  // the staging area is reused by the epilogue
 }
 
+// The step's KV append folded into pass 1 (one new token per sequence, no
+// shared-prefix groups): the wavefront whose run of blocks holds position t
+// = L - 1 of (sequence b, KV head g) stores the new token's K and V rows
+// there, and waits for the stores to complete, before it loads any tile.  No
+// other wavefront or item reads that block (the last of the sequence's own
+// context), and the wavefront's later loads of it miss its compute unit's
+// L1 (stores do not allocate there), so they see the new rows.  A block id
+// outside the pool is skipped, as the separate append does.
+template <int D>
+__device__ __forceinline__ void store_new_token(const StepArgs& a, int b, int g, int t, const int32_t* table_row,
+                                                int lane) {
+  constexpr int CPR = D / 8;  // 16-byte pieces per row
+  const int phys = table_row[t / kBlockTokens];
+  if ((unsigned)phys < (unsigned)a.num_blocks && lane < 2 * CPR) {
+    const int c = lane % CPR;
+    const size_t src = ((size_t)b * a.num_kv_heads + g) * CPR + c;
+    const size_t tile = (size_t)phys * a.num_kv_heads + g;
+    const int o = t % kBlockTokens;
+    if (lane < CPR)
+      reinterpret_cast<uint4*>(a.k_store)[(tile * CPR + c) * kBlockTokens + o] =
+          reinterpret_cast<const uint4*>(a.k_new)[src];
+    else
+      reinterpret_cast<uint4*>(a.v_store)[(tile * kBlockTokens + o) * CPR + c] =
+          reinterpret_cast<const uint4*>(a.v_new)[src];
+  }
+  __builtin_amdgcn_s_waitcnt(0);  // every memory operation of the wavefront has completed
+}
+
 template <int D, int MODE>
 __device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item) {
   PassShared<D>& sh = lds.sh;
@@ -467,6 +495,8 @@ __device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item)
     const int per_slice = (j_end - j_begin + kWaves - 1) / kWaves;
     const int wj0 = min(j_end, j_begin + w * per_slice);
     const int wj1 = min(j_end, wj0 + per_slice);
+    if (a.k_new && L > 0 && wj0 <= (L - 1) / kBlockTokens && (L - 1) / kBlockTokens < wj1)  // wavefront-uniform
+      store_new_token<D>(a, b, g, L - 1, table_row, lane);
     wave.run(table_row, wj0, wj1, L, ca.l_first, max(ca.l_vis, 0), kpool, vpool, block_bytes, a.num_blocks);
   } else if constexpr (MODE != kModeRegister) {  // several tiles: every block staged once through LDS for all of them
     int J1 = j_begin;

@@ -27,7 +27,8 @@ EXPORTED = ("pda_plan", "pda_workspace_bytes", "pda_decode", "pda_partition_atte
             "pda_step_graph_create", "pda_step_graph_launch", "pda_step_graph_destroy", "pda_token_logprobs",
             "pda_logprob_workspace_bytes",
             "pda_validate_host", "pda_work_order", "pda_decode_reusing_order", "pda_decode_noalloc",
-            "pda_gather_ceiling", "pda_stream_ceiling", "pda_status_string")
+            "pda_gather_ceiling", "pda_stream_ceiling", "pda_model_step_graph_create", "pda_decode_append",
+            "pda_status_string")
 PDA_DTYPE_BF16, PDA_DTYPE_F32 = 0, 1
 
 
@@ -49,6 +50,11 @@ class pda_prefix_groups(ctypes.Structure):
     _fields_ = [("num_groups", ctypes.c_int32), ("max_group_size", ctypes.c_int32),
                 ("max_prefix_len", ctypes.c_int32), ("group_start", ctypes.c_void_p),
                 ("group_prefix_len", ctypes.c_void_p)]
+
+
+class pda_layer_buffers(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("k_new", ctypes.c_void_p), ("v_new", ctypes.c_void_p),
+                ("k_cache", ctypes.c_void_p), ("v_cache", ctypes.c_void_p), ("out", ctypes.c_void_p)]
 
 
 class PdaError(RuntimeError):
@@ -86,9 +92,12 @@ def load_library(path: str = LIB_PATH):
     lib.pda_plan_shared_prefix.argtypes = [P, G, ctypes.POINTER(pda_plan_info)]
     lib.pda_decode_shared_prefix.argtypes = [P, G, vp, vp, vp, vp, vp, ctypes.c_float, vp, vp, sz, vp]
     lib.pda_append_kv.argtypes = [P, vp, vp, vp, vp, vp, vp, vp]
+    lib.pda_decode_append.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, ctypes.c_float, vp, vp, sz, vp]
     lib.pda_step_graph_create.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, ctypes.c_float, vp, vp, sz,
                                           ctypes.POINTER(vp)]
     lib.pda_step_graph_launch.argtypes = [vp, vp]
+    lib.pda_model_step_graph_create.argtypes = [P, ctypes.c_int32, ctypes.POINTER(pda_layer_buffers), vp, vp,
+                                                ctypes.c_float, vp, sz, ctypes.POINTER(vp)]
     lib.pda_step_graph_destroy.argtypes = [vp]
     lib.pda_token_logprobs.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, vp, vp,
                                        ctypes.c_float, vp, vp, vp, sz, vp]
@@ -325,6 +334,34 @@ def bind_decode(q, k_cache, v_cache, block_table, context_lens, scale: float, ou
     return BoundCall(name, args, keep, out)
 
 
+def bind_decode_append(q, k_new, v_new, k_cache, v_cache, block_table, context_lens, scale: float, out=None, *,
+                       max_context_len: int, partition_tokens: int = 0, workspace=None, stream=None) -> BoundCall:
+    """pda_decode_append bound to these tensors: the append of each sequence's
+    new token (k_new/v_new bf16 [B][1][Hkv][D]) folded into the decode step."""
+    import torch
+
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    _check_tensors(q, k_cache, v_cache, block_table, context_lens, out)
+    _check_new_kv(k_new, v_new, _query_shape(q), k_cache)
+    prob = _problem_from(q, k_cache, block_table, max_context_len, partition_tokens)
+    workspace, ws_ptr, ws_bytes = _workspace(prob, workspace, q.device)
+    args = (ctypes.byref(prob), q.data_ptr(), k_new.data_ptr(), v_new.data_ptr(), k_cache.data_ptr(),
+            v_cache.data_ptr(), block_table.data_ptr(), context_lens.data_ptr(), ctypes.c_float(scale),
+            out.data_ptr(), ws_ptr, ws_bytes, _stream_handle(stream, q.device))
+    keep = (prob, q, k_new, v_new, k_cache, v_cache, block_table, context_lens, out, workspace)
+    return BoundCall("pda_decode_append", args, keep, out)
+
+
+def pda_decode_append(q, k_new, v_new, k_cache, v_cache, block_table, context_lens, scale: float, out=None, *,
+                      max_context_len: int, partition_tokens: int = 0, workspace=None, stream=None):
+    """pda_append_kv + pda_decode in the launches of pda_decode alone (one new
+    token per sequence)."""
+    return bind_decode_append(q, k_new, v_new, k_cache, v_cache, block_table, context_lens, scale, out,
+                              max_context_len=max_context_len, partition_tokens=partition_tokens,
+                              workspace=workspace, stream=stream)()
+
+
 def pda_work_order(prob: pda_problem, context_lens, workspace, stream=None):
     """The step's work order into `workspace` (see include/pda.h): computed
     once per decode step, reused by every layer's pda_decode_reusing_order."""
@@ -394,6 +431,57 @@ def bind_append_kv(k_new, v_new, block_table, context_lens, k_cache, v_cache, *,
             k_cache.data_ptr(), v_cache.data_ptr(), _stream_handle(stream, k_cache.device))
     keep = (prob, k_new, v_new, block_table, context_lens, k_cache, v_cache)
     return BoundCall("pda_append_kv", args, keep)
+
+
+class ModelStepGraph:
+    """pda_model_step_graph_create: a model's decode step over `layers` (a list
+    of dicts with q, k_new, v_new, k_cache, v_cache and out tensors, one per
+    layer) captured as one HIP graph -- per layer the KV append and the
+    attention step, the work order computed once.  launch() replays it on a
+    stream and reads the buffers' current contents."""
+
+    def __init__(self, layers, block_table, context_lens, scale: float, *, max_context_len: int,
+                 partition_tokens: int = 0, workspace=None):
+        import torch
+
+        if not layers:
+            raise ValueError("at least one layer")
+        arr = (pda_layer_buffers * len(layers))()
+        for i, L in enumerate(layers):
+            _check_tensors(L["q"], L["k_cache"], L["v_cache"], block_table, context_lens, L["out"])
+            _check_new_kv(L["k_new"], L["v_new"], _query_shape(L["q"]), L["k_cache"])
+            arr[i] = pda_layer_buffers(L["q"].data_ptr(), L["k_new"].data_ptr(), L["v_new"].data_ptr(),
+                                       L["k_cache"].data_ptr(), L["v_cache"].data_ptr(), L["out"].data_ptr())
+        L0 = layers[0]
+        self.prob = _problem_from(L0["q"], L0["k_cache"], block_table, max_context_len, partition_tokens)
+        workspace, ws_ptr, ws_bytes = _workspace(self.prob, workspace, L0["q"].device)
+        self.workspace, self._device = workspace, L0["q"].device
+        self._keep = (layers, block_table, context_lens, arr)
+        handle = ctypes.c_void_p()
+        rc = load_library().pda_model_step_graph_create(
+            ctypes.byref(self.prob), len(layers), arr, block_table.data_ptr(), context_lens.data_ptr(),
+            ctypes.c_float(scale), ws_ptr, ws_bytes, ctypes.byref(handle))
+        if rc != PDA_OK:
+            raise PdaError(rc, "pda_model_step_graph_create")
+        self._handle = handle
+
+    def launch(self, stream=None):
+        rc = load_library().pda_step_graph_launch(self._handle, _stream_handle(stream, self._device))
+        if rc != PDA_OK:
+            raise PdaError(rc, "pda_step_graph_launch")
+
+    def close(self):
+        if getattr(self, "_handle", None) is not None:
+            rc = load_library().pda_step_graph_destroy(self._handle)
+            self._handle = None
+            if rc != PDA_OK:
+                raise PdaError(rc, "pda_step_graph_destroy")
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 class StepGraph:

@@ -250,6 +250,31 @@ def test_append_and_graph_validation():
     assert g.value is None
     assert lib.pda_step_graph_launch(None, None) == pda.pda.PDA_ERR_NULL
     assert lib.pda_step_graph_destroy(None) == pda.pda.PDA_OK
+    # the append folded into the decode step: one new token per sequence only
+    da = lib.pda_decode_append
+    big = 1 << 30
+    assert da(ctypes.byref(prob(num_query_tokens=2)), *([0x1000] * 7), ctypes.c_float(0.1), 0x1000, 0x1000, big,
+              None) == pda.pda.PDA_ERR_UNSUPPORTED
+    assert da(ctypes.byref(p), 0x1000, None, *([0x1000] * 5), ctypes.c_float(0.1), 0x1000, 0x1000, big,
+              None) == pda.pda.PDA_ERR_NULL
+    assert da(ctypes.byref(p), *([0x1000] * 7), ctypes.c_float(0.1), 0x1000, None, 0,
+              None) == pda.pda.PDA_ERR_WORKSPACE
+    assert da(ctypes.byref(prob(num_seqs=0)), *([None] * 7), ctypes.c_float(0.1), None, None, 0, None) == pda.pda.PDA_OK
+    # the model-step graph validates every layer before capturing anything
+    m = lib.pda_model_step_graph_create
+    L = pda.pda.pda_layer_buffers
+    two = (L * 2)(L(0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000), L(0x1000, 0x1000, None, 0x1000, 0x1000, 0x1000))
+    ws = pda.pda_workspace_bytes(p)
+    assert m(ctypes.byref(p), 2, two, 0x1000, 0x1000, ctypes.c_float(0.1), 0x1000, ws,
+             ctypes.byref(g)) == pda.pda.PDA_ERR_NULL  # layer 1's v_new
+    assert m(ctypes.byref(p), 0, two, 0x1000, 0x1000, ctypes.c_float(0.1), 0x1000, ws,
+             ctypes.byref(g)) == pda.pda.PDA_ERR_SHAPE
+    assert m(ctypes.byref(p), 1, None, 0x1000, 0x1000, ctypes.c_float(0.1), 0x1000, ws,
+             ctypes.byref(g)) == pda.pda.PDA_ERR_NULL
+    bad = (L * 1)(L(0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 0x1004))  # out not 16-byte aligned
+    assert m(ctypes.byref(p), 1, bad, 0x1000, 0x1000, ctypes.c_float(0.1), 0x1000, ws,
+             ctypes.byref(g)) == pda.pda.PDA_ERR_ALIGNMENT
+    assert g.value is None
 
 
 def test_multi_token_plan():
