@@ -95,10 +95,8 @@ def test_step_graph_replays(dev, n, case):
     try:
         for step in range(4):
             # eager work between replays: new inputs, one more token per sequence
-            torch.manual_seed(step)
-            q.copy_(torch.randn(q.shape, device=dev).to(torch.bfloat16))
-            kn.copy_(torch.randn(kn.shape, device=dev).to(torch.bfloat16))
-            vn.copy_(torch.randn(vn.shape, device=dev).to(torch.bfloat16))
+            for s_, t in enumerate((q, kn, vn)):
+                t.copy_(W.normal_draw(t.shape, 500 + step, s_, dev).to(torch.bfloat16))
             lens.add_(torch.from_numpy(growth[step]).to(dev))
             torch.cuda.synchronize()
             out_g = graph.launch().clone()
@@ -148,10 +146,9 @@ def test_model_step_graph_replays(dev, case):
     graph = ModelStepGraph(graph_bufs, bt, lens, st.scale, max_context_len=st.max_context_len, partition_tokens=tp)
     try:
         for step in range(3):
-            torch.manual_seed(10 + step)
-            for L in graph_bufs:
-                for name in ("q", "k_new", "v_new"):
-                    L[name].copy_(torch.randn(L[name].shape, device=dev).to(torch.bfloat16))
+            for li, L in enumerate(graph_bufs):
+                for s_, name in enumerate(("q", "k_new", "v_new")):
+                    L[name].copy_(W.normal_draw(L[name].shape, 600 + step, 3 * li + s_, dev).to(torch.bfloat16))
             lens.add_(torch.from_numpy(growth[step]).to(dev))
             torch.cuda.synchronize()
             graph.launch()

@@ -1,5 +1,7 @@
 """The seeded input generator (no GPU): determinism, shapes, block tables,
-prefix sharing, poison fill and bf16 rounding."""
+prefix sharing, poison fill, bf16 rounding, and the counter-based value draw
+(SplitMix64 against an independent uint64 implementation and its published
+first output, the normal quantile table, chunked draws)."""
 import math
 
 import numpy as np
@@ -78,6 +80,52 @@ def test_values_are_deterministic_and_poisoned():
     # read slots hold N(0,1) draws
     read = W.k_cache_to_rows(k1).float().permute(0, 2, 1, 3)[~mask]
     assert torch.isfinite(read).all() and abs(read.mean().item()) < 0.1 and abs(read.std().item() - 1) < 0.1
+
+
+def _splitmix64_uint64(key: int, n: int) -> np.ndarray:
+    """SplitMix64 outputs 1..n from `key`, in numpy uint64 arithmetic (which
+    wraps modulo 2^64): state += gamma, then the two xor-shift-multiply
+    rounds and a final xor-shift."""
+    out = np.empty(n, dtype=np.uint64)
+    state = np.uint64(key)
+    with np.errstate(over="ignore"):
+        for i in range(n):
+            state = state + np.uint64(0x9E3779B97F4A7C15)
+            z = state
+            z = (z ^ (z >> np.uint64(30))) * np.uint64(0xBF58476D1CE4E5B9)
+            z = (z ^ (z >> np.uint64(27))) * np.uint64(0x94D049BB133111EB)
+            out[i] = z ^ (z >> np.uint64(31))
+    return out
+
+
+def test_splitmix64_matches_uint64_reference():
+    # the first output of SplitMix64 seeded with 0, as its reference code prints it
+    assert int(W.splitmix64(0, torch.tensor([0])).numpy().view(np.uint64)[0]) == 0xE220A8397B1DCDAF
+    for key in (0, 1, 2**63 + 12345, W._stream_key(2406, 4)):
+        got = W.splitmix64(key, torch.arange(300, dtype=torch.int64)).numpy().view(np.uint64)
+        assert np.array_equal(got, _splitmix64_uint64(key, 300))
+
+
+def test_normal_table_is_the_quantiles():
+    t = W.normal_table()
+    n = t.size
+    assert n == 1 << 20 and t.dtype == np.float32
+    assert np.all(np.diff(t) > 0) and np.array_equal(t, -t[::-1])  # increasing, symmetric
+    from statistics import NormalDist
+    for j in (0, 1, 1000, n // 2 - 1, n - 5):
+        assert abs(float(t[j]) - NormalDist().inv_cdf((j + 0.5) / n)) < 1e-6 * max(1.0, abs(float(t[j])))
+    assert abs(float(t.astype(np.float64).mean())) < 1e-9
+    assert abs(float((t.astype(np.float64) ** 2).mean()) - 1) < 2e-4  # the discrete draw's variance
+
+
+def test_normal_draw_chunks_and_streams():
+    full = W.normal_draw((7, 300), 11, 4)
+    part = W.normal_draw((3, 300), 11, 4, first=4 * 300)
+    assert torch.equal(full[4:], part)  # element i of a stream does not depend on the chunking
+    other = W.normal_draw((7, 300), 11, 5)
+    assert not torch.equal(full, other)
+    x = W.normal_draw((1 << 18,), 1, 3).double()
+    assert abs(x.mean().item()) < 0.01 and abs(x.std().item() - 1) < 0.01
 
 
 def test_bf16_rounds_to_nearest_even():

@@ -7,10 +7,16 @@ A workload has two parts:
 
 * the *structure*, drawn on the host with numpy's counter-based Philox
   generator: context lengths, the block table and the physical block pool;
-* the *values* q, K, V, drawn with torch's seeded generator on any device
-  (``cpu`` for the CPU tests, ``cuda`` for the large configurations, where
-  only a device generator is fast enough) and rounded to bf16 to nearest
-  even by ``Tensor.to(torch.bfloat16)``.
+* the *values* q, K, V, drawn by a counter-based generator written out
+  with torch integer ops, so that the same seed gives the same bits on any
+  device (``cpu`` for the CPU tests, ``cuda`` for the large configurations,
+  where only the device is fast enough): element i of stream (seed, s) is
+  the i-th output of SplitMix64 (Steele, Lea and Flood, "Fast splittable
+  pseudorandom number generators", OOPSLA 2014) started from a 64-bit key
+  of (seed, s), and its top 20 bits pick one of 2^20 equally likely
+  standard-normal quantiles (inverse-CDF sampling; |z| <= 4.9).  The
+  normal values are rounded to bf16 to nearest even by
+  ``Tensor.to(torch.bfloat16)``.
 
 The five named configurations are the rollout decode steps the build is
 measured on: the paper's long chain-of-thought rollouts (Section 4.1 uses
@@ -92,10 +98,6 @@ def default_seed(name: str) -> int:
 
 def _rng(seed: int, stream: int) -> np.random.Generator:
     return np.random.Generator(np.random.Philox(np.random.SeedSequence([int(seed), int(stream)])))
-
-
-def _torch_seed(seed: int, stream: int) -> int:
-    return int(np.random.SeedSequence([int(seed), int(stream)]).generate_state(1, np.uint64)[0]) & (2**63 - 1)
 
 
 @dataclasses.dataclass
@@ -333,6 +335,70 @@ def k_cache_to_rows(k_cache):
     return np.ascontiguousarray(k_cache.transpose(0, 1, 3, 2, 4).reshape(NB, H, S, C * E))
 
 
+# ---- counter-based normal draws (the same bits on every device) ----
+_U64 = (1 << 64) - 1
+_SM_GAMMA = 0x9E3779B97F4A7C15  # SplitMix64's increment
+_SM_M1, _SM_M2 = 0xBF58476D1CE4E5B9, 0x94D049BB133111EB
+_NORMAL_BITS = 20
+_NORMAL_TABLES: Dict[str, object] = {}
+
+
+def _i64(c: int) -> int:
+    """A 64-bit pattern as the signed int64 torch stores."""
+    c &= _U64
+    return c - (1 << 64) if c >= (1 << 63) else c
+
+
+def _lsr(z, k: int):
+    """Logical right shift of int64 bit patterns (torch's >> is arithmetic)."""
+    return (z >> k) & ((1 << (64 - k)) - 1)
+
+
+def splitmix64(key: int, index):
+    """Output number index + 1 of SplitMix64 started at `key`: mix(key +
+    (index + 1) * gamma), on int64 tensors whose bits are the uint64 values
+    (multiplications wrap modulo 2^64)."""
+    z = (index + 1) * _i64(_SM_GAMMA) + _i64(key)
+    z = (z ^ _lsr(z, 30)) * _i64(_SM_M1)
+    z = (z ^ _lsr(z, 27)) * _i64(_SM_M2)
+    return z ^ _lsr(z, 31)
+
+
+def normal_table():
+    """The 2^20 standard-normal quantiles Phi^-1((j + 1/2) / 2^20) in fp32
+    (computed in fp64 on the host)."""
+    from scipy.special import ndtri
+
+    n = 1 << _NORMAL_BITS
+    return ndtri((np.arange(n, dtype=np.float64) + 0.5) / n).astype(np.float32)
+
+
+def _table_on(device):
+    import torch
+
+    dev = torch.device(device)
+    key = str(dev)
+    if key not in _NORMAL_TABLES:
+        _NORMAL_TABLES[key] = torch.from_numpy(normal_table()).to(dev)
+    return _NORMAL_TABLES[key]
+
+
+def _stream_key(seed: int, stream: int) -> int:
+    return int(np.random.SeedSequence([int(seed), int(stream)]).generate_state(1, np.uint64)[0])
+
+
+def normal_draw(shape, seed: int, stream: int, device="cpu", first: int = 0):
+    """fp32 standard-normal values of stream (seed, stream), elements first ..
+    first + prod(shape) - 1 in row-major order, the same bits on any device."""
+    import torch
+
+    dev = torch.device(device)
+    n = int(np.prod(shape, dtype=np.int64))
+    idx = torch.arange(first, first + n, dtype=torch.int64, device=dev)
+    z = splitmix64(_stream_key(seed, stream), idx)
+    return _table_on(dev)[_lsr(z, 64 - _NORMAL_BITS)].reshape(shape)
+
+
 def fill_values(st: Structure, device="cpu", fill: Optional[str] = "nan"):
     """Draw q [B][Hq][D], the K pool [num_blocks][Hkv][D/8][16][8] and the V pool
     [num_blocks][Hkv][16][D] (bf16) on `device`.  `fill` is 'nan', 'zero' or
@@ -340,31 +406,23 @@ def fill_values(st: Structure, device="cpu", fill: Optional[str] = "nan"):
     import torch
 
     dev = torch.device(device)
-
-    def gen(stream):
-        g = torch.Generator(device=dev)
-        g.manual_seed(_torch_seed(st.seed, stream))
-        return g
-
-    q = torch.randn((st.B, st.Hq, st.D), generator=gen(_STREAM_Q), device=dev,
-                    dtype=torch.float32).to(torch.bfloat16)
+    q = normal_draw((st.B, st.Hq, st.D), st.seed, _STREAM_Q, dev).to(torch.bfloat16)
     mu = None
     if st.k_offset_std:
-        mu = (torch.randn((st.Hkv, 1, st.D), generator=gen(_STREAM_KOFF), device=dev,
-                          dtype=torch.float32) * st.k_offset_std)
+        mu = normal_draw((st.Hkv, 1, st.D), st.seed, _STREAM_KOFF, dev) * st.k_offset_std
     shape = (st.num_blocks, st.Hkv, st.block_size, st.D)
+    per_block = st.Hkv * st.block_size * st.D
     k = torch.empty((st.num_blocks, st.Hkv, st.D // 8, st.block_size, 8), dtype=torch.bfloat16, device=dev)
     v = torch.empty(shape, dtype=torch.bfloat16, device=dev)
-    gk, gv = gen(_STREAM_K), gen(_STREAM_V)
     for c0 in range(0, st.num_blocks, _POOL_CHUNK_BLOCKS):
         c1 = min(st.num_blocks, c0 + _POOL_CHUNK_BLOCKS)
         sub = (c1 - c0,) + shape[1:]
-        kf = torch.randn(sub, generator=gk, device=dev, dtype=torch.float32)
+        kf = normal_draw(sub, st.seed, _STREAM_K, dev, first=c0 * per_block)
         if mu is not None:
             kf += mu
         k[c0:c1] = k_rows_to_cache(kf.to(torch.bfloat16))
-        v[c0:c1] = torch.randn(sub, generator=gv, device=dev, dtype=torch.float32).to(torch.bfloat16)
         del kf
+        v[c0:c1] = normal_draw(sub, st.seed, _STREAM_V, dev, first=c0 * per_block).to(torch.bfloat16)
     if fill is not None:
         apply_fill(st, k, v, fill)
     return q, k, v
@@ -425,30 +483,20 @@ def sample_rows(st: Structure, n: int, seed: int = 7) -> np.ndarray:
     return np.asarray(picks[:max(n, len(picks))], dtype=np.int32)
 
 
-def _torch_gen(seed: int, stream: int, device):
-    import torch
-
-    g = torch.Generator(device=torch.device(device))
-    g.manual_seed(_torch_seed(seed, stream))
-    return g
-
-
 def fill_multi_q(st: Structure, n: int, device="cpu"):
     """Queries of n new tokens per sequence: bf16 [B][n][Hq][D], N(0, 1)."""
     import torch
 
-    return torch.randn((st.B, n, st.Hq, st.D), generator=_torch_gen(st.seed, _STREAM_QMULTI, device),
-                       device=torch.device(device), dtype=torch.float32).to(torch.bfloat16)
+    return normal_draw((st.B, n, st.Hq, st.D), st.seed, _STREAM_QMULTI, device).to(torch.bfloat16)
 
 
 def fill_new_kv(st: Structure, n: int, device="cpu"):
     """K and V rows of n new tokens per sequence: bf16 [B][n][Hkv][D] each, N(0, 1)."""
     import torch
 
-    dev = torch.device(device)
     shape = (st.B, n, st.Hkv, st.D)
-    k = torch.randn(shape, generator=_torch_gen(st.seed, _STREAM_KNEW, dev), device=dev, dtype=torch.float32)
-    v = torch.randn(shape, generator=_torch_gen(st.seed, _STREAM_VNEW, dev), device=dev, dtype=torch.float32)
+    k = normal_draw(shape, st.seed, _STREAM_KNEW, device)
+    v = normal_draw(shape, st.seed, _STREAM_VNEW, device)
     return k.to(torch.bfloat16), v.to(torch.bfloat16)
 
 
@@ -487,8 +535,7 @@ def make_logits(B: int, V: int, seed: int, device="cpu", dtype=None, likely: int
     tokens = np.where(pick_likely, likely_ids[np.arange(B), r.integers(0, likely_ids.shape[1], B)]
                       if B else np.zeros(0, np.int64), r.integers(0, V, B)).astype(np.int32)
     dev = torch.device(device)
-    x = torch.randn((B, V), generator=_torch_gen(seed, _STREAM_LOGITS, dev), device=dev,
-                    dtype=torch.float32) * background_std
+    x = normal_draw((B, V), seed, _STREAM_LOGITS, dev) * background_std
     if B:
         rows = torch.arange(B, device=dev)[:, None].expand(B, likely_ids.shape[1])
         x[rows, torch.from_numpy(likely_ids).to(dev)] += torch.from_numpy(boosts).float().to(dev)
