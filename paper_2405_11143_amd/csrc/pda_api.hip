@@ -75,7 +75,7 @@ struct Plan {
   pda_plan_info info;
   int query_chunk;        // new tokens per work item: min(n, 16 / G)
   int num_query_chunks;   // ceil(n / query_chunk)
-  int chunks_per_group;   // 4, or 8 with more than 4 chunks (two 16-row tiles per wavefront)
+  int chunks_per_group;   // 4; 8 with more than 4 chunks (two 16-row tiles per wavefront); 16 with more than 8
   int num_chunk_groups;   // ceil(chunks / chunks_per_group): chunks per work item share its tiles
   int prefix_partitions;  // Pp: partitions of the longest shared prefix (0 without groups)
   size_t regular_items;   // P * B * Hkv * chunk groups (pass-1 workgroups of the sequences' own tokens)
@@ -104,7 +104,9 @@ int make_plan(const pda_problem* p, const pda_prefix_groups* groups, Plan* plan)
   const int G = p->num_q_heads / p->num_kv_heads;
   const int qc = std::min(n, pda::kMaxGroup / G);
   const int nqc = (n + qc - 1) / qc;
-  const int cpg = nqc > pda::kWaves ? pda::kWideChunks : pda::kWaves;  // chunks per work item
+  const int cpg = nqc > pda::kWideChunks ? pda::kWide16Chunks
+                  : nqc > pda::kWaves    ? pda::kWideChunks
+                                         : pda::kWaves;  // chunks per work item
   const int ncg = (nqc + cpg - 1) / cpg;
   const int64_t units = (int64_t)p->num_seqs * p->num_kv_heads * ncg;
   int tp = p->partition_tokens;

@@ -12,6 +12,7 @@ constexpr int kWaveSize = 64;     // CDNA wavefront
 constexpr int kWaves = 4;         // wavefronts per partition workgroup
 constexpr int kMaxGroup = 16;     // query heads per KV head: one 16-row MFMA tile
 constexpr int kWideChunks = 2 * kWaves;  // query chunks of a work item when each wavefront folds two
+constexpr int kWide16Chunks = 4 * kWaves;  // the same with 8 wavefronts per workgroup (more than 8 chunks)
 constexpr int kOrderThreads = 1024;  // the work-order kernel is one workgroup of this size
 constexpr int kOrderBuckets = 256;   // size classes of its counting sort (partition blocks, capped)
 
@@ -41,7 +42,8 @@ struct StepArgs {
   int32_t num_query_tokens;  // n
   int32_t query_chunk;       // new tokens per query chunk (one 16-row tile): min(n, 16 / G)
   int32_t num_query_chunks;  // NQC = ceil(n / query_chunk)
-  int32_t chunks_per_group;  // CPG: 4, or 8 when NQC > 4 (each wavefront then folds two tiles)
+  int32_t chunks_per_group;  // CPG: 4; 8 when NQC > 4 (each wavefront then folds two tiles); 16 when NQC > 8
+                             // (8 wavefronts of two tiles)
   int32_t num_chunk_groups;  // NCG = ceil(NQC / CPG): chunks of one work item share its K/V tiles
   int32_t partition_tokens;  // T_p, multiple of 16
   int32_t num_partitions;    // P = max(1, ceil(max_context_len / T_p))

@@ -40,15 +40,15 @@ namespace {
 
 constexpr int kRows = 16;           // rows of one wavefront (one MFMA tile)
 
-template <int D>
+template <int D, int NW>
 struct PassShared {
-  float o[kWaves][kRows][D];
-  float m[kWaves][kRows];
-  float l[kWaves][kRows];
-  float sc[kWaves][kRows];    // per wavefront and row: 2^(m - M), M the row's max over its slices
-  float mx[kWaves][kRows];    // per tile and row: M
-  float lsum[kWaves][kRows];  // per tile and row: sum of sc * l over the slices
-  int bad[kWaves];
+  float o[NW][kRows][D];
+  float m[NW][kRows];
+  float l[NW][kRows];
+  float sc[NW][kRows];    // per wavefront and row: 2^(m - M), M the row's max over its slices
+  float mx[NW][kRows];    // per tile and row: M
+  float lsum[NW][kRows];  // per tile and row: sum of sc * l over the slices
+  int bad[NW];
 };
 
 // Tile staging for items with several 16-row tiles: every step brings SB
@@ -58,11 +58,11 @@ struct PassShared {
 // (in registers, then written to LDS).  Block ids come through an LDS window.
 constexpr int kIdWindow = 256;
 
-template <int D, int SB>
+template <int D, int SB, int NW>
 struct Staging {
   static constexpr int kStepBlocks = SB;
   static constexpr int TC = WaveAttention<D>::kTileBytes / 16;       // 16-byte pieces per tile
-  static constexpr int kLoads = SB * 2 * TC / (kWaves * kWaveSize);  // per thread and step
+  static constexpr int kLoads = SB * 2 * TC / (NW * kWaveSize);  // per thread and step
   static constexpr int kRowPieces = D / 8;                            // 16-byte pieces per V row
   // A block is its K tile as loaded, then its V tile with 32 bytes of padding
   // after every row: a transposed V read takes 32 bytes from each of 4 rows
@@ -84,23 +84,29 @@ struct Staging {
 // staging buffers (49.5 KiB at D = 128) still leave room for 3 workgroups
 // per compute unit; 4 blocks per step at 2 workgroups per compute unit
 // measured slower on MI355X.
-constexpr int kModeRegister = 1, kModeMixed = 3, kModeWide = 7;
+constexpr int kModeRegister = 1, kModeMixed = 3, kModeWide = 7, kModeWide16 = 15;
 constexpr int kStepBlocks = 2;
+
+// Wavefronts per workgroup: 8 in the variant for items of more than 8 query
+// chunks (two tiles each, 16 chunks sharing every staged step), 4 otherwise.
+constexpr int waves_of(int mode) { return mode == kModeWide16 ? 2 * kWaves : kWaves; }
+constexpr bool wide_mode(int mode) { return mode == kModeWide || mode == kModeWide16; }
 
 template <int D, int MODE>
 union PassLds {
-  PassShared<D> sh;                // the epilogue
-  Staging<D, kStepBlocks> st;      // the staged main loop (never live at the same time)
+  PassShared<D, waves_of(MODE)> sh;                // the epilogue
+  Staging<D, kStepBlocks, waves_of(MODE)> st;      // the staged main loop (never live at the same time)
 };
 
 template <int D>
 union PassLds<D, kModeRegister> {  // no staging in the register-only variant
-  PassShared<D> sh;
+  PassShared<D, kWaves> sh;
 };
 
 // Publish a finished wavefront's state: rows n < rows of the tile.
-template <int D>
-__device__ __forceinline__ void publish(PassShared<D>& sh, const WaveAttention<D>& wave, int w, int lane, int rows) {
+template <int D, int NW>
+__device__ __forceinline__ void publish(PassShared<D, NW>& sh, const WaveAttention<D>& wave, int w, int lane,
+                                        int rows) {
   const int n = lane & 15;
   if (n < rows) {
     if (wave.tr_cols) {  // o[t][i] = column 16t + 4kg + i
@@ -133,8 +139,8 @@ __device__ __forceinline__ void publish(PassShared<D>& sh, const WaveAttention<D
 // saw no token of the row) and the scaled sum of their denominators, all in
 // a fixed order.  Rows past a tile's last one hold values nobody reads.
 // Ends with a barrier.
-template <int D>
-__device__ __forceinline__ void row_weights(PassShared<D>& sh, int ntile, int slices) {
+template <int D, int NW>
+__device__ __forceinline__ void row_weights(PassShared<D, NW>& sh, int ntile, int slices) {
   const int tid = threadIdx.x;
   if (tid < ntile * kRows) {
     const int t = tid / kRows;
@@ -155,8 +161,8 @@ __device__ __forceinline__ void row_weights(PassShared<D>& sh, int ntile, int sl
 }
 
 // One merged output element of tile t, row h, column d (row_weights first).
-template <int D>
-__device__ __forceinline__ float combine(const PassShared<D>& sh, int t, int ntile, int slices, int h, int d) {
+template <int D, int NW>
+__device__ __forceinline__ float combine(const PassShared<D, NW>& sh, int t, int ntile, int slices, int h, int d) {
   float acc = 0.f;
   for (int x = 0; x < slices; ++x) {
     const int w = t + x * ntile;
@@ -194,18 +200,18 @@ __device__ __forceinline__ void store_final4(float* p, const float (&acc)[4], fl
 // With NT = 2 the wavefront also folds a second, later chunk into `wave_b`
 // (blocks below j_stop_b, which is 0 when it has none) from the same K and V
 // fragments.
-template <int D, int SB, int NT>
-__device__ void run_staged(WaveAttention<D>& wave, WaveAttention<D>& wave_b, Staging<D, SB>& st,
+template <int D, int SB, int NT, int NW>
+__device__ void run_staged(WaveAttention<D>& wave, WaveAttention<D>& wave_b, Staging<D, SB, NW>& st,
                            const int32_t* table_row, int J0, int J1, int j_stop, int j_stop_b, bool active, int slice,
                            int slices, int L, int l_first, int l_vis, int l_first_b, int l_vis_b, const char* kpool,
                            const char* vpool, size_t block_bytes, int num_blocks) {
   using WA = WaveAttention<D>;
   static_assert(SB == 2, "a step is one pair of blocks");
-  static_assert(Staging<D, SB>::TC % kWaveSize == 0, "a wavefront's loads stay within one tile");
+  static_assert(Staging<D, SB, NW>::TC % kWaveSize == 0, "a wavefront's loads stay within one tile");
   wave.tr_cols = true;  // every fold here goes through pv_staged
   wave_b.tr_cols = true;
-  constexpr int TC = Staging<D, SB>::TC;
-  constexpr int NL = Staging<D, SB>::kLoads;
+  constexpr int TC = Staging<D, SB, NW>::TC;
+  constexpr int NL = Staging<D, SB, NW>::kLoads;
   const int tid = threadIdx.x;
   bool bad = false;
   // Two steps' loads are in flight in two register sets while a third
@@ -236,7 +242,7 @@ __device__ void run_staged(WaveAttention<D>& wave, WaveAttention<D>& wave_b, Sta
     }
 #pragma unroll
     for (int k = 0; k < NL; ++k) {
-      const int cb = k * kWaves * kWaveSize + wbase;  // the wavefront's first piece
+      const int cb = k * NW * kWaveSize + wbase;  // the wavefront's first piece
       const int blk = cb / (2 * TC);
       const char* pool = ((cb / TC) & 1) ? vpool : kpool;
       r[k] = load_stream(tile_rsrc(pool + (size_t)(blk == 0 ? phys[0] : phys[1]) * block_bytes,
@@ -248,10 +254,10 @@ __device__ void run_staged(WaveAttention<D>& wave, WaveAttention<D>& wave_b, Sta
   int dst[NL];
 #pragma unroll
   for (int k = 0; k < NL; ++k) {
-    const int ci = k * kWaves * kWaveSize + tid;  // [block][K or V][piece]
+    const int ci = k * NW * kWaveSize + tid;  // [block][K or V][piece]
     const int pc = ci % TC;
-    constexpr int RP = Staging<D, SB>::kRowPieces;
-    dst[k] = ci / (2 * TC) * Staging<D, SB>::kBlockPieces +
+    constexpr int RP = Staging<D, SB, NW>::kRowPieces;
+    dst[k] = ci / (2 * TC) * Staging<D, SB, NW>::kBlockPieces +
              (((ci / TC) & 1) ? TC + pc / RP * (RP + 2) + pc % RP : pc);
   }
   auto commit = [&](const uint4(&r)[NL], int buf) {
@@ -310,7 +316,7 @@ __device__ void run_staged(WaveAttention<D>& wave, WaveAttention<D>& wave_b, Sta
   };
   for (int jw = J0; jw < J1; jw += kIdWindow) {
     const int jwe = min(J1, jw + kIdWindow);
-    for (int j = jw + tid; j < jwe; j += kWaves * kWaveSize) st.ids[j - jw] = table_row[j];
+    for (int j = jw + tid; j < jwe; j += NW * kWaveSize) st.ids[j - jw] = table_row[j];
     __syncthreads();
     const int nsteps = (jwe - jw + SB - 1) / SB;
     issue(ra, jw, jwe, 0);
@@ -371,7 +377,8 @@ __device__ __forceinline__ void store_new_token(const StepArgs& a, int b, int g,
 
 template <int D, int MODE>
 __device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item) {
-  PassShared<D>& sh = lds.sh;
+  constexpr int NW = waves_of(MODE);
+  PassShared<D, NW>& sh = lds.sh;
   using WA = WaveAttention<D>;
   const int Hq = a.num_q_heads;
   const int G = a.group;
@@ -387,9 +394,9 @@ __device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item)
   const int nchunk = MODE == kModeRegister ? 1 : min(CPG, a.num_query_chunks - cg * CPG);
   // more than 4 (wide variant only): wavefront w folds chunks w and, when it
   // exists, w + 4, and the epilogue takes the two sets of tiles in turn
-  const bool two = MODE == kModeWide && nchunk > kWaves;
-  const int ntile = two ? kWaves : nchunk;  // tiles of the first (or only) set
-  const int slices = kWaves / ntile;        // slices of blocks per tile
+  const bool two = wide_mode(MODE) && nchunk > NW;
+  const int ntile = two ? NW : nchunk;  // tiles of the first (or only) set
+  const int slices = NW / ntile;        // slices of blocks per tile
   const int tid = threadIdx.x;
   const int lane = tid & (kWaveSize - 1);
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -416,7 +423,7 @@ __device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item)
       if (chunk_visible(a, L, c) > 0) continue;
       const int i0 = c * a.query_chunk;
       const int rows = min(a.query_chunk, nq - i0) * G;
-      for (int i = tid; i < rows * D; i += kWaves * kWaveSize) {
+      for (int i = tid; i < rows * D; i += NW * kWaveSize) {
         const int r = i / D;
         a.out[(((size_t)b * nq + i0 + r / G) * Hq + (size_t)g * G + r % G) * D + i % D] = 0.f;
       }
@@ -462,7 +469,7 @@ __device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item)
     if (first) {
       any_bad = 0;
 #pragma unroll
-      for (int x = 0; x < kWaves; ++x) any_bad |= sh.bad[x];
+      for (int x = 0; x < NW; ++x) any_bad |= sh.bad[x];
     }
     for (int t = 0; t < nt; ++t) {
       const int ct = chunk_of(t_first + t);
@@ -471,7 +478,7 @@ __device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item)
       const int ci0 = ct * a.query_chunk;
       const int crows = min(a.query_chunk, nq - ci0) * G;
       const bool single = ct_parts == 1 && min(t0_all, chunk_visible(a, L, ct)) == 0;
-      for (int idx = tid; idx < crows * (D / 4); idx += kWaves * kWaveSize) {  // 4 columns per thread
+      for (int idx = tid; idx < crows * (D / 4); idx += NW * kWaveSize) {  // 4 columns per thread
         const int h = idx / (D / 4);
         const int d0 = 4 * (idx % (D / 4));
         float acc[4];
@@ -492,7 +499,7 @@ __device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item)
   int any_bad = 0;
   if (ntile == 1) {  // one tile: the 4 wavefronts split the blocks, tiles into registers
     const int j_end = block_end(ca.l_vis, ca.nparts);
-    const int per_slice = (j_end - j_begin + kWaves - 1) / kWaves;
+    const int per_slice = (j_end - j_begin + NW - 1) / NW;
     const int wj0 = min(j_end, j_begin + w * per_slice);
     const int wj1 = min(j_end, wj0 + per_slice);
     if (a.k_new && L > 0 && wj0 <= (L - 1) / kBlockTokens && (L - 1) / kBlockTokens < wj1)  // wavefront-uniform
@@ -504,24 +511,24 @@ __device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item)
       const int ct = chunk_of(t);
       J1 = max(J1, block_end(chunk_visible(a, L, ct), parts_of(ct)));
     }
-    if constexpr (MODE == kModeWide) {
+    if constexpr (wide_mode(MODE)) {
       if (two) {
-        const bool has_b = tile + kWaves < nchunk;
+        const bool has_b = tile + NW < nchunk;
         WA wave_b(a.scale_log2);
-        const ChunkRows cb = setup(wave_b, chunk_of(has_b ? tile + kWaves : tile));
-        run_staged<D, kStepBlocks, 2>(wave, wave_b, lds.st, table_row, j_begin, J1, block_end(ca.l_vis, ca.nparts),
+        const ChunkRows cb = setup(wave_b, chunk_of(has_b ? tile + NW : tile));
+        run_staged<D, kStepBlocks, 2, NW>(wave, wave_b, lds.st, table_row, j_begin, J1, block_end(ca.l_vis, ca.nparts),
                                       has_b ? block_end(cb.l_vis, cb.nparts) : 0, true, 0, 1, L, ca.l_first,
                                       max(ca.l_vis, 0), cb.l_first, max(cb.l_vis, 0), kpool, vpool, block_bytes,
                                       a.num_blocks);
         wave.finish();
         wave_b.finish();
-        epilogue(wave, ca.rows, true, 0, kWaves, 1, any_bad, true);
+        epilogue(wave, ca.rows, true, 0, NW, 1, any_bad, true);
         __syncthreads();  // the second set reuses the epilogue's LDS
-        epilogue(wave_b, cb.rows, has_b, kWaves, nchunk - kWaves, 1, any_bad, false);
+        epilogue(wave_b, cb.rows, has_b, NW, nchunk - NW, 1, any_bad, false);
         return;
       }
     }
-    run_staged<D, kStepBlocks, 1>(wave, wave, lds.st, table_row, j_begin, J1, block_end(ca.l_vis, ca.nparts), 0,
+    run_staged<D, kStepBlocks, 1, NW>(wave, wave, lds.st, table_row, j_begin, J1, block_end(ca.l_vis, ca.nparts), 0,
                                   slice < slices, slice, slices, L, ca.l_first, max(ca.l_vis, 0), 0, 0, kpool, vpool,
                                   block_bytes, a.num_blocks);
   }
@@ -531,7 +538,8 @@ __device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item)
 
 template <int D, int MODE>
 __device__ void prefix_item(const StepArgs& a, PassLds<D, MODE>& lds, int pitem) {
-  PassShared<D>& sh = lds.sh;
+  constexpr int NW = waves_of(MODE);
+  PassShared<D, NW>& sh = lds.sh;
   using WA = WaveAttention<D>;
   const int Hq = a.num_q_heads;
   const int G = a.group;
@@ -551,7 +559,7 @@ __device__ void prefix_item(const StepArgs& a, PassLds<D, MODE>& lds, int pitem)
   if (members <= 0 || pp * Tp >= plen) return;
   const int rows = members * G;                    // member-major, then the G heads
   const int ntile = (rows + kRows - 1) / kRows;    // 16-row tiles: 1 .. 4
-  const int slices = kWaves / ntile;               // slices of blocks per tile
+  const int slices = NW / ntile;                   // slices of blocks per tile
   const int tile = w % ntile;
   const int slice = w / ntile;
   const int t_end = min(plen, (pp + 1) * Tp);
@@ -571,12 +579,12 @@ __device__ void prefix_item(const StepArgs& a, PassLds<D, MODE>& lds, int pitem)
   const size_t block_bytes = (size_t)a.num_kv_heads * WA::kTileBytes;
   if (MODE == kModeRegister && ntile != 1) return;  // not this launch's kind (never: the host picks the mode)
   if (ntile == 1) {  // one tile: the 4 wavefronts split the blocks, tiles into registers
-    const int per_slice = (j_end - j_begin + kWaves - 1) / kWaves;
+    const int per_slice = (j_end - j_begin + NW - 1) / NW;
     const int wj0 = min(j_end, j_begin + w * per_slice);
     const int wj1 = min(j_end, wj0 + per_slice);
     wave.run(table_row, wj0, wj1, plen, plen, plen, kpool, vpool, block_bytes, a.num_blocks);
   } else if constexpr (MODE != kModeRegister) {  // several tiles: every block staged once through LDS for all of them
-    run_staged<D, kStepBlocks, 1>(wave, wave, lds.st, table_row, j_begin, j_end, j_end, 0, slice < slices, slice,
+    run_staged<D, kStepBlocks, 1, NW>(wave, wave, lds.st, table_row, j_begin, j_end, j_end, 0, slice < slices, slice,
                                   slices, plen, plen, plen, 0, 0, kpool, vpool, block_bytes, a.num_blocks);
   }
   wave.finish();
@@ -587,8 +595,8 @@ __device__ void prefix_item(const StepArgs& a, PassLds<D, MODE>& lds, int pitem)
   // ---- merge the slices of each tile in a fixed order; every member row gets a partial state ----
   int any_bad = 0;
 #pragma unroll
-  for (int x = 0; x < kWaves; ++x) any_bad |= sh.bad[x];
-  for (int idx = tid; idx < rows * (D / 4); idx += kWaves * kWaveSize) {  // 4 columns per thread
+  for (int x = 0; x < NW; ++x) any_bad |= sh.bad[x];
+  for (int idx = tid; idx < rows * (D / 4); idx += NW * kWaveSize) {  // 4 columns per thread
     const int rr = idx / (D / 4);
     const int d0 = 4 * (idx % (D / 4));
     const int t = rr / kRows, h = rr % kRows;
@@ -603,7 +611,8 @@ __device__ void prefix_item(const StepArgs& a, PassLds<D, MODE>& lds, int pitem)
 // Occupancy: 3 wavefronts per SIMD (12 per compute unit) at most 168 VGPRs;
 // the wide variant 2 (256 VGPRs).
 template <int D, int MODE>
-__global__ void __launch_bounds__(kWaves * kWaveSize) __attribute__((amdgpu_waves_per_eu(MODE == kModeWide ? 2 : 3)))
+__global__ void __launch_bounds__(waves_of(MODE) * kWaveSize)
+__attribute__((amdgpu_waves_per_eu(wide_mode(MODE) ? 2 : 3)))
 partition_kernel(const StepArgs a) {
   __shared__ __align__(16) PassLds<D, MODE> lds;
   const int item = a.order ? a.order[blockIdx.x] : (int)blockIdx.x;  // no order: every item runs at once
@@ -627,7 +636,10 @@ hipError_t launch_d(const StepArgs& a, hipStream_t stream) {
   const bool one = a.num_query_chunks % kWaves == 1 || groups;
   const bool several = a.num_query_chunks >= 2 || (groups && (int64_t)a.max_group_size * a.group > kRows);
   const dim3 block(kWaves * kWaveSize);
-  if (a.chunks_per_group > kWaves)
+  if (a.chunks_per_group > kWideChunks)
+    hipLaunchKernelGGL((partition_kernel<D, kModeWide16>), dim3(grid), dim3(waves_of(kModeWide16) * kWaveSize), 0,
+                       stream, a);
+  else if (a.chunks_per_group > kWaves)
     hipLaunchKernelGGL((partition_kernel<D, kModeWide>), dim3(grid), block, 0, stream, a);
   else if (one && !several)
     hipLaunchKernelGGL((partition_kernel<D, kModeRegister>), dim3(grid), block, 0, stream, a);

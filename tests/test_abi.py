@@ -280,14 +280,16 @@ def test_append_and_graph_validation():
 def test_multi_token_plan():
     # n new tokens per sequence: query chunks of min(n, 16 // G) tokens; one
     # work item per (partition, sequence, KV head, group of chunks): up to 4,
-    # or up to 8 when there are more than 4
+    # up to 8 when there are more than 4, up to 16 when there are more than 8
     d = pda.pda_plan(llama(num_query_tokens=4, partition_tokens=4096))     # G = 4: one chunk
     assert d["workspace_bytes"] == 256 * 8 * 4
     d = pda.pda_plan(llama(num_query_tokens=7, partition_tokens=4096))     # two chunks, one item
     assert d["workspace_bytes"] == 256 * 8 * 4
     d = pda.pda_plan(llama(num_query_tokens=17, partition_tokens=4096))    # five chunks: one item of up to 8
     assert d["workspace_bytes"] == 256 * 8 * 4
-    d = pda.pda_plan(llama(num_query_tokens=33, partition_tokens=4096))    # nine chunks, two items
+    d = pda.pda_plan(llama(num_query_tokens=33, partition_tokens=4096))    # nine chunks: one item of up to 16
+    assert d["workspace_bytes"] == 256 * 8 * 4
+    d = pda.pda_plan(llama(num_query_tokens=68, partition_tokens=4096))    # seventeen chunks, two items
     assert d["workspace_bytes"] == 256 * 8 * 2 * 4
     d = pda.pda_plan(llama(num_query_tokens=4, partition_tokens=2048))     # 2 partitions: partials per row
     assert d["workspace_bytes"] == 256 * 4 * 32 * 2 * (128 + 2) * 4 + 2 * 256 * 8 * 4
@@ -367,7 +369,7 @@ def test_plan_invariants_over_random_descriptors():
     for _ in range(400):
         G = int(rng.choice([1, 2, 4, 5, 7, 8, 16]))
         hkv = int(rng.integers(1, 9))
-        n = int(rng.choice([1, 1, 2, 4, 8, 16, 33]))
+        n = int(rng.choice([1, 1, 2, 4, 8, 16, 33, 70, 512]))
         max_len = int(rng.integers(0, 40000))
         mb = max(1, -(-max_len // 16) + int(rng.integers(0, 4)))
         p = pda.make_problem(int(rng.integers(1, 600)), G * hkv, hkv, int(rng.choice([64, 128])), 1 << 20, mb,
@@ -376,7 +378,7 @@ def test_plan_invariants_over_random_descriptors():
         tp, parts = info["partition_tokens"], info["num_partitions"]
         qc = min(n, 16 // G)
         nqc = -(-n // qc)
-        cpg = 8 if nqc > 4 else 4
+        cpg = 16 if nqc > 8 else 8 if nqc > 4 else 4
         wide = min(nqc, cpg) * qc * G >= 64
         assert tp % 16 == 0 and 16 <= tp and (wide or tp <= 4608)
         assert tp % 256 == 0 or tp == -(-max(max_len, 1) // 16) * 16

@@ -167,14 +167,14 @@ def test_multi_token_poison_and_shuffle_bit_identical(dev, n):
 
 
 @pytest.mark.parametrize("D", [64, 128])
-@pytest.mark.parametrize("n", [1, 8, 32], ids=["register", "mixed", "wide"])
+@pytest.mark.parametrize("n", [1, 8, 32, 60], ids=["register", "mixed", "wide", "wide16"])
 @pytest.mark.parametrize("partition_tokens", [0, 64])
 def test_run_to_run_bitwise_every_variant(dev, D, n, partition_tokens):
     """Three runs give identical bits in each compiled variant of the
     partition kernel at both head dims: one 16-row tile per item in registers
-    (n = 1), up to 4 tiles staged through LDS (n = 8 at G = 4: 2 tiles), and
-    the wide variant with two tiles per wavefront (n = 32: 8 tiles); with
-    whole and split contexts.  These runs guard the ordering of the score
+    (n = 1), up to 4 tiles staged through LDS (n = 8 at G = 4: 2 tiles), the
+    wide variant with two tiles per wavefront (n = 32: 8 tiles) and its
+    8-wavefront form (n = 60: 15 tiles); with whole and split contexts.  These runs guard the ordering of the score
     MFMAs and their first VALU reads, which the compiler once left without
     the wait states a read of an MFMA result needs."""
     lens = [1, 17, 300, 2049, 40, 64, 1000, 513]

@@ -35,7 +35,7 @@ def plan_of(B, Hq, Hkv, D, mbps, mcl, tp, n, groups=None):
     G = Hq // Hkv
     qc = min(n, MAX_GROUP // G)
     nqc = -(-n // qc)
-    cpg = 2 * WAVES if nqc > WAVES else WAVES
+    cpg = 4 * WAVES if nqc > 2 * WAVES else 2 * WAVES if nqc > WAVES else WAVES
     ncg = -(-nqc // cpg)
     P = info["num_partitions"]
     Tp = info["partition_tokens"]
@@ -109,9 +109,16 @@ def check_regular_item(item, B, Hq, Hkv, D, n, mbps, mcl, lens_c, pl, seq_prefix
     p = item // (HC * B)
     g, cg = gc // ncg, gc % ncg
     assert 0 <= b < B and 0 <= g < Hkv and 0 <= p < pl["P"] and 0 <= cg < ncg
-    wide_mode = cpg > WAVES
+    nw = 2 * WAVES if cpg > 2 * WAVES else WAVES  # wavefronts of the launch's workgroups
     nchunk = min(cpg, nqc - cg * cpg)  # the register-only variant runs only when every item has one chunk
-    assert 1 <= nchunk <= (2 * WAVES if wide_mode else WAVES)
+    assert 1 <= nchunk <= (2 * nw if cpg > WAVES else nw)
+    two = cpg > WAVES and nchunk > nw
+    ntile = nw if two else nchunk
+    slices = nw // ntile
+    # the LDS epilogue arrays have nw entries: row_weights reads entry t + x * ntile (t < ntile, x < slices)
+    assert slices >= 1 and ntile * slices <= nw
+    if two:
+        assert nchunk <= 2 * nw  # wavefront w folds chunks w and w + nw
     L = min(max(lens_c[b], 0), mcl)
     t0_all = seq_prefix[b] if seq_prefix is not None else 0
     rows_q = B * n * Hq
@@ -216,15 +223,16 @@ def check_merge(B, Hq, n, mcl, lens_c, pl, seq_prefix, touched):
     assert len(touched["out"]) == B * n * Hq, "every output row is written"
 
 
-def staged_lds_indices(D):
+def staged_lds_indices(D, nw=WAVES):
     """The staging buffer's piece indices and the transposed V reads stay in one block."""
     TC = 16 * D * 2 // 16
     RP = D // 8
     block_pieces = TC + BS * (RP + 2)
-    loads = 2 * 2 * TC // (WAVES * WAVE)
-    for tid in range(WAVES * WAVE):
+    loads = 2 * 2 * TC // (nw * WAVE)
+    assert loads * nw * WAVE == 2 * 2 * TC  # every piece of a step is loaded once
+    for tid in range(nw * WAVE):
         for k in range(loads):
-            ci = k * WAVES * WAVE + tid
+            ci = k * nw * WAVE + tid
             pc = ci % TC
             blk = ci // (2 * TC)
             dst = blk * block_pieces + (TC + pc // RP * (RP + 2) + pc % RP if (ci // TC) & 1 else pc)
@@ -268,6 +276,7 @@ def run_case(rng, B, Hq, Hkv, D, n, mcl, tp, lens, mbps, groups=None):
 @pytest.mark.parametrize("D", [64, 128])
 def test_staged_lds_indices(D):
     staged_lds_indices(D)
+    staged_lds_indices(D, nw=2 * WAVES)  # workgroups of 8 wavefronts (items of more than 8 chunks)
 
 
 def test_random_descriptors():
@@ -306,10 +315,12 @@ def test_shared_prefix_descriptors():
 
 
 @pytest.mark.parametrize("n,G,Hkv,tp", [(1, 4, 8, 0), (4, 4, 8, 0), (32, 4, 8, 0), (64, 4, 8, 3840),
-                                         (512, 4, 8, 0), (512, 8, 1, 256), (16, 8, 1, 0), (13, 16, 1, 16)])
+                                         (512, 4, 8, 0), (512, 8, 1, 256), (16, 8, 1, 0), (13, 16, 1, 16),
+                                         (40, 4, 8, 0), (68, 4, 8, 0), (36, 8, 1, 0)])
 def test_named_shapes(n, G, Hkv, tp):
     """Small batches in the shapes of the benchmarked steps (4 to 512 new
-    tokens, wide items, two or more chunk groups, split contexts)."""
+    tokens, wide items of 8 and 16 chunks, a last group of one chunk, two or
+    more chunk groups, split contexts)."""
     rng = np.random.default_rng(n + G)
     lens = [1, n, n + 17, 600, 1500, 4096]
     run_case(rng, len(lens), G * Hkv, Hkv, 128, n, 4096, tp, lens, 256)
