@@ -46,7 +46,7 @@
  * are processed independently; a second pass merges the partial softmax
  * states.  Pass 1 runs one workgroup per (partition, sequence, KV head,
  * group of up to 4 chunks of at most 16 / G new tokens each; up to 8 when
- * there are more than 4 chunks), largest
+ * there are more than 4 chunks, up to 16 when there are more than 8), largest
  * partition first (a small kernel sorts the items by size on the GPU; it is
  * skipped when every item runs at once).  The partition size depends
  * only on the problem descriptor and the arithmetic of an item only on its
