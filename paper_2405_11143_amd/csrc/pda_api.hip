@@ -83,6 +83,15 @@ struct Plan {
   size_t slots;           // partial states: (Pp + P) per output row; 0 when nothing is split
 };
 
+// Workgroups the GPU runs at once in a step's pass-1 variant: 3 per compute
+// unit for items of up to 4 query chunks, 2 for the wide variant (229
+// VGPRs), 1 for its 8-wavefront form.
+int64_t concurrent_items(const Plan& plan) {
+  if (plan.chunks_per_group > pda::kWideChunks) return kConcurrentItems / 3;
+  if (plan.chunks_per_group > pda::kWaves) return kConcurrentItems * 2 / 3;
+  return kConcurrentItems;
+}
+
 // Shared-prefix groups: host bounds checked here (the plan needs no more);
 // the arrays are device data, required by the step itself.
 int check_groups(const pda_problem* p, const pda_prefix_groups* g) {
@@ -215,7 +224,7 @@ int prepare_step(const pda_problem* p, const pda_prefix_groups* groups, const vo
   // When the GPU runs every item at once the order is irrelevant: the step
   // skips the work-order kernel (one dependent launch less) and item i is
   // workgroup i.  Shared-prefix groups still need it for the prefix table.
-  if (plan->items <= (size_t)kConcurrentItems && !(groups && groups->num_groups > 0)) args->order = nullptr;
+  if (plan->items <= (size_t)concurrent_items(*plan) && !(groups && groups->num_groups > 0)) args->order = nullptr;
   if (groups && groups->num_groups > 0 && p->num_seqs > 0) {
     args->group_start = groups->group_start;
     args->group_prefix_len = groups->group_prefix_len;
