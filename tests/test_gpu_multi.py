@@ -56,14 +56,17 @@ CASES = [  # (Hq, Hkv, D, n): rows per work item = min(n, 16 // G) * G
     (32, 8, 128, 32),  # G=4: 8 chunks in one item, two tiles per wavefront
     (8, 1, 128, 12),   # G=8: 6 chunks, two tiles on wavefronts 0-1
     (12, 4, 128, 26),  # G=3: 6 chunks of 5 tokens (the last one 1), 15 rows each
-    (32, 8, 128, 37),  # G=4: 10 chunks, two items (8 + 2 chunks)
-    (32, 8, 128, 64),  # G=4: 16 chunks, two items of 8
+    (32, 8, 128, 37),  # G=4: 10 chunks in one item on 8 wavefronts (two tiles on wavefronts 0-1)
+    (32, 8, 128, 64),  # G=4: 16 chunks in one item, two tiles on each of 8 wavefronts
+    (32, 8, 128, 72),  # G=4: 18 chunks, two items (16 + 2 chunks)
+    (8, 1, 128, 40),   # G=8: 20 chunks of 2 tokens, two items (16 + 4 chunks)
 ]
 
 
 def test_many_chunk_groups(dev):
-    """128 new tokens at G = 4: 32 query chunks in 4 wide work items per
-    (partition, sequence, KV head), every element against the oracle."""
+    """128 new tokens at G = 4: 32 query chunks in 2 work items of 16 chunks
+    (8 wavefronts of two tiles) per (partition, sequence, KV head), every
+    element against the oracle."""
     lens = [1, 200, 700, 3000, 128, 1500]
     n = 128
     st = W.custom_structure(len(lens), 32, 8, 128, lens, seed=73)
@@ -72,7 +75,7 @@ def test_many_chunk_groups(dev):
     ref = oracle.decode_multi(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
                               st.context_lens, st.scale, threads=THREADS)
     got = run_multi(st, q, k, v, dev)
-    check(got, ref, "128 new tokens, 4 chunk groups")
+    check(got, ref, "128 new tokens, 2 chunk groups")
 
 
 @pytest.mark.parametrize("Hq,Hkv", [(32, 8), (8, 1)], ids=["G4", "G8"])
