@@ -122,8 +122,11 @@ int make_plan(const pda_problem* p, const pda_prefix_groups* groups, Plan* plan)
   if (tp == 0) {
     const int64_t len = p->max_context_len > 0 ? p->max_context_len : 1;
     // (a product that would overflow only means: as long as allowed)
-    int64_t share = units > (INT64_MAX / 4) / len ? INT64_MAX / 4
-                                                  : (units * len / 2 + kConcurrentItems - 1) / kConcurrentItems;
+    // items of more than 8 chunks (one 8-wavefront workgroup per compute
+    // unit) count 512 at once: long enough to amortise their start-up,
+    // short enough that ragged contexts still balance
+    const int64_t slots = cpg > pda::kWideChunks ? kConcurrentItems * 2 / 3 : kConcurrentItems;
+    int64_t share = units > (INT64_MAX / 4) / len ? INT64_MAX / 4 : (units * len / 2 + slots - 1) / slots;
     const int64_t item_rows = (int64_t)std::min(nqc, cpg) * qc * G;
     if (item_rows >= pda::kMaxGroup) share = share * kRowsShareNum / kRowsShareDen;
     const int64_t cap = item_rows >= kWideItemRows ? kMaxContextTokens : kMaxPartitionTokens;

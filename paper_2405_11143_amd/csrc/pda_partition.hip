@@ -3,8 +3,8 @@
 // every item runs at once.  Two kinds of items share the launch:
 //
 // Regular items: (partition of a context, sequence, KV head, group of up to
-// 4 chunks of new query tokens, or up to 8 when there are more than 4).  A
-// chunk holds up to 16 / G consecutive new
+// 4 chunks of new query tokens, up to 8 when there are more than 4, up to 16
+// when there are more than 8).  A chunk holds up to 16 / G consecutive new
 // tokens of the sequence, so its query rows (token-major, then the G heads of
 // the KV head) fill one 16-row MFMA tile; a decode step has one token, i.e.
 // one chunk of G rows.  New token i of a sequence with n new tokens and
@@ -12,8 +12,9 @@
 // t < L - n + 1 + i.  The 4 wavefronts take the item's chunks first and
 // slices of its blocks second (1 chunk: 4 contiguous runs; 2: every other
 // step of 2 blocks each; 3-4: every block; 5-8, the wide variant: chunks w
-// and w + 4 on wavefront w, every block), so the chunks of one item read
-// each tile on one compute unit.  Each chunk keeps its own causal range and
+// and w + 4 on wavefront w, every block; 9-16, the wide variant on 8
+// wavefronts: chunks w and w + 8), so the chunks of one item read each tile
+// on one compute unit.  Each chunk keeps its own causal range and
 // partition count.  With shared-prefix groups, a sequence's regular items
 // cover only the tokens after its group's prefix.
 //
@@ -80,7 +81,10 @@ struct Staging {
 // path only (136 VGPRs at D = 128, 33 KiB of LDS); with up to 4 query chunks
 // per item both paths are compiled (164 VGPRs, 50.5 KiB); with more, the
 // wide variant also folds two tiles per wavefront (229 VGPRs, 2
-// workgroups per compute unit).  Staging takes 2 blocks per step, so three
+// workgroups per compute unit), and beyond 8 chunks its 8-wavefront form
+// does (206 VGPRs, 67 KiB, one workgroup per compute unit: each staged step
+// then serves 16 tiles, half the staging and barriers per tile of 8).
+// Staging takes 2 blocks per step, so three
 // staging buffers (49.5 KiB at D = 128) still leave room for 3 workgroups
 // per compute unit; 4 blocks per step at 2 workgroups per compute unit
 // measured slower on MI355X.
