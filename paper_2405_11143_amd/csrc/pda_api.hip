@@ -287,7 +287,7 @@ hipError_t launch_append_of(const pda_problem* p, const pda::StepArgs& args, con
 // 3%, more than the separate append kernel (3.4 us), so there the append
 // keeps its own launch.
 bool folds_append(const pda_problem* p, const Plan& plan) {
-  return query_tokens(p) == 1 && plan.items <= (size_t)kConcurrentItems;
+  return query_tokens(p) == 1 && plan.items <= (size_t)concurrent_items(plan);
 }
 
 // Let pass 1 store the step's new K/V rows (one new token per sequence, no
@@ -382,7 +382,7 @@ int pda_work_order(const pda_problem* prob, const int32_t* context_lens, void* w
   if (rc != PDA_OK) return rc;
   if (!workspace || workspace_bytes < plan.info.workspace_bytes) return PDA_ERR_WORKSPACE;
   if (!aligned(workspace, 16)) return PDA_ERR_ALIGNMENT;
-  if (plan.items <= (size_t)kConcurrentItems) return PDA_OK;  // the step runs without an order
+  if (plan.items <= (size_t)concurrent_items(plan)) return PDA_OK;  // the step runs without an order
   pda::StepArgs args;
   fill_args(prob, &plan, workspace, &args);
   args.lens = context_lens;

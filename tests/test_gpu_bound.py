@@ -96,6 +96,33 @@ def test_reused_work_order_matches_decode(dev, n):
     assert torch.equal(got, want)
 
 
+@pytest.mark.parametrize("n,tp,conc", [(24, 2048, 512), (40, 4096, 256)], ids=["wide", "wide16"])
+def test_reused_work_order_between_variant_and_full_concurrency(dev, n, tp, conc):
+    """A step of the wide variants with more items than that variant runs at
+    once but at most 768 (what the one-tile variants run at once): the step
+    takes an ordered list, so pda_work_order must write it too, and the
+    reused order gives pda_decode's bits."""
+    rng = np.random.default_rng(80 + n)
+    B = 48
+    lens = rng.integers(2100, 3000, size=B).tolist()
+    st = W.custom_structure(B, 32, 8, 128, lens, seed=81 + n)
+    _, k, v = W.fill_values(st, dev, fill="nan")
+    q = W.fill_multi_q(st, n, dev)
+    bt = torch.from_numpy(st.block_table).to(dev)
+    ln = torch.from_numpy(st.context_lens).to(dev)
+    kw = dict(max_context_len=st.max_context_len, partition_tokens=tp)
+    prob = make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq, st.max_context_len, tp,
+                        num_query_tokens=n)
+    items = pda_plan(prob)["num_partitions"] * st.B * st.Hkv  # one chunk group per (partition, sequence, head)
+    assert conc < items <= 768, items
+    ws = torch.full((pda_workspace_bytes(prob),), 0xFF, dtype=torch.uint8, device=dev)  # no order left over
+    pda_work_order(prob, ln, ws)
+    got = pda_decode_reusing_order(q, k, v, bt, ln, st.scale, workspace=ws, **kw)
+    want = pda_decode(q, k, v, bt, ln, st.scale, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(got, want)
+
+
 def test_bound_append_matches(dev):
     lens = [5, 33, 16, 1000]
     st = W.custom_structure(len(lens), 8, 2, 64, lens, seed=61)
