@@ -280,3 +280,32 @@ def test_out_of_range_block_ids_give_nan_rows(dev, n, partition_tokens):
     ref = oracle.decode_multi(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
                               st.context_lens, st.scale, threads=THREADS)
     check(got[ok], ref[ok], f"sequences with valid tables n={n} Tp={partition_tokens}")
+
+
+@pytest.mark.parametrize("n,partition_tokens", [(1, 0), (1, 64), (8, 0), (40, 64)], ids=str)
+def test_nan_inside_a_context_propagates_like_the_oracle(dev, n, partition_tokens):
+    """A NaN key element inside a context makes every row that sees that
+    token NaN; a NaN value element makes that output column NaN in those
+    rows; everything else is unaffected.  The positions of NaN outputs equal
+    the oracle's and the other elements meet the bar.  The poisoned tokens
+    come before the new tokens, so every row of the sequence sees them (the
+    register path, the staged path and 8-wavefront items; whole and split
+    contexts)."""
+    lens = [200, 300, 150, 1000, 777]
+    st = W.custom_structure(len(lens), 32, 8, 128, lens, seed=95 + n)
+    _, k, v = W.fill_values(st, dev, fill="nan")
+    q = W.fill_multi_q(st, n, dev)
+    nan = torch.tensor(float("nan"), dtype=torch.bfloat16, device=dev)
+    # key of sequence 1, KV head 2, token 37, element 5; value of sequence 3, KV head 5, token 600, element 77
+    p1 = int(st.block_table[1, 37 // 16])
+    k[p1, 2, 5 // 8, 37 % 16, 5 % 8] = nan
+    p3 = int(st.block_table[3, 600 // 16])
+    v[p3, 5, 600 % 16, 77] = nan
+    got = run(st, q, k, v, dev, partition_tokens)
+    ref = oracle.decode_multi(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table,
+                              st.context_lens, st.scale, threads=THREADS)
+    got = got.reshape(ref.shape)
+    assert np.isnan(ref[1, :, 8:12]).all() and np.isnan(ref[3, :, 20:24, 77]).all()  # the oracle's reading
+    assert np.array_equal(np.isnan(got), np.isnan(ref)), "NaN positions differ from the oracle's"
+    fin = ~np.isnan(ref)
+    check(got[fin], ref[fin], f"finite elements n={n} Tp={partition_tokens}")
