@@ -40,7 +40,10 @@
  *   k_new, v_new bf16  [num_seqs][n][num_kv_heads][head_dim]  (pda_append_kv)
  *   workspace    opaque, pda_workspace_bytes() bytes
  * Pool slots past a sequence's context (the tail of its last block) and pool
- * blocks no sequence references are never used, whatever they hold.
+ * blocks no sequence references are never used, whatever they hold.  K and V
+ * inside a context are expected to be finite: a NaN or infinite element makes
+ * the outputs of the rows that see its token non-finite (and, in a chunk of
+ * several new tokens, possibly rows of that chunk that do not).
  *
  * Long contexts are split into partitions of `partition_tokens` tokens that
  * are processed independently; a second pass merges the partial softmax
