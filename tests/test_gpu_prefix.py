@@ -116,3 +116,36 @@ def test_shared_prefix_config_full_size(dev):
     check(got[rows[:, 0], rows[:, 1]], ref, "shared_prefix sampled rows")
     ref = oracle.decode(qb, kb, vb, st.block_table, st.context_lens, st.scale, threads=THREADS)
     check(got, ref, "shared_prefix every element", f"B*Hq*D = {st.B}*{st.Hq}*{st.D}")
+
+
+def draw_groups(case: int):
+    """Seeded random shared-prefix descriptors: 1-4 groups of 1 to 64/G
+    members with prefixes of 0 to 2048 tokens (whole blocks), members'
+    own tokens 0 to 1500 after it, and 0-3 sequences in no group."""
+    r = np.random.default_rng(7000 + case)
+    G = int(r.choice([1, 2, 4, 5, 8, 16]))
+    Hkv = int(r.choice([1, 2]))
+    D = int(r.choice([64, 128]))
+    groups = []
+    for _ in range(int(r.integers(1, 5))):
+        prefix = 16 * int(r.integers(0, 129))
+        members = int(r.integers(1, 64 // G + 1))
+        groups.append((prefix, [prefix + int(r.choice([0, 1, 15, 16, 17, 300, 1500])) for _ in range(members)]))
+    loners = [int(r.choice([0, 1, 100, 2000])) for _ in range(int(r.integers(0, 4)))]
+    tp = int(r.choice([0, 0, 16, 64, 512]))
+    return G, Hkv, D, groups, loners, tp
+
+
+@pytest.mark.parametrize("case", range(24))
+def test_random_groups(dev, case):
+    """Random group layouts (sizes up to the 64-row bound of a prefix item,
+    prefixes from none to several partitions, empty suffixes, sequences in no
+    group, forced partition sizes): every element against the plain decode
+    definition."""
+    G, Hkv, D, groups, loners, tp = draw_groups(case)
+    st = W.custom_shared_structure(G * Hkv, Hkv, D, groups, loners, seed=300 + case)
+    q, k, v = W.fill_values(st, dev, fill="nan")
+    print(f"case {case}: G={G} Hkv={Hkv} D={D} groups={[(p, len(m)) for p, m in groups]} loners={loners} Tp={tp}",
+          flush=True)
+    got = run(st, q, k, v, dev, tp)
+    check(got, reference(st, q, k, v), f"random groups case {case}")
