@@ -212,7 +212,7 @@ int pda_decode_reusing_order(const pda_problem *prob, const void *q, const void 
  * bounds, never trusted for memory safety). */
 typedef struct pda_prefix_groups {
   int32_t num_groups;               /* >= 0 */
-  int32_t max_group_size;           /* bound on members per group: 1 .. 64 / G */
+  int32_t max_group_size;           /* bound on members per group: 1 .. 64 / (n G) */
   int32_t max_prefix_len;           /* bound on group_prefix_len[]: a multiple of 16, <= max_context_len */
   const int32_t *group_start;       /* device int32 [num_groups + 1], non-decreasing, within [0, num_seqs] */
   const int32_t *group_prefix_len;  /* device int32 [num_groups] */
@@ -222,13 +222,16 @@ typedef struct pda_prefix_groups {
  * only the host bounds of `groups` are read. */
 int pda_plan_shared_prefix(const pda_problem *prob, const pda_prefix_groups *groups, pda_plan_info *plan);
 
-/* The decode step of pda_decode (one new token per sequence: num_query_tokens
- * 0 or 1) with each group's shared prefix attended once for all its members:
- * a work item reads the prefix blocks and computes all members x G query
- * rows of a KV head on one 16-row MFMA tile per wavefront, and every member
- * row then merges the prefix's partial softmax state with those of its own
- * tokens.  The result is the same attention as pda_decode (up to rounding).
- * `workspace` must hold pda_plan_shared_prefix()'s workspace_bytes. */
+/* The step of pda_decode (one new token per sequence, or n = num_query_tokens
+ * with q and out [B][n][Hq][D]) with each group's shared prefix attended once
+ * for all its members: a work item reads the prefix blocks and computes all
+ * members x n x G query rows of a KV head (at most 64: max_group_size * n *
+ * G <= 64, else PDA_ERR_UNSUPPORTED) on one 16-row MFMA tile per wavefront,
+ * each row seeing the prefix tokens before its own position, and every
+ * member row then merges the prefix's partial softmax state with those of
+ * its own tokens.  The result is the same attention as pda_decode (up to
+ * rounding).  `workspace` must hold pda_plan_shared_prefix()'s
+ * workspace_bytes. */
 int pda_decode_shared_prefix(const pda_problem *prob, const pda_prefix_groups *groups, const void *q,
                              const void *k_cache, const void *v_cache, const int32_t *block_table,
                              const int32_t *context_lens, float scale, float *out, void *workspace,

@@ -99,9 +99,10 @@ int check_groups(const pda_problem* p, const pda_prefix_groups* g) {
   if (g->num_groups < 0 || g->max_group_size < 1 || g->max_prefix_len < 0 ||
       g->max_prefix_len % pda::kBlockTokens != 0 || g->max_prefix_len > p->max_context_len)
     return PDA_ERR_SHAPE;
-  if (p->num_query_tokens > 1) return PDA_ERR_UNSUPPORTED;  // one new token per sequence
-  // (in 64 bits: a huge bound must not wrap past the check)
-  if ((int64_t)g->max_group_size * (p->num_q_heads / p->num_kv_heads) > 64) return PDA_ERR_UNSUPPORTED;
+  // a group's rows (members x new tokens x G) fit the 4 tiles of a prefix
+  // item (in 64 bits: a huge bound must not wrap past the check)
+  if ((int64_t)g->max_group_size * query_tokens(p) * (p->num_q_heads / p->num_kv_heads) > 64)
+    return PDA_ERR_UNSUPPORTED;
   return PDA_OK;
 }
 

@@ -20,9 +20,11 @@
 //
 // Prefix items: (shared-prefix group, prefix partition, KV head).  All
 // members of a group read the same prefix blocks (parallel sampling, Section
-// 3.2), so the prefix is attended once for all members x G heads (up to 64
-// query rows): the 4 wavefronts take 16-row tiles first and slices of blocks
-// second, as above, and every block's tiles reach the compute unit once.
+// 3.2), so the prefix is attended once for all members x new tokens x G
+// heads (up to 64 query rows; a row whose position lies inside the prefix
+// sees only the prefix tokens before it): the 4 wavefronts take 16-row tiles
+// first and slices of blocks second, as above, and every block's tiles reach
+// the compute unit once.
 //
 // With one tile, each wavefront streams its run of 16-token blocks with
 // WaveAttention (pda_wave.h), tiles straight into registers.  With several
@@ -439,8 +441,11 @@ __device__ void regular_item(const StepArgs& a, PassLds<D, MODE>& lds, int item)
   const char* vpool = reinterpret_cast<const char*>(a.v) + (size_t)g * WA::kTileBytes;
   const int32_t* table_row = a.table + (size_t)b * a.max_blocks_per_seq;
   const size_t block_bytes = (size_t)a.num_kv_heads * WA::kTileBytes;
-  // the partition's first block: chunk 0's (several chunks come only without a shared prefix)
-  const int j_begin = (min(t0_all, max(chunk_visible(a, L, chunk_of(0)), 0)) + p * Tp) / kBlockTokens;
+  // The partition's first block: that of the item's last chunk.  With a
+  // shared prefix, every chunk with tokens after it starts its own range at
+  // the prefix's end, as the last chunk does; a chunk whose rows see nothing
+  // past the prefix has no own partitions and folds nothing.
+  const int j_begin = (min(t0_all, max(chunk_visible(a, L, chunk_of(nchunk - 1)), 0)) + p * Tp) / kBlockTokens;
   auto block_end = [&](int lv, int parts) {  // end block of this partition for a chunk limit lv
     const int t0 = min(t0_all, max(lv, 0));
     return p < parts ? (min(lv, t0 + (p + 1) * Tp) + kBlockTokens - 1) / kBlockTokens : 0;
@@ -561,7 +566,8 @@ __device__ void prefix_item(const StepArgs& a, PassLds<D, MODE>& lds, int pitem)
   plen = plen < 0 ? 0 : (plen > a.max_prefix_len ? a.max_prefix_len : plen) / kBlockTokens * kBlockTokens;
   const int Tp = a.partition_tokens;
   if (members <= 0 || pp * Tp >= plen) return;
-  const int rows = members * G;                    // member-major, then the G heads
+  const int nq = a.num_query_tokens;
+  const int rows = members * nq * G;               // member-major, then the new tokens, then the G heads
   const int ntile = (rows + kRows - 1) / kRows;    // 16-row tiles: 1 .. 4
   const int slices = NW / ntile;                   // slices of blocks per tile
   const int tile = w % ntile;
@@ -571,11 +577,22 @@ __device__ void prefix_item(const StepArgs& a, PassLds<D, MODE>& lds, int pitem)
   const int j_end = t_end / kBlockTokens;
   const int tile_rows = min(kRows, rows - tile * kRows);
 
+  // The prefix tokens row (member m, new token i) sees: those below its own
+  // position's limit L_m - n + 1 + i, at most the whole prefix (all of it
+  // when the new tokens come after the prefix).
+  auto seen = [&](int m, int i) {
+    int Lm = a.lens[first + m];
+    Lm = Lm < 0 ? 0 : (Lm > a.max_context_len ? a.max_context_len : Lm);
+    return min(plen, max(Lm - nq + 1 + i, 0));
+  };
+  int l_first = plen;  // every row of the item sees the prefix tokens below it
+  for (int m = 0; m < members; ++m) l_first = min(l_first, seen(m, 0));
   // lane row n of this tile repeats real rows past the tile's last one
   const int r = tile * kRows + (lane & 15) % tile_rows;
-  const int b = first + r / G;
+  const int m_r = r / (nq * G), i_r = (r / G) % nq;
+  const int b = first + m_r;
   WA wave(a.scale_log2);
-  wave.start(a.q + ((size_t)b * Hq + (size_t)g * G + r % G) * D, 0);
+  wave.start(a.q + (((size_t)b * nq + i_r) * Hq + (size_t)g * G + r % G) * D, plen - seen(m_r, i_r));
   const char* kpool = reinterpret_cast<const char*>(a.k) + (size_t)g * WA::kTileBytes;
   const char* vpool = reinterpret_cast<const char*>(a.v) + (size_t)g * WA::kTileBytes;
   // the prefix blocks are those of the group's first member (shared by contract)
@@ -586,10 +603,10 @@ __device__ void prefix_item(const StepArgs& a, PassLds<D, MODE>& lds, int pitem)
     const int per_slice = (j_end - j_begin + NW - 1) / NW;
     const int wj0 = min(j_end, j_begin + w * per_slice);
     const int wj1 = min(j_end, wj0 + per_slice);
-    wave.run(table_row, wj0, wj1, plen, plen, plen, kpool, vpool, block_bytes, a.num_blocks);
+    wave.run(table_row, wj0, wj1, plen, l_first, plen, kpool, vpool, block_bytes, a.num_blocks);
   } else if constexpr (MODE != kModeRegister) {  // several tiles: every block staged once through LDS for all of them
     run_staged<D, kStepBlocks, 1, NW>(wave, wave, lds.st, table_row, j_begin, j_end, j_end, 0, slice < slices, slice,
-                                  slices, plen, plen, plen, 0, 0, kpool, vpool, block_bytes, a.num_blocks);
+                                  slices, plen, l_first, plen, 0, 0, kpool, vpool, block_bytes, a.num_blocks);
   }
   wave.finish();
   publish(sh, wave, w, lane, tile_rows);
@@ -607,7 +624,7 @@ __device__ void prefix_item(const StepArgs& a, PassLds<D, MODE>& lds, int pitem)
     float acc[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) acc[e] = any_bad ? __builtin_nanf("") : combine(sh, t, ntile, slices, h, d0 + e);
-    const size_t row = (size_t)(first + rr / G) * Hq + (size_t)g * G + rr % G;
+    const size_t row = ((size_t)(first + rr / (nq * G)) * nq + (rr / G) % nq) * Hq + (size_t)g * G + rr % G;
     store_partial4(a, row * a.slots_per_row + pp, d0, D, acc, sh.mx[t][h], sh.lsum[t][h]);
   }
 }
@@ -638,7 +655,8 @@ hipError_t launch_d(const StepArgs& a, hipStream_t stream) {
   // on a group's rows exceeds one tile
   const bool groups = a.num_groups > 0;
   const bool one = a.num_query_chunks % kWaves == 1 || groups;
-  const bool several = a.num_query_chunks >= 2 || (groups && (int64_t)a.max_group_size * a.group > kRows);
+  const bool several = a.num_query_chunks >= 2 ||
+                       (groups && (int64_t)a.max_group_size * a.num_query_tokens * a.group > kRows);
   const dim3 block(kWaves * kWaveSize);
   if (a.chunks_per_group > kWideChunks)
     hipLaunchKernelGGL((partition_kernel<D, kModeWide16>), dim3(grid), dim3(waves_of(kModeWide16) * kWaveSize), 0,

@@ -313,7 +313,14 @@ def test_shared_prefix_validation():
     assert plan(max_group_size=1 << 30) == pda.pda.PDA_ERR_UNSUPPORTED
     assert plan(llama(num_q_heads=16, num_kv_heads=1), max_group_size=(1 << 28) + 2) == \
         pda.pda.PDA_ERR_UNSUPPORTED
-    assert plan(llama(num_query_tokens=2)) == pda.pda.PDA_ERR_UNSUPPORTED
+    # n new tokens per sequence: a group's members x n x G rows must fit 64
+    assert plan(llama(num_query_tokens=2)) == pda.pda.PDA_OK                        # 8 x 2 x 4 = 64
+    assert plan(llama(num_query_tokens=3)) == pda.pda.PDA_ERR_UNSUPPORTED           # 96 rows
+    assert plan(llama(num_query_tokens=4), max_group_size=4) == pda.pda.PDA_OK      # 64
+    assert plan(llama(num_query_tokens=17), max_group_size=1) == pda.pda.PDA_ERR_UNSUPPORTED  # 68
+    assert plan(llama(num_query_tokens=1 << 29), max_group_size=8) == pda.pda.PDA_ERR_SHAPE  # rows overflow
+    d = pda.pda_plan_shared_prefix(llama(num_query_tokens=2, partition_tokens=1024), G(**ok))
+    assert d["workspace_bytes"] == (256 * 2 * 32 * (1 + 4) * (128 + 2) * 4 + (4 * 256 * 8 + 3 * 1 * 8) * 4 + 256 * 4)
     assert plan(group_start=None) == pda.pda.PDA_OK  # planning reads the host bounds only
     assert plan(num_groups=0, group_start=None, group_prefix_len=None) == pda.pda.PDA_OK
     # workspace: (Pp + P) partial states per row, the work order (regular +

@@ -149,3 +149,57 @@ def test_random_groups(dev, case):
           flush=True)
     got = run(st, q, k, v, dev, tp)
     check(got, reference(st, q, k, v), f"random groups case {case}")
+
+
+@pytest.mark.parametrize("n", [2, 4, 8])
+@pytest.mark.parametrize("partition_tokens", [0, 64])
+def test_groups_with_several_new_tokens(dev, n, partition_tokens):
+    """Shared-prefix groups with n new tokens per sequence (speculative
+    decoding over parallel samples): members x n x G rows per prefix item, up
+    to 64; a member whose new tokens reach back into the prefix (its rows see
+    only the prefix tokens before their positions), a group without a
+    prefix, sequences in no group with fewer tokens than n.  Every element
+    against the oracle's multi-token attention."""
+    G, Hkv = 4, 2
+    size = 64 // (n * G)
+    groups = [
+        (256, [256 + n + 5, 300, 1000, 257, 2000, 400, 256 + n, 777][:size]),
+        (64, [64 + n - 1, 500, 65, 90, 1200, 64, 70, 80][:size]),  # the first member's new tokens start inside
+        (0, [n + 3, 40][:size]),
+    ]
+    st = W.custom_shared_structure(G * Hkv, Hkv, 128, groups, [n + 10, 1, 0], seed=40 + n)
+    _, k, v = W.fill_values(st, dev, fill="nan")
+    q = W.fill_multi_q(st, n, dev)
+    got = run(st, q, k, v, dev, partition_tokens)
+    ref = oracle.decode_multi(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table, st.context_lens,
+                              st.scale, threads=THREADS)
+    check(got, ref, f"groups with {n} new tokens, Tp={partition_tokens}")
+    assert np.array_equal(got, run(st, q, k, v, dev, partition_tokens)), "run-to-run"
+
+
+@pytest.mark.parametrize("case", range(16))
+def test_random_groups_several_new_tokens(dev, case):
+    """Random group layouts with 2 to 8 new tokens per sequence (members up to
+    64 / (n G)), new tokens sometimes reaching back into the prefix."""
+    r = np.random.default_rng(8000 + case)
+    G = int(r.choice([1, 2, 4, 8]))
+    n = int(r.choice([2, 3, 4, 8]))
+    if n * G > 64:
+        n = 64 // G
+    Hkv = int(r.choice([1, 2]))
+    D = int(r.choice([64, 128]))
+    groups = []
+    for _ in range(int(r.integers(1, 4))):
+        prefix = 16 * int(r.integers(0, 65))
+        members = int(r.integers(1, 64 // (n * G) + 1))
+        groups.append((prefix, [prefix + int(r.choice([0, 1, n - 1, n, n + 1, 17, 300, 900])) for _ in range(members)]))
+    loners = [int(r.choice([0, 1, n, 100, 1500])) for _ in range(int(r.integers(0, 3)))]
+    tp = int(r.choice([0, 0, 16, 64, 512]))
+    st = W.custom_shared_structure(G * Hkv, Hkv, D, groups, loners, seed=500 + case)
+    _, k, v = W.fill_values(st, dev, fill="nan")
+    q = W.fill_multi_q(st, n, dev)
+    print(f"case {case}: G={G} n={n} Hkv={Hkv} D={D} groups={[(p, len(m)) for p, m in groups]} Tp={tp}", flush=True)
+    got = run(st, q, k, v, dev, tp)
+    ref = oracle.decode_multi(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table, st.context_lens,
+                              st.scale, threads=THREADS)
+    check(got, ref, f"random groups, {n} new tokens, case {case}")

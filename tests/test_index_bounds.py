@@ -142,8 +142,8 @@ def check_regular_item(item, B, Hq, Hkv, D, n, mbps, mcl, lens_c, pl, seq_prefix
                 touched["out"].add(row)
     if p >= nparts_max:
         return
-    lv0 = chunk_visible(L, n, qc, chunks[0])
-    j_begin = (min(t0_all, max(lv0, 0)) + p * Tp) // BS
+    lv_last = chunk_visible(L, n, qc, chunks[-1])  # the kernel's first block: the item's last chunk's
+    j_begin = (min(t0_all, max(lv_last, 0)) + p * Tp) // BS
 
     def block_end(lv, parts):
         t0 = min(t0_all, max(lv, 0))
@@ -174,7 +174,7 @@ def check_regular_item(item, B, Hq, Hkv, D, n, mbps, mcl, lens_c, pl, seq_prefix
                 touched["slots"].add(slot)
 
 
-def check_prefix_item(pitem, B, Hq, Hkv, D, mcl, mbps, pl, groups, touched):
+def check_prefix_item(pitem, B, Hq, Hkv, D, n, mcl, mbps, lens_c, pl, groups, touched):
     Pp, Tp, G = pl["Pp"], pl["Tp"], pl["G"]
     g = pitem % Hkv
     pp = (pitem // Hkv) % Pp
@@ -187,13 +187,17 @@ def check_prefix_item(pitem, B, Hq, Hkv, D, mcl, mbps, pl, groups, touched):
     plen = 0 if plen < 0 else min(plen, groups["max_prefix"]) // BS * BS
     if members <= 0 or pp * Tp >= plen:
         return
-    rows = members * G
+    rows = members * n * G  # member-major, then the new tokens, then the G heads
     assert rows <= WAVES * MAX_GROUP
     j_begin, j_end = pp * Tp // BS, min(plen, (pp + 1) * Tp) // BS
     assert 0 <= j_begin < j_end <= mbps  # table row of the first member
+    for m in range(members):
+        assert 0 <= first + m < B  # the lengths read for the rows' limits
     for rr in range(rows):
-        row = (first + rr // G) * Hq + g * G + rr % G
-        assert 0 <= row < B * Hq
+        m, i, h = rr // (n * G), (rr // G) % n, rr % G
+        q_row = (first + m) * n + i
+        row = q_row * Hq + g * G + h
+        assert 0 <= row < B * n * Hq  # the query row read and the state written
         slot = row * pl["S"] + pp
         assert 0 <= slot < pl["slots"]
         touched["slots"].add(slot)
@@ -269,7 +273,7 @@ def run_case(rng, B, Hq, Hkv, D, n, mcl, tp, lens, mbps, groups=None):
         if item < pl["regular"]:
             check_regular_item(item, B, Hq, Hkv, D, n, mbps, mcl, lens_c, pl, seq_prefix, touched)
         else:
-            check_prefix_item(item - pl["regular"], B, Hq, Hkv, D, mcl, mbps, pl, groups, touched)
+            check_prefix_item(item - pl["regular"], B, Hq, Hkv, D, n, mcl, mbps, lens_c, pl, groups, touched)
     check_merge(B, Hq, n, mcl, lens_c, pl, seq_prefix, touched)
 
 
@@ -296,10 +300,13 @@ def test_random_descriptors():
 
 def test_shared_prefix_descriptors():
     rng = np.random.default_rng(7)
-    for _ in range(60):
+    for _ in range(100):
         G = int(rng.choice([1, 4, 8, 16]))
         Hkv = int(rng.choice([1, 2, 8]))
-        max_size = int(rng.integers(1, 64 // G + 1))
+        n = int(rng.choice([1, 1, 2, 3, 4, 8]))
+        if n * G > 64:
+            continue
+        max_size = int(rng.integers(1, 64 // (n * G) + 1))
         ngroups = int(rng.integers(1, 5))
         sizes = rng.integers(0, max_size + 1, ngroups)
         start = np.concatenate([[0], np.cumsum(sizes)]).astype(int)
@@ -309,9 +316,10 @@ def test_shared_prefix_descriptors():
         max_prefix = int(rng.choice([16, 64, 256, 512]))
         prefix = [int(rng.choice([0, 16, max_prefix, max_prefix + 16, -16])) for _ in range(ngroups)]
         lens = rng.integers(max_prefix, max_prefix + 700, B)
+        lens[rng.integers(0, B)] = max_prefix + int(rng.integers(0, n + 1))  # new tokens inside the prefix
         mcl = int(lens.max())
         groups = dict(start=start.tolist(), prefix=prefix, max_size=max_size, max_prefix=max_prefix)
-        run_case(rng, B, G * Hkv, Hkv, 128, 1, mcl, int(rng.choice([0, 64])), lens, -(-mcl // BS), groups)
+        run_case(rng, B, G * Hkv, Hkv, 128, n, mcl, int(rng.choice([0, 64])), lens, -(-mcl // BS), groups)
 
 
 @pytest.mark.parametrize("n,G,Hkv,tp", [(1, 4, 8, 0), (4, 4, 8, 0), (32, 4, 8, 0), (64, 4, 8, 3840),
