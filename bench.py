@@ -47,8 +47,9 @@ Other steps around attention (--op):
            calls issued one by one (append and attention, and the folded
            pda_decode_append): per-layer microseconds (default: tiny)
   prefix   the shared-prefix workload (32 prompts x 8 samples) with each
-           prompt's prefix attended once for its samples, against the plain
-           decode step
+           prompt's prefix attended once for its samples (--tokens n: n new
+           tokens per sequence, the prefix read once per 64 / (n G) samples),
+           against the plain step
   logprob  log-probability of each sampled token and the entropy over the
            LM-head logits of one decode step (256 rows x 128256 Llama-3
            vocabulary, bf16; --logits-f32, --config qwen_vocab, --no-entropy);
@@ -626,16 +627,17 @@ def ctypes_ref(x):
 
 
 def op_prefix(args):
-    """The shared-prefix workload with each prompt's prefix attended once
-    (pda_decode_shared_prefix), against the plain decode step on the same
-    inputs."""
+    """The shared-prefix workload with each prompt's prefix attended once per
+    row group of its samples (pda_decode_shared_prefix; one or --tokens new
+    tokens per sequence), against the plain step on the same inputs."""
     import torch
 
     import workloads as W
     from paper_2405_11143_amd import pda_decode, pda_decode_shared_prefix
 
     args.config = args.config if W.CONFIGS.get(args.config, {}).get("prompts") else "shared_prefix"
-    dev, st, q, k, v, bt, lens, plan, out, ws = setup(args, 1)
+    n = args.tokens
+    dev, st, q, k, v, bt, lens, plan, out, ws = setup(args, n)
     gs = torch.from_numpy(st.group_start).to(dev)
     gp = torch.from_numpy(st.group_prefix_len).to(dev)
     cfg = W.CONFIGS[args.config]
@@ -652,7 +654,7 @@ def op_prefix(args):
 
     from paper_2405_11143_amd import make_prefix_groups, make_problem, pda_plan_shared_prefix
     prob = make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq, st.max_context_len,
-                        args.partition_tokens)
+                        args.partition_tokens, num_query_tokens=n)
     need = pda_plan_shared_prefix(prob, make_prefix_groups(len(gp), cfg["samples"], cfg["prefix_len"]))
     ws_sp = torch.empty(max(need["workspace_bytes"], 16), dtype=torch.uint8, device=dev)
     for f in (shared, plain):
@@ -661,17 +663,23 @@ def op_prefix(args):
     torch.cuda.synchronize()
     ms = timed(shared, args.steps, stream)
     ms_plain = timed(plain, args.steps, stream)
-    alg = st.algorithmic_bytes()
+    alg = st.algorithmic_bytes(query_tokens=n)
     value = alg / (ms * 1e-3) / 1e9
-    result = base_result(args, value, "GB/s", ms, "shared-prefix decode HBM GB/s (unique bytes), "
-                         "each prompt's prefix attended once",
+    if n == 1:
+        metric, extra = "shared-prefix decode HBM GB/s (unique bytes), each prompt's prefix attended once", {}
+    else:
+        metric = (f"shared-prefix attention HBM GB/s (unique bytes), {n} new tokens per sequence, each prompt's "
+                  f"prefix attended once per {64 // (n * st.Hq // st.Hkv)} samples")
+        extra = {"query_tokens": n}
+    result = base_result(args, value, "GB/s", ms, metric,
                          config_of(st, cfg["desc"], args.config, need, prompts=cfg["prompts"], samples=cfg["samples"],
-                                   prefix_len=cfg["prefix_len"]))
+                                   prefix_len=cfg["prefix_len"], **extra))
     result.update({"seq_steps_per_s": round(st.B / (ms * 1e-3), 1), "pct_of_peak": round(100.0 * value / PEAK_GBS, 2),
                    "algorithmic_bytes_per_step": alg, "ms_per_step_plain_decode": round(ms_plain, 5),
                    "speedup_vs_plain_decode": round(ms_plain / ms, 3),
-                   "roofline": roofline(value, ms, KERNEL, args.config + "_shared"), "cpu_baseline": None})
-    if not args.no_cpu_baseline:
+                   "roofline": roofline(value, ms, KERNEL, args.config + ("_shared" if n == 1 else f"_shared_x{n}")),
+                   "cpu_baseline": None})
+    if n == 1 and not args.no_cpu_baseline:
         # the oracle computes the same attention (it reads each member's prefix itself); the rate is
         # per unique byte like the GPU's
         import oracle
@@ -771,7 +779,7 @@ def main(argv=None):
                     help="--op logprob: log-probabilities only (what a rollout records), no entropies")
     ap.add_argument("--config", default=None, help="workload (default: llama3_8b; tiny for --op graph)")
     ap.add_argument("--tokens", type=int, default=None,
-                    help="new tokens per sequence (--op multi: 4; append, graph: 1)")
+                    help="new tokens per sequence (--op multi: 4; append, graph, prefix: 1)")
     ap.add_argument("--partition-tokens", type=int, default=0,
                     help="> 0: split-K partition size in tokens (0: the library's choice)")
     ap.add_argument("--no-cpu-baseline", action="store_true")

@@ -212,7 +212,7 @@ int pda_decode_reusing_order(const pda_problem *prob, const void *q, const void 
  * bounds, never trusted for memory safety). */
 typedef struct pda_prefix_groups {
   int32_t num_groups;               /* >= 0 */
-  int32_t max_group_size;           /* bound on members per group: 1 .. 64 / (n G) */
+  int32_t max_group_size;           /* bound on members per group, >= 1 (members past it are not attended) */
   int32_t max_prefix_len;           /* bound on group_prefix_len[]: a multiple of 16, <= max_context_len */
   const int32_t *group_start;       /* device int32 [num_groups + 1], non-decreasing, within [0, num_seqs] */
   const int32_t *group_prefix_len;  /* device int32 [num_groups] */
@@ -224,13 +224,14 @@ int pda_plan_shared_prefix(const pda_problem *prob, const pda_prefix_groups *gro
 
 /* The step of pda_decode (one new token per sequence, or n = num_query_tokens
  * with q and out [B][n][Hq][D]) with each group's shared prefix attended once
- * for all its members: a work item reads the prefix blocks and computes all
- * members x n x G query rows of a KV head (at most 64: max_group_size * n *
- * G <= 64, else PDA_ERR_UNSUPPORTED) on one 16-row MFMA tile per wavefront,
- * each row seeing the prefix tokens before its own position, and every
- * member row then merges the prefix's partial softmax state with those of
- * its own tokens.  The result is the same attention as pda_decode (up to
- * rounding).  `workspace` must hold pda_plan_shared_prefix()'s
+ * per row group of its members: the members are taken 64 / (n G) at a time
+ * (16 at n = 1, G = 4), and a work item reads the prefix blocks and computes
+ * all members x n x G query rows of a KV head (at most 64) of one row group on
+ * 16-row MFMA tiles, each row seeing the prefix tokens before its own
+ * position; every member row then merges the prefix's partial softmax state
+ * with those of its own tokens.  One member's rows must fit an item: n G <= 64,
+ * else PDA_ERR_UNSUPPORTED.  The result is the same attention as pda_decode
+ * (up to rounding).  `workspace` must hold pda_plan_shared_prefix()'s
  * workspace_bytes. */
 int pda_decode_shared_prefix(const pda_problem *prob, const pda_prefix_groups *groups, const void *q,
                              const void *k_cache, const void *v_cache, const int32_t *block_table,

@@ -50,6 +50,7 @@ constexpr int64_t kRowsShareNum = 13, kRowsShareDen = 10;
 constexpr int kMinPartitionTokens = 256;
 constexpr int kPartitionQuantum = 256;
 constexpr int64_t kConcurrentItems = 768;  // 256 compute units x 3 workgroups of 4 wavefronts
+constexpr int64_t kPrefixItemRows = 64;    // query rows of one prefix item: 4 tiles of 16
 
 int query_tokens(const pda_problem* p) { return p->num_query_tokens > 0 ? p->num_query_tokens : 1; }
 
@@ -78,8 +79,10 @@ struct Plan {
   int chunks_per_group;   // 4; 8 with more than 4 chunks (two 16-row tiles per wavefront); 16 with more than 8
   int num_chunk_groups;   // ceil(chunks / chunks_per_group): chunks per work item share its tiles
   int prefix_partitions;  // Pp: partitions of the longest shared prefix (0 without groups)
+  int members_per_row_group;  // MR: members whose query rows (n G each) fill one prefix item of 64 rows
+  int prefix_row_groups;      // RG: prefix items per group, partition and KV head
   size_t regular_items;   // P * B * Hkv * chunk groups (pass-1 workgroups of the sequences' own tokens)
-  size_t items;           // regular items + num_groups * Pp * Hkv prefix items
+  size_t items;           // regular items + num_groups * Pp * RG * Hkv prefix items
   size_t slots;           // partial states: (Pp + P) per output row; 0 when nothing is split
 };
 
@@ -99,11 +102,17 @@ int check_groups(const pda_problem* p, const pda_prefix_groups* g) {
   if (g->num_groups < 0 || g->max_group_size < 1 || g->max_prefix_len < 0 ||
       g->max_prefix_len % pda::kBlockTokens != 0 || g->max_prefix_len > p->max_context_len)
     return PDA_ERR_SHAPE;
-  // a group's rows (members x new tokens x G) fit the 4 tiles of a prefix
-  // item (in 64 bits: a huge bound must not wrap past the check)
-  if ((int64_t)g->max_group_size * query_tokens(p) * (p->num_q_heads / p->num_kv_heads) > 64)
-    return PDA_ERR_UNSUPPORTED;
+  // one member's rows (new tokens x G) fit the 4 tiles of a prefix item; a
+  // group's members are split into row groups of 64 rows at most
+  if ((int64_t)query_tokens(p) * (p->num_q_heads / p->num_kv_heads) > kPrefixItemRows) return PDA_ERR_UNSUPPORTED;
   return PDA_OK;
+}
+
+// a * b for non-negative factors, saturated far above any accepted count
+int64_t mul_sat(int64_t a, int64_t b) {
+  constexpr int64_t kSat = int64_t(1) << 40;
+  if (a == 0 || b == 0) return 0;
+  return a > kSat / b ? kSat : std::min(kSat, a * b);
 }
 
 int make_plan(const pda_problem* p, const pda_prefix_groups* groups, Plan* plan) {
@@ -118,6 +127,9 @@ int make_plan(const pda_problem* p, const pda_prefix_groups* groups, Plan* plan)
                   : nqc > pda::kWaves    ? pda::kWideChunks
                                          : pda::kWaves;  // chunks per work item
   const int ncg = (nqc + cpg - 1) / cpg;
+  // the work order counts Hkv items per pair of either kind: with groups a
+  // work item holds every query chunk of a sequence (n G <= 64 means at most 7)
+  if (groups && ncg != 1) return PDA_ERR_UNSUPPORTED;
   const int64_t units = (int64_t)p->num_seqs * p->num_kv_heads * ncg;
   int tp = p->partition_tokens;
   if (tp == 0) {
@@ -149,8 +161,14 @@ int make_plan(const pda_problem* p, const pda_prefix_groups* groups, Plan* plan)
   const int64_t parts = p->max_context_len > 0 ? ((int64_t)p->max_context_len + tp - 1) / tp : 1;
   const int num_groups = groups ? groups->num_groups : 0;
   const int64_t pparts = num_groups > 0 ? ((int64_t)groups->max_prefix_len + tp - 1) / tp : 0;
-  const int64_t prefix_items = (int64_t)num_groups * pparts * p->num_kv_heads;
-  if (parts * units + prefix_items > 0x7fffffff || parts * p->num_seqs + num_groups * pparts > 0x7fffffff)
+  // members per prefix item, and prefix items per (group, partition, KV head):
+  // a group has at most min(max_group_size, B) members
+  const int mr = (int)(kPrefixItemRows / ((int64_t)n * G));
+  const int64_t group_members = groups ? std::min<int64_t>(groups->max_group_size, std::max(p->num_seqs, 1)) : 0;
+  const int64_t rgroups = num_groups > 0 ? (group_members + mr - 1) / mr : 0;
+  const int64_t prefix_pairs = mul_sat(mul_sat(num_groups, pparts), rgroups);
+  const int64_t prefix_items = mul_sat(prefix_pairs, p->num_kv_heads);
+  if (mul_sat(parts, units) + prefix_items > 0x7fffffff || mul_sat(parts, p->num_seqs) + prefix_pairs > 0x7fffffff)
     return PDA_ERR_SHAPE;
   *plan = Plan{};
   plan->info.partition_tokens = tp;
@@ -160,6 +178,8 @@ int make_plan(const pda_problem* p, const pda_prefix_groups* groups, Plan* plan)
   plan->chunks_per_group = cpg;
   plan->num_chunk_groups = ncg;
   plan->prefix_partitions = (int)pparts;
+  plan->members_per_row_group = num_groups > 0 ? mr : 0;
+  plan->prefix_row_groups = (int)rgroups;
   if (p->num_seqs > 0) {
     plan->regular_items = (size_t)(parts * units);
     plan->items = plan->regular_items + (size_t)prefix_items;
@@ -190,7 +210,10 @@ void fill_args(const pda_problem* p, const Plan* plan, void* ws, pda::StepArgs* 
   }
   args->slots_per_row = plan->prefix_partitions + plan->info.num_partitions;
   args->prefix_partitions = plan->prefix_partitions;
+  args->members_per_row_group = plan->members_per_row_group;
+  args->prefix_row_groups = plan->prefix_row_groups;
   args->num_regular_items = (int32_t)plan->regular_items;
+  args->num_prefix_items = (int32_t)(plan->items - plan->regular_items);
   args->num_seqs = p->num_seqs;
   args->num_q_heads = p->num_q_heads;
   args->num_kv_heads = p->num_kv_heads;

@@ -54,11 +54,14 @@ struct StepArgs {
   const int32_t* group_prefix_len;  // int32 [num_groups], multiples of 16
   int32_t* seq_prefix;              // int32 [B] (workspace): prefix tokens of each sequence's group
   int32_t num_groups;
-  int32_t max_group_size;           // members of one group, <= 64 / G
+  int32_t max_group_size;           // bound on the members of one group
   int32_t max_prefix_len;           // bound on group_prefix_len, multiple of 16
   int32_t prefix_partitions;        // Pp = ceil(max_prefix_len / T_p)
+  int32_t members_per_row_group;    // MR = 64 / (n G): members whose query rows fill one prefix item
+  int32_t prefix_row_groups;        // RG = ceil(min(max_group_size, B) / MR): prefix items per group and partition
   int32_t slots_per_row;            // Pp + P partial states per output row (P when no groups)
   int32_t num_regular_items;        // items below this index are (partition, sequence, KV head, chunk group)
+  int32_t num_prefix_items;         // num_groups * Pp * RG * Hkv items after them
   // The step's KV append folded into pass 1 (one new token per sequence, no
   // shared-prefix groups), or null: the item that reads position L - 1 of
   // (sequence, KV head) first stores that token's K and V rows there.

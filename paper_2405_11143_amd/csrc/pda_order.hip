@@ -12,7 +12,9 @@
 //
 // The items come in pairs of equal size: a regular pair (sequence, partition)
 // stands for its items of every KV head and group of query chunks, a prefix pair
-// (shared-prefix group, prefix partition) for its items of every KV head.
+// (shared-prefix group, prefix partition, row group of members) for its items
+// of every KV head (with groups a work item holds all query chunks of a
+// sequence, so both kinds of pairs hold Hkv items).
 // One workgroup counting-sorts the pairs by size in blocks (classes capped
 // at kOrderBuckets - 1 blocks) with LDS atomics, then writes the items of
 // each pair.  The order within a size class depends on atomic timing; no
@@ -33,9 +35,10 @@ __global__ void __launch_bounds__(kOrderThreads) order_kernel(const StepArgs a) 
   const int B = a.num_seqs;
   const int P = a.num_partitions;
   const int Pp = a.prefix_partitions;
+  const int RG = a.prefix_row_groups;
   const int Tp = a.partition_tokens;
   const int regular_pairs = B * P;
-  const int pairs = regular_pairs + a.num_groups * Pp;
+  const int pairs = regular_pairs + a.num_groups * Pp * RG;
 
   if (a.seq_prefix) {  // per-sequence prefix length (group contents clamped: device data)
     for (int b = tid; b < B; b += kOrderThreads) a.seq_prefix[b] = 0;
@@ -62,12 +65,16 @@ __global__ void __launch_bounds__(kOrderThreads) order_kernel(const StepArgs a) 
       L = L < 0 ? 0 : (L > a.max_context_len ? a.max_context_len : L);
       const int t0 = min(seq_prefix_len(a, b), L);
       tok = max(0, min(L, t0 + (p + 1) * Tp) - (t0 + p * Tp));
-    } else {
-      const int grp = (idx - regular_pairs) / Pp;
-      const int pp = (idx - regular_pairs) % Pp;
+    } else {  // prefix pair idx - regular_pairs = (grp * Pp + pp) * RG + rg
+      const int x = idx - regular_pairs;
+      const int rg = x % RG;
+      const int pp = (x / RG) % Pp;
+      const int grp = x / (RG * Pp);
+      const int first = min(max(a.group_start[grp], 0), B);
+      const int members = min(min(a.group_start[grp + 1], B) - first, a.max_group_size);
       int plen = a.group_prefix_len[grp];
       plen = plen < 0 ? 0 : (plen > a.max_prefix_len ? a.max_prefix_len : plen);
-      tok = max(0, min(plen, (pp + 1) * Tp) - pp * Tp);
+      tok = rg * a.members_per_row_group < members ? max(0, min(plen, (pp + 1) * Tp) - pp * Tp) : 0;
     }
     const int blocks = min((tok + kBlockTokens - 1) / kBlockTokens, kOrderBuckets - 1);
     return kOrderBuckets - 1 - blocks;
@@ -108,7 +115,7 @@ __global__ void __launch_bounds__(kOrderThreads) order_kernel(const StepArgs a) 
   //    starts at pair pos - r (r = pos % 8) and has c <= 8 pairs, and item x
   //    < HC of pair pos goes to slot (pos - r) HC + x c + r, so (with c = 8)
   //    every item of a pair, among them its chunk groups, runs on one XCD.
-  // Prefix pairs (which come with groups only, where HC = Hkv) are placed
+  // Prefix pairs (which come with groups only, where NCG = 1 and HC = Hkv) are placed
   // alike.  Pair idx holds items idx HC .. idx HC + HC - 1 (a regular pair
   // (p, b) has idx = p B + b, and the prefix items follow the regular ones),
   // item idx HC + g NCG + cg being KV head g, chunk group cg.

@@ -18,13 +18,14 @@
 // partition count.  With shared-prefix groups, a sequence's regular items
 // cover only the tokens after its group's prefix.
 //
-// Prefix items: (shared-prefix group, prefix partition, KV head).  All
-// members of a group read the same prefix blocks (parallel sampling, Section
-// 3.2), so the prefix is attended once for all members x new tokens x G
-// heads (up to 64 query rows; a row whose position lies inside the prefix
-// sees only the prefix tokens before it): the 4 wavefronts take 16-row tiles
-// first and slices of blocks second, as above, and every block's tiles reach
-// the compute unit once.
+// Prefix items: (shared-prefix group, prefix partition, row group, KV head).
+// All members of a group read the same prefix blocks (parallel sampling,
+// Section 3.2), so the prefix is attended once for all members x new tokens x
+// G heads of a row group (64 / (n G) members, up to 64 query rows; larger
+// groups take several row groups, each reading the prefix once; a row whose
+// position lies inside the prefix sees only the prefix tokens before it):
+// the 4 wavefronts take 16-row tiles first and slices of blocks second, as
+// above, and every block's tiles reach the compute unit once per row group.
 //
 // With one tile, each wavefront streams its run of 16-token blocks with
 // WaveAttention (pda_wave.h), tiles straight into registers.  With several
@@ -552,16 +553,21 @@ __device__ void prefix_item(const StepArgs& a, PassLds<D, MODE>& lds, int pitem)
   using WA = WaveAttention<D>;
   const int Hq = a.num_q_heads;
   const int G = a.group;
-  const int g = pitem % a.num_kv_heads;  // pitem = (group * Pp + pp) * Hkv + g
-  const int pp = (pitem / a.num_kv_heads) % a.prefix_partitions;
-  const int grp = pitem / (a.num_kv_heads * a.prefix_partitions);
+  const int g = pitem % a.num_kv_heads;  // pitem = ((group * Pp + pp) * RG + rg) * Hkv + g
+  const int RG = a.prefix_row_groups;
+  const int rg = (pitem / a.num_kv_heads) % RG;
+  const int pp = (pitem / (a.num_kv_heads * RG)) % a.prefix_partitions;
+  const int grp = pitem / (a.num_kv_heads * RG * a.prefix_partitions);
   const int tid = threadIdx.x;
   const int lane = tid & (kWaveSize - 1);
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
 
   // group contents are device data: clamp so that nothing is read or written out of bounds
-  const int first = min(max(a.group_start[grp], 0), a.num_seqs);
-  const int members = min(min(a.group_start[grp + 1], a.num_seqs) - first, a.max_group_size);
+  const int first_g = min(max(a.group_start[grp], 0), a.num_seqs);
+  const int members_g = min(min(a.group_start[grp + 1], a.num_seqs) - first_g, a.max_group_size);
+  // this item's row group: members [rg MR, rg MR + MR) of the group
+  const int first = first_g + rg * a.members_per_row_group;
+  const int members = min(a.members_per_row_group, members_g - rg * a.members_per_row_group);
   int plen = a.group_prefix_len[grp];
   plen = plen < 0 ? 0 : (plen > a.max_prefix_len ? a.max_prefix_len : plen) / kBlockTokens * kBlockTokens;
   const int Tp = a.partition_tokens;
@@ -596,7 +602,7 @@ __device__ void prefix_item(const StepArgs& a, PassLds<D, MODE>& lds, int pitem)
   const char* kpool = reinterpret_cast<const char*>(a.k) + (size_t)g * WA::kTileBytes;
   const char* vpool = reinterpret_cast<const char*>(a.v) + (size_t)g * WA::kTileBytes;
   // the prefix blocks are those of the group's first member (shared by contract)
-  const int32_t* table_row = a.table + (size_t)first * a.max_blocks_per_seq;
+  const int32_t* table_row = a.table + (size_t)first_g * a.max_blocks_per_seq;
   const size_t block_bytes = (size_t)a.num_kv_heads * WA::kTileBytes;
   if (MODE == kModeRegister && ntile != 1) return;  // not this launch's kind (never: the host picks the mode)
   if (ntile == 1) {  // one tile: the 4 wavefronts split the blocks, tiles into registers
@@ -638,7 +644,7 @@ partition_kernel(const StepArgs a) {
   __shared__ __align__(16) PassLds<D, MODE> lds;
   const int item = a.order ? a.order[blockIdx.x] : (int)blockIdx.x;  // no order: every item runs at once
   // an order reused from an earlier call is the caller's contract; never step outside the items
-  if ((unsigned)item >= (unsigned)(a.num_regular_items + a.num_groups * a.prefix_partitions * a.num_kv_heads)) return;
+  if ((unsigned)item >= (unsigned)(a.num_regular_items + a.num_prefix_items)) return;
   if (item < a.num_regular_items)
     regular_item<D, MODE>(a, lds, item);
   else
@@ -647,16 +653,16 @@ partition_kernel(const StepArgs a) {
 
 template <int D>
 hipError_t launch_d(const StepArgs& a, hipStream_t stream) {
-  const unsigned grid = (unsigned)a.num_regular_items +
-                        (unsigned)a.num_groups * (unsigned)a.prefix_partitions * (unsigned)a.num_kv_heads;
+  const unsigned grid = (unsigned)a.num_regular_items + (unsigned)a.num_prefix_items;
   // which kinds of items the step has: a regular item has one tile when its
   // chunk group holds one query chunk; a prefix item may have one tile
-  // whenever groups exist (a group can be small) and several when the bound
-  // on a group's rows exceeds one tile
+  // whenever groups exist (a row group can be small) and several when the
+  // bound on a row group's rows exceeds one tile
   const bool groups = a.num_groups > 0;
   const bool one = a.num_query_chunks % kWaves == 1 || groups;
-  const bool several = a.num_query_chunks >= 2 ||
-                       (groups && (int64_t)a.max_group_size * a.num_query_tokens * a.group > kRows);
+  const bool several =
+      a.num_query_chunks >= 2 ||
+      (groups && (int64_t)min(a.max_group_size, a.members_per_row_group) * a.num_query_tokens * a.group > kRows);
   const dim3 block(kWaves * kWaveSize);
   if (a.chunks_per_group > kWideChunks)
     hipLaunchKernelGGL((partition_kernel<D, kModeWide16>), dim3(grid), dim3(waves_of(kModeWide16) * kWaveSize), 0,

@@ -594,7 +594,8 @@ def pda_decode_shared_prefix(q, k_cache, v_cache, block_table, context_lens, sca
     """The decode step with each shared-prefix group's prefix attended once for
     all its members.  group_start int32 [num_groups + 1] and group_prefix_len
     int32 [num_groups] are device tensors; max_group_size and max_prefix_len
-    are their host bounds (max_group_size * n * G <= 64).  Other arguments
+    are their host bounds (n * G <= 64; groups larger than 64 / (n G) members
+    read the prefix once per 64 / (n G) members).  Other arguments
     as pda_decode (q [B][Hq][D], or [B][n][Hq][D] for n new tokens)."""
     import torch
 

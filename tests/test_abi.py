@@ -308,19 +308,27 @@ def test_shared_prefix_validation():
     assert plan(max_group_size=0) == pda.pda.PDA_ERR_SHAPE
     assert plan(max_prefix_len=100) == pda.pda.PDA_ERR_SHAPE        # not a multiple of 16
     assert plan(max_prefix_len=8192) == pda.pda.PDA_ERR_SHAPE       # beyond max_context_len
-    assert plan(max_group_size=17) == pda.pda.PDA_ERR_UNSUPPORTED   # 17 x G=4 > 64 rows
-    # a bound whose product with G wraps in 32 bits (2^30 x 4 = 2^32 -> 0; (2^28 + 2) x 16 -> 32)
-    assert plan(max_group_size=1 << 30) == pda.pda.PDA_ERR_UNSUPPORTED
-    assert plan(llama(num_q_heads=16, num_kv_heads=1), max_group_size=(1 << 28) + 2) == \
-        pda.pda.PDA_ERR_UNSUPPORTED
-    # n new tokens per sequence: a group's members x n x G rows must fit 64
+    # groups of more than 64 / (n G) members take several row groups
+    assert plan(max_group_size=17) == pda.pda.PDA_OK                # 17 x G=4 rows: 2 row groups of 16 members
+    # huge bounds count at most B members per group (no wrap: 2^30 x 4 = 2^32 -> 0 in 32 bits)
+    assert plan(max_group_size=1 << 30) == pda.pda.PDA_OK
+    assert plan(llama(num_q_heads=16, num_kv_heads=1), max_group_size=(1 << 28) + 2) == pda.pda.PDA_OK
+    # n new tokens per sequence: one member's n x G rows must fit the 64 of an item
     assert plan(llama(num_query_tokens=2)) == pda.pda.PDA_OK                        # 8 x 2 x 4 = 64
-    assert plan(llama(num_query_tokens=3)) == pda.pda.PDA_ERR_UNSUPPORTED           # 96 rows
-    assert plan(llama(num_query_tokens=4), max_group_size=4) == pda.pda.PDA_OK      # 64
+    assert plan(llama(num_query_tokens=3)) == pda.pda.PDA_OK                        # 5 members per row group
+    assert plan(llama(num_query_tokens=16), max_group_size=4) == pda.pda.PDA_OK     # 16 x 4 = 64
     assert plan(llama(num_query_tokens=17), max_group_size=1) == pda.pda.PDA_ERR_UNSUPPORTED  # 68
+    assert plan(llama(num_q_heads=16, num_kv_heads=1, num_query_tokens=5)) == pda.pda.PDA_ERR_UNSUPPORTED  # 80
     assert plan(llama(num_query_tokens=1 << 29), max_group_size=8) == pda.pda.PDA_ERR_SHAPE  # rows overflow
+    # items beyond int32: groups x prefix partitions x row groups x KV heads
+    big = llama(num_seqs=1 << 20, max_context_len=1 << 20, max_blocks_per_seq=1 << 16, partition_tokens=16)
+    assert plan(big, num_groups=1 << 20, max_group_size=1 << 20, max_prefix_len=1 << 20) == pda.pda.PDA_ERR_SHAPE
     d = pda.pda_plan_shared_prefix(llama(num_query_tokens=2, partition_tokens=1024), G(**ok))
     assert d["workspace_bytes"] == (256 * 2 * 32 * (1 + 4) * (128 + 2) * 4 + (4 * 256 * 8 + 3 * 1 * 8) * 4 + 256 * 4)
+    # 3 new tokens: 5 members per row group, 8 members -> 2 row groups of prefix items
+    d = pda.pda_plan_shared_prefix(llama(num_query_tokens=3, partition_tokens=1024), G(**ok))
+    assert d["workspace_bytes"] == (256 * 3 * 32 * (1 + 4) * (128 + 2) * 4 + (4 * 256 * 8 + 3 * 1 * 2 * 8) * 4
+                                    + 256 * 4)
     assert plan(group_start=None) == pda.pda.PDA_OK  # planning reads the host bounds only
     assert plan(num_groups=0, group_start=None, group_prefix_len=None) == pda.pda.PDA_OK
     # workspace: (Pp + P) partial states per row, the work order (regular +

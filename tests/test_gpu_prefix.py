@@ -67,13 +67,46 @@ def test_groups_and_loners(dev, Hq, Hkv, D, partition_tokens):
 
 @pytest.mark.parametrize("G,members", [(4, 16), (8, 8), (1, 64), (16, 4), (3, 5)])
 def test_largest_groups(dev, G, members):
-    """Groups of the largest supported size: members x G = 64 (or just below)
+    """Groups that fill one prefix item: members x G = 64 (or just below)
     query rows, i.e. 4 tiles of 16 rows in one work item."""
     r = np.random.default_rng(members)
     lens = [int(x) for x in 256 + r.integers(0, 600, members)]
     st = W.custom_shared_structure(2 * G, 2, 128, [(256, lens)], loner_lens=[300], seed=G)
     q, k, v = W.fill_values(st, dev, fill="nan")
     check(run(st, q, k, v, dev), reference(st, q, k, v), f"G={G} members={members}")
+
+
+@pytest.mark.parametrize("G,Hkv,members,n", [
+    (4, 2, 24, 1),   # 16 + 8 members
+    (8, 1, 16, 1),   # the 70B TP=8 shard's G: 8 + 8
+    (7, 4, 16, 1),   # the R1-Qwen-7B heads (28 / 4): 9 + 7
+    (1, 1, 200, 1),  # 64 + 64 + 64 + 8
+    (16, 1, 9, 1),   # 4 + 4 + 1
+    (4, 2, 8, 4),    # 4 draft tokens over 8 samples: 4 + 4
+    (3, 2, 3, 21),   # 63 rows per member, items of 6 query chunks (the wide variant): 1 + 1 + 1
+    (9, 1, 2, 7),    # 63 rows per member, 7 query chunks: 1 + 1
+    (6, 2, 4, 10),   # 60 rows per member: 1 + 1 + 1 + 1
+], ids=str)
+def test_groups_beyond_one_item(dev, G, Hkv, members, n):
+    """Groups whose rows exceed the 64 of one prefix item: the members are
+    taken 64 / (n G) at a time, each row group reading the prefix once.  One
+    member's new tokens start inside the prefix; sequences in no group; every
+    element against the oracle, and bitwise run to run."""
+    r = np.random.default_rng(members * 31 + G)
+    lens = [256 + n + int(x) for x in r.integers(0, 700, members)]
+    lens[members // 2] = 256 + max(n - 2, 0)  # new tokens reaching back into the prefix (n > 2)
+    groups = [(256, lens), (32, [40, 32 + n][:max(1, members // 4)])]
+    st = W.custom_shared_structure(G * Hkv, Hkv, 128, groups, loner_lens=[n + 5, 0], seed=G + members)
+    q, k, v = W.fill_values(st, dev, fill="nan")
+    if n > 1:
+        q = W.fill_multi_q(st, n, dev)
+    got = run(st, q, k, v, dev)
+    ref = oracle.decode_multi(W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v), st.block_table, st.context_lens,
+                              st.scale, threads=THREADS) if n > 1 else reference(st, q, k, v)
+    check(got, ref, f"G={G} Hkv={Hkv} members={members} n={n}")
+    assert np.array_equal(got, run(st, q, k, v, dev)), "run-to-run"
+    # a host bound above the contents: more (empty) row groups, same result
+    np.testing.assert_allclose(run(st, q, k, v, dev, max_group_size=4 * members), got, rtol=0, atol=1e-5)
 
 
 def test_bitwise_run_to_run_and_shuffle(dev):
@@ -119,17 +152,18 @@ def test_shared_prefix_config_full_size(dev):
 
 
 def draw_groups(case: int):
-    """Seeded random shared-prefix descriptors: 1-4 groups of 1 to 64/G
-    members with prefixes of 0 to 2048 tokens (whole blocks), members'
-    own tokens 0 to 1500 after it, and 0-3 sequences in no group."""
+    """Seeded random shared-prefix descriptors: 1-4 groups of 1 to 3 x 64/G
+    members (up to three row groups) with prefixes of 0 to 2048 tokens (whole
+    blocks), members' own tokens 0 to 1500 after it, and 0-3 sequences in no
+    group."""
     r = np.random.default_rng(7000 + case)
-    G = int(r.choice([1, 2, 4, 5, 8, 16]))
+    G = int(r.choice([1, 2, 4, 5, 7, 8, 16]))
     Hkv = int(r.choice([1, 2]))
     D = int(r.choice([64, 128]))
     groups = []
     for _ in range(int(r.integers(1, 5))):
         prefix = 16 * int(r.integers(0, 129))
-        members = int(r.integers(1, 64 // G + 1))
+        members = int(r.integers(1, 3 * (64 // G) + 1))
         groups.append((prefix, [prefix + int(r.choice([0, 1, 15, 16, 17, 300, 1500])) for _ in range(members)]))
     loners = [int(r.choice([0, 1, 100, 2000])) for _ in range(int(r.integers(0, 4)))]
     tp = int(r.choice([0, 0, 16, 64, 512]))
@@ -138,7 +172,7 @@ def draw_groups(case: int):
 
 @pytest.mark.parametrize("case", range(24))
 def test_random_groups(dev, case):
-    """Random group layouts (sizes up to the 64-row bound of a prefix item,
+    """Random group layouts (sizes up to three prefix items of 64 rows,
     prefixes from none to several partitions, empty suffixes, sequences in no
     group, forced partition sizes): every element against the plain decode
     definition."""
@@ -179,11 +213,12 @@ def test_groups_with_several_new_tokens(dev, n, partition_tokens):
 
 @pytest.mark.parametrize("case", range(16))
 def test_random_groups_several_new_tokens(dev, case):
-    """Random group layouts with 2 to 8 new tokens per sequence (members up to
-    64 / (n G)), new tokens sometimes reaching back into the prefix."""
+    """Random group layouts with 2 to 21 new tokens per sequence (members up
+    to 2 x 64 / (n G) + 1: one to three row groups), new tokens sometimes
+    reaching back into the prefix."""
     r = np.random.default_rng(8000 + case)
-    G = int(r.choice([1, 2, 4, 8]))
-    n = int(r.choice([2, 3, 4, 8]))
+    G = int(r.choice([1, 2, 3, 4, 6, 7, 8, 9]))
+    n = int(r.choice([2, 3, 4, 7, 8, 10, 21]))
     if n * G > 64:
         n = 64 // G
     Hkv = int(r.choice([1, 2]))
@@ -191,7 +226,7 @@ def test_random_groups_several_new_tokens(dev, case):
     groups = []
     for _ in range(int(r.integers(1, 4))):
         prefix = 16 * int(r.integers(0, 65))
-        members = int(r.integers(1, 64 // (n * G) + 1))
+        members = int(r.integers(1, 2 * (64 // (n * G)) + 2))
         groups.append((prefix, [prefix + int(r.choice([0, 1, n - 1, n, n + 1, 17, 300, 900])) for _ in range(members)]))
     loners = [int(r.choice([0, 1, n, 100, 1500])) for _ in range(int(r.integers(0, 3)))]
     tp = int(r.choice([0, 0, 16, 64, 512]))

@@ -40,15 +40,19 @@ def plan_of(B, Hq, Hkv, D, mbps, mcl, tp, n, groups=None):
     P = info["num_partitions"]
     Tp = info["partition_tokens"]
     Pp = -(-groups["max_prefix"] // Tp) if groups else 0
+    MR = 64 // (n * G) if groups else 0  # members per row group (prefix item)
+    RG = -(-min(groups["max_size"], B) // MR) if groups and len(groups["prefix"]) else 0
     regular = P * B * Hkv * ncg
-    items = regular + (len(groups["prefix"]) * Pp * Hkv if groups else 0)
+    if groups:
+        assert ncg == 1  # with groups both kinds of work-order pairs hold Hkv items
+    items = regular + (len(groups["prefix"]) * Pp * RG * Hkv if groups else 0)
     split = P > 1 or groups is not None
     S = Pp + P
     slots = B * n * Hq * S if split else 0
     ws = slots * (D + 2) * 4 + items * 4 + (B * 4 if groups else 0)
     assert info["workspace_bytes"] == ws, (info, ws)  # the carving below matches the library's size
-    return dict(G=G, qc=qc, nqc=nqc, cpg=cpg, ncg=ncg, P=P, Tp=Tp, Pp=Pp, regular=regular, items=items, S=S,
-                slots=slots, split=split, ws=ws)
+    return dict(G=G, qc=qc, nqc=nqc, cpg=cpg, ncg=ncg, P=P, Tp=Tp, Pp=Pp, MR=MR, RG=RG, regular=regular, items=items,
+                S=S, slots=slots, split=split, ws=ws)
 
 
 def chunk_visible(L, n, qc, c):
@@ -57,13 +61,13 @@ def chunk_visible(L, n, qc, c):
     return L - n + i0 + nv
 
 
-def model_order(B, Hkv, lens_c, mcl, pl, seq_prefix=None, prefix_lens=None):
+def model_order(B, Hkv, lens_c, mcl, pl, seq_prefix=None, groups=None):
     """The work-order kernel's writes: returns the order array (every slot
     written once, every value an item index)."""
-    P, Tp, Pp, HC = pl["P"], pl["Tp"], pl["Pp"], Hkv * pl["ncg"]
+    P, Tp, Pp, RG, HC = pl["P"], pl["Tp"], pl["Pp"], pl["RG"], Hkv * pl["ncg"]
     regular_pairs = B * P
-    ngroups = len(prefix_lens) if prefix_lens is not None else 0
-    pairs = regular_pairs + ngroups * Pp
+    ngroups = len(groups["prefix"]) if groups else 0
+    pairs = regular_pairs + ngroups * Pp * RG
     order = np.full(pairs * HC, -1, dtype=np.int64)
 
     def bucket(idx):
@@ -72,10 +76,14 @@ def model_order(B, Hkv, lens_c, mcl, pl, seq_prefix=None, prefix_lens=None):
             L = lens_c[b]
             t0 = min(seq_prefix[b] if seq_prefix is not None else 0, L)
             tok = max(0, min(L, t0 + (p + 1) * Tp) - (t0 + p * Tp))
-        else:
-            grp, pp = (idx - regular_pairs) // Pp, (idx - regular_pairs) % Pp
-            plen = min(max(prefix_lens[grp], 0), mcl)
-            tok = max(0, min(plen, (pp + 1) * Tp) - pp * Tp)
+        else:  # (grp * Pp + pp) * RG + rg
+            x = idx - regular_pairs
+            rg, pp, grp = x % RG, (x // RG) % Pp, x // (RG * Pp)
+            assert 0 <= grp < ngroups
+            first = min(max(groups["start"][grp], 0), B)
+            members = min(min(groups["start"][grp + 1], B) - first, groups["max_size"])
+            plen = min(max(groups["prefix"][grp], 0), groups["max_prefix"])
+            tok = max(0, min(plen, (pp + 1) * Tp) - pp * Tp) if rg * pl["MR"] < members else 0
         return ORDER_BUCKETS - 1 - min(-(-tok // BS), ORDER_BUCKETS - 1)
 
     classes = [bucket(i) for i in range(pairs)]
@@ -175,14 +183,17 @@ def check_regular_item(item, B, Hq, Hkv, D, n, mbps, mcl, lens_c, pl, seq_prefix
 
 
 def check_prefix_item(pitem, B, Hq, Hkv, D, n, mcl, mbps, lens_c, pl, groups, touched):
-    Pp, Tp, G = pl["Pp"], pl["Tp"], pl["G"]
+    Pp, Tp, G, RG, MR = pl["Pp"], pl["Tp"], pl["G"], pl["RG"], pl["MR"]
     g = pitem % Hkv
-    pp = (pitem // Hkv) % Pp
-    grp = pitem // (Hkv * Pp)
+    rg = (pitem // Hkv) % RG
+    pp = (pitem // (Hkv * RG)) % Pp
+    grp = pitem // (Hkv * RG * Pp)
     starts = groups["start"]
     assert 0 <= grp < len(groups["prefix"])
-    first = min(max(starts[grp], 0), B)
-    members = min(min(starts[grp + 1], B) - first, groups["max_size"])
+    first_g = min(max(starts[grp], 0), B)
+    members_g = min(min(starts[grp + 1], B) - first_g, groups["max_size"])
+    first = first_g + rg * MR
+    members = min(MR, members_g - rg * MR)
     plen = groups["prefix"][grp]
     plen = 0 if plen < 0 else min(plen, groups["max_prefix"]) // BS * BS
     if members <= 0 or pp * Tp >= plen:
@@ -190,7 +201,7 @@ def check_prefix_item(pitem, B, Hq, Hkv, D, n, mcl, mbps, lens_c, pl, groups, to
     rows = members * n * G  # member-major, then the new tokens, then the G heads
     assert rows <= WAVES * MAX_GROUP
     j_begin, j_end = pp * Tp // BS, min(plen, (pp + 1) * Tp) // BS
-    assert 0 <= j_begin < j_end <= mbps  # table row of the first member
+    assert 0 <= first_g < B and 0 <= j_begin < j_end <= mbps  # table row of the group's first member
     for m in range(members):
         assert 0 <= first + m < B  # the lengths read for the rows' limits
     for rr in range(rows):
@@ -265,7 +276,7 @@ def run_case(rng, B, Hq, Hkv, D, n, mcl, tp, lens, mbps, groups=None):
             plen = 0 if plen < 0 else min(plen, groups["max_prefix"]) // BS * BS
             for b in range(first, last):
                 seq_prefix[b] = plen
-    order = model_order(B, Hkv, lens_c, mcl, pl, seq_prefix, groups["prefix"] if groups else None)
+    order = model_order(B, Hkv, lens_c, mcl, pl, seq_prefix, groups)
     assert len(order) == pl["items"]
     assert pl["slots"] * (D + 2) * 4 + len(order) * 4 <= pl["ws"]  # states, then the order (then prefixes)
     touched = {"out": set(), "slots": set()}
@@ -300,13 +311,14 @@ def test_random_descriptors():
 
 def test_shared_prefix_descriptors():
     rng = np.random.default_rng(7)
-    for _ in range(100):
-        G = int(rng.choice([1, 4, 8, 16]))
+    for _ in range(160):
+        G = int(rng.choice([1, 3, 4, 6, 8, 9, 16]))
         Hkv = int(rng.choice([1, 2, 8]))
-        n = int(rng.choice([1, 1, 2, 3, 4, 8]))
+        n = int(rng.choice([1, 1, 2, 3, 4, 7, 8, 10, 21]))
         if n * G > 64:
             continue
-        max_size = int(rng.integers(1, 64 // (n * G) + 1))
+        # up to a few row groups of 64 / (n G) members
+        max_size = int(rng.integers(1, 3 * (64 // (n * G)) + 2))
         ngroups = int(rng.integers(1, 5))
         sizes = rng.integers(0, max_size + 1, ngroups)
         start = np.concatenate([[0], np.cumsum(sizes)]).astype(int)
