@@ -74,7 +74,7 @@ __global__ void __launch_bounds__(kOrderThreads) order_kernel(const StepArgs a) 
       const int members = min(min(a.group_start[grp + 1], B) - first, a.max_group_size);
       int plen = a.group_prefix_len[grp];
       plen = plen < 0 ? 0 : (plen > a.max_prefix_len ? a.max_prefix_len : plen);
-      tok = rg * a.members_per_row_group < members ? max(0, min(plen, (pp + 1) * Tp) - pp * Tp) : 0;
+      tok = (int64_t)rg * a.members_per_row_group < members ? max(0, min(plen, (pp + 1) * Tp) - pp * Tp) : 0;
     }
     const int blocks = min((tok + kBlockTokens - 1) / kBlockTokens, kOrderBuckets - 1);
     return kOrderBuckets - 1 - blocks;

@@ -565,9 +565,11 @@ __device__ void prefix_item(const StepArgs& a, PassLds<D, MODE>& lds, int pitem)
   // group contents are device data: clamp so that nothing is read or written out of bounds
   const int first_g = min(max(a.group_start[grp], 0), a.num_seqs);
   const int members_g = min(min(a.group_start[grp + 1], a.num_seqs) - first_g, a.max_group_size);
-  // this item's row group: members [rg MR, rg MR + MR) of the group
-  const int first = first_g + rg * a.members_per_row_group;
-  const int members = min(a.members_per_row_group, members_g - rg * a.members_per_row_group);
+  // this item's row group: members [rg MR, rg MR + MR) of the group (in 64
+  // bits: RG MR may pass B by up to MR - 1)
+  const int64_t m0 = (int64_t)rg * a.members_per_row_group;
+  const int members = (int)min((int64_t)a.members_per_row_group, (int64_t)members_g - m0);
+  const int first = members > 0 ? first_g + (int)m0 : first_g;
   int plen = a.group_prefix_len[grp];
   plen = plen < 0 ? 0 : (plen > a.max_prefix_len ? a.max_prefix_len : plen) / kBlockTokens * kBlockTokens;
   const int Tp = a.partition_tokens;
