@@ -87,7 +87,8 @@ enum pda_status {
   PDA_OK = 0,
   PDA_ERR_NULL = 1,        /* a required pointer is NULL */
   PDA_ERR_SHAPE = 2,       /* a size is negative, zero where it must not be, too large, or inconsistent */
-  PDA_ERR_UNSUPPORTED = 3, /* valid but not built: head_dim not 64/128, block_size not 16, G > 16 */
+  PDA_ERR_UNSUPPORTED = 3, /* valid but not built: head_dim not 64/128, block_size not 16, G > 16;
+                              shared-prefix groups with n G > 64; pda_decode_append with n > 1 */
   PDA_ERR_WORKSPACE = 4,   /* workspace NULL or smaller than pda_workspace_bytes() */
   PDA_ERR_ALIGNMENT = 5,   /* q, k_cache, v_cache, k_new, v_new, out or workspace not 16-byte aligned */
   PDA_ERR_VALUE = 6,       /* non-finite scale, or a host-side content check failed */

@@ -686,10 +686,13 @@ const char* pda_status_string(int status) {
     case PDA_OK: return "PDA_OK: success";
     case PDA_ERR_NULL: return "PDA_ERR_NULL: a required pointer is NULL";
     case PDA_ERR_SHAPE: return "PDA_ERR_SHAPE: sizes out of range or inconsistent";
-    case PDA_ERR_UNSUPPORTED: return "PDA_ERR_UNSUPPORTED: head_dim must be 64 or 128, block_size 16, Hq/Hkv <= 16";
+    case PDA_ERR_UNSUPPORTED:
+      return "PDA_ERR_UNSUPPORTED: head_dim must be 64 or 128, block_size 16, Hq/Hkv <= 16 (shared-prefix "
+             "groups: n Hq/Hkv <= 64; pda_decode_append: one new token; logits bf16 or fp32)";
     case PDA_ERR_WORKSPACE: return "PDA_ERR_WORKSPACE: workspace missing or smaller than pda_workspace_bytes()";
     case PDA_ERR_ALIGNMENT:
-      return "PDA_ERR_ALIGNMENT: q/k_cache/v_cache/k_new/v_new/workspace need 16-byte alignment, out 4-byte";
+      return "PDA_ERR_ALIGNMENT: q/k_cache/v_cache/k_new/v_new/out/workspace/logits need 16-byte alignment "
+             "(log-prob outputs 4-byte)";
     case PDA_ERR_VALUE: return "PDA_ERR_VALUE: non-finite scale or invalid device contents";
     case PDA_ERR_HIP: return "PDA_ERR_HIP: a HIP launch, graph capture or instantiation failed";
     case PDA_ERR_SCRATCH:
