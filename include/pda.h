@@ -213,7 +213,8 @@ int pda_decode_reusing_order(const pda_problem *prob, const void *q, const void 
  * bounds, never trusted for memory safety). */
 typedef struct pda_prefix_groups {
   int32_t num_groups;               /* >= 0 */
-  int32_t max_group_size;           /* bound on members per group, >= 1 (members past it are not attended) */
+  int32_t max_group_size;           /* bound on members per group, >= 1 (members past it attend as sequences
+                                       in no group: the whole context through their own work items) */
   int32_t max_prefix_len;           /* bound on group_prefix_len[]: a multiple of 16, <= max_context_len */
   const int32_t *group_start;       /* device int32 [num_groups + 1], non-decreasing, within [0, num_seqs] */
   const int32_t *group_prefix_len;  /* device int32 [num_groups] */

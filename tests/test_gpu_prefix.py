@@ -131,6 +131,16 @@ def test_host_bounds_above_contents(dev):
     np.testing.assert_allclose(a, b, rtol=0, atol=1e-5)
 
 
+def test_members_past_the_host_bound(dev):
+    """A group with more members than max_group_size: the members past the
+    bound attend as sequences in no group (their own items cover the whole
+    context), so the step still equals the plain decode step."""
+    st = W.custom_shared_structure(32, 8, 128, [(512, [600, 700, 512, 900, 1300, 520, 800, 640, 2000, 515])],
+                                   loner_lens=[77], seed=9)
+    q, k, v = W.fill_values(st, dev, fill="nan")
+    check(run(st, q, k, v, dev, max_group_size=4), reference(st, q, k, v), "10 members, max_group_size 4")
+
+
 def test_shared_prefix_config_full_size(dev):
     """The 32 prompts x 8 samples workload at full size, in the launch
     configuration the benchmark times: sampled rows first, then every one of
