@@ -161,6 +161,27 @@ def test_shared_prefix_config_full_size(dev):
     check(got, ref, "shared_prefix every element", f"B*Hq*D = {st.B}*{st.Hq}*{st.D}")
 
 
+def test_shared_prefix_config_full_size_four_tokens(dev):
+    """The 32 prompts x 8 samples workload with 4 new tokens per sequence,
+    as `bench.py --op prefix --tokens 4` times it (two row groups of 4
+    samples per prompt): every one of the B*n*Hq*D output elements against
+    the oracle's multi-token attention."""
+    n = 4
+    st = W.make_structure("shared_prefix")
+    prob = make_problem(st.B, st.Hq, st.Hkv, st.D, st.num_blocks, st.max_blocks_per_seq, st.max_context_len,
+                        num_query_tokens=n)
+    plan = pda_plan_shared_prefix(prob, make_prefix_groups(len(st.group_prefix_len), 8, 1024))
+    print(f"shared_prefix x {n} tokens plan: {plan}", flush=True)
+    _, k, v = W.fill_values(st, dev, fill="nan")
+    q = W.fill_multi_q(st, n, dev)
+    got = run(st, q, k, v, dev, max_group_size=8, max_prefix_len=1024)
+    assert np.isfinite(got).all()
+    qb, kb, vb = W.bf16_bits(q), W.bf16_bits(k), W.bf16_bits(v)
+    del k, v
+    ref = oracle.decode_multi(qb, kb, vb, st.block_table, st.context_lens, st.scale, threads=THREADS)
+    check(got, ref, f"shared_prefix {n} new tokens, every element", f"B*n*Hq*D = {st.B}*{n}*{st.Hq}*{st.D}")
+
+
 def draw_groups(case: int):
     """Seeded random shared-prefix descriptors: 1-4 groups of 1 to 3 x 64/G
     members (up to three row groups) with prefixes of 0 to 2048 tokens (whole
