@@ -15,6 +15,9 @@
  * each) against the oracle's multi-token attention, and token
  * log-probabilities and entropies of seeded bf16 logits (a small batch,
  * rows split over workgroups through the workspace) against the oracle's.
+ * Last, a shared-prefix group of 20 samples (more than one prefix item's
+ * members) with one and with three new tokens per sequence, against the
+ * oracle's plain attention over the same block tables.
  * Exit status 0 means every check passed.
  */
 #include <math.h>
@@ -282,6 +285,92 @@ int main(void) {
     expect(within(ent, ref_ent, R, 1e-4, 1e-4, "entropies"), "entropies match the oracle");
     hipFree(dlg); hipFree(dtok); hipFree(dlp); hipFree(dent); hipFree(ws);
     free(lg);
+  }
+
+  /* shared-prefix groups (parallel sampling): 20 samples of one prompt whose
+     block tables start with the same 4 prefix blocks (64 tokens), one sample
+     with no tokens of its own, two sequences in no group.  The prefix is
+     attended once per row group: 16 samples at one new token (G = 4), 5 at
+     three.  Expected: the oracle's plain attention over the same tables. */
+  {
+    enum { M = 20, LONERS = 2, B2 = M + LONERS, PL = 64, PB = PL / BS };
+    int32_t lens2[B2];
+    for (int b = 0; b < B2; ++b) lens2[b] = b < M ? PL + 1 + (int)(next_u64() % 300) : 50 + 200 * (b - M);
+    lens2[3] = PL; /* its last token (the new one, or the three new ones) lies in the prefix */
+    int ml = 0, used2 = PB;
+    for (int b = 0; b < B2; ++b) {
+      if (lens2[b] > ml) ml = lens2[b];
+      used2 += (lens2[b] + BS - 1) / BS - (b < M ? PB : 0);
+    }
+    const int MB2 = (ml + BS - 1) / BS, NB2 = used2 + 7;
+    int32_t *perm2 = malloc(sizeof(int32_t) * NB2);
+    for (int i = 0; i < NB2; ++i) perm2[i] = i;
+    for (int i = NB2 - 1; i > 0; --i) {
+      int j = (int)(next_u64() % (uint64_t)(i + 1));
+      int32_t t = perm2[i]; perm2[i] = perm2[j]; perm2[j] = t;
+    }
+    int32_t *bt2 = malloc(sizeof(int32_t) * B2 * MB2);
+    int nxt = PB; /* perm2[0 .. PB-1] are the prefix blocks */
+    for (int b = 0; b < B2; ++b)
+      for (int j = 0; j < MB2; ++j)
+        bt2[b * MB2 + j] = j >= (lens2[b] + BS - 1) / BS ? -1 : (b < M && j < PB) ? perm2[j] : perm2[nxt++];
+    const size_t nkv2 = (size_t)NB2 * HKV * BS * D;
+    uint16_t *k2 = malloc(nkv2 * 2), *v2 = malloc(nkv2 * 2);
+    for (size_t i = 0; i < nkv2; ++i) { k2[i] = 0x7fc0u; v2[i] = 0x7fc0u; } /* unused blocks: NaN */
+    for (int i = 0; i < nxt; ++i) /* every slot of a used block, so shared slots hold one value */
+      for (size_t e = 0; e < (size_t)HKV * BS * D; ++e) {
+        k2[(size_t)perm2[i] * HKV * BS * D + e] = to_bf16(normalish());
+        v2[(size_t)perm2[i] * HKV * BS * D + e] = to_bf16(normalish());
+      }
+    const int32_t gstart[2] = {0, M}, gprefix[1] = {PL};
+    void *dk2, *dv2, *dbt2, *dlens2, *dgs, *dgp;
+    CHECK_HIP(hipMalloc(&dk2, nkv2 * 2));
+    CHECK_HIP(hipMalloc(&dv2, nkv2 * 2));
+    CHECK_HIP(hipMalloc(&dbt2, sizeof(int32_t) * B2 * MB2));
+    CHECK_HIP(hipMalloc(&dlens2, sizeof(lens2)));
+    CHECK_HIP(hipMalloc(&dgs, sizeof(gstart)));
+    CHECK_HIP(hipMalloc(&dgp, sizeof(gprefix)));
+    CHECK_HIP(hipMemcpy(dk2, k2, nkv2 * 2, hipMemcpyHostToDevice));
+    CHECK_HIP(hipMemcpy(dv2, v2, nkv2 * 2, hipMemcpyHostToDevice));
+    CHECK_HIP(hipMemcpy(dbt2, bt2, sizeof(int32_t) * B2 * MB2, hipMemcpyHostToDevice));
+    CHECK_HIP(hipMemcpy(dlens2, lens2, sizeof(lens2), hipMemcpyHostToDevice));
+    CHECK_HIP(hipMemcpy(dgs, gstart, sizeof(gstart), hipMemcpyHostToDevice));
+    CHECK_HIP(hipMemcpy(dgp, gprefix, sizeof(gprefix), hipMemcpyHostToDevice));
+    const pda_prefix_groups groups = {1, M, PL, (const int32_t *)dgs, (const int32_t *)dgp};
+    for (int n = 1; n <= 3; n += 2) {
+      const size_t nq2 = (size_t)B2 * n * HQ * D;
+      uint16_t *q2 = malloc(nq2 * 2);
+      for (size_t i = 0; i < nq2; ++i) q2[i] = to_bf16(normalish());
+      double *ref2 = malloc(sizeof(double) * nq2);
+      expect(pda_oracle_decode_multi(B2, HQ, HKV, D, BS, NB2, MB2, q2, k2, v2, bt2, lens2, scale, n, ref2, 1) == 0,
+             "oracle (shared prefix)");
+      void *dq2, *dout3;
+      CHECK_HIP(hipMalloc(&dq2, nq2 * 2));
+      CHECK_HIP(hipMalloc(&dout3, sizeof(float) * nq2));
+      CHECK_HIP(hipMemcpy(dq2, q2, nq2 * 2, hipMemcpyHostToDevice));
+      pda_problem prob = {B2, HQ, HKV, D, BS, NB2, MB2, ml, 0, n};
+      pda_plan_info plan;
+      expect(pda_plan_shared_prefix(&prob, &groups, &plan) == PDA_OK, "pda_plan_shared_prefix");
+      void *ws;
+      CHECK_HIP(hipMalloc(&ws, plan.workspace_bytes));
+      expect(pda_decode_shared_prefix(&prob, &groups, dq2, dk2, dv2, (const int32_t *)dbt2, (const int32_t *)dlens2,
+                                      (float)scale, (float *)dout3, ws, plan.workspace_bytes, stream) == PDA_OK,
+             "pda_decode_shared_prefix");
+      CHECK_HIP(hipStreamSynchronize(stream));
+      float *out3 = malloc(sizeof(float) * nq2);
+      CHECK_HIP(hipMemcpy(out3, dout3, sizeof(float) * nq2, hipMemcpyDeviceToHost));
+      expect(within(out3, ref2, nq2, 8e-3, 1e-3, n == 1 ? "shared prefix, 20 samples" : "shared prefix, 3 new tokens"),
+             "shared-prefix step matches the oracle");
+      expect(pda_decode_shared_prefix(&prob, &groups, dq2, dk2, dv2, (const int32_t *)dbt2, (const int32_t *)dlens2,
+                                      (float)scale, (float *)dout3, ws, plan.workspace_bytes - 1, stream) ==
+                 PDA_ERR_WORKSPACE,
+             "short workspace -> PDA_ERR_WORKSPACE");
+      CHECK_HIP(hipFree(ws));
+      hipFree(dq2); hipFree(dout3);
+      free(q2); free(ref2); free(out3);
+    }
+    hipFree(dk2); hipFree(dv2); hipFree(dbt2); hipFree(dlens2); hipFree(dgs); hipFree(dgp);
+    free(perm2); free(bt2); free(k2); free(v2);
   }
 
   CHECK_HIP(hipStreamDestroy(stream));
