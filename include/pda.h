@@ -201,6 +201,17 @@ int pda_decode_reusing_order(const pda_problem *prob, const void *q, const void 
                              const int32_t *context_lens, float scale, float *out,
                              void *workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* Pass 1 alone with the order already in `workspace` (pda_partition_attention
+ * without its work-order kernel; the order's contract is that of
+ * pda_decode_reusing_order): a caller that keeps the partial states before
+ * merging them -- e.g. to combine them with states computed elsewhere -- or
+ * that times the attention kernel by itself.  pda_merge_partitions completes
+ * the step. */
+int pda_partition_attention_reusing_order(const pda_problem *prob, const void *q, const void *k_cache,
+                                          const void *v_cache, const int32_t *block_table,
+                                          const int32_t *context_lens, float scale, float *out,
+                                          void *workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Shared-prefix groups for parallel sampling (Section 3.2: PagedAttention
  * lets the samples of one prompt share the prompt's KV blocks).  The members
  * of group i are the sequences [group_start[i], group_start[i+1]) -- a

@@ -427,6 +427,19 @@ int pda_decode_reusing_order(const pda_problem* prob, const void* q, const void*
   return PDA_OK;
 }
 
+int pda_partition_attention_reusing_order(const pda_problem* prob, const void* q, const void* k_cache,
+                                          const void* v_cache, const int32_t* block_table,
+                                          const int32_t* context_lens, float scale, float* out, void* workspace,
+                                          size_t workspace_bytes, hipStream_t stream) {
+  Plan plan;
+  pda::StepArgs args;
+  int rc = prepare_step(prob, nullptr, q, k_cache, v_cache, block_table, context_lens, scale, out, workspace,
+                        workspace_bytes, &plan, &args);
+  if (rc != PDA_OK) return rc;
+  if (prob->num_seqs == 0) return PDA_OK;
+  return pda::launch_partition(args, prob->head_dim, stream) == hipSuccess ? PDA_OK : PDA_ERR_HIP;
+}
+
 int pda_merge_partitions(const pda_problem* prob, const int32_t* context_lens, float* out, const void* workspace,
                          size_t workspace_bytes, hipStream_t stream) {
   int rc = check_problem(prob);

@@ -26,7 +26,8 @@ EXPORTED = ("pda_plan", "pda_workspace_bytes", "pda_decode", "pda_partition_atte
             "pda_merge_partitions", "pda_plan_shared_prefix", "pda_decode_shared_prefix", "pda_append_kv",
             "pda_step_graph_create", "pda_step_graph_launch", "pda_step_graph_destroy", "pda_token_logprobs",
             "pda_logprob_workspace_bytes",
-            "pda_validate_host", "pda_work_order", "pda_decode_reusing_order", "pda_decode_noalloc",
+            "pda_validate_host", "pda_work_order", "pda_decode_reusing_order",
+            "pda_partition_attention_reusing_order", "pda_decode_noalloc",
             "pda_gather_ceiling", "pda_stream_ceiling", "pda_model_step_graph_create", "pda_decode_append",
             "pda_status_string")
 PDA_DTYPE_BF16, PDA_DTYPE_F32 = 0, 1
@@ -83,6 +84,7 @@ def load_library(path: str = LIB_PATH):
     lib.pda_decode.argtypes = step
     lib.pda_partition_attention.argtypes = step
     lib.pda_decode_reusing_order.argtypes = step
+    lib.pda_partition_attention_reusing_order.argtypes = step
     lib.pda_decode_noalloc.argtypes = [P, vp, vp, vp, vp, vp, ctypes.c_float, vp, vp]
     lib.pda_gather_ceiling.argtypes = [i32, i32, i32, vp, vp, vp, i32, i32, vp, vp]
     lib.pda_stream_ceiling.argtypes = [vp, sz, i32, vp, vp]
@@ -316,7 +318,8 @@ def bind_decode(q, k_cache, v_cache, block_table, context_lens, scale: float, ou
                 partition_tokens: int = 0, workspace=None, stream=None, pass1_only: bool = False,
                 reuse_order: bool = False) -> BoundCall:
     """pda_decode (or, with pass1_only, pda_partition_attention; with
-    reuse_order, pda_decode_reusing_order) bound to these tensors and the
+    reuse_order, pda_decode_reusing_order; with both,
+    pda_partition_attention_reusing_order) bound to these tensors and the
     given (else the current) stream; call it to run a step.  The arguments
     are those of pda_decode."""
     import torch
@@ -330,7 +333,9 @@ def bind_decode(q, k_cache, v_cache, block_table, context_lens, scale: float, ou
             context_lens.data_ptr(), ctypes.c_float(scale), out.data_ptr(), ws_ptr, ws_bytes,
             _stream_handle(stream, q.device))
     keep = (prob, q, k_cache, v_cache, block_table, context_lens, out, workspace)
-    name = "pda_partition_attention" if pass1_only else "pda_decode_reusing_order" if reuse_order else "pda_decode"
+    name = {(False, False): "pda_decode", (True, False): "pda_partition_attention",
+            (False, True): "pda_decode_reusing_order",
+            (True, True): "pda_partition_attention_reusing_order"}[(bool(pass1_only), bool(reuse_order))]
     return BoundCall(name, args, keep, out)
 
 

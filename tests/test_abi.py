@@ -140,7 +140,8 @@ def call(fn, p, q=0x1000, k=0x1000, v=0x1000, bt=0x1000, lens=0x1000, scale=0.12
     return getattr(lib, fn)(ctypes.byref(p), q, k, v, bt, lens, ctypes.c_float(scale), out, ws, ws_bytes, None)
 
 
-@pytest.mark.parametrize("fn", ["pda_decode", "pda_partition_attention", "pda_decode_reusing_order"])
+@pytest.mark.parametrize("fn", ["pda_decode", "pda_partition_attention", "pda_decode_reusing_order",
+                                "pda_partition_attention_reusing_order"])
 def test_step_validation(fn):
     lib = pda.load_library()
     assert call(fn, prob(), q=None) == pda.pda.PDA_ERR_NULL

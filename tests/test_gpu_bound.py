@@ -8,8 +8,8 @@ import torch
 
 import workloads as W
 from paper_2405_11143_amd import (bind_append_kv, bind_decode, make_problem, pda_append_kv, pda_decode,
-                                  pda_decode_reusing_order, pda_partition_attention, pda_plan, pda_work_order,
-                                  pda_workspace_bytes)
+                                  pda_decode_reusing_order, pda_merge_partitions, pda_partition_attention, pda_plan,
+                                  pda_work_order, pda_workspace_bytes)
 
 pytestmark = pytest.mark.gpu
 
@@ -92,6 +92,11 @@ def test_reused_work_order_matches_decode(dev, n):
     pda_decode(qs[0], k, v, bt, ln, st.scale, workspace=ws2, **kw)
     got = bind_decode(qs[1], k, v, bt, ln, st.scale, workspace=ws2, reuse_order=True, **kw)()
     want = pda_decode(qs[1], k, v, bt, ln, st.scale, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(got, want)
+    # pass 1 alone with the reused order, then the merge: the same bits again
+    got = bind_decode(qs[1], k, v, bt, ln, st.scale, workspace=ws2, pass1_only=True, reuse_order=True, **kw)()
+    pda_merge_partitions(prob, ln, got, ws2)
     torch.cuda.synchronize()
     assert torch.equal(got, want)
 
