@@ -8,7 +8,9 @@
  * slots hold NaN), runs pda_decode with several partition sizes (the
  * library's own among them), compares each output element with the
  * oracle (max-abs 8e-3, mean-abs 1e-3), checks that a reused work order
- * (pda_work_order + pda_decode_reusing_order) and the entry point without
+ * (pda_work_order + pda_decode_reusing_order, or pass 1 alone on it with
+ * pda_partition_attention_reusing_order + pda_merge_partitions) and the
+ * entry point without
  * allocation (pda_decode_noalloc) give bitwise the same output, and that
  * invalid arguments come back as status codes.  Then 40 new tokens per
  * sequence on the same cache (workgroups of 8 wavefronts, two 16-row tiles
@@ -187,6 +189,15 @@ int main(void) {
     CHECK_HIP(hipStreamSynchronize(stream));
     CHECK_HIP(hipMemcpy(out2, dout2, sizeof(float) * nq, hipMemcpyDeviceToHost));
     expect(memcmp(out, out2, sizeof(float) * nq) == 0, "reused work order: bitwise the same output");
+    /* pass 1 alone on the same order, then the merge: the same bits */
+    CHECK_HIP(hipMemset(dout2, 0, sizeof(float) * nq));
+    expect(pda_partition_attention_reusing_order(&prob, dq, dk, dv, dbt, dlens, (float)scale, dout2, ws, ws_bytes,
+                                                 stream) == PDA_OK,
+           "pda_partition_attention_reusing_order");
+    expect(pda_merge_partitions(&prob, dlens, dout2, ws, ws_bytes, stream) == PDA_OK, "pda_merge_partitions");
+    CHECK_HIP(hipStreamSynchronize(stream));
+    CHECK_HIP(hipMemcpy(out2, dout2, sizeof(float) * nq, hipMemcpyDeviceToHost));
+    expect(memcmp(out, out2, sizeof(float) * nq) == 0, "pass 1 on the reused order + merge: bitwise the same output");
 
     /* errors are status codes, returned before anything is launched */
     expect(pda_decode(&prob, NULL, dk, dv, dbt, dlens, (float)scale, dout, ws, ws_bytes, stream) == PDA_ERR_NULL,
