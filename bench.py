@@ -685,6 +685,8 @@ def op_prefix(args):
                    "speedup_vs_plain_decode": round(ms_plain / ms, 3),
                    "roofline": roofline(value, ms, KERNEL, args.config + ("_shared" if n == 1 else f"_shared_x{n}")),
                    "cpu_baseline": None})
+    result["roofline"]["timed"] = "the whole step: work order, pass 1 (partition_kernel) and merge"
+
     if n == 1 and not args.no_cpu_baseline:
         # the oracle computes the same attention (it reads each member's prefix itself); the rate is
         # per unique byte like the GPU's
