@@ -306,19 +306,19 @@ __device__ void run_staged(WaveAttention<D>& wave, WaveAttention<D>& wave_b, Sta
         const int t_stop = j_lim_b * kBlockTokens;
         const bool tail = tok0 + 2 * kBlockTokens > min(l_first_b, t_stop);  // wave-uniform
         const auto f = wave_b.template probs<2>(sc_b, tok0, L, tail, t_stop);
-        wave_b.pv_staged(aw, f, tail, tok0, min(l_vis_b, t_stop));
+        wave_b.template pv_staged<NW == 2 * kWaves>(aw, f, tail, tok0, min(l_vis_b, t_stop));
       }
       if (fold_a) {
         const int t_stop = j_lim * kBlockTokens;
         const bool tail = tok0 + 2 * kBlockTokens > min(l_first, t_stop);  // wave-uniform
         const auto f = wave.template probs<2>(sc_a, tok0, L, tail, t_stop);
-        wave.pv_staged(aw, f, tail, tok0, min(l_vis, t_stop));
+        wave.template pv_staged<NW == 2 * kWaves>(aw, f, tail, tok0, min(l_vis, t_stop));
       }
     } else {
       const int t_stop = j_lim * kBlockTokens;
       const bool tail = tok0 + 2 * kBlockTokens > min(l_first, t_stop);  // wave-uniform
       const auto f = wave.template softmax<2>(kr, tok0, L, tail, t_stop);
-      wave.pv_staged(aw, f, tail, tok0, min(l_vis, t_stop));
+      wave.template pv_staged<NW == 2 * kWaves>(aw, f, tail, tok0, min(l_vis, t_stop));
     }
   };
   for (int jw = J0; jw < J1; jw += kIdWindow) {
