@@ -300,8 +300,8 @@ __device__ void run_staged(WaveAttention<D>& wave, WaveAttention<D>& wave_b, Sta
       // see, which no row of the earlier chunk sees either; the earlier
       // chunk's rows give the rows between them probability 0.
       float sc_b[2][4], sc_a[2][4];
-      wave_b.template scores<2>(kr, sc_b);
-      wave.template scores<2>(kr, sc_a);
+      wave_b.template scores<2, NW == 2 * kWaves>(kr, sc_b);
+      wave.template scores<2, NW == 2 * kWaves>(kr, sc_a);
       if (fold_b) {
         const int t_stop = j_lim_b * kBlockTokens;
         const bool tail = tok0 + 2 * kBlockTokens > min(l_first_b, t_stop);  // wave-uniform

@@ -215,9 +215,11 @@ struct WaveAttention {
   // The scaled scores are formed here, in the MFMAs' own basic block: the
   // compiler did not insert the wait states a VALU read of an MFMA result
   // needs when the first such read came after the tail branch of probs.
-  template <int NB>
+  // PRIO: the MFMAs issue at raised wave priority (as in pv_staged).
+  template <int NB, bool PRIO = false>
   __device__ __forceinline__ void scores(const uint4 (&kr)[NB][NC], float (&sc)[NB][4]) const {
     floatx4_t acc[NB];
+    if constexpr (PRIO) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
       acc[b] = floatx4_t{0.f, 0.f, 0.f, 0.f};
@@ -225,6 +227,7 @@ struct WaveAttention {
       for (int c = 0; c < NC; ++c)
         acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kr[b][c]), qa[c], acc[b], 0, 0, 0);
     }
+    if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
 #pragma unroll
     for (int b = 0; b < NB; ++b)
 #pragma unroll
@@ -331,8 +334,9 @@ struct WaveAttention {
   // MFMA f32_16x16x32_bf16 per half of P.  In a tail pair, fragment elements
   // of tokens at or past l_vis are zeroed first.  PRIO: the wavefront issues
   // these MFMAs at raised priority (for workgroups of 8 wavefronts, whose
-  // pairs on a SIMD fold the same steps: on MI355X chunked prefill and long
-  // CoT with 64 new tokens ran 2.5% faster; workgroups of 4 gained nothing).
+  // pairs on a SIMD fold the same steps; with the score MFMAs raised too,
+  // chunked prefill and long CoT with 64 new tokens ran 5% faster on MI355X,
+  // while workgroups of 4 gained nothing and lost 4.6% with 16 new tokens).
   template <bool PRIO = false>
   __device__ __forceinline__ void pv_staged(uint4 (&aw)[VT], const PFrag<2>& f, bool tail, int tok0, int l_vis) {
     if (tail) {
