@@ -188,6 +188,10 @@ __global__ void __launch_bounds__(kLpThreads) logprob_kernel(const LogprobArgs a
   if (c < c_end) issue(u, c);
   for (; c < c_end; c += kStride) {
     issue(nu, c + kStride);
+    // The pass's fold at raised wave priority (the next loads are issued at
+    // the normal one): a wavefront that has its data finishes its pass and
+    // issues its next loads sooner (bf16 rows on MI355X 2.5% faster).
+    __builtin_amdgcn_s_setprio(1);
     if (first) {  // a reference from the pass's first logit (always a whole chunk's)
       first = false;
       float x[E];
@@ -224,6 +228,7 @@ __global__ void __launch_bounds__(kLpThreads) logprob_kernel(const LogprobArgs a
         }
       }
     }
+    __builtin_amdgcn_s_setprio(0);
 #pragma unroll
     for (int j = 0; j < kLpUnroll; ++j) u[j] = nu[j];
   }
