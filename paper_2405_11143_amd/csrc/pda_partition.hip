@@ -81,11 +81,11 @@ struct Staging {
 
 // Which paths a launch compiles.  A launch whose items all have one tile
 // (every decode step without shared-prefix groups) compiles the register
-// path only (136 VGPRs at D = 128, 33 KiB of LDS); with up to 4 query chunks
-// per item both paths are compiled (164 VGPRs, 50.5 KiB); with more, the
+// path only (138 VGPRs at D = 128, 33 KiB of LDS); with up to 4 query chunks
+// per item both paths are compiled (167 VGPRs, 50.5 KiB); with more, the
 // wide variant also folds two tiles per wavefront (229 VGPRs, 2
 // workgroups per compute unit), and beyond 8 chunks its 8-wavefront form
-// does (206 VGPRs, 67 KiB, one workgroup per compute unit: each staged step
+// does (217 VGPRs, 67 KiB, one workgroup per compute unit: each staged step
 // then serves 16 tiles, half the staging and barriers per tile of 8).
 // Staging takes 2 blocks per step, so three
 // staging buffers (49.5 KiB at D = 128) still leave room for 3 workgroups
