@@ -83,9 +83,9 @@ struct Staging {
 // (every decode step without shared-prefix groups) compiles the register
 // path only (138 VGPRs at D = 128, 33 KiB of LDS); with up to 4 query chunks
 // per item both paths are compiled (167 VGPRs, 50.5 KiB); with more, the
-// wide variant also folds two tiles per wavefront (229 VGPRs, 2
+// wide variant also folds two tiles per wavefront (243 VGPRs, 2
 // workgroups per compute unit), and beyond 8 chunks its 8-wavefront form
-// does (217 VGPRs, 67 KiB, one workgroup per compute unit: each staged step
+// does (227 VGPRs, 67 KiB, one workgroup per compute unit: each staged step
 // then serves 16 tiles, half the staging and barriers per tile of 8).
 // Staging takes 2 blocks per step, so three
 // staging buffers (49.5 KiB at D = 128) still leave room for 3 workgroups
@@ -222,8 +222,11 @@ __device__ void run_staged(WaveAttention<D>& wave, WaveAttention<D>& wave_b, Sta
   const int tid = threadIdx.x;
   bool bad = false;
   // Two steps' loads are in flight in two register sets while a third
-  // step is folded from LDS (three buffers).
-  uint4 ra[NL], rb[NL];
+  // step is folded from LDS (three buffers); in the wide variants' folds,
+  // three steps in three register sets (their registers allow it at 2
+  // wavefronts per SIMD; on MI355X 0.2-0.8% faster on every wide step).
+  uint4 ra[NL], rb[NL], rc[NL];
+  constexpr bool kThree = NW == 2 * kWaves || (NW == kWaves && NT == 2);
   // Load k of a thread takes piece ci = k * 256 + tid of the step, in
   // [block][K or V][piece] order.  A tile is a multiple of 64 pieces, so the
   // 64 lanes of a wavefront share the block and the K or V side of each load:
@@ -326,27 +329,57 @@ __device__ void run_staged(WaveAttention<D>& wave, WaveAttention<D>& wave_b, Sta
     for (int j = jw + tid; j < jwe; j += NW * kWaveSize) st.ids[j - jw] = table_row[j];
     __syncthreads();
     const int nsteps = (jwe - jw + SB - 1) / SB;
-    issue(ra, jw, jwe, 0);
-    if (nsteps > 1) issue(rb, jw, jwe, 1);
-    commit(ra, 0);
-    __syncthreads();
-    if (nsteps > 2) issue(ra, jw, jwe, 2);
-    // Step s sits in buffer s % 3; before the barrier that ends step s, step
-    // s + 1 moves from its registers into buffer (s + 1) % 3 (last read in
-    // step s - 2), and after it the freed registers take step s + 3.
-    // Unrolled by two so that the register sets stay static.
-    for (int step = 0, buf = 0; step < nsteps; step += 2) {
-      fold_step(jw, jwe, step, buf);
-      buf = buf == 2 ? 0 : buf + 1;
-      if (step + 1 < nsteps) commit(rb, buf);
+    if constexpr (!kThree) {
+      issue(ra, jw, jwe, 0);
+      if (nsteps > 1) issue(rb, jw, jwe, 1);
+      commit(ra, 0);
       __syncthreads();
-      if (step + 3 < nsteps) issue(rb, jw, jwe, step + 3);
-      if (step + 1 >= nsteps) break;
-      fold_step(jw, jwe, step + 1, buf);
-      buf = buf == 2 ? 0 : buf + 1;
-      if (step + 2 < nsteps) commit(ra, buf);
+      if (nsteps > 2) issue(ra, jw, jwe, 2);
+      // Step s sits in buffer s % 3; before the barrier that ends step s, step
+      // s + 1 moves from its registers into buffer (s + 1) % 3 (last read in
+      // step s - 2), and after it the freed registers take step s + 3.
+      // Unrolled by two so that the register sets stay static.
+      for (int step = 0, buf = 0; step < nsteps; step += 2) {
+        fold_step(jw, jwe, step, buf);
+        buf = buf == 2 ? 0 : buf + 1;
+        if (step + 1 < nsteps) commit(rb, buf);
+        __syncthreads();
+        if (step + 3 < nsteps) issue(rb, jw, jwe, step + 3);
+        if (step + 1 >= nsteps) break;
+        fold_step(jw, jwe, step + 1, buf);
+        buf = buf == 2 ? 0 : buf + 1;
+        if (step + 2 < nsteps) commit(ra, buf);
+        __syncthreads();
+        if (step + 4 < nsteps) issue(ra, jw, jwe, step + 4);
+      }
+    } else {
+      // Three register sets: while step s is folded, steps s + 1 .. s + 3 are
+      // in flight; the buffers are as above.  Unrolled by three.
+      issue(ra, jw, jwe, 0);
+      if (nsteps > 1) issue(rb, jw, jwe, 1);
+      if (nsteps > 2) issue(rc, jw, jwe, 2);
+      commit(ra, 0);
       __syncthreads();
-      if (step + 4 < nsteps) issue(ra, jw, jwe, step + 4);
+      if (nsteps > 3) issue(ra, jw, jwe, 3);
+      for (int step = 0, buf = 0; step < nsteps; step += 3) {
+        fold_step(jw, jwe, step, buf);
+        buf = buf == 2 ? 0 : buf + 1;
+        if (step + 1 < nsteps) commit(rb, buf);
+        __syncthreads();
+        if (step + 4 < nsteps) issue(rb, jw, jwe, step + 4);
+        if (step + 1 >= nsteps) break;
+        fold_step(jw, jwe, step + 1, buf);
+        buf = buf == 2 ? 0 : buf + 1;
+        if (step + 2 < nsteps) commit(rc, buf);
+        __syncthreads();
+        if (step + 5 < nsteps) issue(rc, jw, jwe, step + 5);
+        if (step + 2 >= nsteps) break;
+        fold_step(jw, jwe, step + 2, buf);
+        buf = buf == 2 ? 0 : buf + 1;
+        if (step + 3 < nsteps) commit(ra, buf);
+        __syncthreads();
+        if (step + 6 < nsteps) issue(ra, jw, jwe, step + 6);
+      }
     }
   }
   wave.bad |= __builtin_amdgcn_ballot_w64(bad) != 0;
