@@ -87,8 +87,8 @@ struct Plan {
 };
 
 // Workgroups the GPU runs at once in a step's pass-1 variant: 3 per compute
-// unit for items of up to 4 query chunks, 2 for the wide variant (229
-// VGPRs), 1 for its 8-wavefront form.
+// unit for items of up to 4 query chunks, 2 for the wide variant (243
+// VGPRs at D = 128), 1 for its 8-wavefront form.
 int64_t concurrent_items(const Plan& plan) {
   if (plan.chunks_per_group > pda::kWideChunks) return kConcurrentItems / 3;
   if (plan.chunks_per_group > pda::kWaves) return kConcurrentItems * 2 / 3;
