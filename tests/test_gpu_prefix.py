@@ -5,7 +5,11 @@ The operation is the same attention as the decode step, only scheduled so
 that each group's prefix is attended once for all members; the fp64 oracle
 is the plain decode definition.  Bar: max-abs <= 8e-3, mean-abs <= 1e-3 over
 every compared element; bitwise run-to-run and under block shuffles.
+PDA_RANDOM_GROUP_CASES sets the seeds of the two random-group tests (24 and
+16 by default; a wider sweep: PDA_RANDOM_GROUP_CASES=624).
 """
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -201,7 +205,7 @@ def draw_groups(case: int):
     return G, Hkv, D, groups, loners, tp
 
 
-@pytest.mark.parametrize("case", range(24))
+@pytest.mark.parametrize("case", range(int(os.environ.get("PDA_RANDOM_GROUP_CASES", "24"))))
 def test_random_groups(dev, case):
     """Random group layouts (sizes up to three prefix items of 64 rows,
     prefixes from none to several partitions, empty suffixes, sequences in no
@@ -242,7 +246,7 @@ def test_groups_with_several_new_tokens(dev, n, partition_tokens):
     assert np.array_equal(got, run(st, q, k, v, dev, partition_tokens)), "run-to-run"
 
 
-@pytest.mark.parametrize("case", range(16))
+@pytest.mark.parametrize("case", range(int(os.environ.get("PDA_RANDOM_GROUP_CASES", "16"))))
 def test_random_groups_several_new_tokens(dev, case):
     """Random group layouts with 2 to 21 new tokens per sequence (members up
     to 2 x 64 / (n G) + 1: one to three row groups), new tokens sometimes

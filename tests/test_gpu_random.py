@@ -5,7 +5,10 @@ one tile in registers, up to 4 tiles staged, wide items of 5-8 chunks and
 of 9-16 chunks on 8 wavefronts, several chunk groups), ragged contexts with
 empty ones and ones shorter than the new tokens, automatic and forced
 partition sizes (split contexts and the merge).  Same bar as the other
-parity tests."""
+parity tests.  PDA_RANDOM_CASES sets the number of seeds (32 by default; a
+wider sweep: PDA_RANDOM_CASES=2432)."""
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -37,7 +40,7 @@ def draw_case(case: int):
     return G, Hkv, D, n, lens, tp
 
 
-@pytest.mark.parametrize("case", range(32))
+@pytest.mark.parametrize("case", range(int(os.environ.get("PDA_RANDOM_CASES", "32"))))
 def test_random_descriptor(dev, case):
     G, Hkv, D, n, lens, tp = draw_case(case)
     Hq = G * Hkv
