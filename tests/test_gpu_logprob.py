@@ -12,8 +12,11 @@ per-thread reference at most 2^64 (in probability) below the running max:
 - the entropy is formed from sum p d relative to the reference, so its error
   scales with the entropy and the reference's distance from the max (at most
   64 in log2 units), not with |y|.
-1e-4 leaves several times that margin.
+1e-4 leaves several times that margin.  PDA_RANDOM_LOGPROB_CASES sets the
+number of seeded random calls (24 by default).
 """
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -233,3 +236,60 @@ def test_split_rows_with_neg_inf(dev):
     compare(lp, ent, ref_lp, ref_ent, "split rows with -inf logits")
     compare(lp1, ent1, ref_lp, ref_ent, "one workgroup per row with -inf logits")
     assert np.isfinite(ent.cpu().numpy()).all()
+
+
+def draw_logprob_case(case: int):
+    r = np.random.default_rng(7000 + case)
+    dtype = torch.bfloat16 if r.random() < 0.6 else torch.float32
+    rows = int(r.choice([1, 2, 7, 31, 100, 255, 256, 300]))
+    V = int(r.choice([1, 7, 8, 9, 1000, 4097, 33000, 128256, 151936]))
+    per16 = 8 if dtype == torch.bfloat16 else 4  # elements per 16 bytes
+    stride = (V + per16 - 1) // per16 * per16 + per16 * int(r.choice([0, 0, 1, 8]))
+    inv_t = float(r.choice([1.0, 1 / 0.7, 0.5, 2.0, 0.0]))
+    workspace = "auto" if r.random() < 0.7 else None
+    entropy = bool(r.random() < 0.8)
+    # -inf spans in some rows (with a positive inverse temperature), never over
+    # the row's token and never the whole row
+    spans = []
+    for row in range(rows):
+        if V > 2 and inv_t > 0 and r.random() < 0.2:
+            a = int(r.integers(0, V - 1))
+            spans.append((row, a, int(r.integers(a + 1, V + 1))))
+    return dtype, rows, V, stride, inv_t, workspace, entropy, spans
+
+
+@pytest.mark.parametrize("case", range(int(os.environ.get("PDA_RANDOM_LOGPROB_CASES", "24"))))
+def test_random_logprob_case(dev, case):
+    """Seeded random calls: bf16 and fp32, 1-300 rows (so both one workgroup
+    per row and rows split over workgroups), vocabularies from 1 to 151936
+    (ragged ones), rows padded past the vocabulary with NaN, temperatures
+    (0 included), -inf spans, with and without a workspace and the entropy;
+    the same bar against the oracle, and the log-probabilities bitwise the
+    same with and without the entropy."""
+    dtype, rows, V, stride, inv_t, workspace, entropy, spans = draw_logprob_case(case)
+    what = f"case {case}: {dtype} rows={rows} V={V} stride={stride} 1/T={inv_t:.3f} ws={workspace} ent={entropy}"
+    print(what, flush=True)
+    x, tok = W.make_logits(rows, V, seed=case, device=dev, dtype=dtype)
+    for row, a, b in spans:
+        if a == 0 and b == V:  # keep one finite logit
+            b = V - 1
+        x[row, a:b] = float("-inf")
+        t = int(tok[row])
+        if a <= t < b:  # the sampled token keeps a finite logit
+            tok[row] = a - 1 if a > 0 else b
+    padded = torch.full((rows, stride), float("nan"), dtype=dtype, device=dev)
+    padded[:, :V] = x
+    tt = torch.from_numpy(tok).to(dev)
+    lp, ent = pda_token_logprobs(padded, tt, inv_t, entropy=entropy, vocab=V, workspace=workspace)
+    torch.cuda.synchronize()
+    ref_lp, ref_ent = oracle.logprob(host_values(x), tok, np.float32(inv_t), entropy=entropy)
+    e1 = np.abs(lp.cpu().numpy().astype(np.float64) - ref_lp).max()
+    assert e1 <= TOL, (what, e1)
+    if entropy:
+        e2 = np.abs(ent.cpu().numpy().astype(np.float64) - ref_ent).max()
+        assert e2 <= TOL, (what, e2)
+        lp2, none = pda_token_logprobs(padded, tt, inv_t, entropy=False, vocab=V, workspace=workspace)
+        torch.cuda.synchronize()
+        assert none is None and torch.equal(lp, lp2), what
+    else:
+        assert ent is None
